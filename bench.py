@@ -1,0 +1,199 @@
+"""Benchmark of one RoLA attention layer (sparse + rotary low-rank branches) on one MI355X.
+
+One step = the whole hot path over one batch of synthetic input already resident in HBM:
+block selection -> block-sparse attention -> low-rank summary -> fused low-rank readout + gated combine,
+each a call of the C ABI on one HIP stream. Workload: the Wan2.1-14B-shaped 720p layer
+(B1 H40 d128, 21x45x80 grid = 75600 tokens, block 64, 90 % sparsity -> 118 of 1182 key blocks, r 32,
+bf16). The backbone's own steps (rotary tables, Q^r = R(Q^n), K^r = R(K^n)) run once, untimed.
+
+Prints one JSON line: effective TFLOP/s of the layer (sparse FLOPs actually performed + the paper's
+low-rank count 8 B H N d_h r, over the layer time), ms per layer, the roofline of the dominant kernel
+(block-sparse attention against the bf16 MFMA peak, timed with HIP events on its stream) and the CPU
+oracle timed on a bounded sample of the same layer.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2609_06712_amd import synth  # noqa: E402
+
+METRIC = "ms/attention layer + eff. TFLOP/s at Wan-14B 720p shape, 90% sparsity; % roofline"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def sparse_flops_performed(idx: torch.Tensor, N: int, block: int, d: int) -> float:
+    """4 d |I_valid| |K(I)_valid| summed over (b, h, query block): QK^T and PV on valid tokens."""
+    nb = idx.shape[2]
+    sizes = torch.full((nb,), block, dtype=torch.float64, device=idx.device)
+    sizes[-1] = N - (nb - 1) * block
+    keys = sizes[idx.long()].sum(dim=-1)            # [B, H, nb] valid keys per query block
+    return float(4.0 * d * (keys * sizes).sum())
+
+
+def lowrank_bytes(w) -> float:
+    """HBM bytes the low-rank branch + fused combine must move: summary reads K^n, V; the fused
+    readout reads Q^n, O^s and writes O (2-byte elements), plus the rotary-table columns it uses."""
+    per_token_head = 5 * w.d_h * 2
+    return float(w.B * w.H * w.N * per_token_head + 2 * w.N * (w.r // 2) * 4)
+
+
+def cpu_baseline(w, inp_cpu_head0: dict, budget_s: float) -> dict:
+    """The fp64 oracle, as it stands, on head 0: the whole low-rank branch (summary over every token)
+    plus as many query blocks of selection + sparse attention + readout + combine as fit the budget."""
+    import math
+    import oracle as O
+    from threadpoolctl import threadpool_info
+
+    f64 = synth.to_f64(inp_cpu_head0)
+    qn, kn, v = f64["Qn"][0, 0], f64["Kn"][0, 0], f64["V"][0, 0]
+    t0 = time.perf_counter()
+    cos, sin = O.rope_tables(*w.grid, w.split, w.base)
+    qr = O.round_to(O.rotate(qn, cos, sin), w.dtype)
+    kr = O.round_to(O.rotate(kn, cos, sin), w.dtype)
+    nb = O.num_blocks(w.N, w.block)
+    keep = O.keep_blocks(nb, w.sparsity)
+    qbar, kbar = O.pool_blocks(qr, w.block), O.pool_blocks(kr, w.block)
+    C, _ = O.lowrank_summary(kn, v, f64["Pk"][0], cos, sin)
+    flops = 4.0 * w.N * w.d_h * w.r                       # summary: projection + k~ v^T
+    scale = 1.0 / math.sqrt(w.d_h)
+    n_blocks = 0
+    for I in range(nb):
+        if time.perf_counter() - t0 > budget_s:
+            break
+        idx = np.zeros((nb, keep), dtype=np.int64)
+        idx[I] = O.select_blocks(O.block_scores(qbar[I:I + 1], kbar), keep)[0]
+        rows = np.arange(I * w.block, min(w.N, (I + 1) * w.block))
+        o_s = O.sparse_attention_rows(qr, kr, v, idx, w.block, scale, rows)
+        u = O.lowrank_features(qn[rows], f64["Pq"][0], cos[rows], sin[rows]) @ C
+        O.combine(o_s, O.rms_normalize(u, 1e-6), f64["logits"][0, rows], 1e-6)
+        nkeys = sum(min(w.N, (J + 1) * w.block) - J * w.block for J in idx[I])
+        flops += 4.0 * w.d_h * len(rows) * nkeys + 4.0 * len(rows) * w.d_h * w.r
+        n_blocks += 1
+    dt = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"head 0 of {w.H}: full low-rank summary over {w.N} tokens + selection, sparse "
+                      f"attention, readout and combine for query blocks 0..{n_blocks - 1} of {nb}; "
+                      f"{dt:.1f} s on {len(os.sched_getaffinity(0))} host cores"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the layer "
+              "shards by (batch, head) without communication, see the design notes", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(2)
+
+    from paper_2609_06712_amd import rola as R
+
+    w = synth.WAN_14B_720P
+    g = w.grid
+    dev = torch.device("cuda:0")
+    print(f"[bench] generating {w.name} inputs", file=sys.stderr, flush=True)
+    inp = synth.make_inputs(w, 0, device=dev)
+    prob = R.problem(w.B, w.H, w.N, w.d_h, g, w.dtype)
+    cos, sin = R.rola_rope_tables(prob, w.split, w.base)
+    qr = R.rola_rope_apply(inp["Qn"], cos, sin, g)
+    kr = R.rola_rope_apply(inp["Kn"], cos, sin, g)
+    nb = R.num_blocks(w.N, w.block)
+    keep = R.keep_blocks(nb, w.sparsity)
+    idx = torch.empty((w.B, w.H, nb, keep), dtype=torch.int32, device=dev)
+    ws_sel = torch.empty(R.select_workspace_bytes(prob, w.block), dtype=torch.uint8, device=dev)
+    ws_sum = torch.empty(R.summary_workspace_bytes(prob, w.r), dtype=torch.uint8, device=dev)
+    o_s = torch.empty_like(inp["Qn"])
+    out = torch.empty_like(inp["Qn"])
+    C = torch.empty((w.B, w.H, w.r, w.d_h), dtype=torch.float32, device=dev)
+    z = torch.empty((w.B, w.H, w.r), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    names = ["select", "sparse", "summary", "readout_combine"]
+
+    def step(ev=None):
+        def mark(i):
+            if ev is not None:
+                ev[i].record(stream)
+        mark(0)
+        R.rola_block_select(qr, kr, g, w.block, w.sparsity, out=idx, ws=ws_sel)
+        mark(1)
+        R.rola_sparse_attn(qr, kr, inp["V"], g, w.block, w.sparsity, idx, out=o_s)
+        mark(2)
+        R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], w.r, cos, sin, g, C=C, z=z, ws=ws_sum)
+        mark(3)
+        R.rola_lowrank_readout_combine(inp["Qn"], inp["Pq"], w.r, cos, sin, C, o_s, inp["logits"], g,
+                                       out=out)
+        mark(4)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(events[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_kernel = {n: [] for n in names}
+    for ev in events:
+        for i, n in enumerate(names):
+            per_kernel[n].append(ev[i].elapsed_time(ev[i + 1]))
+    kern_ms = {n: float(np.mean(v)) for n, v in per_kernel.items()}
+    ms = wall * 1e3 / args.steps
+
+    f_sparse = sparse_flops_performed(idx, w.N, w.block, w.d_h)
+    f_lowrank = 8.0 * w.B * w.H * w.N * w.d_h * w.r
+    eff = (f_sparse + f_lowrank) / (ms * 1e-3) / 1e12
+    achieved = f_sparse / (kern_ms["sparse"] * 1e-3) / 1e12
+    lr_ms = kern_ms["summary"] + kern_ms["readout_combine"]
+    lr_gbs = lowrank_bytes(w) / (lr_ms * 1e-3) / 1e9
+
+    res = {
+        "metric": METRIC, "value": round(eff, 2), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded smooth-field-plus-noise Q/K/V, random P_q/P_k, gate logits)",
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "N": w.N, "grid": list(g), "d_h": w.d_h,
+                   "block": w.block, "sparsity": w.sparsity, "keep": keep, "r": w.r,
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "kernel": "rola_sparse_attn", "achieved": round(achieved, 2),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None},
+        "lowrank_roofline": {"bound": "hbm", "kernels": "rola_lowrank_summary + "
+                             "rola_lowrank_readout_combine", "achieved": round(lr_gbs, 1),
+                             "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                             "frac": round(lr_gbs / PEAK_HBM_GBS, 4)},
+        "kernels_ms": {k: round(v, 4) for k, v in kern_ms.items()},
+        "flops": {"sparse_performed": f_sparse, "lowrank_paper": f_lowrank,
+                  "sparse_paper_formula": 4.0 * w.B * w.H * w.N ** 2 * (1 - w.sparsity) * w.d_h},
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
+        head0 = {k: inp[k][:, :1].cpu() for k in ("Qn", "Kn", "V")}
+        head0.update(Pq=inp["Pq"][:1].cpu(), Pk=inp["Pk"][:1].cpu(), logits=inp["logits"].cpu())
+        res["cpu_baseline"] = cpu_baseline(w, head0, args.cpu_budget)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,162 @@
+/*
+ * rola.h -- C ABI of librola.so: the RoLA attention module (sparse + rotary low-rank branches) for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * Paper: "RoLA: Rotary-Positioned Low-Rank Linear Attention for Efficient Diffusion Transformers".
+ * One attention layer, per (batch b, head h), is the Algorithm "RoLA attention forward pass":
+ *   Q^r, K^r = R(Q^n), R(K^n)                         step 3   rola_rope_apply (backbone's job)
+ *   blk_idx  = top-k key blocks per query block        step 4   rola_block_select
+ *   O^s      = block-sparse softmax attention          step 4   rola_sparse_attn
+ *   C, z     = sum_q R_r(q) SiLU(P_k k^n_q) v_q^T      steps 5-6 rola_lowrank_summary
+ *   O^lr     = RMSNorm(R_r(p) SiLU(P_q q^n_p))^T C)    steps 5,7 rola_lowrank_readout
+ *   O        = (O^s / r + sigma(logit) O^lr) r          steps 8-10 rola_combine
+ * rola_lowrank_readout_combine fuses the last two; rola_dense_attn is the dense softmax reference.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Tokens lie on a T x Hs x Ws latent grid (Sec. 3, Notation); token n = (t*Hs + y)*Ws + x and
+ *    N = T*Hs*Ws.
+ *  - Activations Q^n, K^n, Q^r, K^r, V, O^s, O^lr, O: [B, H, N, d_h], contiguous, row-major, element
+ *    type `dtype` (fp32 or bf16). P_q, P_k: [H, r, d_h] in `dtype` (the paper's R^{r x d_h} per head).
+ *  - Rotary tables cos/sin: fp32 [N, rope_ld], column j = pair j of the backbone ordering
+ *    (interleaved pairs (x_{2j}, x_{2j+1}) turned by +angle). rope_ld >= d_h/2 for the full rotation,
+ *    >= r/2 for the low-rank branch, which uses columns j < r/2 only (Sec. 4.2).
+ *  - Gate logits (X W_g + b_g, one per token, shared by all heads; Sec. 4.4): fp32 [B, N].
+ *  - C: fp32 [B, H, r, d_h]; z: fp32 [B, H, r]; block index list: int32 [B, H, n_blocks, keep].
+ *  - Every pointer except the problem struct is a device pointer owned by the caller, 16-byte
+ *    aligned. The library allocates nothing: scratch comes from the caller (see *_workspace_bytes).
+ *    Inputs are never written; outputs are fully overwritten; outputs must not overlap inputs unless
+ *    stated.
+ *  - Every call validates all arguments first and launches nothing when one is invalid. It then
+ *    enqueues its kernels on `stream` and returns without synchronising. A failed launch returns
+ *    ROLA_ERR_HIP. rola_last_error() gives a per-thread message for the last non-OK status.
+ *  - Supported: d_h in {64, 128} for fp32, d_h == 128 for bf16; block in {32, 64, 128} (fp32) or
+ *    {64, 128} (bf16); r even with 2 <= r <= d_h (fp32) or r in {16, 32, 64, 128} (bf16).
+ */
+#ifndef ROLA_H_
+#define ROLA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum rola_status {
+  ROLA_OK = 0,
+  ROLA_ERR_INVALID_ARGUMENT = 1, /* null/misaligned pointer, inconsistent sizes, out-of-range value */
+  ROLA_ERR_UNSUPPORTED = 2,      /* valid in principle, not built (d_h, block, r, dtype combination) */
+  ROLA_ERR_WORKSPACE = 3,        /* workspace smaller than the *_workspace_bytes helper asks for */
+  ROLA_ERR_HIP = 4               /* a HIP runtime call or kernel launch failed */
+} rola_status;
+
+typedef enum rola_dtype { ROLA_DTYPE_F32 = 0, ROLA_DTYPE_BF16 = 1 } rola_dtype;
+
+/* Problem shape (Sec. 3): Q/K/V are [B, H, N, d_h] on a T x Hs x Ws grid, N == T*Hs*Ws. */
+typedef struct rola_problem {
+  int32_t B, H, N, d_h;
+  int32_t T, Hs, Ws;
+  int32_t dtype; /* rola_dtype */
+} rola_problem;
+
+/* ---- host-side helpers (no device work) ------------------------------------------------------ */
+
+/* ceil(N / block): contiguous token blocks in flattened order; the last may be partial. -1 if an
+ * argument is not positive. */
+int32_t rola_num_blocks(int32_t N, int32_t block);
+
+/* Key blocks kept per query block at the given sparsity (the fraction of query-key interactions
+ * removed, Sec. 5.1): max(1, min(n_blocks, floor((1 - sparsity) * n_blocks + 0.5))) in double
+ * precision. -1 if n_blocks < 1 or sparsity is outside [0, 1). */
+int32_t rola_keep_blocks(int32_t n_blocks, double sparsity);
+
+/* Bytes of device workspace rola_block_select needs (pooled block means); 0 if the shape is invalid. */
+size_t rola_select_workspace_bytes(const rola_problem* p, int32_t block);
+
+/* Bytes of device workspace rola_lowrank_summary needs (per-chunk partial sums); 0 if invalid. */
+size_t rola_summary_workspace_bytes(const rola_problem* p, int32_t r);
+
+const char* rola_status_string(rola_status s);
+const char* rola_last_error(void);
+
+/* ---- rotary schedule (Sec. 3 3D RoPE; Sec. 4.2) ---------------------------------------------- */
+
+/* The backbone's rotary tables (freqs_cos, freqs_sin), each fp32 [N, d_h/2]. Axes t, y, x own
+ * contiguous runs of d_t/2, d_y/2, d_x/2 pairs (d_t + d_y + d_x == d_h, each even); pair i of an
+ * axis of width d_a turns by (pos_a + off_a) * base^(-2i/d_a). Evaluated in fp64, stored fp32. The
+ * offsets translate every position (shift-invariance checks); use 0 for the backbone's tables. */
+rola_status rola_rope_tables(const rola_problem* p, int32_t d_t, int32_t d_y, int32_t d_x,
+                             double base, int32_t off_t, int32_t off_y, int32_t off_x,
+                             float* cos_tab, float* sin_tab, hipStream_t stream);
+
+/* Xr = R(X): full 3D RoPE of every [d_h] row of X ([B, H, N, d_h]) with pairs j < d_h/2 (Algorithm
+ * step 3, the backbone's main-path rotation). fp32 arithmetic, result rounded to nearest even in
+ * `dtype`. Xr must not overlap X. */
+rola_status rola_rope_apply(const rola_problem* p, const void* X, const float* cos_tab,
+                            const float* sin_tab, int32_t rope_ld, void* Xr, hipStream_t stream);
+
+/* ---- sparse branch (Algorithm step 4; Sec. 4 opening: standard block-sparse attention) -------- */
+
+/* Top-k key blocks for every query block. For each (b, h): q_bar_I, k_bar_J = means of Q^r, K^r over
+ * the valid tokens of block I, J (fp32); score S_IJ = q_bar_I . k_bar_J / sqrt(d_h) (fp32); the
+ * keep = rola_keep_blocks(n_blocks, sparsity) largest scores are kept, equal scores going to the
+ * lower J, and written ascending to blk_idx [B, H, n_blocks, keep]. ws: >=
+ * rola_select_workspace_bytes(p, block) bytes of device scratch. */
+rola_status rola_block_select(const rola_problem* p, const void* Qr, const void* Kr, int32_t block,
+                              double sparsity, int32_t* blk_idx, void* ws, size_t ws_bytes,
+                              hipStream_t stream);
+
+/* Block-sparse attention: for a query token p in block I, O^s_p = sum softmax(q^r_p . k^r_q * scale)
+ * v_q over the valid key tokens q of the blocks blk_idx[b, h, I, :] (keep = rola_keep_blocks(
+ * n_blocks, sparsity) entries, each in [0, n_blocks); order irrelevant, duplicates not allowed).
+ * Online softmax with fp32 statistics and accumulators; bf16 path on MFMA. scale is normally
+ * 1/sqrt(d_h) (Sec. 3). Os: [B, H, N, d_h] in dtype. */
+rola_status rola_sparse_attn(const rola_problem* p, const void* Qr, const void* Kr, const void* V,
+                             int32_t block, double sparsity, const int32_t* blk_idx,
+                             float softmax_scale, void* Os, hipStream_t stream);
+
+/* Dense softmax attention O = softmax(Q^r K^r^T * scale) V (Sec. 3, "Full attention"): the 0 %
+ * sparsity reference, same kernel as rola_sparse_attn walking every key block in order. */
+rola_status rola_dense_attn(const rola_problem* p, const void* Qr, const void* Kr, const void* V,
+                            int32_t block, float softmax_scale, void* O, hipStream_t stream);
+
+/* ---- rotary low-rank branch (eq. qklr, eq. ctx; Algorithm steps 5-7) ------------------------- */
+
+/* Global context C = sum_q k~_q v_q^T (fp32 [B, H, r, d_h]) and z = sum_q k~_q (fp32 [B, H, r];
+ * may be NULL), with k~_q = R_r(q) SiLU(P_k k^n_q): projection to rank r, SiLU, then the rotation of
+ * pairs j < r/2 (RoPE outside the activation, Sec. 4.3). V is not rotated. Reduced in a fixed order
+ * (bitwise reproducible). ws: >= rola_summary_workspace_bytes(p, r) bytes. */
+rola_status rola_lowrank_summary(const rola_problem* p, const void* Kn, const void* V,
+                                 const void* Pk, int32_t r, const float* cos_tab,
+                                 const float* sin_tab, int32_t rope_ld, float* C, float* z,
+                                 void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* O^lr_p = u_p / sqrt(mean_i u_{p,i}^2 + eps_lr) with u_p = q~_p^T C and q~_p = R_r(p) SiLU(P_q q^n_p)
+ * (eq. ctx; RMSNorm without gain over d_h). Olr: [B, H, N, d_h] in dtype. */
+rola_status rola_lowrank_readout(const rola_problem* p, const void* Qn, const void* Pq, int32_t r,
+                                 const float* cos_tab, const float* sin_tab, int32_t rope_ld,
+                                 const float* C, float eps_lr, void* Olr, hipStream_t stream);
+
+/* ---- gated fusion (Sec. 4.4, eq. gate; Algorithm steps 8-10) --------------------------------- */
+
+/* O_p = (O^s_p / r_p + g_p O^lr_p) r_p, r_p = sqrt(mean_i (O^s_{p,i})^2 + eps), g_p =
+ * 1/(1 + exp(-logit_{b,p})). O may alias Os (in place); it must not overlap Olr otherwise. */
+rola_status rola_combine(const rola_problem* p, const void* Os, const void* Olr,
+                         const float* gate_logits, float eps, void* O, hipStream_t stream);
+
+/* rola_lowrank_readout followed by rola_combine in one pass, without materialising O^lr. O may
+ * alias Os. */
+rola_status rola_lowrank_readout_combine(const rola_problem* p, const void* Qn, const void* Pq,
+                                         int32_t r, const float* cos_tab, const float* sin_tab,
+                                         int32_t rope_ld, const float* C, float eps_lr,
+                                         const void* Os, const float* gate_logits, float eps,
+                                         void* O, hipStream_t stream);
+
+#ifdef __cplusplus
+} /* extern "C" */
+#endif
+
+#endif /* ROLA_H_ */

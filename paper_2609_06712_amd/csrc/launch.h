@@ -1,0 +1,49 @@
+// Internal launcher interface between the C ABI (rola_api.cpp) and the kernels (*.hip).
+// Launchers assume their arguments were validated by the ABI layer; they only enqueue work.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace rola {
+
+struct Shape {
+  int B, H, N, d;      // activations [B, H, N, d]
+  int T, Hs, Ws;       // latent grid, N == T*Hs*Ws
+  bool bf16;           // element type: bf16 (true) or fp32
+};
+
+inline int num_blocks(int N, int block) { return (N + block - 1) / block; }
+
+// rope.hip
+hipError_t launch_rope_tables(const Shape& s, int dt, int dy, int dx, double base, int ot, int oy,
+                              int ox, float* cos_tab, float* sin_tab, hipStream_t st);
+hipError_t launch_rope_apply(const Shape& s, const void* X, const float* cos_tab,
+                             const float* sin_tab, int ld, void* Xr, hipStream_t st);
+
+// select.hip
+size_t select_workspace_bytes(const Shape& s, int block);
+hipError_t launch_block_select(const Shape& s, const void* Qr, const void* Kr, int block, int keep,
+                               int32_t* idx, void* ws, hipStream_t st);
+
+// sparse_attn.hip  (idx == nullptr: dense, every key block in order; keep must equal n_blocks)
+hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, const void* V,
+                              int block, int keep, const int32_t* idx, float scale, void* Os,
+                              hipStream_t st);
+
+// lowrank.hip
+int summary_chunks(const Shape& s, int r);
+size_t summary_workspace_bytes(const Shape& s, int r);
+hipError_t launch_lowrank_summary(const Shape& s, const void* Kn, const void* V, const void* Pk,
+                                  int r, const float* cos_tab, const float* sin_tab, int ld,
+                                  float* C, float* z, void* ws, hipStream_t st);
+// Os == nullptr: plain readout into Out; otherwise readout fused with the gated combine.
+hipError_t launch_lowrank_readout(const Shape& s, const void* Qn, const void* Pq, int r,
+                                  const float* cos_tab, const float* sin_tab, int ld,
+                                  const float* C, float eps_lr, const void* Os,
+                                  const float* logits, float eps, void* Out, hipStream_t st);
+hipError_t launch_combine(const Shape& s, const void* Os, const void* Olr, const float* logits,
+                          float eps, void* O, hipStream_t st);
+
+}  // namespace rola

@@ -1,0 +1,701 @@
+// Rotary low-rank branch (eq. qklr, eq. ctx; Algorithm steps 5-7) and gated fusion (eq. gate,
+// Algorithm steps 8-10).
+//
+// Features are the paper's even/odd split (Sec. 4.5, fused inference kernel): projecting with the
+// even rows and the odd rows of P separately puts both members of every rotary pair in the same lane
+// and register slot, so SiLU and the rotation R_r are in-register arithmetic between two MFMA
+// results, no lane exchange.
+//
+// bf16 summary: per (b, h, token chunk) one workgroup of 4 waves, 32 tokens per wave per step.
+//   Psi = K^n P^T      (even and odd P rows)  A = K^n rows straight from HBM (prefetched one step
+//                      ahead), B = P fragments in registers; lane = pair j, 4 tokens per 16-token tile
+//   k~ = R_r SiLU(Psi) in registers (fp32), rounded to bf16 as the B operand of
+//   C^T += V^T k~      A = V^T from LDS (V transposed while staged), fp32 accumulators in registers.
+// Waves are summed through LDS in a fixed order, chunks by a second kernel in a fixed order: C and z
+// are bitwise reproducible (no float atomics).
+//
+// bf16 readout (+ combine): per wave 16-token tiles.
+//   Phi = P Q^T        A = P fragments (registers), B = Q^n rows from HBM; lane = token, 4 pairs
+//   q~ = R_r SiLU(Phi) in registers, rounded to bf16
+//   u^T = C^T q~       A = C^T (bf16, registers, loaded once per workgroup)
+//   RMSNorm over d_h (in-lane sums + 2 shuffles); fused: O = (O^s/r_s + g O^lr) r_s.
+// Both kernels are HBM-bound; grids are ordered head-minor and remapped so an XCD works on one token
+// range for all heads, reading each rotary-table row once into its L2.
+#include "common.h"
+#include "launch.h"
+
+namespace rola {
+namespace {
+
+constexpr int kSummaryStep = 128;  // tokens per workgroup step (4 waves x 32)
+
+__device__ __forceinline__ f32x4 mfma16x16x32(const bf16x8& a, const bf16x8& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+int summary_chunk_len(const Shape& s) {
+  const long heads = (long)s.B * s.H;
+  const long want = (1024 + heads - 1) / heads;  // chunks per head that fill the chip
+  long len = (s.N + want - 1) / want;
+  len = (len + kSummaryStep - 1) / kSummaryStep * kSummaryStep;
+  return (int)(len < kSummaryStep ? kSummaryStep : len);
+}
+
+// ------------------------------------------------------------------------------------------------
+// bf16 summary
+// ------------------------------------------------------------------------------------------------
+template <int JT>
+__global__ __launch_bounds__(256) void summary_mfma_kernel(
+    int N, int H, int r, int chunk_len, int n_chunks, int total, int ld,
+    const bf16* __restrict__ Kn, const bf16* __restrict__ V, const bf16* __restrict__ Pk,
+    const float* __restrict__ cos_tab, const float* __restrict__ sin_tab,
+    float* __restrict__ part) {
+  constexpr int D = 128, TOK = kSummaryStep, VP = TOK + 8;
+  __shared__ __attribute__((aligned(16))) float smem_f[D * VP / 2];  // V^T tile, reused for reductions
+  bf16* Vt = reinterpret_cast<bf16*>(smem_f);
+
+  const int BH = total / n_chunks;
+  const int L = xcd_remap(blockIdx.x, total);
+  const int head = L % BH, chunk = L / BH;
+  const int h = head % H;
+  const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64, lr = lane % 16, g = lane / 16;
+  const int half = r / 2;
+  const bf16* Kh = Kn + (long)head * N * D;
+  const bf16* Vh = V + (long)head * N * D;
+  const bf16* Ph = Pk + (long)h * r * D;
+
+  bf16x8 pe[JT][4], po[JT][4];
+#pragma unroll
+  for (int jt = 0; jt < JT; ++jt) {
+    const int j = 16 * jt + lr;
+#pragma unroll
+    for (int kc = 0; kc < 4; ++kc) {
+      if (j < half) {
+        pe[jt][kc] = *reinterpret_cast<const bf16x8*>(Ph + (long)(2 * j) * D + 32 * kc + 8 * g);
+        po[jt][kc] = *reinterpret_cast<const bf16x8*>(Ph + (long)(2 * j + 1) * D + 32 * kc + 8 * g);
+      } else {
+        pe[jt][kc] = bf16x8{};
+        po[jt][kc] = bf16x8{};
+      }
+    }
+  }
+  f32x4 ce[JT][8], co[JT][8];
+  float ze[JT], zo[JT];
+#pragma unroll
+  for (int jt = 0; jt < JT; ++jt) {
+    ze[jt] = zo[jt] = 0.f;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) ce[jt][w] = co[jt][w] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  const int t0 = chunk * chunk_len, t1 = min(N, t0 + chunk_len);
+  bf16x8 kf[2][4];
+  uint4 vreg[2][4];
+  auto load_step = [&](int base) {
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt) {
+      const int tok = base + wave * 32 + tt * 16 + lr;
+#pragma unroll
+      for (int kc = 0; kc < 4; ++kc)
+        kf[tt][kc] = tok < t1 ? *reinterpret_cast<const bf16x8*>(Kh + (long)tok * D + 32 * kc + 8 * g)
+                              : bf16x8{};
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int e = tid + 256 * i, kg = e / 16, dc = (e % 16) * 8;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int tok = base + 4 * kg + q;
+        vreg[i][q] = tok < t1 ? *reinterpret_cast<const uint4*>(Vh + (long)tok * D + dc)
+                              : make_uint4(0, 0, 0, 0);
+      }
+    }
+  };
+
+  load_step(t0);
+  for (int base = t0; base < t1; base += TOK) {
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int e = tid + 256 * i, kg = e / 16, dc = (e % 16) * 8;
+      const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&vreg[i][0]);
+      const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&vreg[i][1]);
+      const uint32_t* r2 = reinterpret_cast<const uint32_t*>(&vreg[i][2]);
+      const uint32_t* r3 = reinterpret_cast<const uint32_t*>(&vreg[i][3]);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        uint2 lo, hi;
+        lo.x = (r0[c] & 0xFFFFu) | (r1[c] << 16);
+        lo.y = (r2[c] & 0xFFFFu) | (r3[c] << 16);
+        hi.x = (r0[c] >> 16) | (r1[c] & 0xFFFF0000u);
+        hi.y = (r2[c] >> 16) | (r3[c] & 0xFFFF0000u);
+        *reinterpret_cast<uint2*>(&Vt[(dc + 2 * c) * VP + 4 * kg]) = lo;
+        *reinterpret_cast<uint2*>(&Vt[(dc + 2 * c + 1) * VP + 4 * kg]) = hi;
+      }
+    }
+    bf16x8 kc_cur[2][4];
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int kc = 0; kc < 4; ++kc) kc_cur[tt][kc] = kf[tt][kc];
+    __syncthreads();
+    if (base + TOK < t1) load_step(base + TOK);
+
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt) {
+      const int j = 16 * jt + lr;
+      bf16x8 be, bo;
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt) {
+        f32x4 ye = {0.f, 0.f, 0.f, 0.f}, yo = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kc = 0; kc < 4; ++kc) {
+          ye = mfma16x16x32(kc_cur[tt][kc], pe[jt][kc], ye);
+          yo = mfma16x16x32(kc_cur[tt][kc], po[jt][kc], yo);
+        }
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int tok = base + wave * 32 + tt * 16 + 4 * g + v;
+          float c = 1.f, s = 0.f;
+          if (tok < t1 && j < half) {
+            c = cos_tab[(long)tok * ld + j];
+            s = sin_tab[(long)tok * ld + j];
+          }
+          const float a = silu(ye[v]), b = silu(yo[v]);
+          const float ke = a * c - b * s, ko = a * s + b * c;
+          ze[jt] += ke;
+          zo[jt] += ko;
+          be[4 * tt + v] = (bf16)ke;
+          bo[4 * tt + v] = (bf16)ko;
+        }
+      }
+#pragma unroll
+      for (int w = 0; w < 8; ++w) {
+        const bf16* vrow = &Vt[(16 * w + lr) * VP + wave * 32 + 4 * g];
+        const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow);
+        const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 16);
+        const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        ce[jt][w] = mfma16x16x32(a, be, ce[jt][w]);
+        co[jt][w] = mfma16x16x32(a, bo, co[jt][w]);
+      }
+    }
+  }
+
+  // z: the four lane groups hold different tokens of the same pair j
+#pragma unroll
+  for (int jt = 0; jt < JT; ++jt) {
+    ze[jt] += __shfl_xor(ze[jt], 16);
+    ze[jt] += __shfl_xor(ze[jt], 32);
+    zo[jt] += __shfl_xor(zo[jt], 16);
+    zo[jt] += __shfl_xor(zo[jt], 32);
+  }
+  // Sum the four waves in a fixed order: wave 3 -> 2 -> 1 -> 0, one pair-tile at a time.
+  constexpr int PER = 2 * 8 * 4 + 2;  // floats per lane per pair tile
+  float* red = smem_f;
+#pragma unroll
+  for (int jt = 0; jt < JT; ++jt) {
+    for (int src = 3; src >= 1; --src) {
+      __syncthreads();
+      if (wave == src) {
+#pragma unroll
+        for (int w = 0; w < 8; ++w)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            red[((0 * 8 + w) * 4 + v) * 64 + lane] = ce[jt][w][v];
+            red[((1 * 8 + w) * 4 + v) * 64 + lane] = co[jt][w][v];
+          }
+        red[(PER - 2) * 64 + lane] = ze[jt];
+        red[(PER - 1) * 64 + lane] = zo[jt];
+      }
+      __syncthreads();
+      if (wave == src - 1) {
+#pragma unroll
+        for (int w = 0; w < 8; ++w)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            ce[jt][w][v] += red[((0 * 8 + w) * 4 + v) * 64 + lane];
+            co[jt][w][v] += red[((1 * 8 + w) * 4 + v) * 64 + lane];
+          }
+        ze[jt] += red[(PER - 2) * 64 + lane];
+        zo[jt] += red[(PER - 1) * 64 + lane];
+      }
+    }
+  }
+  if (wave == 0) {
+    float* P = part + ((long)head * n_chunks + chunk) * (long)(r * D + r);
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt) {
+      const int j = 16 * jt + lr;
+      if (j >= half) continue;
+#pragma unroll
+      for (int w = 0; w < 8; ++w)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int dim = 16 * w + 4 * g + v;
+          P[(long)(2 * j) * D + dim] = ce[jt][w][v];
+          P[(long)(2 * j + 1) * D + dim] = co[jt][w][v];
+        }
+      if (g == 0) {
+        P[(long)r * D + 2 * j] = ze[jt];
+        P[(long)r * D + 2 * j + 1] = zo[jt];
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
+// Plain summary for the fp32 path: 32-token sub-tiles through LDS, thread per (pair) then (r, c).
+// ------------------------------------------------------------------------------------------------
+template <typename T, int D>
+__global__ __launch_bounds__(256) void summary_simple_kernel(
+    int N, int H, int r, int chunk_len, int n_chunks, int ld, const T* __restrict__ Kn,
+    const T* __restrict__ V, const T* __restrict__ Pk, const float* __restrict__ cos_tab,
+    const float* __restrict__ sin_tab, float* __restrict__ part) {
+  constexpr int TT = 32, MAXR = 128;
+  __shared__ float Ks[TT][D];
+  __shared__ float Vs[TT][D];
+  __shared__ float kt[TT][MAXR];
+  const int chunk = blockIdx.x;
+  const long head = (long)blockIdx.z * gridDim.y + blockIdx.y;
+  const int h = blockIdx.y;
+  const T* Kh = Kn + head * (long)N * D;
+  const T* Vh = V + head * (long)N * D;
+  const T* Ph = Pk + (long)h * r * D;
+  const int half = r / 2;
+  const int t0 = chunk * chunk_len, t1 = min(N, t0 + chunk_len);
+  constexpr int MAXE = MAXR * D / 256;
+  float acc[MAXE];
+  float zacc = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXE; ++i) acc[i] = 0.f;
+  for (int b0 = t0; b0 < t1; b0 += TT) {
+    __syncthreads();
+    for (int e = threadIdx.x; e < TT * D; e += 256) {
+      const int tr = e / D, c = e % D, tok = b0 + tr;
+      Ks[tr][c] = tok < t1 ? to_f32(Kh[(long)tok * D + c]) : 0.f;
+      Vs[tr][c] = tok < t1 ? to_f32(Vh[(long)tok * D + c]) : 0.f;
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < TT * half; e += 256) {
+      const int tr = e / half, j = e % half, tok = b0 + tr;
+      float ae = 0.f, ao = 0.f;
+      for (int c = 0; c < D; ++c) {
+        ae = fmaf(to_f32(Ph[(long)(2 * j) * D + c]), Ks[tr][c], ae);
+        ao = fmaf(to_f32(Ph[(long)(2 * j + 1) * D + c]), Ks[tr][c], ao);
+      }
+      const float a = silu(ae), b = silu(ao);
+      float cs = 1.f, sn = 0.f;
+      if (tok < t1) { cs = cos_tab[(long)tok * ld + j]; sn = sin_tab[(long)tok * ld + j]; }
+      kt[tr][2 * j] = a * cs - b * sn;
+      kt[tr][2 * j + 1] = a * sn + b * cs;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < MAXE; ++i) {
+      const int e = threadIdx.x + 256 * i;
+      if (e < r * D) {
+        const int ri = e / D, c = e % D;
+        float s = acc[i];
+        for (int tr = 0; tr < TT; ++tr) s = fmaf(kt[tr][ri], Vs[tr][c], s);
+        acc[i] = s;
+      }
+    }
+    if (threadIdx.x < r)
+      for (int tr = 0; tr < TT; ++tr) zacc += kt[tr][threadIdx.x];
+  }
+  float* P = part + (head * n_chunks + chunk) * (long)(r * D + r);
+#pragma unroll
+  for (int i = 0; i < MAXE; ++i) {
+    const int e = threadIdx.x + 256 * i;
+    if (e < r * D) P[e] = acc[i];
+  }
+  if (threadIdx.x < r) P[(long)r * D + threadIdx.x] = zacc;
+}
+
+// C, z = sum over chunks in chunk order (fixed order: reproducible).
+__global__ __launch_bounds__(256) void summary_reduce_kernel(int rd, int r, int n_chunks,
+                                                             const float* __restrict__ part,
+                                                             float* __restrict__ C,
+                                                             float* __restrict__ z) {
+  const long head = blockIdx.y;
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  const int per = rd + r;
+  if (e >= per) return;
+  const float* P = part + head * n_chunks * (long)per + e;
+  float s = 0.f;
+  for (int c = 0; c < n_chunks; ++c) s += P[(long)c * per];
+  if (e < rd) C[head * rd + e] = s;
+  else if (z) z[head * r + (e - rd)] = s;
+}
+
+// ------------------------------------------------------------------------------------------------
+// bf16 readout, optionally fused with the gated combine
+// ------------------------------------------------------------------------------------------------
+constexpr int kReadoutTilesPerWave = 4;  // 16-token tiles per wave per workgroup
+
+template <int JT, bool COMBINE>
+__global__ __launch_bounds__(256) void readout_mfma_kernel(
+    int N, int H, int r, int n_groups, int total, int ld, const bf16* __restrict__ Qn,
+    const bf16* __restrict__ Pq, const float* __restrict__ cos_tab,
+    const float* __restrict__ sin_tab, const float* __restrict__ C, float eps_lr,
+    const bf16* Os, const float* __restrict__ logits, float eps, bf16* Out) {
+  constexpr int D = 128, TPW = kReadoutTilesPerWave;
+  const int BH = total / n_groups;
+  const int L = xcd_remap(blockIdx.x, total);
+  const int head = L % BH, grp = L / BH;
+  const int h = head % H, b = head / H;
+  const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64, lr = lane % 16, g = lane / 16;
+  const int half = r / 2;
+  const bf16* Qh = Qn + (long)head * N * D;
+  const bf16* Ph = Pq + (long)h * r * D;
+  const float* Ch = C + (long)head * r * D;
+
+  // A operand of Phi = P Q^T: even / odd rows of P for pair j = 16 jt + lr.
+  bf16x8 pe[JT][4], po[JT][4];
+  // A operand of u^T = C^T q~: row = channel 16 w + lr; slots 0-3 = even rows 2(16jt+4g+s),
+  // slots 4-7 = odd rows 2(16jt+4g+s)+1.
+  bf16x8 ca[JT][8];
+#pragma unroll
+  for (int jt = 0; jt < JT; ++jt) {
+    const int j = 16 * jt + lr;
+#pragma unroll
+    for (int kc = 0; kc < 4; ++kc) {
+      if (j < half) {
+        pe[jt][kc] = *reinterpret_cast<const bf16x8*>(Ph + (long)(2 * j) * D + 32 * kc + 8 * g);
+        po[jt][kc] = *reinterpret_cast<const bf16x8*>(Ph + (long)(2 * j + 1) * D + 32 * kc + 8 * g);
+      } else {
+        pe[jt][kc] = bf16x8{};
+        po[jt][kc] = bf16x8{};
+      }
+    }
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+      const int ch = 16 * w + lr;
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const int jj = 16 * jt + 4 * g + s;
+        ca[jt][w][s] = jj < half ? (bf16)Ch[(long)(2 * jj) * D + ch] : (bf16)0.f;
+        ca[jt][w][4 + s] = jj < half ? (bf16)Ch[(long)(2 * jj + 1) * D + ch] : (bf16)0.f;
+      }
+    }
+  }
+
+  for (int it = 0; it < TPW; ++it) {
+    const int tok0 = (grp * 4 * TPW + it * 4 + wave) * 16;
+    if (tok0 >= N) break;
+    const int tok = tok0 + lr;
+    const bool valid = tok < N;
+    bf16x8 qf[4];
+#pragma unroll
+    for (int kc = 0; kc < 4; ++kc)
+      qf[kc] = valid ? *reinterpret_cast<const bf16x8*>(Qh + (long)tok * D + 32 * kc + 8 * g)
+                     : bf16x8{};
+    f32x4 u[8];
+#pragma unroll
+    for (int w = 0; w < 8; ++w) u[w] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt) {
+      f32x4 ye = {0.f, 0.f, 0.f, 0.f}, yo = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kc = 0; kc < 4; ++kc) {
+        ye = mfma16x16x32(pe[jt][kc], qf[kc], ye);
+        yo = mfma16x16x32(po[jt][kc], qf[kc], yo);
+      }
+      const int jb = 16 * jt + 4 * g;  // pairs jb..jb+3 of token `tok`
+      float4 c4 = make_float4(1.f, 1.f, 1.f, 1.f), s4 = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (valid && jb < half) {
+        c4 = *reinterpret_cast<const float4*>(cos_tab + (long)tok * ld + jb);
+        s4 = *reinterpret_cast<const float4*>(sin_tab + (long)tok * ld + jb);
+      }
+      const float cc[4] = {c4.x, c4.y, c4.z, c4.w}, ss[4] = {s4.x, s4.y, s4.z, s4.w};
+      bf16x8 bq;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const float a = silu(ye[v]), bb = silu(yo[v]);
+        bq[v] = (bf16)(a * cc[v] - bb * ss[v]);
+        bq[4 + v] = (bf16)(a * ss[v] + bb * cc[v]);
+      }
+#pragma unroll
+      for (int w = 0; w < 8; ++w) u[w] = mfma16x16x32(ca[jt][w], bq, u[w]);
+    }
+    float ss_u = 0.f;
+#pragma unroll
+    for (int w = 0; w < 8; ++w)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) ss_u = fmaf(u[w][v], u[w][v], ss_u);
+    ss_u += __shfl_xor(ss_u, 16);
+    ss_u += __shfl_xor(ss_u, 32);
+    const float inv_u = rsqrtf(ss_u * (1.0f / D) + eps_lr);
+    bf16* orow = Out + (long)head * N * D + (long)tok * D;
+    if constexpr (COMBINE) {
+      const bf16* srow = Os + (long)head * N * D + (long)tok * D;
+      float os[8][4];
+      float ss_s = 0.f;
+#pragma unroll
+      for (int w = 0; w < 8; ++w) {
+        bf16x4 x = valid ? *reinterpret_cast<const bf16x4*>(srow + 16 * w + 4 * g) : bf16x4{};
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          os[w][v] = (float)x[v];
+          ss_s = fmaf(os[w][v], os[w][v], ss_s);
+        }
+      }
+      ss_s += __shfl_xor(ss_s, 16);
+      ss_s += __shfl_xor(ss_s, 32);
+      const float rs = sqrtf(ss_s * (1.0f / D) + eps);
+      const float gate = valid ? sigmoid(logits[(long)b * N + tok]) : 0.f;
+      const float inv_rs = 1.0f / rs;
+      if (valid) {
+#pragma unroll
+        for (int w = 0; w < 8; ++w) {
+          bf16x4 o;
+#pragma unroll
+          for (int v = 0; v < 4; ++v) o[v] = (bf16)((os[w][v] * inv_rs + gate * u[w][v] * inv_u) * rs);
+          *reinterpret_cast<bf16x4*>(orow + 16 * w + 4 * g) = o;
+        }
+      }
+    } else {
+      if (valid) {
+#pragma unroll
+        for (int w = 0; w < 8; ++w) {
+          bf16x4 o;
+#pragma unroll
+          for (int v = 0; v < 4; ++v) o[v] = (bf16)(u[w][v] * inv_u);
+          *reinterpret_cast<bf16x4*>(orow + 16 * w + 4 * g) = o;
+        }
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
+// Plain readout (+ combine) for the fp32 path: 32 tokens per workgroup, 8 threads per token.
+// ------------------------------------------------------------------------------------------------
+template <typename T, int D, bool COMBINE>
+__global__ __launch_bounds__(256) void readout_simple_kernel(
+    int N, int H, int r, int ld, const T* __restrict__ Qn, const T* __restrict__ Pq,
+    const float* __restrict__ cos_tab, const float* __restrict__ sin_tab,
+    const float* __restrict__ C, float eps_lr, const T* Os, const float* __restrict__ logits,
+    float eps, T* Out) {
+  constexpr int TT = 32, MAXR = 128;
+  __shared__ float Cs[MAXR * D];
+  __shared__ float Qs[TT][D];
+  __shared__ float ft[TT][MAXR];
+  const long head = (long)blockIdx.z * gridDim.y + blockIdx.y;
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int tok0 = blockIdx.x * TT;
+  const T* Qh = Qn + head * (long)N * D;
+  const T* Ph = Pq + (long)h * r * D;
+  const int half = r / 2;
+  for (int e = threadIdx.x; e < r * D; e += 256) Cs[e] = C[head * r * D + e];
+  for (int e = threadIdx.x; e < TT * D; e += 256) {
+    const int tr = e / D, c = e % D, tok = tok0 + tr;
+    Qs[tr][c] = tok < N ? to_f32(Qh[(long)tok * D + c]) : 0.f;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < TT * half; e += 256) {
+    const int tr = e / half, j = e % half, tok = tok0 + tr;
+    float ae = 0.f, ao = 0.f;
+    for (int c = 0; c < D; ++c) {
+      ae = fmaf(to_f32(Ph[(long)(2 * j) * D + c]), Qs[tr][c], ae);
+      ao = fmaf(to_f32(Ph[(long)(2 * j + 1) * D + c]), Qs[tr][c], ao);
+    }
+    const float a = silu(ae), bb = silu(ao);
+    float cs = 1.f, sn = 0.f;
+    if (tok < N) { cs = cos_tab[(long)tok * ld + j]; sn = sin_tab[(long)tok * ld + j]; }
+    ft[tr][2 * j] = a * cs - bb * sn;
+    ft[tr][2 * j + 1] = a * sn + bb * cs;
+  }
+  __syncthreads();
+  const int tr = threadIdx.x / 8, sub = threadIdx.x % 8, tok = tok0 + tr;
+  constexpr int PER = D / 8;
+  float u[PER];
+  float ss_u = 0.f;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int c = sub + 8 * k;
+    float s = 0.f;
+    for (int ri = 0; ri < r; ++ri) s = fmaf(ft[tr][ri], Cs[ri * D + c], s);
+    u[k] = s;
+    ss_u = fmaf(s, s, ss_u);
+  }
+  ss_u += __shfl_xor(ss_u, 1);
+  ss_u += __shfl_xor(ss_u, 2);
+  ss_u += __shfl_xor(ss_u, 4);
+  const float inv_u = 1.0f / sqrtf(ss_u / D + eps_lr);
+  T* orow = Out + head * (long)N * D + (long)tok * D;
+  if constexpr (COMBINE) {
+    const T* srow = Os + head * (long)N * D + (long)tok * D;
+    float os[PER];
+    float ss_s = 0.f;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      os[k] = tok < N ? to_f32(srow[sub + 8 * k]) : 0.f;
+      ss_s = fmaf(os[k], os[k], ss_s);
+    }
+    ss_s += __shfl_xor(ss_s, 1);
+    ss_s += __shfl_xor(ss_s, 2);
+    ss_s += __shfl_xor(ss_s, 4);
+    const float rs = sqrtf(ss_s / D + eps);
+    if (tok < N) {
+      const float gate = 1.0f / (1.0f + expf(-logits[(long)b * N + tok]));
+#pragma unroll
+      for (int k = 0; k < PER; ++k)
+        orow[sub + 8 * k] = from_f32<T>((os[k] / rs + gate * (u[k] * inv_u)) * rs);
+    }
+  } else {
+    if (tok < N) {
+#pragma unroll
+      for (int k = 0; k < PER; ++k) orow[sub + 8 * k] = from_f32<T>(u[k] * inv_u);
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
+// Gated combine alone: one row of d_h elements per d_h/8 lanes, 8 elements per lane.
+// ------------------------------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void combine_kernel(long rows, int N, int H, int d,
+                                                      const T* Os, const T* __restrict__ Olr,
+                                                      const float* __restrict__ logits, float eps,
+                                                      T* O) {
+  const int G = d / 8;
+  const long gidx = (long)blockIdx.x * 256 + threadIdx.x;
+  const long row = gidx / G;
+  const int sub = (int)(gidx % G);
+  const bool valid = row < rows;
+  float os[8] = {}, ol[8] = {};
+  if (valid) {
+    load8(Os + row * d + sub * 8, os);
+    load8(Olr + row * d + sub * 8, ol);
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) ss = fmaf(os[i], os[i], ss);
+  for (int m = 1; m < G; m <<= 1) ss += __shfl_xor(ss, m);
+  if (!valid) return;
+  const float rs = sqrtf(ss / d + eps);
+  const long b = row / ((long)H * N);
+  const int n = (int)(row % N);
+  const float gate = 1.0f / (1.0f + expf(-logits[b * N + n]));
+  float o[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) o[i] = (os[i] / rs + gate * ol[i]) * rs;
+  store8(O + row * d + sub * 8, o);
+}
+
+template <int JT>
+hipError_t summary_mfma(const Shape& s, const void* Kn, const void* V, const void* Pk, int r,
+                        const float* ct, const float* st_, int ld, float* part, int chunk_len,
+                        int n_chunks, hipStream_t st) {
+  const int total = s.B * s.H * n_chunks;
+  hipLaunchKernelGGL((summary_mfma_kernel<JT>), dim3(total), dim3(256), 0, st, s.N, s.H, r,
+                     chunk_len, n_chunks, total, ld, (const bf16*)Kn, (const bf16*)V,
+                     (const bf16*)Pk, ct, st_, part);
+  return hipGetLastError();
+}
+
+template <int JT, bool COMBINE>
+hipError_t readout_mfma(const Shape& s, const void* Qn, const void* Pq, int r, const float* ct,
+                        const float* st_, int ld, const float* C, float eps_lr, const void* Os,
+                        const float* logits, float eps, void* Out, hipStream_t st) {
+  const int per_group = 4 * kReadoutTilesPerWave * 16;
+  const int n_groups = (s.N + per_group - 1) / per_group;
+  const int total = s.B * s.H * n_groups;
+  hipLaunchKernelGGL((readout_mfma_kernel<JT, COMBINE>), dim3(total), dim3(256), 0, st, s.N, s.H,
+                     r, n_groups, total, ld, (const bf16*)Qn, (const bf16*)Pq, ct, st_, C, eps_lr,
+                     (const bf16*)Os, logits, eps, (bf16*)Out);
+  return hipGetLastError();
+}
+
+template <bool COMBINE>
+hipError_t readout_dispatch(const Shape& s, const void* Qn, const void* Pq, int r, const float* ct,
+                            const float* st_, int ld, const float* C, float eps_lr, const void* Os,
+                            const float* logits, float eps, void* Out, hipStream_t st) {
+  if (s.bf16) {
+    if (r <= 32)
+      return readout_mfma<1, COMBINE>(s, Qn, Pq, r, ct, st_, ld, C, eps_lr, Os, logits, eps, Out, st);
+    if (r <= 64)
+      return readout_mfma<2, COMBINE>(s, Qn, Pq, r, ct, st_, ld, C, eps_lr, Os, logits, eps, Out, st);
+    return readout_mfma<4, COMBINE>(s, Qn, Pq, r, ct, st_, ld, C, eps_lr, Os, logits, eps, Out, st);
+  }
+  const dim3 grid((s.N + 31) / 32, s.H, s.B);
+  if (s.d == 64)
+    hipLaunchKernelGGL((readout_simple_kernel<float, 64, COMBINE>), grid, dim3(256), 0, st, s.N,
+                       s.H, r, ld, (const float*)Qn, (const float*)Pq, ct, st_, C, eps_lr,
+                       (const float*)Os, logits, eps, (float*)Out);
+  else
+    hipLaunchKernelGGL((readout_simple_kernel<float, 128, COMBINE>), grid, dim3(256), 0, st, s.N,
+                       s.H, r, ld, (const float*)Qn, (const float*)Pq, ct, st_, C, eps_lr,
+                       (const float*)Os, logits, eps, (float*)Out);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int summary_chunks(const Shape& s, int r) {
+  (void)r;
+  const int len = summary_chunk_len(s);
+  return (s.N + len - 1) / len;
+}
+
+size_t summary_workspace_bytes(const Shape& s, int r) {
+  return (size_t)s.B * s.H * summary_chunks(s, r) * (size_t)(r * s.d + r) * sizeof(float);
+}
+
+hipError_t launch_lowrank_summary(const Shape& s, const void* Kn, const void* V, const void* Pk,
+                                  int r, const float* cos_tab, const float* sin_tab, int ld,
+                                  float* C, float* z, void* ws, hipStream_t st) {
+  const int chunk_len = summary_chunk_len(s);
+  const int n_chunks = (s.N + chunk_len - 1) / chunk_len;
+  float* part = (float*)ws;
+  hipError_t e;
+  if (s.bf16) {
+    if (r <= 32) e = summary_mfma<1>(s, Kn, V, Pk, r, cos_tab, sin_tab, ld, part, chunk_len, n_chunks, st);
+    else if (r <= 64) e = summary_mfma<2>(s, Kn, V, Pk, r, cos_tab, sin_tab, ld, part, chunk_len, n_chunks, st);
+    else e = summary_mfma<4>(s, Kn, V, Pk, r, cos_tab, sin_tab, ld, part, chunk_len, n_chunks, st);
+  } else {
+    const dim3 grid(n_chunks, s.H, s.B);
+    if (s.d == 64)
+      hipLaunchKernelGGL((summary_simple_kernel<float, 64>), grid, dim3(256), 0, st, s.N, s.H, r,
+                         chunk_len, n_chunks, ld, (const float*)Kn, (const float*)V,
+                         (const float*)Pk, cos_tab, sin_tab, part);
+    else
+      hipLaunchKernelGGL((summary_simple_kernel<float, 128>), grid, dim3(256), 0, st, s.N, s.H, r,
+                         chunk_len, n_chunks, ld, (const float*)Kn, (const float*)V,
+                         (const float*)Pk, cos_tab, sin_tab, part);
+    e = hipGetLastError();
+  }
+  if (e != hipSuccess) return e;
+  const int per = r * s.d + r;
+  hipLaunchKernelGGL(summary_reduce_kernel, dim3((per + 255) / 256, s.B * s.H), dim3(256), 0, st,
+                     r * s.d, r, n_chunks, part, C, z);
+  return hipGetLastError();
+}
+
+hipError_t launch_lowrank_readout(const Shape& s, const void* Qn, const void* Pq, int r,
+                                  const float* cos_tab, const float* sin_tab, int ld,
+                                  const float* C, float eps_lr, const void* Os,
+                                  const float* logits, float eps, void* Out, hipStream_t st) {
+  if (Os)
+    return readout_dispatch<true>(s, Qn, Pq, r, cos_tab, sin_tab, ld, C, eps_lr, Os, logits, eps,
+                                  Out, st);
+  return readout_dispatch<false>(s, Qn, Pq, r, cos_tab, sin_tab, ld, C, eps_lr, nullptr, nullptr,
+                                 0.f, Out, st);
+}
+
+hipError_t launch_combine(const Shape& s, const void* Os, const void* Olr, const float* logits,
+                          float eps, void* O, hipStream_t st) {
+  const long rows = (long)s.B * s.H * s.N;
+  const long threads = rows * (s.d / 8);
+  const dim3 grid((unsigned)((threads + 255) / 256));
+  if (s.bf16)
+    hipLaunchKernelGGL(combine_kernel<bf16>, grid, dim3(256), 0, st, rows, s.N, s.H, s.d,
+                       (const bf16*)Os, (const bf16*)Olr, logits, eps, (bf16*)O);
+  else
+    hipLaunchKernelGGL(combine_kernel<float>, grid, dim3(256), 0, st, rows, s.N, s.H, s.d,
+                       (const float*)Os, (const float*)Olr, logits, eps, (float*)O);
+  return hipGetLastError();
+}
+
+}  // namespace rola

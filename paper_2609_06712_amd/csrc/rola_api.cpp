@@ -1,0 +1,298 @@
+// C ABI of librola.so (declared in include/rola.h): argument validation, workspace sizing, status
+// reporting, then dispatch to the kernel launchers. Validation runs entirely on the host and touches
+// no device, so every invalid call returns before anything is enqueued.
+#include "rola.h"
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "launch.h"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+rola_status fail(rola_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+rola_status hip_status(hipError_t e, const char* where) {
+  if (e == hipSuccess) return ROLA_OK;
+  return fail(ROLA_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool aligned(const void* p) { return p != nullptr && ((uintptr_t)p & 15u) == 0; }
+
+#define REQUIRE_PTR(p)                                                                      \
+  do {                                                                                      \
+    if (!aligned(p))                                                                        \
+      return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: pointer '%s' is null or not 16-byte aligned", \
+                  __func__, #p);                                                            \
+  } while (0)
+
+rola_status check_problem(const rola_problem* p, const char* fn, rola::Shape* out) {
+  if (!p) return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: problem is null", fn);
+  if (p->B < 1 || p->H < 1 || p->N < 1 || p->T < 1 || p->Hs < 1 || p->Ws < 1)
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: sizes must be positive (B=%d H=%d N=%d T=%d Hs=%d Ws=%d)",
+                fn, p->B, p->H, p->N, p->T, p->Hs, p->Ws);
+  if ((long long)p->T * p->Hs * p->Ws != (long long)p->N)
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: N=%d differs from T*Hs*Ws=%lld", fn, p->N,
+                (long long)p->T * p->Hs * p->Ws);
+  if (p->dtype != ROLA_DTYPE_F32 && p->dtype != ROLA_DTYPE_BF16)
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: unknown dtype %d", fn, p->dtype);
+  if (p->d_h != 64 && p->d_h != 128)
+    return fail(ROLA_ERR_UNSUPPORTED, "%s: d_h=%d (built: 64, 128)", fn, p->d_h);
+  if (p->dtype == ROLA_DTYPE_BF16 && p->d_h != 128)
+    return fail(ROLA_ERR_UNSUPPORTED, "%s: bf16 path is built for d_h=128 only (got %d)", fn, p->d_h);
+  if ((long long)p->B * p->H * p->N * p->d_h >= (1ll << 40))
+    return fail(ROLA_ERR_UNSUPPORTED, "%s: tensor too large", fn);
+  if ((long long)p->B * p->H * p->N > (1ll << 31) - 1)
+    return fail(ROLA_ERR_UNSUPPORTED, "%s: B*H*N must fit in int32", fn);
+  *out = rola::Shape{p->B, p->H, p->N, p->d_h, p->T, p->Hs, p->Ws, p->dtype == ROLA_DTYPE_BF16};
+  return ROLA_OK;
+}
+
+rola_status check_block(const rola::Shape& s, int32_t block, const char* fn) {
+  if (block != 32 && block != 64 && block != 128)
+    return fail(ROLA_ERR_UNSUPPORTED, "%s: block=%d (built: 32, 64, 128)", fn, block);
+  if (s.bf16 && block == 32)
+    return fail(ROLA_ERR_UNSUPPORTED, "%s: bf16 path is built for block 64 and 128", fn);
+  if (rola::num_blocks(s.N, block) > 8192)
+    return fail(ROLA_ERR_UNSUPPORTED, "%s: more than 8192 blocks", fn);
+  if ((long long)rola::num_blocks(s.N, block) * s.H * s.B > 0x7fffffffll)
+    return fail(ROLA_ERR_UNSUPPORTED, "%s: too many blocks", fn);
+  return ROLA_OK;
+}
+
+rola_status check_rank(const rola::Shape& s, int32_t r, const char* fn) {
+  if (r < 2 || r > s.d || (r & 1))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: rank r=%d must be even with 2 <= r <= d_h=%d", fn, r, s.d);
+  if (s.bf16 && r != 16 && r != 32 && r != 64 && r != 128)
+    return fail(ROLA_ERR_UNSUPPORTED, "%s: bf16 path is built for r in {16, 32, 64, 128} (got %d)", fn, r);
+  return ROLA_OK;
+}
+
+rola_status check_tables(const float* c, const float* s, int32_t ld, int32_t need, const char* fn) {
+  if (!aligned(c) || !aligned(s))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: rotary tables null or not 16-byte aligned", fn);
+  if (ld < need || (ld % 4) != 0)
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: rope_ld=%d must be a multiple of 4 and >= %d", fn, ld, need);
+  return ROLA_OK;
+}
+
+rola_status check_sparsity(double sparsity, const char* fn) {
+  if (!(sparsity >= 0.0 && sparsity < 1.0))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: sparsity %g outside [0, 1)", fn, sparsity);
+  return ROLA_OK;
+}
+
+#define TRY(expr)                     \
+  do {                                \
+    rola_status _s = (expr);          \
+    if (_s != ROLA_OK) return _s;     \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+int32_t rola_num_blocks(int32_t N, int32_t block) {
+  if (N < 1 || block < 1) return -1;
+  return rola::num_blocks(N, block);
+}
+
+int32_t rola_keep_blocks(int32_t n_blocks, double sparsity) {
+  if (n_blocks < 1 || !(sparsity >= 0.0 && sparsity < 1.0)) return -1;
+  const double k = floor((1.0 - sparsity) * (double)n_blocks + 0.5);
+  if (k < 1.0) return 1;
+  if (k > (double)n_blocks) return n_blocks;
+  return (int32_t)k;
+}
+
+size_t rola_select_workspace_bytes(const rola_problem* p, int32_t block) {
+  rola::Shape s;
+  if (check_problem(p, __func__, &s) != ROLA_OK || check_block(s, block, __func__) != ROLA_OK) return 0;
+  return rola::select_workspace_bytes(s, block);
+}
+
+size_t rola_summary_workspace_bytes(const rola_problem* p, int32_t r) {
+  rola::Shape s;
+  if (check_problem(p, __func__, &s) != ROLA_OK || check_rank(s, r, __func__) != ROLA_OK) return 0;
+  return rola::summary_workspace_bytes(s, r);
+}
+
+const char* rola_status_string(rola_status s) {
+  switch (s) {
+    case ROLA_OK: return "ROLA_OK";
+    case ROLA_ERR_INVALID_ARGUMENT: return "ROLA_ERR_INVALID_ARGUMENT";
+    case ROLA_ERR_UNSUPPORTED: return "ROLA_ERR_UNSUPPORTED";
+    case ROLA_ERR_WORKSPACE: return "ROLA_ERR_WORKSPACE";
+    case ROLA_ERR_HIP: return "ROLA_ERR_HIP";
+  }
+  return "ROLA_ERR_UNKNOWN";
+}
+
+const char* rola_last_error(void) { return g_last_error; }
+
+rola_status rola_rope_tables(const rola_problem* p, int32_t d_t, int32_t d_y, int32_t d_x,
+                             double base, int32_t off_t, int32_t off_y, int32_t off_x,
+                             float* cos_tab, float* sin_tab, hipStream_t stream) {
+  rola::Shape s;
+  TRY(check_problem(p, __func__, &s));
+  REQUIRE_PTR(cos_tab);
+  REQUIRE_PTR(sin_tab);
+  if (d_t < 2 || d_y < 2 || d_x < 2 || (d_t | d_y | d_x) & 1 || d_t + d_y + d_x != s.d)
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: axis widths (%d, %d, %d) must be even, >= 2, and sum to d_h=%d",
+                __func__, d_t, d_y, d_x, s.d);
+  if (!(base > 1.0) || !isfinite(base))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: base %g must be finite and > 1", __func__, base);
+  return hip_status(rola::launch_rope_tables(s, d_t, d_y, d_x, base, off_t, off_y, off_x, cos_tab,
+                                             sin_tab, stream), __func__);
+}
+
+rola_status rola_rope_apply(const rola_problem* p, const void* X, const float* cos_tab,
+                            const float* sin_tab, int32_t rope_ld, void* Xr, hipStream_t stream) {
+  rola::Shape s;
+  TRY(check_problem(p, __func__, &s));
+  REQUIRE_PTR(X);
+  REQUIRE_PTR(Xr);
+  TRY(check_tables(cos_tab, sin_tab, rope_ld, s.d / 2, __func__));
+  if (X == Xr) return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: Xr must not alias X", __func__);
+  return hip_status(rola::launch_rope_apply(s, X, cos_tab, sin_tab, rope_ld, Xr, stream), __func__);
+}
+
+rola_status rola_block_select(const rola_problem* p, const void* Qr, const void* Kr, int32_t block,
+                              double sparsity, int32_t* blk_idx, void* ws, size_t ws_bytes,
+                              hipStream_t stream) {
+  rola::Shape s;
+  TRY(check_problem(p, __func__, &s));
+  TRY(check_block(s, block, __func__));
+  TRY(check_sparsity(sparsity, __func__));
+  REQUIRE_PTR(Qr);
+  REQUIRE_PTR(Kr);
+  REQUIRE_PTR(blk_idx);
+  REQUIRE_PTR(ws);
+  const size_t need = rola::select_workspace_bytes(s, block);
+  if (ws_bytes < need)
+    return fail(ROLA_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", __func__, ws_bytes, need);
+  const int nb = rola::num_blocks(s.N, block);
+  const int keep = rola_keep_blocks(nb, sparsity);
+  return hip_status(rola::launch_block_select(s, Qr, Kr, block, keep, blk_idx, ws, stream), __func__);
+}
+
+rola_status rola_sparse_attn(const rola_problem* p, const void* Qr, const void* Kr, const void* V,
+                             int32_t block, double sparsity, const int32_t* blk_idx,
+                             float softmax_scale, void* Os, hipStream_t stream) {
+  rola::Shape s;
+  TRY(check_problem(p, __func__, &s));
+  TRY(check_block(s, block, __func__));
+  TRY(check_sparsity(sparsity, __func__));
+  REQUIRE_PTR(Qr);
+  REQUIRE_PTR(Kr);
+  REQUIRE_PTR(V);
+  REQUIRE_PTR(blk_idx);
+  REQUIRE_PTR(Os);
+  if (!(softmax_scale > 0.f) || !isfinite(softmax_scale))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: softmax_scale must be finite and positive", __func__);
+  const int keep = rola_keep_blocks(rola::num_blocks(s.N, block), sparsity);
+  return hip_status(rola::launch_sparse_attn(s, Qr, Kr, V, block, keep, blk_idx, softmax_scale, Os,
+                                             stream), __func__);
+}
+
+rola_status rola_dense_attn(const rola_problem* p, const void* Qr, const void* Kr, const void* V,
+                            int32_t block, float softmax_scale, void* O, hipStream_t stream) {
+  rola::Shape s;
+  TRY(check_problem(p, __func__, &s));
+  TRY(check_block(s, block, __func__));
+  REQUIRE_PTR(Qr);
+  REQUIRE_PTR(Kr);
+  REQUIRE_PTR(V);
+  REQUIRE_PTR(O);
+  if (!(softmax_scale > 0.f) || !isfinite(softmax_scale))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: softmax_scale must be finite and positive", __func__);
+  const int nb = rola::num_blocks(s.N, block);
+  return hip_status(rola::launch_sparse_attn(s, Qr, Kr, V, block, nb, nullptr, softmax_scale, O,
+                                             stream), __func__);
+}
+
+rola_status rola_lowrank_summary(const rola_problem* p, const void* Kn, const void* V,
+                                 const void* Pk, int32_t r, const float* cos_tab,
+                                 const float* sin_tab, int32_t rope_ld, float* C, float* z,
+                                 void* ws, size_t ws_bytes, hipStream_t stream) {
+  rola::Shape s;
+  TRY(check_problem(p, __func__, &s));
+  TRY(check_rank(s, r, __func__));
+  REQUIRE_PTR(Kn);
+  REQUIRE_PTR(V);
+  REQUIRE_PTR(Pk);
+  REQUIRE_PTR(C);
+  REQUIRE_PTR(ws);
+  if (z != nullptr && !aligned(z))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: z not 16-byte aligned", __func__);
+  TRY(check_tables(cos_tab, sin_tab, rope_ld, r / 2, __func__));
+  const size_t need = rola::summary_workspace_bytes(s, r);
+  if (ws_bytes < need)
+    return fail(ROLA_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", __func__, ws_bytes, need);
+  return hip_status(rola::launch_lowrank_summary(s, Kn, V, Pk, r, cos_tab, sin_tab, rope_ld, C, z,
+                                                 ws, stream), __func__);
+}
+
+rola_status rola_lowrank_readout(const rola_problem* p, const void* Qn, const void* Pq, int32_t r,
+                                 const float* cos_tab, const float* sin_tab, int32_t rope_ld,
+                                 const float* C, float eps_lr, void* Olr, hipStream_t stream) {
+  rola::Shape s;
+  TRY(check_problem(p, __func__, &s));
+  TRY(check_rank(s, r, __func__));
+  REQUIRE_PTR(Qn);
+  REQUIRE_PTR(Pq);
+  REQUIRE_PTR(C);
+  REQUIRE_PTR(Olr);
+  TRY(check_tables(cos_tab, sin_tab, rope_ld, r / 2, __func__));
+  if (!(eps_lr >= 0.f) || !isfinite(eps_lr))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: eps_lr must be finite and >= 0", __func__);
+  return hip_status(rola::launch_lowrank_readout(s, Qn, Pq, r, cos_tab, sin_tab, rope_ld, C, eps_lr,
+                                                 nullptr, nullptr, 0.f, Olr, stream), __func__);
+}
+
+rola_status rola_combine(const rola_problem* p, const void* Os, const void* Olr,
+                         const float* gate_logits, float eps, void* O, hipStream_t stream) {
+  rola::Shape s;
+  TRY(check_problem(p, __func__, &s));
+  REQUIRE_PTR(Os);
+  REQUIRE_PTR(Olr);
+  REQUIRE_PTR(gate_logits);
+  REQUIRE_PTR(O);
+  if (O == Olr) return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: O must not alias Olr", __func__);
+  if (!(eps >= 0.f) || !isfinite(eps))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: eps must be finite and >= 0", __func__);
+  return hip_status(rola::launch_combine(s, Os, Olr, gate_logits, eps, O, stream), __func__);
+}
+
+rola_status rola_lowrank_readout_combine(const rola_problem* p, const void* Qn, const void* Pq,
+                                         int32_t r, const float* cos_tab, const float* sin_tab,
+                                         int32_t rope_ld, const float* C, float eps_lr,
+                                         const void* Os, const float* gate_logits, float eps,
+                                         void* O, hipStream_t stream) {
+  rola::Shape s;
+  TRY(check_problem(p, __func__, &s));
+  TRY(check_rank(s, r, __func__));
+  REQUIRE_PTR(Qn);
+  REQUIRE_PTR(Pq);
+  REQUIRE_PTR(C);
+  REQUIRE_PTR(Os);
+  REQUIRE_PTR(gate_logits);
+  REQUIRE_PTR(O);
+  TRY(check_tables(cos_tab, sin_tab, rope_ld, r / 2, __func__));
+  if (!(eps_lr >= 0.f) || !isfinite(eps_lr) || !(eps >= 0.f) || !isfinite(eps))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: eps values must be finite and >= 0", __func__);
+  return hip_status(rola::launch_lowrank_readout(s, Qn, Pq, r, cos_tab, sin_tab, rope_ld, C, eps_lr,
+                                                 Os, gate_logits, eps, O, stream), __func__);
+}
+
+}  // extern "C"

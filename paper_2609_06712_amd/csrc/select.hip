@@ -1,0 +1,201 @@
+// Block selection of the sparse branch (Algorithm step 4): mean-pool rotated Q/K per block of
+// tokens, score every (query block, key block) pair with an fp32 dot product, keep the top-k key
+// blocks of every query block (ties to the lower index), written ascending.
+//
+//   pool_kernel   HBM-bound: reads Q^r and K^r once (coalesced 16-byte loads), writes means (fp32).
+//   score_kernel  per (b, h): S = q_bar k_bar^T, a small fp32 GEMM tiled 64 x 64 through LDS. The
+//                 positive factor 1/sqrt(d_h) is left out: it cannot change the ranking.
+//   topk_kernel   one wave per score row: 4-pass 8-bit radix select on order-preserving uint32 keys,
+//                 then an ascending ballot/popcount compaction. Integer work, bit-reproducible.
+#include "common.h"
+#include "launch.h"
+
+namespace rola {
+namespace {
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+template <typename T>
+__global__ __launch_bounds__(256) void pool_kernel(int N, int d, int block, const T* __restrict__ X,
+                                                   float* __restrict__ out) {
+  const int I = blockIdx.x, nb = gridDim.x;
+  const long head = (long)blockIdx.z * gridDim.y + blockIdx.y;
+  const T* xh = X + head * (long)N * d;
+  const int G = d / 8, L = 256 / G;
+  const int g = threadIdx.x % G, lane = threadIdx.x / G;
+  const int n0 = I * block, n1 = min(N, n0 + block);
+  float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  for (int n = n0 + lane; n < n1; n += L) {
+    float v[8];
+    load8(xh + (long)n * d + g * 8, v);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] += v[i];
+  }
+  __shared__ float red[256 * 8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) red[threadIdx.x * 8 + i] = acc[i];
+  __syncthreads();
+  if (threadIdx.x < d) {
+    const int c = threadIdx.x, gc = c / 8, ic = c % 8;
+    float s = 0.f;
+    for (int l = 0; l < L; ++l) s += red[(l * G + gc) * 8 + ic];
+    out[(head * nb + I) * d + c] = s / (float)(n1 - n0);
+  }
+}
+
+// S[I][J] = sum_c qbar[I][c] * kbar[J][c] for one (b, h) per blockIdx.z; 64 x 64 tile per workgroup.
+__global__ __launch_bounds__(256) void score_kernel(int nb, int d, const float* __restrict__ qbar,
+                                                    const float* __restrict__ kbar,
+                                                    float* __restrict__ S) {
+  constexpr int TS = 64, KC = 32;
+  __shared__ float As[KC][TS + 4];
+  __shared__ float Bs[KC][TS + 4];
+  const long head = blockIdx.z;
+  const float* q = qbar + head * (long)nb * d;
+  const float* k = kbar + head * (long)nb * d;
+  const int I0 = blockIdx.y * TS, J0 = blockIdx.x * TS;
+  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
+  const int lr = threadIdx.x / 4, lc = (threadIdx.x % 4) * 8;
+  float acc[4][4] = {};
+  for (int c0 = 0; c0 < d; c0 += KC) {
+    float a[8], b[8];
+    if (I0 + lr < nb) load8(q + (long)(I0 + lr) * d + c0 + lc, a);
+    else for (int i = 0; i < 8; ++i) a[i] = 0.f;
+    if (J0 + lr < nb) load8(k + (long)(J0 + lr) * d + c0 + lc, b);
+    else for (int i = 0; i < 8; ++i) b[i] = 0.f;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 8; ++i) { As[lc + i][lr] = a[i]; Bs[lc + i][lr] = b[i]; }
+    __syncthreads();
+#pragma unroll 8
+    for (int c = 0; c < KC; ++c) {
+      float av[4], bv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) { av[i] = As[c][ty + 16 * i]; bv[i] = Bs[c][tx + 16 * i]; }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(av[i], bv[j], acc[i][j]);
+    }
+  }
+  float* Sh = S + head * (long)nb * nb;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int I = I0 + ty + 16 * i;
+    if (I >= nb) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int J = J0 + tx + 16 * j;
+      if (J < nb) Sh[(long)I * nb + J] = acc[i][j];
+    }
+  }
+}
+
+__device__ __forceinline__ uint32_t order_key(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);  // larger float -> larger key
+}
+
+// One 64-lane workgroup per score row; dynamic LDS holds the row's nb keys.
+__global__ __launch_bounds__(64) void topk_kernel(int nb, int keep, const float* __restrict__ S,
+                                                  int32_t* __restrict__ idx) {
+  extern __shared__ uint32_t keys[];
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t part[64];
+  __shared__ uint32_t found[2];
+  const long row = ((long)blockIdx.z * gridDim.y + blockIdx.y) * nb + blockIdx.x;
+  const float* s = S + row * nb;
+  int32_t* out = idx + row * keep;
+  const int lane = threadIdx.x;
+  if (keep >= nb) {
+    for (int j = lane; j < nb; j += 64) out[j] = j;
+    return;
+  }
+  for (int j = lane; j < nb; j += 64) keys[j] = order_key(s[j]);
+  uint32_t prefix = 0, mask = 0;
+  uint32_t remaining = (uint32_t)keep;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int i = lane; i < 256; i += 64) hist[i] = 0;
+    __syncthreads();
+    for (int j = lane; j < nb; j += 64) {
+      const uint32_t k = keys[j];
+      if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    uint32_t c[4];
+#pragma unroll
+    for (int b = 0; b < 4; ++b) c[b] = hist[4 * lane + b];
+    part[lane] = c[0] + c[1] + c[2] + c[3];
+    __syncthreads();
+    uint32_t above = 0;  // elements whose digit lies in higher lanes' bins
+    for (int m = lane + 1; m < 64; ++m) above += part[m];
+    uint32_t g = above;
+#pragma unroll
+    for (int b = 3; b >= 0; --b) {
+      if (g < remaining && remaining <= g + c[b]) { found[0] = 4 * lane + b; found[1] = g; }
+      g += c[b];
+    }
+    __syncthreads();
+    const uint32_t D = found[0], gt = found[1];
+    __syncthreads();
+    remaining -= gt;
+    prefix |= D << shift;
+    mask |= 255u << shift;
+  }
+  // Keys > prefix are all kept; of the keys == prefix, the `remaining` lowest indices are kept.
+  uint32_t written = 0, eq_seen = 0;
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int base = 0; base < nb; base += 64) {
+    const int j = base + lane;
+    const uint32_t k = j < nb ? keys[j] : 0u;
+    const bool gt = j < nb && k > prefix;
+    const bool eq = j < nb && k == prefix;
+    const uint64_t eqm = __ballot(eq);
+    const uint32_t eq_rank = eq_seen + (uint32_t)__popcll(eqm & below);
+    const bool sel = gt || (eq && eq_rank < remaining);
+    const uint64_t selm = __ballot(sel);
+    const uint32_t pos = written + (uint32_t)__popcll(selm & below);
+    if (sel && pos < (uint32_t)keep) out[pos] = j;
+    written += (uint32_t)__popcll(selm);
+    eq_seen += (uint32_t)__popcll(eqm);
+  }
+}
+
+}  // namespace
+
+size_t select_workspace_bytes(const Shape& s, int block) {
+  const size_t nb = (size_t)num_blocks(s.N, block);
+  const size_t heads = (size_t)s.B * s.H;
+  return 2 * align_up(heads * nb * s.d * sizeof(float)) + align_up(heads * nb * nb * sizeof(float));
+}
+
+hipError_t launch_block_select(const Shape& s, const void* Qr, const void* Kr, int block, int keep,
+                               int32_t* idx, void* ws, hipStream_t st) {
+  const int nb = num_blocks(s.N, block);
+  const size_t heads = (size_t)s.B * s.H;
+  char* w = (char*)ws;
+  float* qbar = (float*)w;
+  float* kbar = (float*)(w + align_up(heads * nb * s.d * sizeof(float)));
+  float* S = (float*)(w + 2 * align_up(heads * nb * s.d * sizeof(float)));
+  const dim3 pgrid(nb, s.H, s.B);
+  if (s.bf16) {
+    hipLaunchKernelGGL(pool_kernel<bf16>, pgrid, dim3(256), 0, st, s.N, s.d, block, (const bf16*)Qr,
+                       qbar);
+    hipLaunchKernelGGL(pool_kernel<bf16>, pgrid, dim3(256), 0, st, s.N, s.d, block, (const bf16*)Kr,
+                       kbar);
+  } else {
+    hipLaunchKernelGGL(pool_kernel<float>, pgrid, dim3(256), 0, st, s.N, s.d, block,
+                       (const float*)Qr, qbar);
+    hipLaunchKernelGGL(pool_kernel<float>, pgrid, dim3(256), 0, st, s.N, s.d, block,
+                       (const float*)Kr, kbar);
+  }
+  const int tiles = (nb + 63) / 64;
+  hipLaunchKernelGGL(score_kernel, dim3(tiles, tiles, (unsigned)heads), dim3(256), 0, st, nb, s.d,
+                     qbar, kbar, S);
+  hipLaunchKernelGGL(topk_kernel, pgrid, dim3(64), (size_t)nb * sizeof(uint32_t), st, nb, keep, S,
+                     idx);
+  return hipGetLastError();
+}
+
+}  // namespace rola

@@ -1,0 +1,310 @@
+// Block-sparse softmax attention of the sparse branch (Algorithm step 4; attention as in Sec. 3):
+// every query block attends to the valid tokens of its `keep` selected key blocks, by online
+// softmax with fp32 running max / sum / accumulators. With no index list every key block is walked
+// in order, which is dense softmax attention (the 0 % sparsity reference).
+//
+// bf16 path (d_h = 128), one workgroup per (b, h, query block), NW waves, each owning QT tiles of 16
+// queries. Per selected key block:
+//   S^T = K Q^T     v_mfma_f32_16x16x32_bf16, A = K tile from LDS, B = Q fragments held in registers;
+//                   lane (g = lane/16, c = lane%16) ends up with keys 4g+v of each 16-key tile for
+//                   query c, so softmax statistics stay per lane (cross-group max: 2 shuffles).
+//   P = exp2(S^T * scale*log2e - m), rounded to bf16 in registers; it is directly the B operand of
+//   O^T = V^T P^T   A = V^T from LDS, read as two 8-byte runs of 4 keys; the V tile is transposed
+//                   while being written to LDS (4 keys x 8 channels per thread, register shuffle).
+// K/V tiles of the next selected block are fetched into registers while the current one computes.
+// The grid is remapped so consecutive query blocks of one head share an XCD (and its L2).
+#include "common.h"
+#include "launch.h"
+
+namespace rola {
+namespace {
+
+__device__ __forceinline__ f32x4 mfma16x16x32(const bf16x8& a, const bf16x8& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+template <int BLK, int QT, int NW>
+__global__ __launch_bounds__(NW * 64) void sparse_mfma_kernel(
+    int N, int nb, int keep, int total, const int32_t* __restrict__ idx, float scale_log2,
+    const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
+    bf16* __restrict__ O) {
+  static_assert(NW * QT * 16 == BLK, "queries per workgroup must equal the block size");
+  constexpr int D = 128, KP = D + 8, VP = BLK + 8, NT = NW * 64;
+  constexpr int KLOADS = BLK * D / 8 / NT;   // 16-byte K loads per thread
+  constexpr int VGROUPS = BLK * D / 32 / NT; // 4-key x 8-channel V groups per thread
+  constexpr int KT = BLK / 16;               // 16-key tiles per block
+  __shared__ __attribute__((aligned(16))) bf16 Ks[BLK * KP];
+  __shared__ __attribute__((aligned(16))) bf16 Vt[D * VP];
+
+  const int L = xcd_remap(blockIdx.x, total);
+  const int I = L % nb;
+  const long head = L / nb;
+  const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64, lr = lane % 16, g = lane / 16;
+  const bf16* Qh = Q + head * (long)N * D;
+  const bf16* Kh = K + head * (long)N * D;
+  const bf16* Vh = V + head * (long)N * D;
+  bf16* Oh = O + head * (long)N * D;
+  const int32_t* sel = idx ? idx + (head * nb + I) * (long)keep : nullptr;
+
+  bf16x8 qf[QT][4];
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    const int q = I * BLK + (wave * QT + qt) * 16 + lr;
+#pragma unroll
+    for (int kc = 0; kc < 4; ++kc) {
+      if (q < N) qf[qt][kc] = *reinterpret_cast<const bf16x8*>(Qh + (long)q * D + 32 * kc + 8 * g);
+      else qf[qt][kc] = bf16x8{};
+    }
+  }
+
+  f32x4 acc[QT][8];
+  float m[QT], l[QT];
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    m[qt] = -INFINITY;
+    l[qt] = 0.f;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) acc[qt][w] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  uint4 kreg[KLOADS];
+  uint4 vreg[VGROUPS][4];
+  auto load_tile = [&](int J) {
+    const int k0 = J < 0 ? N : J * BLK;  // J < 0: zero tile
+#pragma unroll
+    for (int i = 0; i < KLOADS; ++i) {
+      const int e = tid + NT * i, row = e / 16, col = (e % 16) * 8;
+      kreg[i] = (k0 + row < N) ? *reinterpret_cast<const uint4*>(Kh + (long)(k0 + row) * D + col)
+                               : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < VGROUPS; ++i) {
+      const int e = tid + NT * i, kg = e / 16, dc = (e % 16) * 8;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = k0 + 4 * kg + r;
+        vreg[i][r] = (row < N) ? *reinterpret_cast<const uint4*>(Vh + (long)row * D + dc)
+                               : make_uint4(0, 0, 0, 0);
+      }
+    }
+  };
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int i = 0; i < KLOADS; ++i) {
+      const int e = tid + NT * i, row = e / 16, col = (e % 16) * 8;
+      *reinterpret_cast<uint4*>(&Ks[row * KP + col]) = kreg[i];
+    }
+#pragma unroll
+    for (int i = 0; i < VGROUPS; ++i) {
+      const int e = tid + NT * i, kg = e / 16, dc = (e % 16) * 8;
+      const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&vreg[i][0]);
+      const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&vreg[i][1]);
+      const uint32_t* r2 = reinterpret_cast<const uint32_t*>(&vreg[i][2]);
+      const uint32_t* r3 = reinterpret_cast<const uint32_t*>(&vreg[i][3]);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {  // channels dc+2c (low halves) and dc+2c+1 (high halves)
+        uint2 lo, hi;
+        lo.x = (r0[c] & 0xFFFFu) | (r1[c] << 16);
+        lo.y = (r2[c] & 0xFFFFu) | (r3[c] << 16);
+        hi.x = (r0[c] >> 16) | (r1[c] & 0xFFFF0000u);
+        hi.y = (r2[c] >> 16) | (r3[c] & 0xFFFF0000u);
+        *reinterpret_cast<uint2*>(&Vt[(dc + 2 * c) * VP + 4 * kg]) = lo;
+        *reinterpret_cast<uint2*>(&Vt[(dc + 2 * c + 1) * VP + 4 * kg]) = hi;
+      }
+    }
+  };
+
+  // Block id of step t; an out-of-range entry of a caller's list yields -1 and is skipped.
+  auto block_at = [&](int t) {
+    const int J = sel ? sel[t] : t;
+    return (unsigned)J < (unsigned)nb ? J : -1;
+  };
+  load_tile(block_at(0));
+  for (int t = 0; t < keep; ++t) {
+    const int J = block_at(t);
+    __syncthreads();
+    store_tile();
+    __syncthreads();
+    if (t + 1 < keep) load_tile(block_at(t + 1));
+    if (J < 0) continue;
+
+    const int k0 = J * BLK;
+    const bool partial = k0 + BLK > N;
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+      f32x4 s[KT];
+#pragma unroll
+      for (int kt = 0; kt < KT; ++kt) {
+        s[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kc = 0; kc < 4; ++kc) {
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(&Ks[(16 * kt + lr) * KP + 32 * kc + 8 * g]);
+          s[kt] = mfma16x16x32(a, qf[qt][kc], s[kt]);
+        }
+      }
+      if (partial) {
+#pragma unroll
+        for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            if (k0 + 16 * kt + 4 * g + v >= N) s[kt][v] = -INFINITY;
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) mx = fmaxf(mx, s[kt][v]);
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mnew = fmaxf(m[qt], mx * scale_log2);
+      const float alpha = __builtin_amdgcn_exp2f(m[qt] - mnew);
+      m[qt] = mnew;
+      l[qt] *= alpha;
+#pragma unroll
+      for (int w = 0; w < 8; ++w) acc[qt][w] *= alpha;
+      bf16 pk[KT][4];
+#pragma unroll
+      for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[kt][v], scale_log2, -mnew));
+          l[qt] += p;
+          pk[kt][v] = (bf16)p;
+        }
+#pragma unroll
+      for (int h = 0; h < BLK / 32; ++h) {
+        bf16x8 b;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) { b[v] = pk[2 * h][v]; b[4 + v] = pk[2 * h + 1][v]; }
+#pragma unroll
+        for (int w = 0; w < 8; ++w) {
+          const bf16* vrow = &Vt[(16 * w + lr) * VP + 32 * h + 4 * g];
+          const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow);
+          const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 16);
+          const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          acc[qt][w] = mfma16x16x32(a, b, acc[qt][w]);
+        }
+      }
+    }
+  }
+
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    float lt = l[qt];
+    lt += __shfl_xor(lt, 16);
+    lt += __shfl_xor(lt, 32);
+    const float inv = 1.0f / lt;
+    const int q = I * BLK + (wave * QT + qt) * 16 + lr;
+    if (q < N) {
+#pragma unroll
+      for (int w = 0; w < 8; ++w) {
+        bf16x4 o;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) o[v] = (bf16)(acc[qt][w][v] * inv);
+        *reinterpret_cast<bf16x4*>(Oh + (long)q * D + 16 * w + 4 * g) = o;
+      }
+    }
+  }
+}
+
+// Plain kernel for the fp32 path: one thread per query, keys streamed through LDS 32 at a time.
+template <typename T, int D>
+__global__ __launch_bounds__(128) void sparse_simple_kernel(int N, int block, int nb, int keep,
+                                                            const int32_t* __restrict__ idx,
+                                                            float scale, const T* __restrict__ Q,
+                                                            const T* __restrict__ K,
+                                                            const T* __restrict__ V,
+                                                            T* __restrict__ O) {
+  constexpr int KC = 32;
+  __shared__ float Ks[KC][D];
+  __shared__ float Vs[KC][D];
+  const int I = blockIdx.x;
+  const long head = (long)blockIdx.z * gridDim.y + blockIdx.y;
+  const T* Qh = Q + head * (long)N * D;
+  const T* Kh = K + head * (long)N * D;
+  const T* Vh = V + head * (long)N * D;
+  const int32_t* sel = idx ? idx + (head * nb + I) * (long)keep : nullptr;
+  const int p = I * block + threadIdx.x;
+  const bool valid = threadIdx.x < block && p < N;
+  float q[D], o[D];
+#pragma unroll
+  for (int c = 0; c < D; ++c) { q[c] = valid ? to_f32(Qh[(long)p * D + c]) : 0.f; o[c] = 0.f; }
+  float m = -INFINITY, l = 0.f;
+  for (int t = 0; t < keep; ++t) {
+    const int J = sel ? sel[t] : t;
+    if ((unsigned)J >= (unsigned)nb) continue;  // out-of-range entry: skipped
+    const int k0 = J * block, k1 = min(N, k0 + block);
+    for (int c0 = k0; c0 < k1; c0 += KC) {
+      const int cn = min(KC, k1 - c0);
+      __syncthreads();
+      for (int e = threadIdx.x; e < KC * D; e += blockDim.x) {
+        const int r = e / D, c = e % D;
+        Ks[r][c] = r < cn ? to_f32(Kh[(long)(c0 + r) * D + c]) : 0.f;
+        Vs[r][c] = r < cn ? to_f32(Vh[(long)(c0 + r) * D + c]) : 0.f;
+      }
+      __syncthreads();
+      float s[KC];
+      float mx = m;
+#pragma unroll
+      for (int j = 0; j < KC; ++j) {
+        float a = 0.f;
+#pragma unroll
+        for (int c = 0; c < D; ++c) a = fmaf(q[c], Ks[j][c], a);
+        s[j] = j < cn ? a * scale : -INFINITY;
+        mx = fmaxf(mx, s[j]);
+      }
+      const float alpha = expf(m - mx);
+      l *= alpha;
+#pragma unroll
+      for (int c = 0; c < D; ++c) o[c] *= alpha;
+#pragma unroll
+      for (int j = 0; j < KC; ++j) {
+        const float w = expf(s[j] - mx);
+        l += w;
+#pragma unroll
+        for (int c = 0; c < D; ++c) o[c] = fmaf(w, Vs[j][c], o[c]);
+      }
+      m = mx;
+    }
+  }
+  if (valid) {
+    const float inv = 1.0f / l;
+#pragma unroll
+    for (int c = 0; c < D; ++c) O[head * (long)N * D + (long)p * D + c] = from_f32<T>(o[c] * inv);
+  }
+}
+
+template <int BLK, int QT, int NW>
+hipError_t launch_mfma(const Shape& s, const void* Qr, const void* Kr, const void* V, int keep,
+                       const int32_t* idx, float scale, void* Os, hipStream_t st) {
+  const int nb = num_blocks(s.N, BLK);
+  const int total = nb * s.H * s.B;
+  hipLaunchKernelGGL((sparse_mfma_kernel<BLK, QT, NW>), dim3(total), dim3(NW * 64), 0, st, s.N, nb,
+                     keep, total, idx, scale * 1.4426950408889634f, (const bf16*)Qr,
+                     (const bf16*)Kr, (const bf16*)V, (bf16*)Os);
+  return hipGetLastError();
+}
+
+template <typename T, int D>
+hipError_t launch_simple(const Shape& s, const void* Qr, const void* Kr, const void* V, int block,
+                         int keep, const int32_t* idx, float scale, void* Os, hipStream_t st) {
+  const int nb = num_blocks(s.N, block);
+  hipLaunchKernelGGL((sparse_simple_kernel<T, D>), dim3(nb, s.H, s.B), dim3(block), 0, st, s.N,
+                     block, nb, keep, idx, scale, (const T*)Qr, (const T*)Kr, (const T*)V, (T*)Os);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, const void* V,
+                              int block, int keep, const int32_t* idx, float scale, void* Os,
+                              hipStream_t st) {
+  if (s.bf16) {
+    if (block == 64) return launch_mfma<64, 1, 4>(s, Qr, Kr, V, keep, idx, scale, Os, st);
+    return launch_mfma<128, 2, 4>(s, Qr, Kr, V, keep, idx, scale, Os, st);
+  }
+  if (s.d == 64) return launch_simple<float, 64>(s, Qr, Kr, V, block, keep, idx, scale, Os, st);
+  return launch_simple<float, 128>(s, Qr, Kr, V, block, keep, idx, scale, Os, st);
+}
+
+}  // namespace rola

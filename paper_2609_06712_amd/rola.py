@@ -1,0 +1,224 @@
+"""ctypes binding of librola.so (include/rola.h), with the same entry-point names.
+
+Argument marshalling only: tensors are passed as raw device pointers together with the current HIP
+stream, and every step runs in the library's kernels. Importing this module fails loudly when the
+library has not been built; there is no fallback path.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "librola.so")
+
+ROLA_OK, ROLA_ERR_INVALID_ARGUMENT, ROLA_ERR_UNSUPPORTED, ROLA_ERR_WORKSPACE, ROLA_ERR_HIP = range(5)
+DTYPE_F32, DTYPE_BF16 = 0, 1
+
+# Every function include/rola.h declares, with (restype, argtypes).
+_p, _i32, _f32, _f64, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float, ctypes.c_double, ctypes.c_size_t
+
+
+class Problem(ctypes.Structure):
+    """rola_problem: [B, H, N, d_h] activations on a T x Hs x Ws grid."""
+    _fields_ = [("B", _i32), ("H", _i32), ("N", _i32), ("d_h", _i32),
+                ("T", _i32), ("Hs", _i32), ("Ws", _i32), ("dtype", _i32)]
+
+
+_PP = ctypes.POINTER(Problem)
+SIGNATURES = {
+    "rola_num_blocks": (_i32, [_i32, _i32]),
+    "rola_keep_blocks": (_i32, [_i32, _f64]),
+    "rola_select_workspace_bytes": (_sz, [_PP, _i32]),
+    "rola_summary_workspace_bytes": (_sz, [_PP, _i32]),
+    "rola_status_string": (ctypes.c_char_p, [_i32]),
+    "rola_last_error": (ctypes.c_char_p, []),
+    "rola_rope_tables": (_i32, [_PP, _i32, _i32, _i32, _f64, _i32, _i32, _i32, _p, _p, _p]),
+    "rola_rope_apply": (_i32, [_PP, _p, _p, _p, _i32, _p, _p]),
+    "rola_block_select": (_i32, [_PP, _p, _p, _i32, _f64, _p, _p, _sz, _p]),
+    "rola_sparse_attn": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p]),
+    "rola_dense_attn": (_i32, [_PP, _p, _p, _p, _i32, _f32, _p, _p]),
+    "rola_lowrank_summary": (_i32, [_PP, _p, _p, _p, _i32, _p, _p, _i32, _p, _p, _p, _sz, _p]),
+    "rola_lowrank_readout": (_i32, [_PP, _p, _p, _i32, _p, _p, _i32, _p, _f32, _p, _p]),
+    "rola_combine": (_i32, [_PP, _p, _p, _p, _f32, _p, _p]),
+    "rola_lowrank_readout_combine": (_i32, [_PP, _p, _p, _i32, _p, _p, _i32, _p, _f32, _p, _p, _f32,
+                                            _p, _p]),
+}
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it first (python -m paper_2609_06712_amd.build)")
+    lib = ctypes.CDLL(LIB_PATH)
+    for name, (res, args) in SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype, fn.argtypes = res, args
+    return lib
+
+
+LIB = _load()
+
+
+class RolaError(RuntimeError):
+    def __init__(self, status: int, fn: str):
+        self.status = status
+        msg = LIB.rola_last_error().decode()
+        super().__init__(f"{fn}: {LIB.rola_status_string(status).decode()}: {msg}")
+
+
+def _check(status: int, fn: str):
+    if status != ROLA_OK:
+        raise RolaError(status, fn)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def problem(B, H, N, d_h, grid, dtype) -> Problem:
+    T, Hs, Ws = grid
+    code = {"f32": DTYPE_F32, "bf16": DTYPE_BF16, torch.float32: DTYPE_F32,
+            torch.bfloat16: DTYPE_BF16}[dtype]
+    return Problem(B, H, N, d_h, T, Hs, Ws, code)
+
+
+def problem_of(x: torch.Tensor, grid) -> Problem:
+    """Problem descriptor of a [B, H, N, d_h] activation tensor."""
+    B, H, N, d = x.shape
+    return problem(B, H, N, d, grid, x.dtype)
+
+
+def _act(x, name):
+    if not (x.is_cuda and x.is_contiguous() and x.dim() == 4):
+        raise ValueError(f"{name} must be a contiguous [B, H, N, d_h] device tensor")
+
+
+# ---- host helpers ---------------------------------------------------------------------------------
+
+def num_blocks(N: int, block: int) -> int:
+    return LIB.rola_num_blocks(N, block)
+
+
+def keep_blocks(n_blocks: int, sparsity: float) -> int:
+    return LIB.rola_keep_blocks(n_blocks, sparsity)
+
+
+def select_workspace_bytes(prob: Problem, block: int) -> int:
+    return LIB.rola_select_workspace_bytes(ctypes.byref(prob), block)
+
+
+def summary_workspace_bytes(prob: Problem, r: int) -> int:
+    return LIB.rola_summary_workspace_bytes(ctypes.byref(prob), r)
+
+
+# ---- entry points (same names as the C ABI) -------------------------------------------------------
+
+def rola_rope_tables(prob: Problem, split, base=10000.0, offset=(0, 0, 0), stream=None, device="cuda"):
+    half = prob.d_h // 2
+    cos = torch.empty((prob.N, half), dtype=torch.float32, device=device)
+    sin = torch.empty_like(cos)
+    _check(LIB.rola_rope_tables(ctypes.byref(prob), split[0], split[1], split[2], base, offset[0],
+                                offset[1], offset[2], _ptr(cos), _ptr(sin), _stream(stream)),
+           "rola_rope_tables")
+    return cos, sin
+
+
+def rola_rope_apply(X, cos, sin, grid, out=None, stream=None):
+    _act(X, "X")
+    out = torch.empty_like(X) if out is None else out
+    prob = problem_of(X, grid)
+    _check(LIB.rola_rope_apply(ctypes.byref(prob), _ptr(X), _ptr(cos), _ptr(sin), cos.stride(0),
+                               _ptr(out), _stream(stream)), "rola_rope_apply")
+    return out
+
+
+def rola_block_select(Qr, Kr, grid, block, sparsity, out=None, ws=None, stream=None):
+    _act(Qr, "Qr")
+    _act(Kr, "Kr")
+    prob = problem_of(Qr, grid)
+    nb = num_blocks(prob.N, block)
+    keep = keep_blocks(nb, sparsity)
+    if out is None:
+        out = torch.empty((prob.B, prob.H, nb, keep), dtype=torch.int32, device=Qr.device)
+    need = select_workspace_bytes(prob, block)
+    if ws is None:
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=Qr.device)
+    _check(LIB.rola_block_select(ctypes.byref(prob), _ptr(Qr), _ptr(Kr), block, sparsity, _ptr(out),
+                                 _ptr(ws), ws.numel(), _stream(stream)), "rola_block_select")
+    return out
+
+
+def rola_sparse_attn(Qr, Kr, V, grid, block, sparsity, blk_idx, scale=None, out=None, stream=None):
+    _act(Qr, "Qr")
+    prob = problem_of(Qr, grid)
+    scale = prob.d_h ** -0.5 if scale is None else scale
+    out = torch.empty_like(Qr) if out is None else out
+    _check(LIB.rola_sparse_attn(ctypes.byref(prob), _ptr(Qr), _ptr(Kr), _ptr(V), block, sparsity,
+                                _ptr(blk_idx), scale, _ptr(out), _stream(stream)), "rola_sparse_attn")
+    return out
+
+
+def rola_dense_attn(Qr, Kr, V, grid, block=64, scale=None, out=None, stream=None):
+    _act(Qr, "Qr")
+    prob = problem_of(Qr, grid)
+    scale = prob.d_h ** -0.5 if scale is None else scale
+    out = torch.empty_like(Qr) if out is None else out
+    _check(LIB.rola_dense_attn(ctypes.byref(prob), _ptr(Qr), _ptr(Kr), _ptr(V), block, scale,
+                               _ptr(out), _stream(stream)), "rola_dense_attn")
+    return out
+
+
+def rola_lowrank_summary(Kn, V, Pk, r, cos, sin, grid, C=None, z=None, ws=None, stream=None,
+                         want_z=True):
+    _act(Kn, "Kn")
+    prob = problem_of(Kn, grid)
+    if C is None:
+        C = torch.empty((prob.B, prob.H, r, prob.d_h), dtype=torch.float32, device=Kn.device)
+    if z is None and want_z:
+        z = torch.empty((prob.B, prob.H, r), dtype=torch.float32, device=Kn.device)
+    need = summary_workspace_bytes(prob, r)
+    if ws is None:
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=Kn.device)
+    _check(LIB.rola_lowrank_summary(ctypes.byref(prob), _ptr(Kn), _ptr(V), _ptr(Pk), r, _ptr(cos),
+                                    _ptr(sin), cos.stride(0), _ptr(C), _ptr(z), _ptr(ws), ws.numel(),
+                                    _stream(stream)), "rola_lowrank_summary")
+    return C, z
+
+
+def rola_lowrank_readout(Qn, Pq, r, cos, sin, C, grid, eps_lr=1e-6, out=None, stream=None):
+    _act(Qn, "Qn")
+    prob = problem_of(Qn, grid)
+    out = torch.empty_like(Qn) if out is None else out
+    _check(LIB.rola_lowrank_readout(ctypes.byref(prob), _ptr(Qn), _ptr(Pq), r, _ptr(cos), _ptr(sin),
+                                    cos.stride(0), _ptr(C), eps_lr, _ptr(out), _stream(stream)),
+           "rola_lowrank_readout")
+    return out
+
+
+def rola_combine(Os, Olr, logits, grid, eps=1e-6, out=None, stream=None):
+    _act(Os, "Os")
+    prob = problem_of(Os, grid)
+    out = torch.empty_like(Os) if out is None else out
+    _check(LIB.rola_combine(ctypes.byref(prob), _ptr(Os), _ptr(Olr), _ptr(logits), eps, _ptr(out),
+                            _stream(stream)), "rola_combine")
+    return out
+
+
+def rola_lowrank_readout_combine(Qn, Pq, r, cos, sin, C, Os, logits, grid, eps_lr=1e-6, eps=1e-6,
+                                 out=None, stream=None):
+    _act(Qn, "Qn")
+    prob = problem_of(Qn, grid)
+    out = torch.empty_like(Os) if out is None else out
+    _check(LIB.rola_lowrank_readout_combine(ctypes.byref(prob), _ptr(Qn), _ptr(Pq), r, _ptr(cos),
+                                            _ptr(sin), cos.stride(0), _ptr(C), eps_lr, _ptr(Os),
+                                            _ptr(logits), eps, _ptr(out), _stream(stream)),
+           "rola_lowrank_readout_combine")
+    return out

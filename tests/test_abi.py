@@ -1,0 +1,115 @@
+"""Host-side checks of the C ABI (no GPU work): every declared symbol is exported and bound, the
+host helpers agree with the oracle's definitions, and invalid arguments are rejected before any
+launch."""
+
+import ctypes
+import os
+import re
+
+import pytest
+import torch
+
+import oracle as O
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rola.h")
+
+R = pytest.importorskip("paper_2609_06712_amd.rola")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rola_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported_and_bound():
+    names = declared_functions()
+    assert len(names) >= 15
+    lib = ctypes.CDLL(R.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+        assert n in R.SIGNATURES, n
+    assert set(R.SIGNATURES) == set(names)
+
+
+@pytest.mark.parametrize("N,block", [(256, 32), (32760, 64), (75600, 64), (75600, 128), (1, 64),
+                                     (8400, 64)])
+def test_num_blocks(N, block):
+    assert R.num_blocks(N, block) == O.num_blocks(N, block)
+
+
+def test_keep_blocks_matches_oracle():
+    for nb in list(range(1, 70)) + [512, 591, 1182, 4096]:
+        for s in [0.0, 0.05, 0.1, 0.25, 0.5, 0.75, 0.8, 0.9, 0.95, 0.99, 0.999]:
+            assert R.keep_blocks(nb, s) == O.keep_blocks(nb, s), (nb, s)
+    assert R.keep_blocks(10, 1.0) == -1 and R.keep_blocks(0, 0.5) == -1
+
+
+def test_workspace_helpers():
+    p = R.problem(1, 40, 75600, 128, (21, 45, 80), "bf16")
+    nb = 1182
+    assert R.select_workspace_bytes(p, 64) >= 4 * (2 * 40 * nb * 128 + 40 * nb * nb)
+    assert R.summary_workspace_bytes(p, 32) > 0
+    assert R.select_workspace_bytes(p, 48) == 0          # unsupported block
+    assert R.summary_workspace_bytes(p, 33) == 0         # odd rank
+    bad = R.problem(1, 40, 75601, 128, (21, 45, 80), "bf16")
+    assert R.select_workspace_bytes(bad, 64) == 0
+
+
+def test_status_strings():
+    assert R.LIB.rola_status_string(0) == b"ROLA_OK"
+    assert R.LIB.rola_status_string(3) == b"ROLA_ERR_WORKSPACE"
+
+
+# Invalid-argument checks pass fake (aligned, never dereferenced) addresses. They are host logic and
+# run where no GPU is present, so a validation bug can never turn into a launch on a real device.
+no_gpu = pytest.mark.skipif(torch.cuda.device_count() > 0, reason="host-validation test: CPU only")
+FAKE = ctypes.c_void_p(1 << 20)
+MIS = ctypes.c_void_p((1 << 20) + 4)
+
+
+def _call(name, *args):
+    return getattr(R.LIB, name)(*args)
+
+
+@no_gpu
+def test_invalid_arguments_are_rejected_before_launch():
+    g = (21, 45, 80)
+    ok = R.problem(1, 2, 75600, 128, g, "bf16")
+    P = ctypes.byref
+    cases = [
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn", P(ok), None, FAKE, FAKE, 64, 0.9, FAKE, 0.1, FAKE, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn", P(ok), MIS, FAKE, FAKE, 64, 0.9, FAKE, 0.1, FAKE, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn", P(ok), FAKE, FAKE, FAKE, 64, 1.0, FAKE, 0.1, FAKE, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn", P(ok), FAKE, FAKE, FAKE, 64, 0.9, FAKE, -1.0, FAKE, None),
+        (R.ROLA_ERR_UNSUPPORTED, "rola_sparse_attn", P(ok), FAKE, FAKE, FAKE, 32, 0.9, FAKE, 0.1, FAKE, None),
+        (R.ROLA_ERR_UNSUPPORTED, "rola_dense_attn", P(ok), FAKE, FAKE, FAKE, 96, 0.1, FAKE, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_block_select", P(R.problem(1, 2, 75601, 128, g, "bf16")),
+         FAKE, FAKE, 64, 0.9, FAKE, FAKE, 1 << 40, None),
+        (R.ROLA_ERR_WORKSPACE, "rola_block_select", P(ok), FAKE, FAKE, 64, 0.9, FAKE, FAKE, 16, None),
+        (R.ROLA_ERR_UNSUPPORTED, "rola_block_select", P(R.problem(1, 2, 75600, 96, g, "f32")),
+         FAKE, FAKE, 64, 0.9, FAKE, FAKE, 1 << 40, None),
+        (R.ROLA_ERR_UNSUPPORTED, "rola_block_select", P(R.problem(1, 2, 75600, 64, g, "bf16")),
+         FAKE, FAKE, 64, 0.9, FAKE, FAKE, 1 << 40, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_lowrank_summary", P(ok), FAKE, FAKE, FAKE, 31, FAKE, FAKE,
+         64, FAKE, None, FAKE, 1 << 40, None),
+        (R.ROLA_ERR_UNSUPPORTED, "rola_lowrank_summary", P(ok), FAKE, FAKE, FAKE, 48, FAKE, FAKE,
+         64, FAKE, None, FAKE, 1 << 40, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_lowrank_summary", P(ok), FAKE, FAKE, FAKE, 32, FAKE, FAKE,
+         6, FAKE, None, FAKE, 1 << 40, None),
+        (R.ROLA_ERR_WORKSPACE, "rola_lowrank_summary", P(ok), FAKE, FAKE, FAKE, 32, FAKE, FAKE,
+         64, FAKE, None, FAKE, 64, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_lowrank_readout", P(ok), FAKE, FAKE, 32, FAKE, FAKE, 64,
+         FAKE, -1.0, FAKE, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_combine", P(ok), FAKE, FAKE, FAKE, 1e-6, FAKE, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_rope_tables", P(ok), 44, 42, 40, 10000.0, 0, 0, 0, FAKE,
+         FAKE, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_rope_apply", P(ok), FAKE, FAKE, FAKE, 64, FAKE, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_lowrank_readout_combine", P(ok), FAKE, FAKE, 32, FAKE, FAKE,
+         64, FAKE, 1e-6, None, FAKE, 1e-6, FAKE, None),
+    ]
+    for want, name, *args in cases:
+        got = _call(name, *args)
+        assert got == want, (name, got, want, R.LIB.rola_last_error())
+        assert R.LIB.rola_last_error()  # a message is always left behind
