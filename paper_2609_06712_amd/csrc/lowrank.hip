@@ -352,9 +352,6 @@ __global__ __launch_bounds__(256) void readout_mfma_kernel(
 
   // A operand of Phi = P Q^T: even / odd rows of P for pair j = 16 jt + lr.
   bf16x8 pe[JT][4], po[JT][4];
-  // A operand of u^T = C^T q~: row = channel 16 w + lr; slots 0-3 = even rows 2(16jt+4g+s),
-  // slots 4-7 = odd rows 2(16jt+4g+s)+1.
-  bf16x8 ca[JT][8];
 #pragma unroll
   for (int jt = 0; jt < JT; ++jt) {
     const int j = 16 * jt + lr;
@@ -368,17 +365,27 @@ __global__ __launch_bounds__(256) void readout_mfma_kernel(
         po[jt][kc] = bf16x8{};
       }
     }
-#pragma unroll
-    for (int w = 0; w < 8; ++w) {
-      const int ch = 16 * w + lr;
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        const int jj = 16 * jt + 4 * g + s;
-        ca[jt][w][s] = jj < half ? (bf16)Ch[(long)(2 * jj) * D + ch] : (bf16)0.f;
-        ca[jt][w][4 + s] = jj < half ? (bf16)Ch[(long)(2 * jj + 1) * D + ch] : (bf16)0.f;
-      }
-    }
   }
+  // A operand of u^T = C^T q~, staged once per workgroup in LDS in the order lanes read it:
+  // fragment (jt, w) of lane (g, c) holds channel 16 w + c; slots 0-3 = even rows 2(16jt+4g+s),
+  // slots 4-7 = odd rows 2(16jt+4g+s)+1. C = hi + lo (two bf16 terms) keeps the contraction
+  // accurate to ~2^-16 relative with fp32 accumulation.
+  __shared__ bf16x8 cfrag[2][JT * 8 * 64];
+  for (int e = tid; e < JT * 8 * 64; e += 256) {
+    const int ln = e % 64, w = (e / 64) % 8, jt = e / 512;
+    const int ch = 16 * w + ln % 16, gg = ln / 16;
+    bf16x8 hi, lo;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      const int jj = 16 * jt + 4 * gg + (s & 3);
+      const float c = jj < half ? Ch[(long)(2 * jj + (s >> 2)) * D + ch] : 0.f;
+      hi[s] = (bf16)c;
+      lo[s] = (bf16)(c - (float)hi[s]);
+    }
+    cfrag[0][e] = hi;
+    cfrag[1][e] = lo;
+  }
+  __syncthreads();
 
   for (int it = 0; it < TPW; ++it) {
     const int tok0 = (grp * 4 * TPW + it * 4 + wave) * 16;
@@ -408,15 +415,24 @@ __global__ __launch_bounds__(256) void readout_mfma_kernel(
         s4 = *reinterpret_cast<const float4*>(sin_tab + (long)tok * ld + jb);
       }
       const float cc[4] = {c4.x, c4.y, c4.z, c4.w}, ss[4] = {s4.x, s4.y, s4.z, s4.w};
-      bf16x8 bq;
+      bf16x8 bq, bl;  // q~ = hi + lo
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const float a = silu(ye[v]), bb = silu(yo[v]);
-        bq[v] = (bf16)(a * cc[v] - bb * ss[v]);
-        bq[4 + v] = (bf16)(a * ss[v] + bb * cc[v]);
+        const float qe = a * cc[v] - bb * ss[v], qo = a * ss[v] + bb * cc[v];
+        bq[v] = (bf16)qe;
+        bq[4 + v] = (bf16)qo;
+        bl[v] = (bf16)(qe - (float)bq[v]);
+        bl[4 + v] = (bf16)(qo - (float)bq[4 + v]);
       }
 #pragma unroll
-      for (int w = 0; w < 8; ++w) u[w] = mfma16x16x32(ca[jt][w], bq, u[w]);
+      for (int w = 0; w < 8; ++w) {
+        const bf16x8 ch = cfrag[0][(jt * 8 + w) * 64 + lane];
+        const bf16x8 cl = cfrag[1][(jt * 8 + w) * 64 + lane];
+        u[w] = mfma16x16x32(ch, bq, u[w]);
+        u[w] = mfma16x16x32(cl, bq, u[w]);
+        u[w] = mfma16x16x32(ch, bl, u[w]);
+      }
     }
     float ss_u = 0.f;
 #pragma unroll

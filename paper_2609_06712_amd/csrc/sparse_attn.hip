@@ -9,12 +9,17 @@
 //                   lane (g = lane/16, c = lane%16) ends up with keys 4g+v of each 16-key tile for
 //                   query c, so softmax statistics stay per lane (cross-group max: 2 shuffles).
 //   P = exp2(S^T * scale*log2e - m), rounded to bf16 in registers; it is directly the B operand of
-//   O^T = V^T P^T   A = V^T from LDS, read as two 8-byte runs of 4 keys; the V tile is transposed
-//                   while being written to LDS (4 keys x 8 channels per thread, register shuffle).
+//   O^T = V^T P^T   A = V^T: V stays row-major in LDS (16-byte chunks XOR-swizzled by row) and is
+//                   read with the gfx950 transposing LDS read ds_read_b64_tr_b16, which hands lane i
+//                   of each 16-lane group channel i of 4 consecutive keys -- exactly the MFMA operand.
 // K/V tiles of the next selected block are fetched into registers while the current one computes.
 // The grid is remapped so consecutive query blocks of one head share an XCD (and its L2).
 #include "common.h"
 #include "launch.h"
+
+#ifndef ROLA_B64_QT
+#define ROLA_B64_QT 1  // 16-query tiles per wave at block 64 (waves = 4 / QT)
+#endif
 
 namespace rola {
 namespace {
@@ -29,12 +34,11 @@ __global__ __launch_bounds__(NW * 64) void sparse_mfma_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
     bf16* __restrict__ O) {
   static_assert(NW * QT * 16 == BLK, "queries per workgroup must equal the block size");
-  constexpr int D = 128, KP = D + 8, VP = BLK + 8, NT = NW * 64;
-  constexpr int KLOADS = BLK * D / 8 / NT;   // 16-byte K loads per thread
-  constexpr int VGROUPS = BLK * D / 32 / NT; // 4-key x 8-channel V groups per thread
+  constexpr int D = 128, KP = D + 8, NT = NW * 64;
+  constexpr int LOADS = BLK * D / 8 / NT;    // 16-byte K (and V) loads per thread
   constexpr int KT = BLK / 16;               // 16-key tiles per block
   __shared__ __attribute__((aligned(16))) bf16 Ks[BLK * KP];
-  __shared__ __attribute__((aligned(16))) bf16 Vt[D * VP];
+  __shared__ __attribute__((aligned(16))) char Vs[BLK * D * 2];  // row-major, swizzled chunks
 
   const int L = xcd_remap(blockIdx.x, total);
   const int I = L % nb;
@@ -67,51 +71,34 @@ __global__ __launch_bounds__(NW * 64) void sparse_mfma_kernel(
     for (int w = 0; w < 8; ++w) acc[qt][w] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  uint4 kreg[KLOADS];
-  uint4 vreg[VGROUPS][4];
+  uint4 kreg[LOADS], vreg[LOADS];
   auto load_tile = [&](int J) {
     const int k0 = J < 0 ? N : J * BLK;  // J < 0: zero tile
 #pragma unroll
-    for (int i = 0; i < KLOADS; ++i) {
+    for (int i = 0; i < LOADS; ++i) {
       const int e = tid + NT * i, row = e / 16, col = (e % 16) * 8;
-      kreg[i] = (k0 + row < N) ? *reinterpret_cast<const uint4*>(Kh + (long)(k0 + row) * D + col)
-                               : make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < VGROUPS; ++i) {
-      const int e = tid + NT * i, kg = e / 16, dc = (e % 16) * 8;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = k0 + 4 * kg + r;
-        vreg[i][r] = (row < N) ? *reinterpret_cast<const uint4*>(Vh + (long)row * D + dc)
-                               : make_uint4(0, 0, 0, 0);
-      }
+      const bool ok = k0 + row < N;
+      kreg[i] = ok ? *reinterpret_cast<const uint4*>(Kh + (long)(k0 + row) * D + col) : make_uint4(0, 0, 0, 0);
+      vreg[i] = ok ? *reinterpret_cast<const uint4*>(Vh + (long)(k0 + row) * D + col) : make_uint4(0, 0, 0, 0);
     }
   };
+  // V chunk c (16 bytes) of key row r lives at byte r*256 + ((c ^ 2(r%8)) * 16): the 8 rows one
+  // transposing read touches then fall into 8 distinct 32-byte bank groups.
   auto store_tile = [&]() {
 #pragma unroll
-    for (int i = 0; i < KLOADS; ++i) {
-      const int e = tid + NT * i, row = e / 16, col = (e % 16) * 8;
-      *reinterpret_cast<uint4*>(&Ks[row * KP + col]) = kreg[i];
+    for (int i = 0; i < LOADS; ++i) {
+      const int e = tid + NT * i, row = e / 16, c = e % 16;
+      *reinterpret_cast<uint4*>(&Ks[row * KP + c * 8]) = kreg[i];
+      *reinterpret_cast<uint4*>(&Vs[row * 256 + ((c ^ ((row & 7) << 1)) << 4)]) = vreg[i];
     }
-#pragma unroll
-    for (int i = 0; i < VGROUPS; ++i) {
-      const int e = tid + NT * i, kg = e / 16, dc = (e % 16) * 8;
-      const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&vreg[i][0]);
-      const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&vreg[i][1]);
-      const uint32_t* r2 = reinterpret_cast<const uint32_t*>(&vreg[i][2]);
-      const uint32_t* r3 = reinterpret_cast<const uint32_t*>(&vreg[i][3]);
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {  // channels dc+2c (low halves) and dc+2c+1 (high halves)
-        uint2 lo, hi;
-        lo.x = (r0[c] & 0xFFFFu) | (r1[c] << 16);
-        lo.y = (r2[c] & 0xFFFFu) | (r3[c] << 16);
-        hi.x = (r0[c] >> 16) | (r1[c] & 0xFFFF0000u);
-        hi.y = (r2[c] >> 16) | (r3[c] & 0xFFFF0000u);
-        *reinterpret_cast<uint2*>(&Vt[(dc + 2 * c) * VP + 4 * kg]) = lo;
-        *reinterpret_cast<uint2*>(&Vt[(dc + 2 * c + 1) * VP + 4 * kg]) = hi;
-      }
-    }
+  };
+  // Lane (g, j = 4 s' + m') reads key row 4g + s' (+ offset), channels 16w + 4m' .. +3.
+  const int sp = (lane & 15) >> 2, mp = lane & 3;
+  auto v_frag = [&](int row, int w) {
+    const int c = 2 * w + (mp >> 1);
+    const int off = row * 256 + ((c ^ ((row & 7) << 1)) << 4) + ((mp & 1) << 3);
+    typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+    return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Vs + off));
   };
 
   // Block id of step t; an out-of-range entry of a caller's list yields -1 and is skipped.
@@ -178,10 +165,9 @@ __global__ __launch_bounds__(NW * 64) void sparse_mfma_kernel(
         for (int v = 0; v < 4; ++v) { b[v] = pk[2 * h][v]; b[4 + v] = pk[2 * h + 1][v]; }
 #pragma unroll
         for (int w = 0; w < 8; ++w) {
-          const bf16* vrow = &Vt[(16 * w + lr) * VP + 32 * h + 4 * g];
-          const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow);
-          const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 16);
-          const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          const bf16x4 lo = v_frag(32 * h + 4 * g + sp, w);
+          const bf16x4 hi = v_frag(32 * h + 16 + 4 * g + sp, w);
+          const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
           acc[qt][w] = mfma16x16x32(a, b, acc[qt][w]);
         }
       }
@@ -300,7 +286,8 @@ hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, co
                               int block, int keep, const int32_t* idx, float scale, void* Os,
                               hipStream_t st) {
   if (s.bf16) {
-    if (block == 64) return launch_mfma<64, 1, 4>(s, Qr, Kr, V, keep, idx, scale, Os, st);
+    if (block == 64)
+      return launch_mfma<64, ROLA_B64_QT, 4 / ROLA_B64_QT>(s, Qr, Kr, V, keep, idx, scale, Os, st);
     return launch_mfma<128, 2, 4>(s, Qr, Kr, V, keep, idx, scale, Os, st);
   }
   if (s.d == 64) return launch_simple<float, 64>(s, Qr, Kr, V, block, keep, idx, scale, Os, st);
