@@ -21,7 +21,7 @@ LIB = os.path.join(PKG, "librola.so")
 ARCH = "gfx950"
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
-    "-I", INCLUDE, "-I", CSRC,
+    "-I", INCLUDE, "-I", CSRC, "-fno-honor-nans",
     # no packed-fp32 instructions in device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]
