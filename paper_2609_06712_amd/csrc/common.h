@@ -67,8 +67,9 @@ __device__ __forceinline__ float rows_sum(float x) {
   return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
-__device__ __forceinline__ float silu(float x) { return x / (1.0f + __expf(-x)); }
-__device__ __forceinline__ float sigmoid(float x) { return 1.0f / (1.0f + __expf(-x)); }
+// SiLU and the logistic gate with a hardware reciprocal (1 ulp) instead of an IEEE divide.
+__device__ __forceinline__ float sigmoid(float x) { return __builtin_amdgcn_rcpf(1.0f + __expf(-x)); }
+__device__ __forceinline__ float silu(float x) { return x * sigmoid(x); }
 
 // Bijective remap of a linear workgroup id so that consecutive logical ids run on the same XCD:
 // hardware deals workgroup w to XCD w % 8, so XCD x gets the logical range [x*q(+rem), ...).

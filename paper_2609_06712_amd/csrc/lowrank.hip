@@ -35,7 +35,8 @@ __device__ __forceinline__ f32x4 mfma16x16x32(const bf16x8& a, const bf16x8& b, 
 
 int summary_chunk_len(const Shape& s) {
   const long heads = (long)s.B * s.H;
-  const long want = (1024 + heads - 1) / heads;  // chunks per head that fill the chip
+  // About 2048 workgroups: several full rounds over the chip, so the last partial round is short.
+  const long want = (2048 + heads - 1) / heads;
   long len = (s.N + want - 1) / want;
   len = (len + kSummaryStep - 1) / kSummaryStep * kSummaryStep;
   return (int)(len < kSummaryStep ? kSummaryStep : len);
@@ -45,23 +46,26 @@ int summary_chunk_len(const Shape& s) {
 // bf16 summary
 // ------------------------------------------------------------------------------------------------
 template <int JT>
-__global__ __launch_bounds__(256) void summary_mfma_kernel(
+__global__ __launch_bounds__(256, JT == 1 ? 2 : 1) void summary_mfma_kernel(
     int N, int H, int r, int chunk_len, int n_chunks, int total, int ld,
     const bf16* __restrict__ Kn, const bf16* __restrict__ V, const bf16* __restrict__ Pk,
     const float* __restrict__ cos_tab, const float* __restrict__ sin_tab,
     float* __restrict__ part) {
-  constexpr int D = 128, TOK = kSummaryStep, VP = TOK + 8;
-  __shared__ __attribute__((aligned(16))) float smem_f[D * VP / 2];  // V^T tile, reused for reductions
-  bf16* Vt = reinterpret_cast<bf16*>(smem_f);
+  constexpr int D = 128, TOK = kSummaryStep;
+  constexpr int TILE = TOK * D * 2;  // one step's V tile: 32 KB, row-major, chunks swizzled
+  // Two V stages filled by direct global-to-LDS loads; the first stage is reused for the final
+  // cross-wave reduction.
+  __shared__ __attribute__((aligned(1024))) char lds[2 * TILE];
 
   const int BH = total / n_chunks;
   const int L = xcd_remap(blockIdx.x, total);
   const int head = L % BH, chunk = L / BH;
   const int h = head % H;
-  const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64, lr = lane % 16, g = lane / 16;
+  const int tid = threadIdx.x, lane = tid % 64, lr = lane % 16, g = lane / 16;
+  const int wave = wave_uniform(tid / 64);
   const int half = r / 2;
   const bf16* Kh = Kn + (long)head * N * D;
-  const bf16* Vh = V + (long)head * N * D;
+  const char* Vh = reinterpret_cast<const char*>(V + (long)head * N * D);
   const bf16* Ph = Pk + (long)h * r * D;
 
   bf16x8 pe[JT][4], po[JT][4];
@@ -89,9 +93,44 @@ __global__ __launch_bounds__(256) void summary_mfma_kernel(
   }
 
   const int t0 = chunk * chunk_len, t1 = min(N, t0 + chunk_len);
-  bf16x8 kf[2][4];
-  uint4 vreg[2][4];
-  auto load_step = [&](int base) {
+  // V tile DMA: lane l of 1-KB slot q (8 slots per wave) fills row 4q + l/16, position l%16 with
+  // source chunk position ^ 2(row%8); rows past the chunk re-read its last row (V rows of tokens
+  // beyond the chunk meet zero features, so they add nothing).
+  typedef __attribute__((address_space(3))) void lds_void;
+  // Slot i's row is row0 + 4i; its swizzle depends only on i's parity (rows advance by 4).
+  const int row0 = 32 * wave + lane / 16, pos = lane % 16;
+  int dvp[2];
+#pragma unroll
+  for (int p = 0; p < 2; ++p)
+    dvp[p] = (row0 + 4 * p) * D * 2 + ((pos ^ (((row0 + 4 * p) & 7) << 1)) << 4);
+  auto issue_v = [&](int base, int buf) {
+    char* dst = lds + buf * TILE;
+    if (base + TOK <= t1) {
+      const char* vb = Vh + (long)base * D * 2;
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        __builtin_amdgcn_global_load_lds((const void*)(vb + dvp[i & 1] + (i >> 1) * 2048),
+                                         (lds_void*)(dst + (wave * 8 + i) * 1024), 16, 0, 0);
+    } else {  // tail: rows past the chunk re-read its last row
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int row = row0 + 4 * i;
+        const long shift = (long)(min(base + row, t1 - 1) - row) * D * 2;
+        __builtin_amdgcn_global_load_lds((const void*)(Vh + shift + dvp[i & 1] + (i >> 1) * 2048),
+                                         (lds_void*)(dst + (wave * 8 + i) * 1024), 16, 0, 0);
+      }
+    }
+  };
+  // Transposing-read offsets of the V^T operand: lane (g, 4 s' + m') reads token row
+  // wave*32 + 4g + s' (+16), channels 16w + 4m'.
+  const int sp = lr >> 2, mp = lr & 3, vr = wave * 32 + 4 * g + sp;
+  int vo[8];
+#pragma unroll
+  for (int w = 0; w < 8; ++w)
+    vo[w] = vr * 256 + (((2 * w + (mp >> 1)) ^ ((vr & 7) << 1)) << 4) + ((mp & 1) << 3);
+
+  bf16x8 kf[2][4];  // K^n operand rows of the next step (prefetched one step ahead)
+  auto load_regs = [&](int base) {
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt) {
       const int tok = base + wave * 32 + tt * 16 + lr;
@@ -100,50 +139,36 @@ __global__ __launch_bounds__(256) void summary_mfma_kernel(
         kf[tt][kc] = tok < t1 ? *reinterpret_cast<const bf16x8*>(Kh + (long)tok * D + 32 * kc + 8 * g)
                               : bf16x8{};
     }
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int e = tid + 256 * i, kg = e / 16, dc = (e % 16) * 8;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int tok = base + 4 * kg + q;
-        vreg[i][q] = tok < t1 ? *reinterpret_cast<const uint4*>(Vh + (long)tok * D + dc)
-                              : make_uint4(0, 0, 0, 0);
-      }
-    }
   };
 
-  load_step(t0);
-  for (int base = t0; base < t1; base += TOK) {
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int e = tid + 256 * i, kg = e / 16, dc = (e % 16) * 8;
-      const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&vreg[i][0]);
-      const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&vreg[i][1]);
-      const uint32_t* r2 = reinterpret_cast<const uint32_t*>(&vreg[i][2]);
-      const uint32_t* r3 = reinterpret_cast<const uint32_t*>(&vreg[i][3]);
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        uint2 lo, hi;
-        lo.x = (r0[c] & 0xFFFFu) | (r1[c] << 16);
-        lo.y = (r2[c] & 0xFFFFu) | (r3[c] << 16);
-        hi.x = (r0[c] >> 16) | (r1[c] & 0xFFFF0000u);
-        hi.y = (r2[c] >> 16) | (r3[c] & 0xFFFF0000u);
-        *reinterpret_cast<uint2*>(&Vt[(dc + 2 * c) * VP + 4 * kg]) = lo;
-        *reinterpret_cast<uint2*>(&Vt[(dc + 2 * c + 1) * VP + 4 * kg]) = hi;
-      }
-    }
+  auto step = [&](int base, int buf) {
     bf16x8 kc_cur[2][4];
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
       for (int kc = 0; kc < 4; ++kc) kc_cur[tt][kc] = kf[tt][kc];
-    __syncthreads();
-    if (base + TOK < t1) load_step(base + TOK);
-
+    float tc[JT][2][4], ts[JT][2][4];  // rotary table entries of this step (L2-resident rows)
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int tok = base + wave * 32 + tt * 16 + 4 * g + v, j = 16 * jt + lr;
+          const bool ok = tok < t1 && j < half;
+          tc[jt][tt][v] = ok ? cos_tab[(long)tok * ld + j] : 1.f;
+          ts[jt][tt][v] = ok ? sin_tab[(long)tok * ld + j] : 0.f;
+        }
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's V tile loads (and register loads) of this step
+    __syncthreads();                // all waves' V loads landed; the other stage is free again
+    if (base + TOK < t1) {
+      issue_v(base + TOK, buf ^ 1);
+      load_regs(base + TOK);
+    }
+    const char* Vs = lds + buf * TILE;
+    typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 #pragma unroll
     for (int jt = 0; jt < JT; ++jt) {
-      const int j = 16 * jt + lr;
       bf16x8 be, bo;
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt) {
@@ -155,12 +180,7 @@ __global__ __launch_bounds__(256) void summary_mfma_kernel(
         }
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const int tok = base + wave * 32 + tt * 16 + 4 * g + v;
-          float c = 1.f, s = 0.f;
-          if (tok < t1 && j < half) {
-            c = cos_tab[(long)tok * ld + j];
-            s = sin_tab[(long)tok * ld + j];
-          }
+          const float c = tc[jt][tt][v], s = ts[jt][tt][v];
           const float a = silu(ye[v]), b = silu(yo[v]);
           const float ke = a * c - b * s, ko = a * s + b * c;
           ze[jt] += ke;
@@ -171,27 +191,33 @@ __global__ __launch_bounds__(256) void summary_mfma_kernel(
       }
 #pragma unroll
       for (int w = 0; w < 8; ++w) {
-        const bf16* vrow = &Vt[(16 * w + lr) * VP + wave * 32 + 4 * g];
-        const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow);
-        const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 16);
-        const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-        ce[jt][w] = mfma16x16x32(a, be, ce[jt][w]);
-        co[jt][w] = mfma16x16x32(a, bo, co[jt][w]);
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Vs + vo[w]));
+        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Vs + vo[w] + 16 * 256));
+        const bf16x8 va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        ce[jt][w] = mfma16x16x32(va, be, ce[jt][w]);
+        co[jt][w] = mfma16x16x32(va, bo, co[jt][w]);
       }
     }
+  };
+
+  issue_v(t0, 0);
+  load_regs(t0);
+  int base = t0;
+  for (; base + TOK < t1; base += 2 * TOK) {
+    step(base, 0);
+    step(base + TOK, 1);
   }
+  if (base < t1) step(base, 0);
 
   // z: the four lane groups hold different tokens of the same pair j
 #pragma unroll
   for (int jt = 0; jt < JT; ++jt) {
-    ze[jt] += __shfl_xor(ze[jt], 16);
-    ze[jt] += __shfl_xor(ze[jt], 32);
-    zo[jt] += __shfl_xor(zo[jt], 16);
-    zo[jt] += __shfl_xor(zo[jt], 32);
+    ze[jt] = rows_sum(ze[jt]);
+    zo[jt] = rows_sum(zo[jt]);
   }
   // Sum the four waves in a fixed order: wave 3 -> 2 -> 1 -> 0, one pair-tile at a time.
   constexpr int PER = 2 * 8 * 4 + 2;  // floats per lane per pair tile
-  float* red = smem_f;
+  float* red = reinterpret_cast<float*>(lds);
 #pragma unroll
   for (int jt = 0; jt < JT; ++jt) {
     for (int src = 3; src >= 1; --src) {
@@ -366,14 +392,15 @@ __global__ __launch_bounds__(256) void readout_mfma_kernel(
       }
     }
   }
-  // A operand of u^T = C^T q~, staged once per workgroup in LDS in the order lanes read it:
-  // fragment (jt, w) of lane (g, c) holds channel 16 w + c; slots 0-3 = even rows 2(16jt+4g+s),
-  // slots 4-7 = odd rows 2(16jt+4g+s)+1. C = hi + lo (two bf16 terms) keeps the contraction
-  // accurate to ~2^-16 relative with fp32 accumulation.
+  // A operand of u^T = C^T q~, staged once per workgroup in LDS in the order lanes read it.
+  // Fragment (jt, w) row c holds channel 32(w/2) + 8(c/4) + 4(w%2) + c%4, so the output lane
+  // (g, token) of tiles 2p and 2p+1 ends up with the 8 consecutive channels 32p + 8g .. +7 (16-byte
+  // O^s loads and O stores). Slots 0-3 = even rows 2(16jt+4g+s), slots 4-7 = odd rows. C = hi + lo
+  // (two bf16 terms) keeps the contraction accurate to ~2^-16 relative with fp32 accumulation.
   __shared__ bf16x8 cfrag[2][JT * 8 * 64];
   for (int e = tid; e < JT * 8 * 64; e += 256) {
     const int ln = e % 64, w = (e / 64) % 8, jt = e / 512;
-    const int ch = 16 * w + ln % 16, gg = ln / 16;
+    const int c = ln % 16, ch = 32 * (w >> 1) + 8 * (c >> 2) + 4 * (w & 1) + (c & 3), gg = ln / 16;
     bf16x8 hi, lo;
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
@@ -387,97 +414,118 @@ __global__ __launch_bounds__(256) void readout_mfma_kernel(
   }
   __syncthreads();
 
-  for (int it = 0; it < TPW; ++it) {
-    const int tok0 = (grp * 4 * TPW + it * 4 + wave) * 16;
-    if (tok0 >= N) break;
-    const int tok = tok0 + lr;
-    const bool valid = tok < N;
-    bf16x8 qf[4];
+  // Two 16-token tiles per wave at a time: every load of both tiles (Q^n rows, table entries, O^s,
+  // gate logits) is issued before either is computed, so HBM sees both tiles' traffic in flight.
+  constexpr int TG = 2;
+  for (int it0 = 0; it0 < TPW; it0 += TG) {
+    bf16x8 qf[TG][4];
+    float4 c4[TG][JT], s4[TG][JT];
+    bf16x8 osr[TG][4];
+    float lg[TG];
+    int tokv[TG];
 #pragma unroll
-    for (int kc = 0; kc < 4; ++kc)
-      qf[kc] = valid ? *reinterpret_cast<const bf16x8*>(Qh + (long)tok * D + 32 * kc + 8 * g)
-                     : bf16x8{};
-    f32x4 u[8];
+    for (int tg = 0; tg < TG; ++tg) {
+      const int tok = (grp * 4 * TPW + (it0 + tg) * 4 + wave) * 16 + lr;
+      const bool valid = tok < N;
+      tokv[tg] = tok;
 #pragma unroll
-    for (int w = 0; w < 8; ++w) u[w] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int kc = 0; kc < 4; ++kc)
+        qf[tg][kc] = valid ? *reinterpret_cast<const bf16x8*>(Qh + (long)tok * D + 32 * kc + 8 * g)
+                           : bf16x8{};
 #pragma unroll
-    for (int jt = 0; jt < JT; ++jt) {
-      f32x4 ye = {0.f, 0.f, 0.f, 0.f}, yo = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kc = 0; kc < 4; ++kc) {
-        ye = mfma16x16x32(pe[jt][kc], qf[kc], ye);
-        yo = mfma16x16x32(po[jt][kc], qf[kc], yo);
+      for (int jt = 0; jt < JT; ++jt) {
+        const int jb = 16 * jt + 4 * g;  // pairs jb..jb+3 of token `tok`
+        c4[tg][jt] = make_float4(1.f, 1.f, 1.f, 1.f);
+        s4[tg][jt] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (valid && jb < half) {
+          c4[tg][jt] = *reinterpret_cast<const float4*>(cos_tab + (long)tok * ld + jb);
+          s4[tg][jt] = *reinterpret_cast<const float4*>(sin_tab + (long)tok * ld + jb);
+        }
       }
-      const int jb = 16 * jt + 4 * g;  // pairs jb..jb+3 of token `tok`
-      float4 c4 = make_float4(1.f, 1.f, 1.f, 1.f), s4 = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (valid && jb < half) {
-        c4 = *reinterpret_cast<const float4*>(cos_tab + (long)tok * ld + jb);
-        s4 = *reinterpret_cast<const float4*>(sin_tab + (long)tok * ld + jb);
-      }
-      const float cc[4] = {c4.x, c4.y, c4.z, c4.w}, ss[4] = {s4.x, s4.y, s4.z, s4.w};
-      bf16x8 bq, bl;  // q~ = hi + lo
+      if constexpr (COMBINE) {
+        const bf16* srow = Os + (long)head * N * D + (long)tok * D;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const float a = silu(ye[v]), bb = silu(yo[v]);
-        const float qe = a * cc[v] - bb * ss[v], qo = a * ss[v] + bb * cc[v];
-        bq[v] = (bf16)qe;
-        bq[4 + v] = (bf16)qo;
-        bl[v] = (bf16)(qe - (float)bq[v]);
-        bl[4 + v] = (bf16)(qo - (float)bq[4 + v]);
-      }
-#pragma unroll
-      for (int w = 0; w < 8; ++w) {
-        const bf16x8 ch = cfrag[0][(jt * 8 + w) * 64 + lane];
-        const bf16x8 cl = cfrag[1][(jt * 8 + w) * 64 + lane];
-        u[w] = mfma16x16x32(ch, bq, u[w]);
-        u[w] = mfma16x16x32(cl, bq, u[w]);
-        u[w] = mfma16x16x32(ch, bl, u[w]);
+        for (int p = 0; p < 4; ++p)
+          osr[tg][p] = valid ? *reinterpret_cast<const bf16x8*>(srow + 32 * p + 8 * g) : bf16x8{};
+        lg[tg] = valid ? logits[(long)b * N + tok] : 0.f;
       }
     }
-    float ss_u = 0.f;
 #pragma unroll
-    for (int w = 0; w < 8; ++w)
+    for (int tg = 0; tg < TG; ++tg) {
+      const int tok = tokv[tg];
+      if (tok - lr >= N) continue;  // whole tile past the end (uniform)
+      const bool valid = tok < N;
+      f32x4 u[8];
 #pragma unroll
-      for (int v = 0; v < 4; ++v) ss_u = fmaf(u[w][v], u[w][v], ss_u);
-    ss_u += __shfl_xor(ss_u, 16);
-    ss_u += __shfl_xor(ss_u, 32);
-    const float inv_u = rsqrtf(ss_u * (1.0f / D) + eps_lr);
-    bf16* orow = Out + (long)head * N * D + (long)tok * D;
-    if constexpr (COMBINE) {
-      const bf16* srow = Os + (long)head * N * D + (long)tok * D;
-      float os[8][4];
-      float ss_s = 0.f;
+      for (int w = 0; w < 8; ++w) u[w] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int w = 0; w < 8; ++w) {
-        bf16x4 x = valid ? *reinterpret_cast<const bf16x4*>(srow + 16 * w + 4 * g) : bf16x4{};
+      for (int jt = 0; jt < JT; ++jt) {
+        f32x4 ye = {0.f, 0.f, 0.f, 0.f}, yo = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kc = 0; kc < 4; ++kc) {
+          ye = mfma16x16x32(pe[jt][kc], qf[tg][kc], ye);
+          yo = mfma16x16x32(po[jt][kc], qf[tg][kc], yo);
+        }
+        const float cc[4] = {c4[tg][jt].x, c4[tg][jt].y, c4[tg][jt].z, c4[tg][jt].w};
+        const float ss[4] = {s4[tg][jt].x, s4[tg][jt].y, s4[tg][jt].z, s4[tg][jt].w};
+        bf16x8 bq, bl;  // q~ = hi + lo
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          os[w][v] = (float)x[v];
-          ss_s = fmaf(os[w][v], os[w][v], ss_s);
+          const float a = silu(ye[v]), bb = silu(yo[v]);
+          const float qe = a * cc[v] - bb * ss[v], qo = a * ss[v] + bb * cc[v];
+          bq[v] = (bf16)qe;
+          bq[4 + v] = (bf16)qo;
+          bl[v] = (bf16)(qe - (float)bq[v]);
+          bl[4 + v] = (bf16)(qo - (float)bq[4 + v]);
         }
-      }
-      ss_s += __shfl_xor(ss_s, 16);
-      ss_s += __shfl_xor(ss_s, 32);
-      const float rs = sqrtf(ss_s * (1.0f / D) + eps);
-      const float gate = valid ? sigmoid(logits[(long)b * N + tok]) : 0.f;
-      const float inv_rs = 1.0f / rs;
-      if (valid) {
 #pragma unroll
         for (int w = 0; w < 8; ++w) {
-          bf16x4 o;
-#pragma unroll
-          for (int v = 0; v < 4; ++v) o[v] = (bf16)((os[w][v] * inv_rs + gate * u[w][v] * inv_u) * rs);
-          *reinterpret_cast<bf16x4*>(orow + 16 * w + 4 * g) = o;
+          const bf16x8 ch = cfrag[0][(jt * 8 + w) * 64 + lane];
+          const bf16x8 cl = cfrag[1][(jt * 8 + w) * 64 + lane];
+          u[w] = mfma16x16x32(ch, bq, u[w]);
+          u[w] = mfma16x16x32(cl, bq, u[w]);
+          u[w] = mfma16x16x32(ch, bl, u[w]);
         }
       }
-    } else {
-      if (valid) {
+      float ss_u = 0.f;
 #pragma unroll
-        for (int w = 0; w < 8; ++w) {
-          bf16x4 o;
+      for (int w = 0; w < 8; ++w)
 #pragma unroll
-          for (int v = 0; v < 4; ++v) o[v] = (bf16)(u[w][v] * inv_u);
-          *reinterpret_cast<bf16x4*>(orow + 16 * w + 4 * g) = o;
+        for (int v = 0; v < 4; ++v) ss_u = fmaf(u[w][v], u[w][v], ss_u);
+      const float inv_u = rsqrtf(rows_sum(ss_u) * (1.0f / D) + eps_lr);
+      bf16* orow = Out + (long)head * N * D + (long)tok * D;
+      // Lane holds channels 32p + 8g + 4h + v in u[2p + h][v].
+      if constexpr (COMBINE) {
+        float ss_s = 0.f;
+#pragma unroll
+        for (int p = 0; p < 4; ++p)
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const float x = (float)osr[tg][p][i];
+            ss_s = fmaf(x, x, ss_s);
+          }
+        const float rs = sqrtf(rows_sum(ss_s) * (1.0f / D) + eps);
+        // (O^s / r + g O^lr) r  ==  O^s + (g r / rms(u)) u
+        const float coef = sigmoid(lg[tg]) * rs * inv_u;
+        if (valid) {
+#pragma unroll
+          for (int p = 0; p < 4; ++p) {
+            bf16x8 o;
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+              o[i] = (bf16)fmaf(coef, u[2 * p + (i >> 2)][i & 3], (float)osr[tg][p][i]);
+            *reinterpret_cast<bf16x8*>(orow + 32 * p + 8 * g) = o;
+          }
+        }
+      } else {
+        if (valid) {
+#pragma unroll
+          for (int p = 0; p < 4; ++p) {
+            bf16x8 o;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) o[i] = (bf16)(u[2 * p + (i >> 2)][i & 3] * inv_u);
+            *reinterpret_cast<bf16x8*>(orow + 32 * p + 8 * g) = o;
+          }
         }
       }
     }
