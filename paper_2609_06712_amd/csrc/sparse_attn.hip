@@ -3,31 +3,30 @@
 // softmax with fp32 running max / sum / accumulators. With no index list every key block is walked
 // in order, which is dense softmax attention (the 0 % sparsity reference).
 //
-// bf16 path (d_h = 128), one workgroup per (b, h, query block), NW waves, each owning QT tiles of 16
-// queries. Per selected key block:
-//   S^T = K Q^T     v_mfma_f32_16x16x32_bf16, A = K tile from LDS, B = Q fragments held in registers;
-//                   lane (g = lane/16, c = lane%16) ends up with keys 4g+v of each 16-key tile for
-//                   query c, so softmax statistics stay per lane (cross-group max: 2 shuffles).
-//   P = exp2(S^T * scale*log2e - m), rounded to bf16 in registers; it is directly the B operand of
-//   O^T = V^T P^T   A = V^T: V stays row-major in LDS (16-byte chunks XOR-swizzled by row) and is
-//                   read with the gfx950 transposing LDS read ds_read_b64_tr_b16, which hands lane i
-//                   of each 16-lane group channel i of 4 consecutive keys -- exactly the MFMA operand.
-// K/V tiles of the next selected block are fetched into registers while the current one computes.
-// The grid is remapped so consecutive query blocks of one head share an XCD (and its L2).
+// bf16 path (d_h = 128): one workgroup per (b, h, query block of BLK tokens), BLK/32 waves of 32
+// queries (two 16-query MFMA tiles) each, Q fragments in registers. Keys stream in 32-key sub-tiles:
+//   S^T = K Q^T     v_mfma_f32_16x16x32_bf16, A = K sub-tile from LDS, B = Q fragments; lane
+//                   (g = lane/16, c = lane%16) receives keys 4g+v of each 16-key tile for query c,
+//                   so softmax statistics stay per lane (row max: two permlane swaps).
+//   P = exp2(S^T * scale*log2e - m), rounded to bf16 in registers: directly the B operand of
+//   O^T = V^T P^T   A = V^T: V stays row-major in LDS and is read with the gfx950 transposing LDS read
+//                   ds_read_b64_tr_b16, which hands lane i of each 16-lane group channel i of 4
+//                   consecutive keys -- exactly the MFMA operand layout.
+// Row sums come from one more MFMA against a ones operand. Sub-tiles are double-buffered in LDS and
+// filled by direct global-to-LDS loads (global_load_lds_dwordx4): no staging registers. The 16-byte
+// chunks of every row are XOR-swizzled (K: chunk ^ row%16, V: chunk ^ 2(row%8)) so that the K
+// operand reads (16 rows per cycle) and the transposing V reads (8 rows per cycle) are free of
+// bank conflicts. O is rescaled only when a sub-tile raises a row max by more than 2^8: the softmax
+// ratio does not depend on the reference max, so this is exact. The grid is remapped so that
+// consecutive query blocks of one head run on the same XCD (sharing its L2).
 #include "common.h"
 #include "launch.h"
 
 #ifndef ROLA_SPARSE_NBUF
-#define ROLA_SPARSE_NBUF 2  // LDS stages of the pipelined kernel
+#define ROLA_SPARSE_NBUF 2  // LDS stages of the K/V pipeline
 #endif
 #ifndef ROLA_SPARSE_REMAP
-#define ROLA_SPARSE_REMAP 1  // 1: XCD-contiguous logical ranges; 0: hardware round-robin
-#endif
-#ifndef ROLA_SPARSE_PIPE
-#define ROLA_SPARSE_PIPE 1
-#endif
-#ifndef ROLA_B64_QT
-#define ROLA_B64_QT 1  // 16-query tiles per wave at block 64 (waves = 4 / QT)
+#define ROLA_SPARSE_REMAP 1  // 1: XCD-contiguous logical ranges; 2: interleaved chunks; 0: none
 #endif
 
 namespace rola {
@@ -35,171 +34,6 @@ namespace {
 
 __device__ __forceinline__ f32x4 mfma16x16x32(const bf16x8& a, const bf16x8& b, const f32x4& c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
-
-template <int BLK, int QT, int NW>
-__global__ __launch_bounds__(NW * 64) void sparse_mfma_kernel(
-    int N, int nb, int keep, int total, const int32_t* __restrict__ idx, float scale_log2,
-    const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
-    bf16* __restrict__ O) {
-  static_assert(NW * QT * 16 == BLK, "queries per workgroup must equal the block size");
-  constexpr int D = 128, KP = D + 8, NT = NW * 64;
-  constexpr int LOADS = BLK * D / 8 / NT;    // 16-byte K (and V) loads per thread
-  constexpr int KT = BLK / 16;               // 16-key tiles per block
-  __shared__ __attribute__((aligned(16))) bf16 Ks[BLK * KP];
-  __shared__ __attribute__((aligned(16))) char Vs[BLK * D * 2];  // row-major, swizzled chunks
-
-  const int L = xcd_remap(blockIdx.x, total);
-  const int I = L % nb;
-  const long head = L / nb;
-  const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64, lr = lane % 16, g = lane / 16;
-  const bf16* Qh = Q + head * (long)N * D;
-  const bf16* Kh = K + head * (long)N * D;
-  const bf16* Vh = V + head * (long)N * D;
-  bf16* Oh = O + head * (long)N * D;
-  const int32_t* sel = idx ? idx + (head * nb + I) * (long)keep : nullptr;
-
-  bf16x8 qf[QT][4];
-#pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    const int q = I * BLK + (wave * QT + qt) * 16 + lr;
-#pragma unroll
-    for (int kc = 0; kc < 4; ++kc) {
-      if (q < N) qf[qt][kc] = *reinterpret_cast<const bf16x8*>(Qh + (long)q * D + 32 * kc + 8 * g);
-      else qf[qt][kc] = bf16x8{};
-    }
-  }
-
-  f32x4 acc[QT][8];
-  float m[QT], l[QT];
-#pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    m[qt] = -INFINITY;
-    l[qt] = 0.f;
-#pragma unroll
-    for (int w = 0; w < 8; ++w) acc[qt][w] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-
-  uint4 kreg[LOADS], vreg[LOADS];
-  auto load_tile = [&](int J) {
-    const int k0 = J < 0 ? N : J * BLK;  // J < 0: zero tile
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      const int e = tid + NT * i, row = e / 16, col = (e % 16) * 8;
-      const bool ok = k0 + row < N;
-      kreg[i] = ok ? *reinterpret_cast<const uint4*>(Kh + (long)(k0 + row) * D + col) : make_uint4(0, 0, 0, 0);
-      vreg[i] = ok ? *reinterpret_cast<const uint4*>(Vh + (long)(k0 + row) * D + col) : make_uint4(0, 0, 0, 0);
-    }
-  };
-  // V chunk c (16 bytes) of key row r lives at byte r*256 + ((c ^ 2(r%8)) * 16): the 8 rows one
-  // transposing read touches then fall into 8 distinct 32-byte bank groups.
-  auto store_tile = [&]() {
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      const int e = tid + NT * i, row = e / 16, c = e % 16;
-      *reinterpret_cast<uint4*>(&Ks[row * KP + c * 8]) = kreg[i];
-      *reinterpret_cast<uint4*>(&Vs[row * 256 + ((c ^ ((row & 7) << 1)) << 4)]) = vreg[i];
-    }
-  };
-  // Lane (g, j = 4 s' + m') reads key row 4g + s' (+ offset), channels 16w + 4m' .. +3.
-  const int sp = (lane & 15) >> 2, mp = lane & 3;
-  auto v_frag = [&](int row, int w) {
-    const int c = 2 * w + (mp >> 1);
-    const int off = row * 256 + ((c ^ ((row & 7) << 1)) << 4) + ((mp & 1) << 3);
-    typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
-    return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Vs + off));
-  };
-
-  // Block id of step t; an out-of-range entry of a caller's list yields -1 and is skipped.
-  auto block_at = [&](int t) {
-    const int J = sel ? sel[t] : t;
-    return (unsigned)J < (unsigned)nb ? J : -1;
-  };
-  load_tile(block_at(0));
-  for (int t = 0; t < keep; ++t) {
-    const int J = block_at(t);
-    __syncthreads();
-    store_tile();
-    __syncthreads();
-    if (t + 1 < keep) load_tile(block_at(t + 1));
-    if (J < 0) continue;
-
-    const int k0 = J * BLK;
-    const bool partial = k0 + BLK > N;
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
-      f32x4 s[KT];
-#pragma unroll
-      for (int kt = 0; kt < KT; ++kt) {
-        s[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kc = 0; kc < 4; ++kc) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(&Ks[(16 * kt + lr) * KP + 32 * kc + 8 * g]);
-          s[kt] = mfma16x16x32(a, qf[qt][kc], s[kt]);
-        }
-      }
-      if (partial) {
-#pragma unroll
-        for (int kt = 0; kt < KT; ++kt)
-#pragma unroll
-          for (int v = 0; v < 4; ++v)
-            if (k0 + 16 * kt + 4 * g + v >= N) s[kt][v] = -INFINITY;
-      }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kt = 0; kt < KT; ++kt)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) mx = fmaxf(mx, s[kt][v]);
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mnew = fmaxf(m[qt], mx * scale_log2);
-      const float alpha = __builtin_amdgcn_exp2f(m[qt] - mnew);
-      m[qt] = mnew;
-      l[qt] *= alpha;
-#pragma unroll
-      for (int w = 0; w < 8; ++w) acc[qt][w] *= alpha;
-      bf16 pk[KT][4];
-#pragma unroll
-      for (int kt = 0; kt < KT; ++kt)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(s[kt][v], scale_log2, -mnew));
-          l[qt] += p;
-          pk[kt][v] = (bf16)p;
-        }
-#pragma unroll
-      for (int h = 0; h < BLK / 32; ++h) {
-        bf16x8 b;
-#pragma unroll
-        for (int v = 0; v < 4; ++v) { b[v] = pk[2 * h][v]; b[4 + v] = pk[2 * h + 1][v]; }
-#pragma unroll
-        for (int w = 0; w < 8; ++w) {
-          const bf16x4 lo = v_frag(32 * h + 4 * g + sp, w);
-          const bf16x4 hi = v_frag(32 * h + 16 + 4 * g + sp, w);
-          const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-          acc[qt][w] = mfma16x16x32(a, b, acc[qt][w]);
-        }
-      }
-    }
-  }
-
-#pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    float lt = l[qt];
-    lt += __shfl_xor(lt, 16);
-    lt += __shfl_xor(lt, 32);
-    const float inv = 1.0f / lt;
-    const int q = I * BLK + (wave * QT + qt) * 16 + lr;
-    if (q < N) {
-#pragma unroll
-      for (int w = 0; w < 8; ++w) {
-        bf16x4 o;
-#pragma unroll
-        for (int v = 0; v < 4; ++v) o[v] = (bf16)(acc[qt][w][v] * inv);
-        *reinterpret_cast<bf16x4*>(Oh + (long)q * D + 16 * w + 4 * g) = o;
-      }
-    }
-  }
 }
 
 // bf16 kernel, pipelined: one workgroup per (b, h, query block of BLK tokens) with BLK/32 waves of
@@ -226,7 +60,8 @@ __global__ __launch_bounds__(BLK * 2, 2) void sparse_pipe_kernel(
   constexpr int NBUF = ROLA_SPARSE_NBUF;
   __shared__ __attribute__((aligned(1024))) char lds[NBUF * BUF_BYTES];
 
-  const int L = ROLA_SPARSE_REMAP ? xcd_remap(blockIdx.x, total) : (int)blockIdx.x;
+  const int L = ROLA_SPARSE_REMAP == 2 ? xcd_chunk_remap(blockIdx.x, total, (nb + kNumXcd - 1) / kNumXcd)
+              : ROLA_SPARSE_REMAP ? xcd_remap(blockIdx.x, total) : (int)blockIdx.x;
   const int I = L % nb;
   const long head = L / nb;
   const int tid = threadIdx.x, lane = tid % 64, lr = lane % 16, g = lane / 16;
@@ -284,8 +119,12 @@ __global__ __launch_bounds__(BLK * 2, 2) void sparse_pipe_kernel(
   for (int w = 0; w < 8; ++w)
     vo[w] = TILE_BYTES + vr * 256 + (((2 * w + (mp >> 1)) ^ ((vr & 7) << 1)) << 4) + ((mp & 1) << 3);
 
+  // The block list is read through the constant address space: uniform scalar loads, counted by
+  // lgkmcnt, so reading an index never drains the DMA loads in flight (vmcnt).
+  typedef const __attribute__((address_space(4))) int32_t* const_i32;
+  const const_i32 sel_s = (const_i32)sel;
   auto step_key0 = [&](int t) {  // first key of step t; -1 if its block index is out of range
-    const int J = sel ? sel[t / SUBS] : t / SUBS;
+    const int J = sel ? sel_s[t / SUBS] : t / SUBS;
     return (unsigned)J < (unsigned)nb ? J * BLK + (t % SUBS) * kSub : -1;
   };
   typedef __attribute__((address_space(3))) void lds_void;
@@ -481,17 +320,6 @@ __global__ __launch_bounds__(128) void sparse_simple_kernel(int N, int block, in
   }
 }
 
-template <int BLK, int QT, int NW>
-hipError_t launch_mfma(const Shape& s, const void* Qr, const void* Kr, const void* V, int keep,
-                       const int32_t* idx, float scale, void* Os, hipStream_t st) {
-  const int nb = num_blocks(s.N, BLK);
-  const int total = nb * s.H * s.B;
-  hipLaunchKernelGGL((sparse_mfma_kernel<BLK, QT, NW>), dim3(total), dim3(NW * 64), 0, st, s.N, nb,
-                     keep, total, idx, scale * 1.4426950408889634f, (const bf16*)Qr,
-                     (const bf16*)Kr, (const bf16*)V, (bf16*)Os);
-  return hipGetLastError();
-}
-
 template <int BLK>
 hipError_t launch_pipe(const Shape& s, const void* Qr, const void* Kr, const void* V, int keep,
                        const int32_t* idx, float scale, void* Os, hipStream_t st) {
@@ -518,14 +346,8 @@ hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, co
                               int block, int keep, const int32_t* idx, float scale, void* Os,
                               hipStream_t st) {
   if (s.bf16) {
-#if ROLA_SPARSE_PIPE
     if (block == 64) return launch_pipe<64>(s, Qr, Kr, V, keep, idx, scale, Os, st);
     return launch_pipe<128>(s, Qr, Kr, V, keep, idx, scale, Os, st);
-#else
-    if (block == 64)
-      return launch_mfma<64, ROLA_B64_QT, 4 / ROLA_B64_QT>(s, Qr, Kr, V, keep, idx, scale, Os, st);
-    return launch_mfma<128, 2, 4>(s, Qr, Kr, V, keep, idx, scale, Os, st);
-#endif
   }
   if (s.d == 64) return launch_simple<float, 64>(s, Qr, Kr, V, block, keep, idx, scale, Os, st);
   return launch_simple<float, 128>(s, Qr, Kr, V, block, keep, idx, scale, Os, st);
