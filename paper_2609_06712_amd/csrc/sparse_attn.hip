@@ -22,8 +22,8 @@
 #include "common.h"
 #include "launch.h"
 
-#ifndef ROLA_SPARSE_NBUF
-#define ROLA_SPARSE_NBUF 2  // LDS stages of the K/V pipeline
+#ifndef ROLA_B128_NBUF
+#define ROLA_B128_NBUF 2  // LDS stages of the 128-token-block kernel with a block list
 #endif
 #ifndef ROLA_SPARSE_REMAP
 #define ROLA_SPARSE_REMAP 1  // 1: XCD-contiguous logical ranges; 2: interleaved chunks; 0: none
@@ -47,7 +47,7 @@ __device__ __forceinline__ f32x4 mfma16x16x32(const bf16x8& a, const bf16x8& b, 
 constexpr int kSub = 32;          // keys per sub-tile
 constexpr float kRescaleTau = 8.f;  // log2 headroom before O is rescaled
 
-template <int BLK>
+template <int BLK, int NBUF>
 __global__ __launch_bounds__(BLK * 2, 2) void sparse_pipe_kernel(
     int N, int nb, int keep, int total, const int32_t* __restrict__ idx, float scale_log2,
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
@@ -57,7 +57,6 @@ __global__ __launch_bounds__(BLK * 2, 2) void sparse_pipe_kernel(
   constexpr int DMA_PER_WAVE = TILE_BYTES / 1024 / NW;  // 1 KB instructions per wave per tensor
   constexpr int SUBS = BLK / kSub;                     // sub-tiles per selected block
   constexpr int BUF_BYTES = 2 * TILE_BYTES;            // K then V
-  constexpr int NBUF = ROLA_SPARSE_NBUF;
   __shared__ __attribute__((aligned(1024))) char lds[NBUF * BUF_BYTES];
 
   const int L = ROLA_SPARSE_REMAP == 2 ? xcd_chunk_remap(blockIdx.x, total, (nb + kNumXcd - 1) / kNumXcd)
@@ -320,12 +319,12 @@ __global__ __launch_bounds__(128) void sparse_simple_kernel(int N, int block, in
   }
 }
 
-template <int BLK>
+template <int BLK, int NBUF>
 hipError_t launch_pipe(const Shape& s, const void* Qr, const void* Kr, const void* V, int keep,
                        const int32_t* idx, float scale, void* Os, hipStream_t st) {
   const int nb = num_blocks(s.N, BLK);
   const int total = nb * s.H * s.B;
-  hipLaunchKernelGGL((sparse_pipe_kernel<BLK>), dim3(total), dim3(BLK * 2), 0, st, s.N, nb, keep,
+  hipLaunchKernelGGL((sparse_pipe_kernel<BLK, NBUF>), dim3(total), dim3(BLK * 2), 0, st, s.N, nb, keep,
                      total, idx, scale * 1.4426950408889634f, (const bf16*)Qr, (const bf16*)Kr,
                      (const bf16*)V, (bf16*)Os);
   return hipGetLastError();
@@ -346,8 +345,13 @@ hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, co
                               int block, int keep, const int32_t* idx, float scale, void* Os,
                               hipStream_t st) {
   if (s.bf16) {
-    if (block == 64) return launch_pipe<64>(s, Qr, Kr, V, keep, idx, scale, Os, st);
-    return launch_pipe<128>(s, Qr, Kr, V, keep, idx, scale, Os, st);
+    // Three LDS stages for gathered blocks (latency of scattered K/V reads); the dense walk, whose
+    // reads are L2-friendly, keeps two stages and the higher occupancy.
+    if (block == 64)
+      return idx ? launch_pipe<64, 3>(s, Qr, Kr, V, keep, idx, scale, Os, st)
+                 : launch_pipe<64, 2>(s, Qr, Kr, V, keep, idx, scale, Os, st);
+    return idx ? launch_pipe<128, ROLA_B128_NBUF>(s, Qr, Kr, V, keep, idx, scale, Os, st)
+               : launch_pipe<128, 2>(s, Qr, Kr, V, keep, idx, scale, Os, st);
   }
   if (s.d == 64) return launch_simple<float, 64>(s, Qr, Kr, V, block, keep, idx, scale, Os, st);
   return launch_simple<float, 128>(s, Qr, Kr, V, block, keep, idx, scale, Os, st);
