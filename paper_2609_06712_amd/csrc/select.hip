@@ -44,52 +44,62 @@ __global__ __launch_bounds__(256) void pool_kernel(int N, int d, int block, cons
   }
 }
 
-// S[I][J] = sum_c qbar[I][c] * kbar[J][c] for one (b, h) per blockIdx.z; 64 x 64 tile per workgroup.
+// S[I][J] = sum_c qbar[I][c] * kbar[J][c] for one (b, h) per blockIdx.z; 64 x 64 tile per workgroup
+// of 4 waves (32 x 32 each), on v_mfma_f32_16x16x4_f32: fp32 operands and fp32 accumulation, so the
+// scores keep fp32 accuracy (the 1e-4 tie gap of the selection rules out bf16 operands).
 __global__ __launch_bounds__(256) void score_kernel(int nb, int d, const float* __restrict__ qbar,
                                                     const float* __restrict__ kbar,
                                                     float* __restrict__ S) {
-  constexpr int TS = 64, KC = 32;
-  __shared__ float As[KC][TS + 4];
-  __shared__ float Bs[KC][TS + 4];
+  constexpr int TS = 64, KC = 32, PAD = 4;
+  __shared__ float As[TS][KC + PAD];
+  __shared__ float Bs[TS][KC + PAD];
   const long head = blockIdx.z;
   const float* q = qbar + head * (long)nb * d;
   const float* k = kbar + head * (long)nb * d;
   const int I0 = blockIdx.y * TS, J0 = blockIdx.x * TS;
-  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
-  const int lr = threadIdx.x / 4, lc = (threadIdx.x % 4) * 8;
-  float acc[4][4] = {};
+  const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64, lr = lane % 16, g = lane / 16;
+  const int wi = (wave >> 1) * 32, wj = (wave & 1) * 32;  // this wave's 32 x 32 sub-tile
+  const int lrow = tid / 4, lcol = (tid % 4) * 8;
+  f32x4 acc[2][2];
+#pragma unroll
+  for (int a2 = 0; a2 < 2; ++a2)
+#pragma unroll
+    for (int b2 = 0; b2 < 2; ++b2) acc[a2][b2] = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int c0 = 0; c0 < d; c0 += KC) {
     float a[8], b[8];
-    if (I0 + lr < nb) load8(q + (long)(I0 + lr) * d + c0 + lc, a);
+    if (I0 + lrow < nb) load8(q + (long)(I0 + lrow) * d + c0 + lcol, a);
     else for (int i = 0; i < 8; ++i) a[i] = 0.f;
-    if (J0 + lr < nb) load8(k + (long)(J0 + lr) * d + c0 + lc, b);
+    if (J0 + lrow < nb) load8(k + (long)(J0 + lrow) * d + c0 + lcol, b);
     else for (int i = 0; i < 8; ++i) b[i] = 0.f;
     __syncthreads();
 #pragma unroll
-    for (int i = 0; i < 8; ++i) { As[lc + i][lr] = a[i]; Bs[lc + i][lr] = b[i]; }
+    for (int i = 0; i < 8; ++i) { As[lrow][lcol + i] = a[i]; Bs[lrow][lcol + i] = b[i]; }
     __syncthreads();
-#pragma unroll 8
-    for (int c = 0; c < KC; ++c) {
-      float av[4], bv[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) { av[i] = As[c][ty + 16 * i]; bv[i] = Bs[c][tx + 16 * i]; }
+    for (int kk = 0; kk < KC; kk += 4) {
+      float av[2], bv[2];  // lane holds A[row lr][k g] and B[k g][col lr] of each 16 x 16 tile
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int t = 0; t < 2; ++t) {
+        av[t] = As[wi + 16 * t + lr][kk + g];
+        bv[t] = Bs[wj + 16 * t + lr][kk + g];
+      }
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(av[i], bv[j], acc[i][j]);
+      for (int a2 = 0; a2 < 2; ++a2)
+#pragma unroll
+        for (int b2 = 0; b2 < 2; ++b2)
+          acc[a2][b2] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[a2], bv[b2], acc[a2][b2], 0, 0, 0);
     }
   }
   float* Sh = S + head * (long)nb * nb;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int I = I0 + ty + 16 * i;
-    if (I >= nb) continue;
+  for (int a2 = 0; a2 < 2; ++a2)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int J = J0 + tx + 16 * j;
-      if (J < nb) Sh[(long)I * nb + J] = acc[i][j];
-    }
-  }
+    for (int b2 = 0; b2 < 2; ++b2)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int I = I0 + wi + 16 * a2 + 4 * g + v, J = J0 + wj + 16 * b2 + lr;
+        if (I < nb && J < nb) Sh[(long)I * nb + J] = acc[a2][b2][v];
+      }
 }
 
 __device__ __forceinline__ uint32_t order_key(float f) {
@@ -102,7 +112,6 @@ __global__ __launch_bounds__(64) void topk_kernel(int nb, int keep, const float*
                                                   int32_t* __restrict__ idx) {
   extern __shared__ uint32_t keys[];
   __shared__ uint32_t hist[256];
-  __shared__ uint32_t part[64];
   __shared__ uint32_t found[2];
   const long row = ((long)blockIdx.z * gridDim.y + blockIdx.y) * nb + blockIdx.x;
   const float* s = S + row * nb;
@@ -126,11 +135,15 @@ __global__ __launch_bounds__(64) void topk_kernel(int nb, int keep, const float*
     uint32_t c[4];
 #pragma unroll
     for (int b = 0; b < 4; ++b) c[b] = hist[4 * lane + b];
-    part[lane] = c[0] + c[1] + c[2] + c[3];
-    __syncthreads();
-    uint32_t above = 0;  // elements whose digit lies in higher lanes' bins
-    for (int m = lane + 1; m < 64; ++m) above += part[m];
-    uint32_t g = above;
+    // elements whose digit lies in higher lanes' bins: exclusive suffix sum across the wave
+    const uint32_t mine = c[0] + c[1] + c[2] + c[3];
+    uint32_t incl = mine;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const uint32_t o = __shfl_down(incl, off);
+      if (lane + off < 64) incl += o;
+    }
+    uint32_t g = incl - mine;
 #pragma unroll
     for (int b = 3; b >= 0; --b) {
       if (g < remaining && remaining <= g + c[b]) { found[0] = 4 * lane + b; found[1] = g; }
