@@ -31,6 +31,32 @@ from paper_2609_06712_amd import synth  # noqa: E402
 METRIC = "ms/attention layer + eff. TFLOP/s at Wan-14B 720p shape, 90% sparsity; % roofline"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "sparse_attn_wan14b_720p_traffic.txt")
+SPARSE_SRC = os.path.join(ROOT, "paper_2609_06712_amd", "csrc", "sparse_attn.hip")
+
+
+def source_digest(path: str) -> str:
+    import hashlib
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per launch of the sparse kernel from the committed counter summary (FETCH_SIZE and
+    WRITE_SIZE, each calibrated on a plain copy of known size), or None when the kernel source has
+    changed since the counters were taken."""
+    try:
+        rec = {}
+        with open(TRAFFIC_FILE) as f:
+            for line in f:
+                if "=" in line and not line.startswith("#"):
+                    k, v = line.split("=", 1)
+                    rec[k.strip()] = v.strip()
+        if rec.get("source_sha256") != source_digest(SPARSE_SRC):
+            return None
+        return float(rec["bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def sparse_flops_performed(idx: torch.Tensor, N: int, block: int, d: int) -> float:
@@ -96,6 +122,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibration-copy", action="store_true",
+                    help="one untimed device copy of one activation tensor (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the layer "
@@ -143,6 +171,11 @@ def main():
                                        out=out)
         mark(4)
 
+    if args.calibration_copy:  # a plain copy of known size, for scaling FETCH_SIZE / WRITE_SIZE
+        scratch = torch.empty_like(inp["V"])
+        scratch.copy_(inp["V"])
+        torch.cuda.synchronize()
+        del scratch
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -178,7 +211,7 @@ def main():
                    "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "kernel": "rola_sparse_attn", "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None},
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": measured_traffic()},
         "lowrank_roofline": {"bound": "hbm", "kernels": "rola_lowrank_summary + "
                              "rola_lowrank_readout_combine", "achieved": round(lr_gbs, 1),
                              "peak": PEAK_HBM_GBS, "unit": "GB/s",
