@@ -149,6 +149,8 @@ def main():
     idx = torch.empty((w.B, w.H, nb, keep), dtype=torch.int32, device=dev)
     ws_sel = torch.empty(R.select_workspace_bytes(prob, w.block), dtype=torch.uint8, device=dev)
     ws_sum = torch.empty(R.summary_workspace_bytes(prob, w.r), dtype=torch.uint8, device=dev)
+    ws_sp = torch.empty(R.sparse_workspace_bytes(prob, w.block, w.sparsity), dtype=torch.uint8,
+                        device=dev)
     o_s = torch.empty_like(inp["Qn"])
     out = torch.empty_like(inp["Qn"])
     C = torch.empty((w.B, w.H, w.r, w.d_h), dtype=torch.float32, device=dev)
@@ -163,7 +165,7 @@ def main():
         mark(0)
         R.rola_block_select(qr, kr, g, w.block, w.sparsity, out=idx, ws=ws_sel)
         mark(1)
-        R.rola_sparse_attn(qr, kr, inp["V"], g, w.block, w.sparsity, idx, out=o_s)
+        R.rola_sparse_attn(qr, kr, inp["V"], g, w.block, w.sparsity, idx, out=o_s, ws=ws_sp)
         mark(2)
         R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], w.r, cos, sin, g, C=C, z=z, ws=ws_sum)
         mark(3)

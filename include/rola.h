@@ -113,10 +113,16 @@ rola_status rola_block_select(const rola_problem* p, const void* Qr, const void*
  * v_q over the valid key tokens q of the blocks blk_idx[b, h, I, :] (keep = rola_keep_blocks(
  * n_blocks, sparsity) entries, each in [0, n_blocks); order irrelevant, duplicates not allowed).
  * Online softmax with fp32 statistics and accumulators; bf16 path on MFMA. scale is normally
- * 1/sqrt(d_h) (Sec. 3). Os: [B, H, N, d_h] in dtype. */
+ * 1/sqrt(d_h) (Sec. 3). Os: [B, H, N, d_h] in dtype.
+ * ws: rola_sparse_workspace_bytes(p, block, sparsity) bytes of device scratch, in which the bf16
+ * path with 64-token blocks merges the lists of adjacent query blocks so that they share their K/V
+ * loads; ws may be NULL (ws_bytes 0), which gives the same results without that sharing. A
+ * non-NULL ws smaller than needed is ROLA_ERR_WORKSPACE. */
+size_t rola_sparse_workspace_bytes(const rola_problem* p, int32_t block, double sparsity);
 rola_status rola_sparse_attn(const rola_problem* p, const void* Qr, const void* Kr, const void* V,
                              int32_t block, double sparsity, const int32_t* blk_idx,
-                             float softmax_scale, void* Os, hipStream_t stream);
+                             float softmax_scale, void* Os, void* ws, size_t ws_bytes,
+                             hipStream_t stream);
 
 /* Dense softmax attention O = softmax(Q^r K^r^T * scale) V (Sec. 3, "Full attention"): the 0 %
  * sparsity reference, same kernel as rola_sparse_attn walking every key block in order. */

@@ -48,6 +48,27 @@ __device__ __forceinline__ void store8(bf16* p, const float v[8]) {
   *reinterpret_cast<bf16x8*>(p) = a;
 }
 
+// Direct global-to-LDS load of 16 bytes per lane (global_load_lds_dwordx4, scalar-base form): lane l
+// reads base + voff(l) and the wave's 64 x 16 bytes land at LDS byte address lds_addr + 16 l
+// (base and lds_addr wave-uniform). Issued as inline assembly on purpose: the compiler then does
+// not track these LDS writes and adds no drains of its own (s_waitcnt vmcnt(0)) before later LDS
+// reads, which would empty the prefetch pipeline; callers wait for completion themselves with
+// s_waitcnt vmcnt(n) and a workgroup barrier.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(const void* base, uint32_t voff, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(base), "s"(lds_addr)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// LDS byte address of a pointer into a __shared__ array.
+__device__ __forceinline__ uint32_t lds_address(const void* p) {
+  return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) char*)p);
+}
+
 // Marks a value as wave-uniform (moves it to a scalar register).
 __device__ __forceinline__ int wave_uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 

@@ -28,9 +28,12 @@ hipError_t launch_block_select(const Shape& s, const void* Qr, const void* Kr, i
                                int32_t* idx, void* ws, hipStream_t st);
 
 // sparse_attn.hip  (idx == nullptr: dense, every key block in order; keep must equal n_blocks)
+// ws: sparse_workspace_bytes(s, block, keep) bytes, or nullptr (then no K/V loads are shared
+// between query blocks).
+size_t sparse_workspace_bytes(const Shape& s, int block, int keep);
 hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, const void* V,
                               int block, int keep, const int32_t* idx, float scale, void* Os,
-                              hipStream_t st);
+                              void* ws, hipStream_t st);
 
 // lowrank.hip
 int summary_chunks(const Shape& s, int r);

@@ -186,9 +186,18 @@ rola_status rola_block_select(const rola_problem* p, const void* Qr, const void*
   return hip_status(rola::launch_block_select(s, Qr, Kr, block, keep, blk_idx, ws, stream), __func__);
 }
 
+size_t rola_sparse_workspace_bytes(const rola_problem* p, int32_t block, double sparsity) {
+  rola::Shape s;
+  if (check_problem(p, __func__, &s) != ROLA_OK || check_block(s, block, __func__) != ROLA_OK ||
+      check_sparsity(sparsity, __func__) != ROLA_OK)
+    return 0;
+  return rola::sparse_workspace_bytes(s, block, rola_keep_blocks(rola::num_blocks(s.N, block), sparsity));
+}
+
 rola_status rola_sparse_attn(const rola_problem* p, const void* Qr, const void* Kr, const void* V,
                              int32_t block, double sparsity, const int32_t* blk_idx,
-                             float softmax_scale, void* Os, hipStream_t stream) {
+                             float softmax_scale, void* Os, void* ws, size_t ws_bytes,
+                             hipStream_t stream) {
   rola::Shape s;
   TRY(check_problem(p, __func__, &s));
   TRY(check_block(s, block, __func__));
@@ -201,8 +210,15 @@ rola_status rola_sparse_attn(const rola_problem* p, const void* Qr, const void* 
   if (!(softmax_scale > 0.f) || !isfinite(softmax_scale))
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: softmax_scale must be finite and positive", __func__);
   const int keep = rola_keep_blocks(rola::num_blocks(s.N, block), sparsity);
+  const size_t need = rola::sparse_workspace_bytes(s, block, keep);
+  if (ws && need > 0) {
+    if (reinterpret_cast<uintptr_t>(ws) % 16)
+      return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: ws must be 16-byte aligned", __func__);
+    if (ws_bytes < need)
+      return fail(ROLA_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", __func__, ws_bytes, need);
+  }
   return hip_status(rola::launch_sparse_attn(s, Qr, Kr, V, block, keep, blk_idx, softmax_scale, Os,
-                                             stream), __func__);
+                                             need > 0 ? ws : nullptr, stream), __func__);
 }
 
 rola_status rola_dense_attn(const rola_problem* p, const void* Qr, const void* Kr, const void* V,
@@ -218,7 +234,7 @@ rola_status rola_dense_attn(const rola_problem* p, const void* Qr, const void* K
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: softmax_scale must be finite and positive", __func__);
   const int nb = rola::num_blocks(s.N, block);
   return hip_status(rola::launch_sparse_attn(s, Qr, Kr, V, block, nb, nullptr, softmax_scale, O,
-                                             stream), __func__);
+                                             nullptr, stream), __func__);
 }
 
 rola_status rola_lowrank_summary(const rola_problem* p, const void* Kn, const void* V,

@@ -3,252 +3,363 @@
 // softmax with fp32 running max / sum / accumulators. With no index list every key block is walked
 // in order, which is dense softmax attention (the 0 % sparsity reference).
 //
-// bf16 path (d_h = 128): one workgroup per (b, h, query block of BLK tokens), BLK/32 waves of 32
-// queries (two 16-query MFMA tiles) each, Q fragments in registers. Keys stream in 32-key sub-tiles:
-//   S^T = K Q^T     v_mfma_f32_16x16x32_bf16, A = K sub-tile from LDS, B = Q fragments; lane
-//                   (g = lane/16, c = lane%16) receives keys 4g+v of each 16-key tile for query c,
-//                   so softmax statistics stay per lane (row max: two permlane swaps).
-//   P = exp2(S^T * scale*log2e - m), rounded to bf16 in registers: directly the B operand of
-//   O^T = V^T P^T   A = V^T: V stays row-major in LDS and is read with the gfx950 transposing LDS read
-//                   ds_read_b64_tr_b16, which hands lane i of each 16-lane group channel i of 4
-//                   consecutive keys -- exactly the MFMA operand layout.
-// Row sums come from one more MFMA against a ones operand. Sub-tiles are double-buffered in LDS and
-// filled by direct global-to-LDS loads (global_load_lds_dwordx4): no staging registers. The 16-byte
-// chunks of every row are XOR-swizzled (K: chunk ^ row%16, V: chunk ^ 2(row%8)) so that the K
-// operand reads (16 rows per cycle) and the transposing V reads (8 rows per cycle) are free of
-// bank conflicts. O is rescaled only when a sub-tile raises a row max by more than 2^8: the softmax
-// ratio does not depend on the reference max, so this is exact. The grid is remapped so that
-// consecutive query blocks of one head run on the same XCD (sharing its L2).
+// bf16 path (d_h = 128). A workgroup serves G = 1 or 2 consecutive query blocks of BLK tokens, with
+// BLK/32 waves of 32 queries per query block. With G = 2 it walks the ascending union of the two
+// blocks' lists (built by pair_union_kernel): a key block both hold is fetched into LDS once, and
+// each wave computes only on the blocks its own query block selected. Adjacent query blocks share
+// about half of their selections, so this cuts the K/V bytes that cross L2 by about a quarter.
+// Keys stream in 32-key sub-tiles through NBUF LDS stages filled by direct global-to-LDS loads.
+// Per wave and sub-tile, on v_mfma_f32_32x32x16_bf16:
+//   S^T = K Q^T   A = K rows from LDS (ds_read_b128), B = Q fragments held in registers; lane l gets
+//                 query l%32 and keys 8j + 4(l/32) + i, so a row max needs one permlane32 swap.
+//   P = exp2(S^T * scale*log2e - m) rounded to bf16 in registers: directly the B operand of
+//   O^T = V^T P^T A = V^T through the transposing LDS read ds_read_b64_tr_b16 of row-major V; the
+//                 sum over keys runs in the order the S^T layout hands them out (two reads of four
+//                 keys per operand), which leaves the result unchanged.
+// Row sums accumulate per lane with v_dot2 on the bf16 probabilities. A step holds few registers
+// (about 160), so three workgroups of four waves share a CU and the matrix and vector work of one
+// wave overlaps that of the others. O is rescaled only when a sub-tile raises a row max by more
+// than 2^8: the softmax ratio does not depend on the reference max, so this is exact.
+#include <climits>
+
 #include "common.h"
 #include "launch.h"
 
-#ifndef ROLA_B128_NBUF
-#define ROLA_B128_NBUF 2  // LDS stages of the 128-token-block kernel with a block list
+#ifndef ROLA_B64_GROUP
+#define ROLA_B64_GROUP 2  // query blocks per workgroup of the 64-token-block kernel with a block list
 #endif
-#ifndef ROLA_SPARSE_REMAP
-#define ROLA_SPARSE_REMAP 1  // 1: XCD-contiguous logical ranges; 2: interleaved chunks; 0: none
+#ifndef ROLA_B64_NBUF
+#define ROLA_B64_NBUF 3  // its LDS stages (16 KB each)
 #endif
 
 namespace rola {
 namespace {
 
-__device__ __forceinline__ f32x4 mfma16x16x32(const bf16x8& a, const bf16x8& b, const f32x4& c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
-
-// bf16 kernel, pipelined: one workgroup per (b, h, query block of BLK tokens) with BLK/32 waves of
-// 32 queries each; keys stream in 32-key sub-tiles (two or four per selected block) that are
-// double-buffered in LDS and filled by direct global-to-LDS loads (global_load_lds_dwordx4), so no
-// registers stage them. Rows are stored with their 16-byte chunks XOR-swizzled (K: chunk ^ row%16,
-// V: chunk ^ 2(row%8)), which makes both the K operand reads (ds_read_b128, 16 rows per cycle) and
-// the transposing V reads (ds_read_b64_tr_b16, 8 rows per cycle) bank-conflict free.
-// Online softmax keeps a per-query reference max and rescales O only when a new tile raises the max
-// by more than 2^8: the softmax ratio is independent of the reference, so this is exact.
-constexpr int kSub = 32;          // keys per sub-tile
+constexpr int kSub = 32;            // keys per sub-tile: one LDS stage holds its K and V (8 KB each)
 constexpr float kRescaleTau = 8.f;  // log2 headroom before O is rescaled
 
-template <int BLK, int NBUF>
-__global__ __launch_bounds__(BLK * 2, 2) void sparse_pipe_kernel(
-    int N, int nb, int keep, int total, const int32_t* __restrict__ idx, float scale_log2,
-    const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
-    bf16* __restrict__ O) {
-  constexpr int D = 128, NW = BLK / 32, QT = 2;
-  constexpr int TILE_BYTES = kSub * D * 2;              // 8 KB
-  constexpr int DMA_PER_WAVE = TILE_BYTES / 1024 / NW;  // 1 KB instructions per wave per tensor
-  constexpr int SUBS = BLK / kSub;                     // sub-tiles per selected block
-  constexpr int BUF_BYTES = 2 * TILE_BYTES;            // K then V
-  __shared__ __attribute__((aligned(1024))) char lds[NBUF * BUF_BYTES];
+__device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
 
-  const int L = ROLA_SPARSE_REMAP == 2 ? xcd_chunk_remap(blockIdx.x, total, (nb + kNumXcd - 1) / kNumXcd)
-              : ROLA_SPARSE_REMAP ? xcd_remap(blockIdx.x, total) : (int)blockIdx.x;
-  const int I = L % nb;
-  const long head = L / nb;
-  const int tid = threadIdx.x, lane = tid % 64, lr = lane % 16, g = lane / 16;
-  const int wave = wave_uniform(tid / 64);  // wave-uniform: LDS DMA bases in SGPRs
+// LDS layouts of a sub-tile: rows of 256 bytes (128 channels), the 16-byte chunks of each row
+// XOR-swizzled. K: chunk ^ row%16, so the 16 rows of an operand read (ds_read_b128) hit distinct
+// banks. V: chunk ^ 2*{0,3,5,6}[row%4], so the four rows x 64 bytes of each half of a transposing
+// read land in distinct banks whether the LDS serves 128 or 256 bytes per pass.
+__device__ __forceinline__ int k_swizzle(int row) { return row & 15; }
+__device__ __forceinline__ int v_swizzle(int row) { return 2 * ((0x6530 >> (4 * (row & 3))) & 15); }
+
+// Pairs of adjacent query blocks share a workgroup of the attention kernel. For each (b, h, pair)
+// this writes the entry count and then the ascending union of the two block lists, each entry
+// J | (bit 0: the first block selected J, bit 1: the second) << 16. Built through a bitmap, so the
+// lists may come in any order; out-of-range entries are dropped, as the attention skips them.
+__global__ __launch_bounds__(256) void pair_union_kernel(int nb, int keep, int npairs, int stride,
+                                                         const int32_t* __restrict__ idx,
+                                                         int32_t* __restrict__ out) {
+  extern __shared__ uint32_t sh[];
+  const int words = (nb + 31) >> 5;
+  uint32_t* bits = sh;                       // [2][words]: membership of each list
+  int* scan = reinterpret_cast<int*>(sh + 2 * words);  // [256]
+  const long gp = blockIdx.x;
+  const long head = gp / npairs;
+  const int I0 = 2 * (int)(gp % npairs);
+  const int tid = threadIdx.x;
+  for (int w = tid; w < 2 * words; w += 256) bits[w] = 0u;
+  __syncthreads();
+  for (int b = 0; b < 2 && I0 + b < nb; ++b) {
+    const int32_t* sel = idx + (head * nb + I0 + b) * (long)keep;
+    for (int i = tid; i < keep; i += 256) {
+      const int J = sel[i];
+      if ((unsigned)J < (unsigned)nb) atomicOr(&bits[b * words + (J >> 5)], 1u << (J & 31));
+    }
+  }
+  __syncthreads();
+  const int per = (words + 255) / 256, w0 = min(words, tid * per), w1 = min(words, w0 + per);
+  int cnt = 0;
+  for (int w = w0; w < w1; ++w) cnt += __popc(bits[w] | bits[words + w]);
+  scan[tid] = cnt;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {  // inclusive scan of the per-thread counts
+    const int v = tid >= off ? scan[tid - off] : 0;
+    __syncthreads();
+    scan[tid] += v;
+    __syncthreads();
+  }
+  int32_t* o = out + gp * (long)stride;
+  if (tid == 255) o[0] = scan[255];
+  int pos = 1 + scan[tid] - cnt;
+  for (int w = w0; w < w1; ++w) {
+    const uint32_t a = bits[w], b = bits[words + w];
+    for (uint32_t u = a | b; u; u &= u - 1) {
+      const int bit = __ffs(u) - 1;
+      o[pos++] = (w * 32 + bit) | (int)((((a >> bit) & 1u) | (((b >> bit) & 1u) << 1)) << 16);
+    }
+  }
+}
+
+// bf16 attention kernel: one workgroup per (b, h, G consecutive query blocks); see the file comment.
+// lists: G = 1: the block lists [B, H, nb, list_stride] (list_len entries used; nullptr: every key
+//        block in order); G = 2: pair_union_kernel output, list_stride ints per (b, h, pair).
+template <int BLK, int G, int NBUF, int TAB>
+__global__ __launch_bounds__(G * BLK * 2, 2) void sparse_attn_kernel(
+    int N, int nb, int ngroups, int total, const int32_t* __restrict__ lists, int list_len,
+    int list_stride, float scale_log2, const bf16* __restrict__ Q, const bf16* __restrict__ K,
+    const bf16* __restrict__ V, bf16* __restrict__ O) {
+  static_assert(G == 1 || G == 2, "one or two query blocks per workgroup");
+  static_assert(NBUF >= 3, "loads of later sub-tiles stay in flight during a step");
+  constexpr int D = 128, WPB = BLK / 32, NW = G * WPB;
+  constexpr int TILE = kSub * D * 2;              // 8 KB: K (or V) of one sub-tile
+  constexpr int STAGE = 2 * TILE;                 // K then V
+  constexpr int DMA_PER_WAVE = TILE / 1024 / NW;  // 1 KB loads per wave per tensor and sub-tile
+  constexpr int SUBS = BLK / kSub;                // sub-tiles per key block
+  static_assert(DMA_PER_WAVE >= 1, "at most 8 waves");
+  __shared__ __attribute__((aligned(1024))) char lds[NBUF * STAGE];
+  __shared__ int tab[TAB > 0 ? TAB : 1];  // the workgroup's block list (TAB > 0)
+
+  const int L = xcd_remap(blockIdx.x, total);
+  const int grp = L % ngroups;
+  const long head = L / ngroups;
+  const int tid = threadIdx.x, lane = tid % 64, hh = lane / 32;
+  const int wave = wave_uniform(tid / 64);   // wave-uniform: LDS DMA bases in SGPRs
+  const int qb = wave / WPB;                 // which of the group's query blocks this wave serves
+  const int I = grp * G + qb;                // its index (== nb for a missing second block)
+  const int q = I * BLK + (wave % WPB) * 32 + lane % 32;  // this lane's query (column of S^T, O^T)
+  const bool qvalid = I < nb && q < N;
+  const int mybit = 1 << qb;
   const bf16* Qh = Q + head * (long)N * D;
   const char* Kh = reinterpret_cast<const char*>(K + head * (long)N * D);
   const char* Vh = reinterpret_cast<const char*>(V + head * (long)N * D);
-  bf16* Oh = O + head * (long)N * D;
-  const int32_t* sel = idx ? idx + (head * nb + I) * (long)keep : nullptr;
-  const int steps = keep * SUBS;
 
-  bf16x8 qf[QT][4];
-#pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    const int q = I * BLK + (wave * QT + qt) * 16 + lr;
-#pragma unroll
-    for (int kc = 0; kc < 4; ++kc)
-      qf[qt][kc] = q < N ? *reinterpret_cast<const bf16x8*>(Qh + (long)q * D + 32 * kc + 8 * g)
-                         : bf16x8{};
+  // The workgroup's block list: with TAB > 0 it is copied into LDS once (E <= TAB) and each step
+  // reads the entries of the next step, which the barrier of that step finds complete, so list reads
+  // never stall a step; otherwise entries come through uniform scalar loads.
+  typedef const __attribute__((address_space(4))) int32_t* const_i32;
+  const int32_t* glist = nullptr;
+  int E = list_len;
+  if (G == 2) {
+    glist = lists + (head * ngroups + grp) * (long)list_stride;
+    E = ((const_i32)glist)[0];
+    glist += 1;
+  } else if (lists) {
+    glist = lists + (head * nb + grp) * (long)list_stride;
   }
-  f32x4 acc[QT][8], accl[QT];  // O^T tiles and the row sums (all four rows of accl are equal)
-  float m[QT];
-#pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    m[qt] = -INFINITY;
-    accl[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int w = 0; w < 8; ++w) acc[qt][w] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const const_i32 slist = (const_i32)glist;
+  const int T = E * SUBS;  // sub-tiles the workgroup walks
+  if (TAB > 0 && glist) {
+    for (int i = tid; i < E; i += NW * 64) tab[i] = glist[i];
   }
-  bf16x8 ones;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) ones[i] = (bf16)1.0f;
+  struct Step {
+    int k0;    // first key, -1 if the block index is out of range
+    int mask;  // query blocks of the group that selected the block
+  };
+  // raw(e): entry e of the list (in a VGPR when it comes from the LDS table); step_of decodes the
+  // entry of sub-tile t.
+  auto raw = [&](int e) -> int {
+    if (!glist) return e;
+    const int i = min(e, max(E - 1, 0));
+    return TAB > 0 ? tab[i] : (int)slist[i];
+  };
+  auto step_of = [&](int v, int t) {
+    v = TAB > 0 ? wave_uniform(v) : v;
+    const int J = G == 2 ? (v & 0xFFFF) : v;
+    const int mask = G == 2 ? (v >> 16) : 1;
+    return Step{(unsigned)J < (unsigned)nb ? J * BLK + (t % SUBS) * kSub : -1, mask};
+  };
+  auto active = [&](const Step& s) { return (s.mask & mybit) && s.k0 >= 0 && s.k0 < N; };
 
-  // Per-lane constant offsets. DMA: lane l of 1-KB slot q fills row 4q + l/16, position l%16 with
-  // source chunk (position ^ swizzle(row)). Reads: K operand of (kt, kc) and V^T operand of w.
-  int dk[DMA_PER_WAVE], dv[DMA_PER_WAVE], drow[DMA_PER_WAVE];
+  // Q^T fragments of the 8 k-steps (d = 16s + 8(l/32) .. +7) stay in registers. They are complete
+  // before the first K/V load is issued: a wait for them inside the loop would also drain the
+  // K/V loads in flight.
+  bf16x8 qf[8];
+#pragma unroll
+  for (int s = 0; s < 8; ++s)
+    qf[s] = qvalid ? *reinterpret_cast<const bf16x8*>(Qh + (long)q * D + 16 * s + 8 * hh) : bf16x8{};
+  __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
+  if (TAB > 0) __syncthreads();  // the list table is complete
+
+  f32x16 acc[4];        // O^T channel tiles 32w .. 32w+31
+  float m = -INFINITY;  // running reference max (log2 units) of this lane's query
+  float l = 0.f;        // running sum of this lane's 16 keys per sub-tile (the other 16: lane l^32)
+#pragma unroll
+  for (int w = 0; w < 4; ++w) acc[w] = f32x16{};
+
+  // Per-lane LDS offsets. DMA: lane l of 1-KB slot s fills row 4s + l/16 at chunk position l%16
+  // with source chunk (position ^ swizzle(row)). K operand of k-step s: row l%32, chunk 2s + l/32.
+  // V^T operand of channel tile w: the lane supplies row 4(l/32) + (l%16)/4 (plus 16u + 8 for the
+  // second four keys of k-step u) and channels 32w + 16((l/16)%2) + 4(l%4) .. +3.
+  uint32_t dk[DMA_PER_WAVE], dv[DMA_PER_WAVE];
 #pragma unroll
   for (int i = 0; i < DMA_PER_WAVE; ++i) {
-    const int q = wave * DMA_PER_WAVE + i, row = 4 * q + lane / 16, pos = lane % 16;
-    drow[i] = row;
-    dk[i] = row * D * 2 + ((pos ^ (row & 15)) << 4);
-    dv[i] = row * D * 2 + ((pos ^ ((row & 7) << 1)) << 4);
+    const int row = 4 * (wave * DMA_PER_WAVE + i) + lane / 16, pos = lane % 16;
+    dk[i] = row * D * 2 + ((pos ^ k_swizzle(row)) << 4);
+    dv[i] = row * D * 2 + ((pos ^ v_swizzle(row)) << 4);
   }
-  int ko[2][4];
+  int ko[8];
 #pragma unroll
-  for (int kt = 0; kt < 2; ++kt)
+  for (int s = 0; s < 8; ++s) {
+    const int row = lane % 32;
+    ko[s] = row * 256 + (((2 * s + hh) ^ k_swizzle(row)) << 4);
+  }
+  int vo[4];
+  {
+    const int i16 = lane % 16, row = 4 * hh + i16 / 4;
+    const int c = 2 * ((lane / 16) & 1) + ((i16 & 3) >> 1);
 #pragma unroll
-    for (int kc = 0; kc < 4; ++kc) {
-      const int row = 16 * kt + lr;
-      ko[kt][kc] = row * 256 + (((4 * kc + g) ^ (row & 15)) << 4);
-    }
-  const int sp = lr >> 2, mp = lr & 3, vr = 4 * g + sp;
-  int vo[8];
-#pragma unroll
-  for (int w = 0; w < 8; ++w)
-    vo[w] = TILE_BYTES + vr * 256 + (((2 * w + (mp >> 1)) ^ ((vr & 7) << 1)) << 4) + ((mp & 1) << 3);
+    for (int w = 0; w < 4; ++w)
+      vo[w] = TILE + row * 256 + (((4 * w + c) ^ v_swizzle(row)) << 4) + 8 * (i16 & 1);
+  }
 
-  // The block list is read through the constant address space: uniform scalar loads, counted by
-  // lgkmcnt, so reading an index never drains the DMA loads in flight (vmcnt).
-  typedef const __attribute__((address_space(4))) int32_t* const_i32;
-  const const_i32 sel_s = (const_i32)sel;
-  auto step_key0 = [&](int t) {  // first key of step t; -1 if its block index is out of range
-    const int J = sel ? sel_s[t / SUBS] : t / SUBS;
-    return (unsigned)J < (unsigned)nb ? J * BLK + (t % SUBS) * kSub : -1;
-  };
-  typedef __attribute__((address_space(3))) void lds_void;
-  auto issue = [&](int t, int buf) {  // always DMA_PER_WAVE * 2 instructions (fixed vmcnt per step)
-    const int k0 = max(step_key0(t), 0);
-    char* dst = lds + buf * BUF_BYTES;
+  const uint32_t lds0 = lds_address(lds);
+  auto issue = [&](const Step& s, int buf) {  // always 2 * DMA_PER_WAVE loads (fixed vmcnt per step)
+    const int k0 = max(s.k0, 0);
+    const uint32_t dst = lds0 + buf * STAGE;
     if (k0 + kSub <= N) {
       const char* kb = Kh + (long)k0 * D * 2;
       const char* vb = Vh + (long)k0 * D * 2;
 #pragma unroll
       for (int i = 0; i < DMA_PER_WAVE; ++i) {
-        const int q = wave * DMA_PER_WAVE + i;
-        __builtin_amdgcn_global_load_lds((const void*)(kb + dk[i]), (lds_void*)(dst + q * 1024), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds((const void*)(vb + dv[i]), (lds_void*)(dst + TILE_BYTES + q * 1024), 16, 0, 0);
+        const uint32_t slot = (wave * DMA_PER_WAVE + i) * 1024;
+        dma16(kb, dk[i], dst + slot);
+        dma16(vb, dv[i], dst + TILE + slot);
       }
-    } else {  // tail: rows past N re-read row N-1 (finite data, masked out of the softmax)
+    } else {  // ragged tail: rows past N re-read row N-1 (a valid key, see mask_tail)
 #pragma unroll
       for (int i = 0; i < DMA_PER_WAVE; ++i) {
-        const int q = wave * DMA_PER_WAVE + i;
-        const long shift = (long)(min(k0 + drow[i], N - 1) - drow[i]) * D * 2;
-        __builtin_amdgcn_global_load_lds((const void*)(Kh + shift + dk[i]), (lds_void*)(dst + q * 1024), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds((const void*)(Vh + shift + dv[i]), (lds_void*)(dst + TILE_BYTES + q * 1024), 16, 0, 0);
+        const uint32_t slot = (wave * DMA_PER_WAVE + i) * 1024;
+        const int r = 4 * (wave * DMA_PER_WAVE + i) + lane / 16;
+        const uint32_t row = (uint32_t)(min(k0 + r, N - 1) - r) * (D * 2);
+        dma16(Kh, row + dk[i], dst + slot);
+        dma16(Vh, row + dv[i], dst + TILE + slot);
       }
     }
   };
 
-  auto compute = [&](const char* base, int k0) {
-    f32x4 s[QT][2];
+  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+  auto load_k = [&](int buf, int s0, bf16x8 (&kf)[4]) {  // K operands of k-steps s0 .. s0+3
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt)
+    for (int s = 0; s < 4; ++s)
+      kf[s] = *reinterpret_cast<const bf16x8*>(lds + buf * STAGE + ko[s0 + s]);
+  };
+  auto load_v = [&](int buf, int u, bf16x8 (&vf)[4]) {  // V^T operands of key k-step u
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt) s[qt][kt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    bf16x8 kfr[4][2];  // all K operands of the step first, then four independent MFMA chains
-#pragma unroll
-    for (int kc = 0; kc < 4; ++kc)
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) kfr[kc][kt] = *reinterpret_cast<const bf16x8*>(base + ko[kt][kc]);
-#pragma unroll
-    for (int kc = 0; kc < 4; ++kc)
-#pragma unroll
-      for (int qt = 0; qt < QT; ++qt) {
-        s[qt][0] = mfma16x16x32(kfr[kc][0], qf[qt][kc], s[qt][0]);
-        s[qt][1] = mfma16x16x32(kfr[kc][1], qf[qt][kc], s[qt][1]);
-      }
-    if (k0 + kSub > N) {
-#pragma unroll
-      for (int qt = 0; qt < QT; ++qt)
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-          for (int v = 0; v < 4; ++v)
-            if (k0 + 16 * kt + 4 * g + v >= N) s[qt][kt][v] = -INFINITY;
+    for (int w = 0; w < 4; ++w) {
+      const char* p = lds + buf * STAGE + vo[w] + 16 * u * 256;
+      const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p);
+      const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p + 8 * 256));
+      vf[w] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
     }
-    bf16x8 pb[QT];
+  };
+  // Softmax pieces on S^T of one sub-tile (16 keys of this lane's query; the other 16 in lane l^32).
+  auto row_max = [&](const f32x16& s) {
+    float mx = s[0];
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
-      float mx = fmaxf(fmaxf(fmaxf(s[qt][0][0], s[qt][0][1]), fmaxf(s[qt][0][2], s[qt][0][3])),
-                       fmaxf(fmaxf(s[qt][1][0], s[qt][1][1]), fmaxf(s[qt][1][2], s[qt][1][3])));
-      const float mt = rows_max(mx) * scale_log2;
-      if (__any(mt > m[qt] + kRescaleTau)) {
-        const float mnew = fmaxf(m[qt], mt);
-        const float alpha = __builtin_amdgcn_exp2f(m[qt] - mnew);
-        m[qt] = mnew;
-        accl[qt] *= alpha;
+    for (int k = 1; k < 16; ++k) mx = fmaxf(mx, s[k]);
+    const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+    return fmaxf(__uint_as_float(x[0]), __uint_as_float(x[1])) * scale_log2;
+  };
+  auto rescale = [&](float mt) {  // lazy: only when the max grew by more than 2^tau
+    if (__any(mt > m + kRescaleTau)) {
+      const float mnew = fmaxf(m, mt);
+      const float alpha = __builtin_amdgcn_exp2f(m - mnew);
+      m = mnew;
+      l *= alpha;
 #pragma unroll
-        for (int w = 0; w < 8; ++w) acc[qt][w] *= alpha;
-      }
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-          pb[qt][4 * kt + v] = (bf16)__builtin_amdgcn_exp2f(fmaf(s[qt][kt][v], scale_log2, -m[qt]));
-      accl[qt] = mfma16x16x32(ones, pb[qt], accl[qt]);
+      for (int w = 0; w < 4; ++w) acc[w] *= alpha;
     }
-    typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
-    bf16x8 vfr[8];
+  };
+  // Rows of a ragged last sub-tile repeat key N-1, whose score is a valid one: they leave the row
+  // max unchanged and only their probabilities are zeroed. The row sum adds exactly the bf16
+  // probabilities that enter P V (v_dot2 against (1, 1), fp32 accumulation).
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  auto probs = [&](const f32x16& s, int k0, bf16x8 (&pb)[2]) {
 #pragma unroll
-    for (int w = 0; w < 8; ++w) {
-      const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(base + vo[w]));
-      const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(base + vo[w] + 16 * 256));
-      vfr[w] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    for (int k = 0; k < 16; ++k)
+      pb[k / 8][k % 8] = (bf16)__builtin_amdgcn_exp2f(fmaf(s[k], scale_log2, -m));
+    if (k0 + kSub > N) {  // value k holds key k0 + 8(k/4) + 4(l/32) + k%4
+      const int lim = N - k0 - 4 * hh;
+#pragma unroll
+      for (int k = 0; k < 16; ++k)
+        if (8 * (k / 4) + k % 4 >= lim) pb[k / 8][k % 8] = (bf16)0.f;
     }
+    const bf16x2 one2 = {(bf16)1.0f, (bf16)1.0f};
 #pragma unroll
-    for (int w = 0; w < 8; ++w)
+    for (int k = 0; k < 16; k += 2)
+      l = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[k / 8][k % 8], pb[k / 8][k % 8 + 1]}, one2, l, false);
+  };
+  auto pv = [&](int u, const bf16x8 (&vf)[4], const bf16x8 (&pb)[2]) {
 #pragma unroll
-      for (int qt = 0; qt < QT; ++qt) acc[qt][w] = mfma16x16x32(vfr[w], pb[qt], acc[qt][w]);
+    for (int w = 0; w < 4; ++w) acc[w] = mfma32(vf[w], pb[u], acc[w]);
+  };
+  auto qk = [&](int s0, const bf16x8* kf, f32x16& sacc, int n) {  // k-steps s0 .. s0+n-1
+#pragma unroll
+    for (int s = 0; s < n; ++s) sacc = mfma32(kf[s], qf[s0 + s], sacc);
   };
 
-  // Step t computes buffer t % NBUF while the loads of the next NBUF-1 steps fill the others. The
-  // loop is unrolled by NBUF so each buffer's base is a compile-time offset.
-  constexpr int PER_STEP = 2 * DMA_PER_WAVE;  // vector-memory instructions this wave issues per step
-  auto run_step = [&](int t, int buf) {
-    if (t + NBUF - 1 <= steps) {  // loads of steps t+1 .. t+NBUF-2 may stay in flight
-      constexpr int allowed = PER_STEP * (NBUF - 2);
-      __builtin_amdgcn_s_waitcnt((allowed & 15) | ((allowed >> 4) << 14) | (7 << 4) | (15 << 8));
-    } else {
-      __builtin_amdgcn_s_waitcnt(0);
-    }
-    __syncthreads();  // everyone's loads of step t landed; step t-1 is done with its buffer
-    if (t + NBUF - 1 < steps) issue(t + NBUF - 1, (buf + NBUF - 1) % NBUF);
-    const int k0 = step_key0(t);
-    if (k0 >= 0 && k0 < N) compute(lds + buf * BUF_BYTES, k0);
-  };
+  // Pipeline: step t waits for the loads of sub-tile t and a barrier, issues the loads of sub-tile
+  // t+NBUF-1 into the buffer sub-tile t-1 has released, then S = QK(t), softmax, O += P V(t). The
+  // second wave on each SIMD overlaps its matrix and vector work with this one's. Unrolled by NBUF
+  // so each buffer is a compile-time offset.
+  constexpr int PER_STEP = 2 * DMA_PER_WAVE;  // vector-memory instructions per wave per sub-tile
+  int issued = 0;
 #pragma unroll
   for (int j = 0; j < NBUF - 1; ++j)
-    if (j < steps) issue(j, j);
-  for (int t = 0; t < steps; t += NBUF) {
+    if (j < T) {
+      issue(step_of(raw(j / SUBS), j), j);
+      ++issued;
+    }
+  int pi = raw(issued / SUBS), pc = raw(0);  // entries the next step decodes
+  for (int t = 0; t < T;) {
 #pragma unroll
-    for (int j = 0; j < NBUF; ++j)
-      if (t + j < steps) run_step(t + j, j);
+    for (int j = 0; j < NBUF; ++j) {
+      if (t >= T) break;
+      if (issued == t + NBUF - 1) {  // loads of t+1 .. t+NBUF-2 may stay in flight
+        constexpr int allowed = PER_STEP * (NBUF - 2);
+        __builtin_amdgcn_s_waitcnt((allowed & 15) | ((allowed >> 4) << 14) | (7 << 4) | (15 << 8));
+      } else {
+        __builtin_amdgcn_s_waitcnt(0);
+      }
+      __syncthreads();  // sub-tile t landed for every wave; every wave is done with sub-tile t-1
+      if (issued < T) {
+        issue(step_of(pi, issued), (j + NBUF - 1) % NBUF);
+        ++issued;
+      }
+      const Step cur = step_of(pc, t);
+      pi = raw(issued / SUBS);
+      pc = raw((t + 1) / SUBS);
+      if (active(cur)) {
+        bf16x8 kf[4], kg[4], vf[4], pb[2];
+        load_k(j, 0, kf);
+        load_k(j, 4, kg);
+        f32x16 sc = mfma32(kf[0], qf[0], f32x16{});
+        qk(1, kf + 1, sc, 3);
+        qk(4, kg, sc, 4);
+        load_v(j, 0, vf);
+        rescale(row_max(sc));
+        probs(sc, cur.k0, pb);
+        pv(0, vf, pb);
+        load_v(j, 1, vf);
+        pv(1, vf, pb);
+      }
+      ++t;
+    }
   }
 
+  {
+    const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(l), __float_as_uint(l), false, false);
+    l = __uint_as_float(x[0]) + __uint_as_float(x[1]);
+  }
+  if (qvalid) {
+    const float inv = 1.0f / l;
+    bf16* Oq = O + head * (long)N * D + (long)q * D;
 #pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    const float inv = 1.0f / accl[qt][0];
-    const int q = I * BLK + (wave * QT + qt) * 16 + lr;
-    if (q < N) {
+    for (int w = 0; w < 4; ++w)
 #pragma unroll
-      for (int w = 0; w < 8; ++w) {
+      for (int j = 0; j < 4; ++j) {
         bf16x4 o;
 #pragma unroll
-        for (int v = 0; v < 4; ++v) o[v] = (bf16)(acc[qt][w][v] * inv);
-        *reinterpret_cast<bf16x4*>(Oh + (long)q * D + 16 * w + 4 * g) = o;
+        for (int i = 0; i < 4; ++i) o[i] = (bf16)(acc[w][4 * j + i] * inv);
+        *reinterpret_cast<bf16x4*>(Oq + 32 * w + 8 * j + 4 * hh) = o;
       }
-    }
   }
 }
 
@@ -319,15 +430,30 @@ __global__ __launch_bounds__(128) void sparse_simple_kernel(int N, int block, in
   }
 }
 
-template <int BLK, int NBUF>
-hipError_t launch_pipe(const Shape& s, const void* Qr, const void* Kr, const void* V, int keep,
-                       const int32_t* idx, float scale, void* Os, hipStream_t st) {
+template <int BLK, int G, int NBUF, int TAB>
+hipError_t launch_bf16_tab(const Shape& s, const void* Qr, const void* Kr, const void* V,
+                       const int32_t* lists, int list_len, int list_stride, float scale, void* Os,
+                       hipStream_t st) {
   const int nb = num_blocks(s.N, BLK);
-  const int total = nb * s.H * s.B;
-  hipLaunchKernelGGL((sparse_pipe_kernel<BLK, NBUF>), dim3(total), dim3(BLK * 2), 0, st, s.N, nb, keep,
-                     total, idx, scale * 1.4426950408889634f, (const bf16*)Qr, (const bf16*)Kr,
-                     (const bf16*)V, (bf16*)Os);
+  const int ngroups = (nb + G - 1) / G;
+  const int total = ngroups * s.H * s.B;
+  hipLaunchKernelGGL((sparse_attn_kernel<BLK, G, NBUF, TAB>), dim3(total), dim3(G * BLK * 2), 0, st,
+                     s.N, nb, ngroups, total, lists, list_len, list_stride,
+                     scale * 1.4426950408889634f, (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V,
+                     (bf16*)Os);
   return hipGetLastError();
+}
+
+// Lists of up to kTable entries go through the LDS table; longer ones through scalar loads.
+constexpr int kTable = 1024;
+template <int BLK, int G, int NBUF>
+hipError_t launch_bf16(const Shape& s, const void* Qr, const void* Kr, const void* V,
+                       const int32_t* lists, int list_len, int list_stride, float scale, void* Os,
+                       hipStream_t st) {
+  const int max_len = G == 2 ? list_stride - 1 : list_len;
+  if (lists && max_len <= kTable)
+    return launch_bf16_tab<BLK, G, NBUF, kTable>(s, Qr, Kr, V, lists, list_len, list_stride, scale, Os, st);
+  return launch_bf16_tab<BLK, G, NBUF, 0>(s, Qr, Kr, V, lists, list_len, list_stride, scale, Os, st);
 }
 
 template <typename T, int D>
@@ -339,19 +465,38 @@ hipError_t launch_simple(const Shape& s, const void* Qr, const void* Kr, const v
   return hipGetLastError();
 }
 
+bool uses_pairs(const Shape& s, int block) { return s.bf16 && block == 64 && ROLA_B64_GROUP == 2; }
+
 }  // namespace
+
+size_t sparse_workspace_bytes(const Shape& s, int block, int keep) {
+  if (!uses_pairs(s, block)) return 0;
+  const long npairs = (num_blocks(s.N, block) + 1) / 2;
+  return (size_t)s.B * s.H * npairs * (2 * (size_t)keep + 1) * sizeof(int32_t);
+}
 
 hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, const void* V,
                               int block, int keep, const int32_t* idx, float scale, void* Os,
-                              hipStream_t st) {
+                              void* ws, hipStream_t st) {
   if (s.bf16) {
-    // Three LDS stages for gathered blocks (latency of scattered K/V reads); the dense walk, whose
-    // reads are L2-friendly, keeps two stages and the higher occupancy.
-    if (block == 64)
-      return idx ? launch_pipe<64, 3>(s, Qr, Kr, V, keep, idx, scale, Os, st)
-                 : launch_pipe<64, 2>(s, Qr, Kr, V, keep, idx, scale, Os, st);
-    return idx ? launch_pipe<128, ROLA_B128_NBUF>(s, Qr, Kr, V, keep, idx, scale, Os, st)
-               : launch_pipe<128, 2>(s, Qr, Kr, V, keep, idx, scale, Os, st);
+    const int nb = num_blocks(s.N, block);
+    if (block == 64) {
+      if (!idx) return launch_bf16<64, 1, 3>(s, Qr, Kr, V, nullptr, nb, 0, scale, Os, st);
+      if (ws && uses_pairs(s, block)) {
+        const int npairs = (nb + 1) / 2, stride = 2 * keep + 1;
+        const int words = (nb + 31) / 32;
+        hipLaunchKernelGGL(pair_union_kernel, dim3(npairs * s.H * s.B), dim3(256),
+                           (2 * words + 256) * sizeof(uint32_t), st, nb, keep, npairs, stride, idx,
+                           (int32_t*)ws);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        return launch_bf16<64, 2, ROLA_B64_NBUF>(s, Qr, Kr, V, (const int32_t*)ws, 0, stride, scale,
+                                                 Os, st);
+      }
+      return launch_bf16<64, 1, 3>(s, Qr, Kr, V, idx, keep, keep, scale, Os, st);
+    }
+    if (!idx) return launch_bf16<128, 1, 3>(s, Qr, Kr, V, nullptr, nb, 0, scale, Os, st);
+    return launch_bf16<128, 1, 3>(s, Qr, Kr, V, idx, keep, keep, scale, Os, st);
   }
   if (s.d == 64) return launch_simple<float, 64>(s, Qr, Kr, V, block, keep, idx, scale, Os, st);
   return launch_simple<float, 128>(s, Qr, Kr, V, block, keep, idx, scale, Os, st);

@@ -39,7 +39,8 @@ SIGNATURES = {
     "rola_rope_tables": (_i32, [_PP, _i32, _i32, _i32, _f64, _i32, _i32, _i32, _p, _p, _p]),
     "rola_rope_apply": (_i32, [_PP, _p, _p, _p, _i32, _p, _p]),
     "rola_block_select": (_i32, [_PP, _p, _p, _i32, _f64, _p, _p, _sz, _p]),
-    "rola_sparse_attn": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p]),
+    "rola_sparse_workspace_bytes": (_sz, [_PP, _i32, _f64]),
+    "rola_sparse_attn": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p, _sz, _p]),
     "rola_dense_attn": (_i32, [_PP, _p, _p, _p, _i32, _f32, _p, _p]),
     "rola_lowrank_summary": (_i32, [_PP, _p, _p, _p, _i32, _p, _p, _i32, _p, _p, _p, _sz, _p]),
     "rola_lowrank_readout": (_i32, [_PP, _p, _p, _i32, _p, _p, _i32, _p, _f32, _p, _p]),
@@ -115,6 +116,10 @@ def select_workspace_bytes(prob: Problem, block: int) -> int:
     return LIB.rola_select_workspace_bytes(ctypes.byref(prob), block)
 
 
+def sparse_workspace_bytes(prob: Problem, block: int, sparsity: float) -> int:
+    return LIB.rola_sparse_workspace_bytes(ctypes.byref(prob), block, sparsity)
+
+
 def summary_workspace_bytes(prob: Problem, r: int) -> int:
     return LIB.rola_summary_workspace_bytes(ctypes.byref(prob), r)
 
@@ -156,13 +161,20 @@ def rola_block_select(Qr, Kr, grid, block, sparsity, out=None, ws=None, stream=N
     return out
 
 
-def rola_sparse_attn(Qr, Kr, V, grid, block, sparsity, blk_idx, scale=None, out=None, stream=None):
+def rola_sparse_attn(Qr, Kr, V, grid, block, sparsity, blk_idx, scale=None, out=None, ws=None,
+                     stream=None, share=True):
+    """share=False passes no workspace: each workgroup then serves one query block."""
     _act(Qr, "Qr")
     prob = problem_of(Qr, grid)
     scale = prob.d_h ** -0.5 if scale is None else scale
     out = torch.empty_like(Qr) if out is None else out
+    if ws is None and share:
+        need = sparse_workspace_bytes(prob, block, sparsity)
+        ws = torch.empty(need, dtype=torch.uint8, device=Qr.device) if need else None
     _check(LIB.rola_sparse_attn(ctypes.byref(prob), _ptr(Qr), _ptr(Kr), _ptr(V), block, sparsity,
-                                _ptr(blk_idx), scale, _ptr(out), _stream(stream)), "rola_sparse_attn")
+                                _ptr(blk_idx), scale, _ptr(out), _ptr(ws) if ws is not None else None,
+                                ws.numel() if ws is not None else 0, _stream(stream)),
+           "rola_sparse_attn")
     return out
 
 

@@ -55,6 +55,12 @@ def test_workspace_helpers():
     assert R.summary_workspace_bytes(p, 33) == 0         # odd rank
     bad = R.problem(1, 40, 75601, 128, (21, 45, 80), "bf16")
     assert R.select_workspace_bytes(bad, 64) == 0
+    # pair-union lists: per (b, h, pair of query blocks) a count and at most 2 * keep entries
+    keep = O.keep_blocks(nb, 0.9)
+    assert R.sparse_workspace_bytes(p, 64, 0.9) == 4 * 40 * ((nb + 1) // 2) * (2 * keep + 1)
+    assert R.sparse_workspace_bytes(p, 128, 0.9) == 0    # 128-token blocks share nothing
+    assert R.sparse_workspace_bytes(R.problem(1, 2, 256, 64, (1, 16, 16), "f32"), 64, 0.5) == 0
+    assert R.sparse_workspace_bytes(bad, 64, 0.9) == 0
 
 
 def test_status_strings():
@@ -79,11 +85,13 @@ def test_invalid_arguments_are_rejected_before_launch():
     ok = R.problem(1, 2, 75600, 128, g, "bf16")
     P = ctypes.byref
     cases = [
-        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn", P(ok), None, FAKE, FAKE, 64, 0.9, FAKE, 0.1, FAKE, None),
-        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn", P(ok), MIS, FAKE, FAKE, 64, 0.9, FAKE, 0.1, FAKE, None),
-        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn", P(ok), FAKE, FAKE, FAKE, 64, 1.0, FAKE, 0.1, FAKE, None),
-        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn", P(ok), FAKE, FAKE, FAKE, 64, 0.9, FAKE, -1.0, FAKE, None),
-        (R.ROLA_ERR_UNSUPPORTED, "rola_sparse_attn", P(ok), FAKE, FAKE, FAKE, 32, 0.9, FAKE, 0.1, FAKE, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn", P(ok), None, FAKE, FAKE, 64, 0.9, FAKE, 0.1, FAKE, None, 0, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn", P(ok), MIS, FAKE, FAKE, 64, 0.9, FAKE, 0.1, FAKE, None, 0, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn", P(ok), FAKE, FAKE, FAKE, 64, 1.0, FAKE, 0.1, FAKE, None, 0, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn", P(ok), FAKE, FAKE, FAKE, 64, 0.9, FAKE, -1.0, FAKE, None, 0, None),
+        (R.ROLA_ERR_UNSUPPORTED, "rola_sparse_attn", P(ok), FAKE, FAKE, FAKE, 32, 0.9, FAKE, 0.1, FAKE, None, 0, None),
+        (R.ROLA_ERR_WORKSPACE, "rola_sparse_attn", P(ok), FAKE, FAKE, FAKE, 64, 0.9, FAKE, 0.1, FAKE, FAKE, 64, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn", P(ok), FAKE, FAKE, FAKE, 64, 0.9, FAKE, 0.1, FAKE, MIS, 1 << 40, None),
         (R.ROLA_ERR_UNSUPPORTED, "rola_dense_attn", P(ok), FAKE, FAKE, FAKE, 96, 0.1, FAKE, None),
         (R.ROLA_ERR_INVALID_ARGUMENT, "rola_block_select", P(R.problem(1, 2, 75601, 128, g, "bf16")),
          FAKE, FAKE, 64, 0.9, FAKE, FAKE, 1 << 40, None),

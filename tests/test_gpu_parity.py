@@ -147,6 +147,42 @@ def test_dense_reference_kernel(dtype, grid, block):
         T.assert_close(T.to_np(out[0, h]), want, w.dtype, "dense")
 
 
+@pytest.mark.parametrize("grid,s", [((3, 10, 13), 0.5), ((2, 9, 20), 0.7), ((4, 8, 16), 0.0)],
+                         ids=["odd-nb", "batchlike", "keep-all"])
+def test_sparse_shared_loads(grid, s):
+    """The path in which adjacent query blocks share K/V loads (merged block lists) against the
+    one-block-per-workgroup path and the oracle, on random block lists: ascending lists visit the
+    same blocks in the same order on both paths (bitwise equal results); shuffled lists are valid
+    input too (any order) and must still match the oracle."""
+    w = synth.WAN_1_3B_480P.replace(grid=grid, H=2, sparsity=s)
+    inp, f64 = _inputs(w, seed=6)
+    g = w.grid
+    prob = R.problem(w.B, w.H, w.N, w.d_h, g, w.dtype)
+    cos, sin = R.rola_rope_tables(prob, w.split)
+    qr = R.rola_rope_apply(inp["Qn"], cos, sin, g)
+    kr = R.rola_rope_apply(inp["Kn"], cos, sin, g)
+    nb = O.num_blocks(w.N, 64)
+    keep = O.keep_blocks(nb, s)
+    rng = np.random.default_rng(7)
+    lists = np.stack([np.stack([rng.choice(nb, keep, replace=False) for _ in range(nb)])
+                      for _ in range(w.H)])[None]
+    ocos, osin = O.rope_tables(*g, w.split)
+    for order in ("ascending", "shuffled"):
+        idx_np = np.sort(lists, axis=-1) if order == "ascending" else lists
+        idx = torch.from_numpy(idx_np.astype(np.int32)).cuda()
+        shared = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, s, idx, share=True)
+        single = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, s, idx, share=False)
+        torch.cuda.synchronize()
+        if order == "ascending":
+            assert torch.equal(shared, single)
+        for h in range(w.H):
+            q = O.round_to(O.rotate(f64["Qn"][0, h], ocos, osin), w.dtype)
+            k = O.round_to(O.rotate(f64["Kn"][0, h], ocos, osin), w.dtype)
+            want = O.sparse_attention(q, k, f64["V"][0, h], idx_np[0, h], 64, 1.0 / math.sqrt(w.d_h))
+            T.assert_close(T.to_np(shared[0, h]), want, w.dtype, f"shared {order} h{h}")
+            T.assert_close(T.to_np(single[0, h]), want, w.dtype, f"single {order} h{h}")
+
+
 def test_exact_ties_go_to_lower_block():
     """Identical key blocks tie exactly: every row must keep the lowest block indices."""
     w = synth.WAN_1_3B_480P.replace(grid=(2, 8, 16), H=2)
