@@ -115,6 +115,127 @@ def cpu_baseline(w, inp_cpu_head0: dict, budget_s: float) -> dict:
                       f"{dt:.1f} s on {len(os.sched_getaffinity(0))} host cores"}
 
 
+def time_call(fn, reps: int, cold=None):
+    """Median, p10, p90 (ms) of fn() over reps runs, HIP events on the current stream; cold() runs
+    between the timed intervals (e.g. a scratch write that evicts the caches)."""
+    fn()
+    torch.cuda.synchronize()
+    st = torch.cuda.current_stream()
+    out = []
+    for _ in range(reps):
+        if cold is not None:
+            cold()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(st)
+        fn()
+        b.record(st)
+        b.synchronize()
+        out.append(a.elapsed_time(b))
+    return float(np.median(out)), float(np.percentile(out, 10)), float(np.percentile(out, 90))
+
+
+def sweep(reps: int) -> None:
+    """Measurement sweeps besides the headline line, printed as markdown: the 1.3B 480p layer, the
+    low-rank branch over N x r (summary and readout separately, warm and cold cache) and the sparse
+    branch over sparsity x block size with the dense reference."""
+    from paper_2609_06712_amd import rola as R
+    dev = torch.device("cuda:0")
+    scratch = torch.empty(1 << 30, dtype=torch.uint8, device=dev)   # 1 GiB: evicts L2 and MALL
+    evict = lambda: scratch.fill_(1)  # noqa: E731
+
+    # the 1.3B 480p layer (same step as the headline)
+    w = synth.WAN_1_3B_480P
+    g = w.grid
+    inp = synth.make_inputs(w, 0, device=dev)
+    prob = R.problem(w.B, w.H, w.N, w.d_h, g, w.dtype)
+    cos, sin = R.rola_rope_tables(prob, w.split, w.base)
+    qr = R.rola_rope_apply(inp["Qn"], cos, sin, g)
+    kr = R.rola_rope_apply(inp["Kn"], cos, sin, g)
+    ws_sp = torch.empty(max(R.sparse_workspace_bytes(prob, w.block, w.sparsity), 16), dtype=torch.uint8,
+                        device=dev)
+    idx = R.rola_block_select(qr, kr, g, w.block, w.sparsity)
+    o_s = torch.empty_like(qr)
+
+    def layer():
+        R.rola_block_select(qr, kr, g, w.block, w.sparsity, out=idx)
+        R.rola_sparse_attn(qr, kr, inp["V"], g, w.block, w.sparsity, idx, out=o_s, ws=ws_sp)
+        C, _ = R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], w.r, cos, sin, g)
+        R.rola_lowrank_readout_combine(inp["Qn"], inp["Pq"], w.r, cos, sin, C, o_s, inp["logits"], g)
+    ms, lo, hi = time_call(layer, reps)
+    f = sparse_flops_performed(idx, w.N, w.block, w.d_h) + 8.0 * w.B * w.H * w.N * w.d_h * w.r
+    print(f"## Layer, {w.name}\n\n| ms (median) | p10 | p90 | eff. TFLOP/s |\n|---|---|---|---|")
+    print(f"| {ms:.3f} | {lo:.3f} | {hi:.3f} | {f / ms / 1e9:.1f} |\n", flush=True)
+    del inp, qr, kr, idx, o_s
+
+    # low-rank branch: N x r, summary and readout separately (warm / cold cache)
+    print("## Low-rank branch, H40 d128 bf16 (HBM roofline 8 TB/s)\n")
+    print("| N | r | kernel | bytes (MB) | warm ms | warm GB/s | cold ms | cold GB/s | cold % of 8 TB/s |")
+    print("|---|---|---|---|---|---|---|---|---|", flush=True)
+    for N in (8400, 32760, 75600):
+        for r in (16, 32, 64):
+            w = synth.lowrank_sweep(N, r)
+            g = w.grid
+            inp = synth.make_inputs(w, 0, device=dev)
+            prob = R.problem(w.B, w.H, w.N, w.d_h, g, w.dtype)
+            cos, sin = R.rola_rope_tables(prob, w.split, w.base)
+            tensor = w.B * w.H * w.N * w.d_h * 2
+            tables = 2 * w.N * (r // 2) * 4
+            C, z = R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], r, cos, sin, g)
+            ws = torch.empty(R.summary_workspace_bytes(prob, r), dtype=torch.uint8, device=dev)
+            olr = torch.empty_like(inp["Qn"])
+            out = torch.empty_like(inp["Qn"])
+            cases = [
+                ("summary", 2 * tensor + tables,
+                 lambda: R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], r, cos, sin, g, C=C,
+                                                z=z, ws=ws)),
+                ("readout", 2 * tensor + tables,
+                 lambda: R.rola_lowrank_readout(inp["Qn"], inp["Pq"], r, cos, sin, C, g, out=olr)),
+                ("readout+combine", 3 * tensor + tables,
+                 lambda: R.rola_lowrank_readout_combine(inp["Qn"], inp["Pq"], r, cos, sin, C, inp["V"],
+                                                        inp["logits"], g, out=out)),
+            ]
+            for name, nbytes, fn in cases:
+                wm = time_call(fn, reps)[0]
+                cm = time_call(fn, reps, cold=evict)[0]
+                print(f"| {N} | {r} | {name} | {nbytes / 1e6:.0f} | {wm:.4f} | {nbytes / wm / 1e6:.0f} | "
+                      f"{cm:.4f} | {nbytes / cm / 1e6:.0f} | {100 * nbytes / cm / 1e6 / PEAK_HBM_GBS:.1f} |",
+                      flush=True)
+            del inp, C, z, ws, olr, out
+    print()
+
+    # sparse branch: sparsity x block, dense reference
+    print("## Sparse branch, H40 d128 N75600 bf16 (MFMA roofline 2.5 PFLOP/s)\n")
+    print("| block | sparsity | keep | select ms | sparse ms | TFLOP/s performed | % of peak | "
+          "sparse/dense time | keep/n_b |")
+    print("|---|---|---|---|---|---|---|---|---|", flush=True)
+    base = synth.sparse_sweep(0.9, 64)
+    inp = synth.make_inputs(base, 0, device=dev)
+    g = base.grid
+    prob = R.problem(base.B, base.H, base.N, base.d_h, g, base.dtype)
+    cos, sin = R.rola_rope_tables(prob, base.split, base.base)
+    qr = R.rola_rope_apply(inp["Qn"], cos, sin, g)
+    kr = R.rola_rope_apply(inp["Kn"], cos, sin, g)
+    o_s = torch.empty_like(qr)
+    for block in (64, 128):
+        nb = R.num_blocks(base.N, block)
+        dense_ms = time_call(lambda: R.rola_dense_attn(qr, kr, inp["V"], g, block, out=o_s), max(3, reps // 4))[0]
+        f_dense = 4.0 * base.B * base.H * base.N * base.N * base.d_h
+        for s in (0.8, 0.9, 0.95):
+            keep = R.keep_blocks(nb, s)
+            idx = R.rola_block_select(qr, kr, g, block, s)
+            ws = torch.empty(max(R.sparse_workspace_bytes(prob, block, s), 16), dtype=torch.uint8,
+                             device=dev)
+            sel_ms = time_call(lambda: R.rola_block_select(qr, kr, g, block, s, out=idx), reps)[0]
+            sp_ms = time_call(lambda: R.rola_sparse_attn(qr, kr, inp["V"], g, block, s, idx, out=o_s,
+                                                         ws=ws), reps)[0]
+            f = sparse_flops_performed(idx, base.N, block, base.d_h)
+            print(f"| {block} | {s} | {keep} | {sel_ms:.3f} | {sp_ms:.3f} | {f / sp_ms / 1e9:.1f} | "
+                  f"{100 * f / sp_ms / 1e9 / PEAK_BF16_TFLOPS:.1f} | {sp_ms / dense_ms:.4f} | "
+                  f"{keep / nb:.4f} |", flush=True)
+        print(f"| {block} | dense | {nb} | - | {dense_ms:.3f} | {f_dense / dense_ms / 1e9:.1f} | "
+              f"{100 * f_dense / dense_ms / 1e9 / PEAK_BF16_TFLOPS:.1f} | 1 | 1 |", flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -122,6 +243,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep", action="store_true",
+                    help="print the measurement sweeps (1.3B layer, low-rank N x r, sparse S x block) "
+                         "as markdown instead of the JSON line")
+    ap.add_argument("--sweep-reps", type=int, default=10)
     ap.add_argument("--calibration-copy", action="store_true",
                     help="one untimed device copy of one activation tensor (counter calibration)")
     args = ap.parse_args()
@@ -133,6 +258,9 @@ def main():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(2)
 
+    if args.sweep:
+        sweep(args.sweep_reps)
+        return
     from paper_2609_06712_amd import rola as R
 
     w = synth.WAN_14B_720P

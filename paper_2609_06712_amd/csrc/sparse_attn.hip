@@ -5,7 +5,7 @@
 //
 // bf16 path (d_h = 128). A workgroup serves G = 1 or 2 consecutive query blocks of BLK tokens, with
 // BLK/32 waves of 32 queries per query block. With G = 2 it walks the ascending union of the two
-// blocks' lists (built by pair_union_kernel): a key block both hold is fetched into LDS once, and
+// blocks' lists (built by group_union_kernel): a key block both hold is fetched into LDS once, and
 // each wave computes only on the blocks its own query block selected. Adjacent query blocks share
 // about half of their selections, so this cuts the K/V bytes that cross L2 by about a quarter.
 // Keys stream in 32-key sub-tiles through NBUF LDS stages filled by direct global-to-LDS loads.
@@ -31,6 +31,9 @@
 #ifndef ROLA_B64_NBUF
 #define ROLA_B64_NBUF 3  // its LDS stages (16 KB each)
 #endif
+#ifndef ROLA_B64_WAVE_Q
+#define ROLA_B64_WAVE_Q 32  // queries per wave of that kernel: 32 (32x32 MFMA) or 16 (16x16 MFMA)
+#endif
 
 namespace rola {
 namespace {
@@ -49,24 +52,25 @@ __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const
 __device__ __forceinline__ int k_swizzle(int row) { return row & 15; }
 __device__ __forceinline__ int v_swizzle(int row) { return 2 * ((0x6530 >> (4 * (row & 3))) & 15); }
 
-// Pairs of adjacent query blocks share a workgroup of the attention kernel. For each (b, h, pair)
-// this writes the entry count and then the ascending union of the two block lists, each entry
-// J | (bit 0: the first block selected J, bit 1: the second) << 16. Built through a bitmap, so the
-// lists may come in any order; out-of-range entries are dropped, as the attention skips them.
-__global__ __launch_bounds__(256) void pair_union_kernel(int nb, int keep, int npairs, int stride,
-                                                         const int32_t* __restrict__ idx,
-                                                         int32_t* __restrict__ out) {
+// G consecutive query blocks share a workgroup of the attention kernel. For each (b, h, group)
+// this writes the entry count and then the ascending union of the G block lists, each entry
+// J | (bit i: query block i of the group selected J) << 16. Built through bitmaps, so the lists may
+// come in any order; out-of-range entries are dropped, as the attention skips them.
+template <int G>
+__global__ __launch_bounds__(256) void group_union_kernel(int nb, int keep, int ngroups, int stride,
+                                                          const int32_t* __restrict__ idx,
+                                                          int32_t* __restrict__ out) {
   extern __shared__ uint32_t sh[];
   const int words = (nb + 31) >> 5;
-  uint32_t* bits = sh;                       // [2][words]: membership of each list
-  int* scan = reinterpret_cast<int*>(sh + 2 * words);  // [256]
+  uint32_t* bits = sh;                                 // [G][words]: membership of each list
+  int* scan = reinterpret_cast<int*>(sh + G * words);  // [256]
   const long gp = blockIdx.x;
-  const long head = gp / npairs;
-  const int I0 = 2 * (int)(gp % npairs);
+  const long head = gp / ngroups;
+  const int I0 = G * (int)(gp % ngroups);
   const int tid = threadIdx.x;
-  for (int w = tid; w < 2 * words; w += 256) bits[w] = 0u;
+  for (int w = tid; w < G * words; w += 256) bits[w] = 0u;
   __syncthreads();
-  for (int b = 0; b < 2 && I0 + b < nb; ++b) {
+  for (int b = 0; b < G && I0 + b < nb; ++b) {
     const int32_t* sel = idx + (head * nb + I0 + b) * (long)keep;
     for (int i = tid; i < keep; i += 256) {
       const int J = sel[i];
@@ -76,7 +80,12 @@ __global__ __launch_bounds__(256) void pair_union_kernel(int nb, int keep, int n
   __syncthreads();
   const int per = (words + 255) / 256, w0 = min(words, tid * per), w1 = min(words, w0 + per);
   int cnt = 0;
-  for (int w = w0; w < w1; ++w) cnt += __popc(bits[w] | bits[words + w]);
+  for (int w = w0; w < w1; ++w) {
+    uint32_t u = 0;
+#pragma unroll
+    for (int b = 0; b < G; ++b) u |= bits[b * words + w];
+    cnt += __popc(u);
+  }
   scan[tid] = cnt;
   __syncthreads();
   for (int off = 1; off < 256; off <<= 1) {  // inclusive scan of the per-thread counts
@@ -89,23 +98,29 @@ __global__ __launch_bounds__(256) void pair_union_kernel(int nb, int keep, int n
   if (tid == 255) o[0] = scan[255];
   int pos = 1 + scan[tid] - cnt;
   for (int w = w0; w < w1; ++w) {
-    const uint32_t a = bits[w], b = bits[words + w];
-    for (uint32_t u = a | b; u; u &= u - 1) {
+    uint32_t m[G], u = 0;
+#pragma unroll
+    for (int b = 0; b < G; ++b) u |= (m[b] = bits[b * words + w]);
+    for (; u; u &= u - 1) {
       const int bit = __ffs(u) - 1;
-      o[pos++] = (w * 32 + bit) | (int)((((a >> bit) & 1u) | (((b >> bit) & 1u) << 1)) << 16);
+      uint32_t mask = 0;
+#pragma unroll
+      for (int b = 0; b < G; ++b) mask |= ((m[b] >> bit) & 1u) << b;
+      o[pos++] = (w * 32 + bit) | (int)(mask << 16);
     }
   }
 }
 
 // bf16 attention kernel: one workgroup per (b, h, G consecutive query blocks); see the file comment.
-// lists: G = 1: the block lists [B, H, nb, list_stride] (list_len entries used; nullptr: every key
-//        block in order); G = 2: pair_union_kernel output, list_stride ints per (b, h, pair).
+// lists: G = 1: the block lists [B, H, nb, list_stride] (list_len entries used); G > 1:
+//        group_union_kernel output, list_stride ints per (b, h, group); nullptr: every key block in
+//        order for all query blocks of the group (list_len = nb).
 template <int BLK, int G, int NBUF, int TAB>
 __global__ __launch_bounds__(G * BLK * 2, 2) void sparse_attn_kernel(
     int N, int nb, int ngroups, int total, const int32_t* __restrict__ lists, int list_len,
     int list_stride, float scale_log2, const bf16* __restrict__ Q, const bf16* __restrict__ K,
     const bf16* __restrict__ V, bf16* __restrict__ O) {
-  static_assert(G == 1 || G == 2, "one or two query blocks per workgroup");
+  static_assert(G == 1 || G == 2 || G == 4, "one, two or four query blocks per workgroup");
   static_assert(NBUF >= 3, "loads of later sub-tiles stay in flight during a step");
   constexpr int D = 128, WPB = BLK / 32, NW = G * WPB;
   constexpr int TILE = kSub * D * 2;              // 8 KB: K (or V) of one sub-tile
@@ -136,7 +151,7 @@ __global__ __launch_bounds__(G * BLK * 2, 2) void sparse_attn_kernel(
   typedef const __attribute__((address_space(4))) int32_t* const_i32;
   const int32_t* glist = nullptr;
   int E = list_len;
-  if (G == 2) {
+  if (lists && G > 1) {
     glist = lists + (head * ngroups + grp) * (long)list_stride;
     E = ((const_i32)glist)[0];
     glist += 1;
@@ -155,14 +170,14 @@ __global__ __launch_bounds__(G * BLK * 2, 2) void sparse_attn_kernel(
   // raw(e): entry e of the list (in a VGPR when it comes from the LDS table); step_of decodes the
   // entry of sub-tile t.
   auto raw = [&](int e) -> int {
-    if (!glist) return e;
+    if (!glist) return G > 1 ? (e | (((1 << G) - 1) << 16)) : e;  // dense: every block, all
     const int i = min(e, max(E - 1, 0));
     return TAB > 0 ? tab[i] : (int)slist[i];
   };
   auto step_of = [&](int v, int t) {
     v = TAB > 0 ? wave_uniform(v) : v;
-    const int J = G == 2 ? (v & 0xFFFF) : v;
-    const int mask = G == 2 ? (v >> 16) : 1;
+    const int J = G > 1 ? (v & 0xFFFF) : v;
+    const int mask = G > 1 ? (v >> 16) : 1;
     return Step{(unsigned)J < (unsigned)nb ? J * BLK + (t % SUBS) * kSub : -1, mask};
   };
   auto active = [&](const Step& s) { return (s.mask & mybit) && s.k0 >= 0 && s.k0 < N; };
@@ -363,6 +378,227 @@ __global__ __launch_bounds__(G * BLK * 2, 2) void sparse_attn_kernel(
   }
 }
 
+// bf16 attention kernel with 16-query waves (v_mfma_f32_16x16x32_bf16): one workgroup per (b, h,
+// G consecutive query blocks), BLK/16 waves per query block. A wave holds about a hundred VGPRs,
+// so sixteen waves share a CU; this makes groups of four query blocks (whose list union saves about
+// 45 % of the K/V bytes of single blocks) affordable although each wave computes on only about half
+// of the union. Per wave and 32-key sub-tile:
+//   S^T = K Q^T   two 16-key tiles x four 32-channel k-steps; lane (c = l%16, g = l/16) receives
+//                 keys 4g+v of each tile for query c, so a row max takes two permlane swaps;
+//   P = exp2(S^T * scale*log2e - m) in bf16, the B operand of O^T = V^T P^T (eight 16-channel
+//                 tiles; V^T through ds_read_b64_tr_b16 of row-major V, keys in the order S^T hands
+//                 them out), row sums from one more MFMA against ones.
+// K rows are stored with chunk ^ row%16 and V rows with chunk ^ 2(row%8), which makes the operand
+// reads (16 rows per pass) and the transposing reads (8 rows per pass) bank-conflict free.
+template <int BLK, int G, int NBUF, int TAB>
+__global__ __launch_bounds__(G * BLK * 4) void sparse_attn16_kernel(
+    int N, int nb, int ngroups, int total, const int32_t* __restrict__ lists, int list_len,
+    int list_stride, float scale_log2, const bf16* __restrict__ Q, const bf16* __restrict__ K,
+    const bf16* __restrict__ V, bf16* __restrict__ O) {
+  static_assert(G == 1 || G == 2 || G == 4, "one, two or four query blocks per workgroup");
+  static_assert(NBUF >= 3, "loads of later sub-tiles stay in flight during a step");
+  constexpr int D = 128, WPB = BLK / 16, NW = G * WPB, NT = NW * 64;
+  constexpr int TILE = kSub * D * 2;   // 8 KB: K (or V) of one sub-tile
+  constexpr int STAGE = 2 * TILE;      // K then V
+  constexpr int SLOTS = STAGE / 1024;  // 1-KB direct loads per stage (K: 0-7, V: 8-15)
+  static_assert(SLOTS % NW == 0, "whole loads per wave");
+  constexpr int SPW = SLOTS / NW;      // loads per wave per sub-tile
+  constexpr int SUBS = BLK / kSub;     // sub-tiles per key block
+  __shared__ __attribute__((aligned(1024))) char lds[NBUF * STAGE];
+  __shared__ int tab[TAB > 0 ? TAB : 1];
+
+  const int L = xcd_remap(blockIdx.x, total);
+  const int grp = L % ngroups;
+  const long head = L / ngroups;
+  const int tid = threadIdx.x, lane = tid % 64, lr = lane % 16, g = lane / 16;
+  const int wave = wave_uniform(tid / 64);
+  const int qb = wave / WPB;
+  const int I = grp * G + qb;
+  const int q = I * BLK + (wave % WPB) * 16 + lr;  // this lane's query (column of S^T, O^T)
+  const bool qvalid = I < nb && q < N;
+  const int mybit = 1 << qb;
+  const bf16* Qh = Q + head * (long)N * D;
+  const char* Kh = reinterpret_cast<const char*>(K + head * (long)N * D);
+  const char* Vh = reinterpret_cast<const char*>(V + head * (long)N * D);
+
+  // The block list (as in sparse_attn_kernel): LDS table read a step ahead, or scalar loads.
+  typedef const __attribute__((address_space(4))) int32_t* const_i32;
+  const int32_t* glist = nullptr;
+  int E = list_len;
+  if (lists && G > 1) {
+    glist = lists + (head * ngroups + grp) * (long)list_stride;
+    E = ((const_i32)glist)[0];
+    glist += 1;
+  } else if (lists) {
+    glist = lists + (head * nb + grp) * (long)list_stride;
+  }
+  const const_i32 slist = (const_i32)glist;
+  const int T = E * SUBS;
+  if (TAB > 0 && glist)
+    for (int i = tid; i < E; i += NT) tab[i] = glist[i];
+  struct Step {
+    int k0, mask;
+  };
+  auto raw = [&](int e) -> int {
+    if (!glist) return G > 1 ? (e | (((1 << G) - 1) << 16)) : e;  // dense: every block, all
+    const int i = min(e, max(E - 1, 0));
+    return TAB > 0 ? tab[i] : (int)slist[i];
+  };
+  auto step_of = [&](int v, int t) {
+    v = TAB > 0 ? wave_uniform(v) : v;
+    const int J = G > 1 ? (v & 0xFFFF) : v;
+    const int mask = G > 1 ? (v >> 16) : 1;
+    return Step{(unsigned)J < (unsigned)nb ? J * BLK + (t % SUBS) * kSub : -1, mask};
+  };
+  auto active = [&](const Step& s) { return (s.mask & mybit) && s.k0 >= 0 && s.k0 < N; };
+
+  bf16x8 qf[4];  // Q^T fragments of the four k-steps (d = 32kc + 8g .. +7)
+#pragma unroll
+  for (int kc = 0; kc < 4; ++kc)
+    qf[kc] = qvalid ? *reinterpret_cast<const bf16x8*>(Qh + (long)q * D + 32 * kc + 8 * g) : bf16x8{};
+  __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0): Q and the list are in registers
+  if (TAB > 0) __syncthreads();
+
+  f32x4 acc[8], accl = f32x4{0.f, 0.f, 0.f, 0.f};  // O^T tiles and the row sums
+  float m = -INFINITY;
+#pragma unroll
+  for (int w = 0; w < 8; ++w) acc[w] = f32x4{0.f, 0.f, 0.f, 0.f};
+  bf16x8 ones;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) ones[i] = (bf16)1.0f;
+
+  // DMA: slot s of a stage fills rows 4(s%8) .. +3 of K (s < 8) or V; lane l fills row
+  // 4(s%8) + l/16 at chunk position l%16 with source chunk (position ^ swizzle(row)).
+  uint32_t dsrc[SPW];
+#pragma unroll
+  for (int i = 0; i < SPW; ++i) {
+    const int slot = wave * SPW + i, row = 4 * (slot % 8) + lane / 16, pos = lane % 16;
+    const int sw = slot < 8 ? (row & 15) : ((row & 7) << 1);
+    dsrc[i] = row * D * 2 + ((pos ^ sw) << 4);
+  }
+  int ko[2][4];
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+    for (int kc = 0; kc < 4; ++kc) {
+      const int row = 16 * kt + lr;
+      ko[kt][kc] = row * 256 + (((4 * kc + g) ^ (row & 15)) << 4);
+    }
+  const int sp = lr >> 2, mp = lr & 3, vr = 4 * g + sp;
+  int vo[8];
+#pragma unroll
+  for (int w = 0; w < 8; ++w)
+    vo[w] = TILE + vr * 256 + (((2 * w + (mp >> 1)) ^ ((vr & 7) << 1)) << 4) + ((mp & 1) << 3);
+
+  const uint32_t lds0 = lds_address(lds);
+  auto issue = [&](const Step& s, int buf) {  // always SPW loads per wave (fixed vmcnt per step)
+    const int k0 = max(s.k0, 0);
+    const uint32_t dst = lds0 + buf * STAGE;
+#pragma unroll
+    for (int i = 0; i < SPW; ++i) {
+      const int slot = wave * SPW + i;
+      const char* base = slot < 8 ? Kh : Vh;
+      const uint32_t d = dst + (slot < 8 ? 0 : TILE) + (slot % 8) * 1024;
+      if (k0 + kSub <= N) {
+        dma16(base + (long)k0 * D * 2, dsrc[i], d);
+      } else {  // ragged tail: rows past N re-read row N-1 (a valid key; its probabilities are zeroed)
+        const int r = 4 * (slot % 8) + lane / 16;
+        dma16(base, (uint32_t)(min(k0 + r, N - 1) - r) * (D * 2) + dsrc[i], d);
+      }
+    }
+  };
+
+  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+  auto compute = [&](const char* base, int k0) {
+    bf16x8 kf[4][2];
+#pragma unroll
+    for (int kc = 0; kc < 4; ++kc)
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) kf[kc][kt] = *reinterpret_cast<const bf16x8*>(base + ko[kt][kc]);
+    f32x4 s0 = f32x4{0.f, 0.f, 0.f, 0.f}, s1 = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kc = 0; kc < 4; ++kc) {
+      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kc][0], qf[kc], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kc][1], qf[kc], s1, 0, 0, 0);
+    }
+    const float mx = fmaxf(fmaxf(fmaxf(s0[0], s0[1]), fmaxf(s0[2], s0[3])),
+                           fmaxf(fmaxf(s1[0], s1[1]), fmaxf(s1[2], s1[3])));
+    const float mt = rows_max(mx) * scale_log2;
+    if (__any(mt > m + kRescaleTau)) {  // lazy rescale, exact (see sparse_attn_kernel)
+      const float mnew = fmaxf(m, mt);
+      const float alpha = __builtin_amdgcn_exp2f(m - mnew);
+      m = mnew;
+      accl *= alpha;
+#pragma unroll
+      for (int w = 0; w < 8; ++w) acc[w] *= alpha;
+    }
+    bf16x8 pb;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      pb[v] = (bf16)__builtin_amdgcn_exp2f(fmaf(s0[v], scale_log2, -m));
+      pb[4 + v] = (bf16)__builtin_amdgcn_exp2f(fmaf(s1[v], scale_log2, -m));
+    }
+    if (k0 + kSub > N) {  // value 4kt + v holds key k0 + 16kt + 4g + v
+      const int lim = N - k0 - 4 * g;
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (16 * (k / 4) + k % 4 >= lim) pb[k] = (bf16)0.f;
+    }
+    accl = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb, accl, 0, 0, 0);
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+      const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(base + vo[w]));
+      const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(base + vo[w] + 16 * 256));
+      acc[w] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+          __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7), pb, acc[w], 0, 0, 0);
+    }
+  };
+
+  // Pipeline as in sparse_attn_kernel: wait for sub-tile t, barrier, issue t+NBUF-1, compute t.
+  int issued = 0;
+#pragma unroll
+  for (int j = 0; j < NBUF - 1; ++j)
+    if (j < T) {
+      issue(step_of(raw(j / SUBS), j), j);
+      ++issued;
+    }
+  int pi = raw(issued / SUBS), pc = raw(0);
+  for (int t = 0; t < T;) {
+#pragma unroll
+    for (int j = 0; j < NBUF; ++j) {
+      if (t >= T) break;
+      if (issued == t + NBUF - 1) {
+        constexpr int allowed = SPW * (NBUF - 2);
+        __builtin_amdgcn_s_waitcnt((allowed & 15) | ((allowed >> 4) << 14) | (7 << 4) | (15 << 8));
+      } else {
+        __builtin_amdgcn_s_waitcnt(0);
+      }
+      __syncthreads();
+      if (issued < T) {
+        issue(step_of(pi, issued), (j + NBUF - 1) % NBUF);
+        ++issued;
+      }
+      const Step cur = step_of(pc, t);
+      pi = raw(issued / SUBS);
+      pc = raw((t + 1) / SUBS);
+      if (active(cur)) compute(lds + j * STAGE, cur.k0);
+      ++t;
+    }
+  }
+
+  if (qvalid) {
+    const float inv = 1.0f / accl[0];
+    bf16* Oq = O + head * (long)N * D + (long)q * D;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+      bf16x4 o;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) o[v] = (bf16)(acc[w][v] * inv);
+      *reinterpret_cast<bf16x4*>(Oq + 16 * w + 4 * g) = o;
+    }
+  }
+}
+
 // Plain kernel for the fp32 path: one thread per query, keys streamed through LDS 32 at a time.
 template <typename T, int D>
 __global__ __launch_bounds__(128) void sparse_simple_kernel(int N, int block, int nb, int keep,
@@ -430,30 +666,37 @@ __global__ __launch_bounds__(128) void sparse_simple_kernel(int N, int block, in
   }
 }
 
-template <int BLK, int G, int NBUF, int TAB>
+template <int WAVE_Q, int BLK, int G, int NBUF, int TAB>
 hipError_t launch_bf16_tab(const Shape& s, const void* Qr, const void* Kr, const void* V,
-                       const int32_t* lists, int list_len, int list_stride, float scale, void* Os,
-                       hipStream_t st) {
+                           const int32_t* lists, int list_len, int list_stride, float scale,
+                           void* Os, hipStream_t st) {
   const int nb = num_blocks(s.N, BLK);
   const int ngroups = (nb + G - 1) / G;
   const int total = ngroups * s.H * s.B;
-  hipLaunchKernelGGL((sparse_attn_kernel<BLK, G, NBUF, TAB>), dim3(total), dim3(G * BLK * 2), 0, st,
-                     s.N, nb, ngroups, total, lists, list_len, list_stride,
-                     scale * 1.4426950408889634f, (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V,
-                     (bf16*)Os);
+  const float sl = scale * 1.4426950408889634f;
+  if constexpr (WAVE_Q == 32)
+    hipLaunchKernelGGL((sparse_attn_kernel<BLK, G, NBUF, TAB>), dim3(total), dim3(G * BLK * 2), 0,
+                       st, s.N, nb, ngroups, total, lists, list_len, list_stride, sl,
+                       (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V, (bf16*)Os);
+  else
+    hipLaunchKernelGGL((sparse_attn16_kernel<BLK, G, NBUF, TAB>), dim3(total), dim3(G * BLK * 4),
+                       0, st, s.N, nb, ngroups, total, lists, list_len, list_stride, sl,
+                       (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V, (bf16*)Os);
   return hipGetLastError();
 }
 
 // Lists of up to kTable entries go through the LDS table; longer ones through scalar loads.
 constexpr int kTable = 1024;
-template <int BLK, int G, int NBUF>
+template <int WAVE_Q, int BLK, int G, int NBUF>
 hipError_t launch_bf16(const Shape& s, const void* Qr, const void* Kr, const void* V,
                        const int32_t* lists, int list_len, int list_stride, float scale, void* Os,
                        hipStream_t st) {
-  const int max_len = G == 2 ? list_stride - 1 : list_len;
+  const int max_len = G > 1 ? list_stride - 1 : list_len;
   if (lists && max_len <= kTable)
-    return launch_bf16_tab<BLK, G, NBUF, kTable>(s, Qr, Kr, V, lists, list_len, list_stride, scale, Os, st);
-  return launch_bf16_tab<BLK, G, NBUF, 0>(s, Qr, Kr, V, lists, list_len, list_stride, scale, Os, st);
+    return launch_bf16_tab<WAVE_Q, BLK, G, NBUF, kTable>(s, Qr, Kr, V, lists, list_len, list_stride,
+                                                         scale, Os, st);
+  return launch_bf16_tab<WAVE_Q, BLK, G, NBUF, 0>(s, Qr, Kr, V, lists, list_len, list_stride, scale,
+                                                  Os, st);
 }
 
 template <typename T, int D>
@@ -465,14 +708,16 @@ hipError_t launch_simple(const Shape& s, const void* Qr, const void* Kr, const v
   return hipGetLastError();
 }
 
-bool uses_pairs(const Shape& s, int block) { return s.bf16 && block == 64 && ROLA_B64_GROUP == 2; }
+// Query blocks per workgroup when a workspace for the merged lists is given.
+int group_of(const Shape& s, int block) { return s.bf16 && block == 64 ? ROLA_B64_GROUP : 1; }
 
 }  // namespace
 
 size_t sparse_workspace_bytes(const Shape& s, int block, int keep) {
-  if (!uses_pairs(s, block)) return 0;
-  const long npairs = (num_blocks(s.N, block) + 1) / 2;
-  return (size_t)s.B * s.H * npairs * (2 * (size_t)keep + 1) * sizeof(int32_t);
+  const int G = group_of(s, block);
+  if (G == 1) return 0;
+  const long ngroups = (num_blocks(s.N, block) + G - 1) / G;
+  return (size_t)s.B * s.H * ngroups * ((size_t)G * keep + 1) * sizeof(int32_t);
 }
 
 hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, const void* V,
@@ -481,22 +726,23 @@ hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, co
   if (s.bf16) {
     const int nb = num_blocks(s.N, block);
     if (block == 64) {
-      if (!idx) return launch_bf16<64, 1, 3>(s, Qr, Kr, V, nullptr, nb, 0, scale, Os, st);
-      if (ws && uses_pairs(s, block)) {
-        const int npairs = (nb + 1) / 2, stride = 2 * keep + 1;
+      constexpr int G = ROLA_B64_GROUP;
+      if (!idx) return launch_bf16<32, 64, 2, 3>(s, Qr, Kr, V, nullptr, nb, 0, scale, Os, st);
+      if (ws && G > 1) {
+        const int ngroups = (nb + G - 1) / G, stride = G * keep + 1;
         const int words = (nb + 31) / 32;
-        hipLaunchKernelGGL(pair_union_kernel, dim3(npairs * s.H * s.B), dim3(256),
-                           (2 * words + 256) * sizeof(uint32_t), st, nb, keep, npairs, stride, idx,
+        hipLaunchKernelGGL(group_union_kernel<G>, dim3(ngroups * s.H * s.B), dim3(256),
+                           (G * words + 256) * sizeof(uint32_t), st, nb, keep, ngroups, stride, idx,
                            (int32_t*)ws);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
-        return launch_bf16<64, 2, ROLA_B64_NBUF>(s, Qr, Kr, V, (const int32_t*)ws, 0, stride, scale,
-                                                 Os, st);
+        return launch_bf16<ROLA_B64_WAVE_Q, 64, G, ROLA_B64_NBUF>(s, Qr, Kr, V, (const int32_t*)ws,
+                                                                  0, stride, scale, Os, st);
       }
-      return launch_bf16<64, 1, 3>(s, Qr, Kr, V, idx, keep, keep, scale, Os, st);
+      return launch_bf16<32, 64, 1, 3>(s, Qr, Kr, V, idx, keep, keep, scale, Os, st);
     }
-    if (!idx) return launch_bf16<128, 1, 3>(s, Qr, Kr, V, nullptr, nb, 0, scale, Os, st);
-    return launch_bf16<128, 1, 3>(s, Qr, Kr, V, idx, keep, keep, scale, Os, st);
+    if (!idx) return launch_bf16<32, 128, 1, 3>(s, Qr, Kr, V, nullptr, nb, 0, scale, Os, st);
+    return launch_bf16<32, 128, 1, 3>(s, Qr, Kr, V, idx, keep, keep, scale, Os, st);
   }
   if (s.d == 64) return launch_simple<float, 64>(s, Qr, Kr, V, block, keep, idx, scale, Os, st);
   return launch_simple<float, 128>(s, Qr, Kr, V, block, keep, idx, scale, Os, st);
