@@ -115,9 +115,11 @@ rola_status rola_block_select(const rola_problem* p, const void* Qr, const void*
  * Online softmax with fp32 statistics and accumulators; bf16 path on MFMA. scale is normally
  * 1/sqrt(d_h) (Sec. 3). Os: [B, H, N, d_h] in dtype.
  * ws: rola_sparse_workspace_bytes(p, block, sparsity) bytes of device scratch, in which the bf16
- * path with 64-token blocks merges the lists of adjacent query blocks so that they share their K/V
- * loads; ws may be NULL (ws_bytes 0), which gives the same results without that sharing. A
- * non-NULL ws smaller than needed is ROLA_ERR_WORKSPACE. */
+ * path with 64-token blocks pairs query blocks (each with the block among its next 64 whose list
+ * it shares most, up to 4064 query blocks; adjacent blocks beyond) and merges the lists of each
+ * pair so that the two share their K/V loads; ws may be NULL (ws_bytes 0), which gives the same
+ * results without that sharing (bitwise the same when every list is ascending). A non-NULL ws
+ * smaller than needed is ROLA_ERR_WORKSPACE. */
 size_t rola_sparse_workspace_bytes(const rola_problem* p, int32_t block, double sparsity);
 rola_status rola_sparse_attn(const rola_problem* p, const void* Qr, const void* Kr, const void* V,
                              int32_t block, double sparsity, const int32_t* blk_idx,

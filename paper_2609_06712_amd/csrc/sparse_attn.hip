@@ -20,6 +20,7 @@
 // (about 160), so three workgroups of four waves share a CU and the matrix and vector work of one
 // wave overlaps that of the others. O is rescaled only when a sub-tile raises a row max by more
 // than 2^8: the softmax ratio does not depend on the reference max, so this is exact.
+#include <algorithm>
 #include <climits>
 
 #include "common.h"
@@ -30,6 +31,9 @@
 #endif
 #ifndef ROLA_B64_NBUF
 #define ROLA_B64_NBUF 3  // its LDS stages (16 KB each)
+#endif
+#ifndef ROLA_B64_PAIRING
+#define ROLA_B64_PAIRING 1  // pair query blocks by list overlap (1) or take adjacent pairs (0)
 #endif
 #ifndef ROLA_B64_WAVE_Q
 #define ROLA_B64_WAVE_Q 32  // queries per wave of that kernel: 32 (32x32 MFMA) or 16 (16x16 MFMA)
@@ -52,13 +56,128 @@ __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const
 __device__ __forceinline__ int k_swizzle(int row) { return row & 15; }
 __device__ __forceinline__ int v_swizzle(int row) { return 2 * ((0x6530 >> (4 * (row & 3))) & 15); }
 
-// G consecutive query blocks share a workgroup of the attention kernel. For each (b, h, group)
-// this writes the entry count and then the ascending union of the G block lists, each entry
+// Data-adaptive pairing of query blocks (G = 2). Query blocks whose lists overlap most are put in
+// one workgroup; neighbours share about half of their selections, the best partner among the
+// following 64 blocks often shares more. The pairing changes only which query blocks share K/V
+// loads: each query block still walks its own selections in ascending order, so results are
+// bitwise those of any other pairing.
+constexpr int kPairWindow = 64;  // candidate partners of a query block: the next 64 blocks
+constexpr int kPairRows = 128;   // bitmap rows one overlap workgroup holds (64 blocks + window)
+
+// Row stride (words) of the membership bitmaps in LDS: odd, so a wave reading one word of 64
+// consecutive rows hits 64 distinct banks.
+__host__ __device__ inline int pair_row_stride(int nb) { return ((nb + 31) >> 5) | 1; }
+
+// Candidate preference of every query block, one workgroup per (head, chunk of 64 query blocks).
+// The membership bitmaps of the chunk's blocks and of the 64 after them are built in LDS from the
+// lists (out-of-range entries dropped); lane d of a wave then intersects row I with row I+1+d and
+// ranks the 64 candidates by overlap, larger first, the nearer first on equal overlap, candidates
+// past the last block after all others. pref[head][chunk][k][r] = offset d of the k-th choice of
+// query block chunk*64 + r: k-major, so that the greedy pass reads its column per lane.
+__global__ __launch_bounds__(256) void pair_rank_kernel(int nb, int keep, int nchunks,
+                                                        const int32_t* __restrict__ idx,
+                                                        uint8_t* __restrict__ pref) {
+  extern __shared__ uint32_t bits[];  // [kPairRows][rs]
+  const int words = (nb + 31) >> 5, rs = pair_row_stride(nb);
+  const long head = blockIdx.x / nchunks;
+  const int chunk = (int)(blockIdx.x % nchunks), I0 = chunk * kPairWindow;
+  const int rows = min(kPairRows, nb - I0);
+  const int tid = threadIdx.x;
+  for (int w = tid; w < kPairRows * rs; w += 256) bits[w] = 0u;
+  __syncthreads();
+  const int32_t* sel = idx + (head * nb + I0) * (long)keep;  // rows I0 .. I0+rows-1, contiguous
+  for (int e = tid; e < rows * keep; e += 256) {
+    const int J = sel[e];
+    if ((unsigned)J < (unsigned)nb) atomicOr(&bits[(e / keep) * rs + (J >> 5)], 1u << (J & 31));
+  }
+  __syncthreads();
+  const int d = tid % 64;
+  uint8_t* out = pref + (head * nchunks + chunk) * (long)(kPairWindow * kPairWindow);
+  for (int i = tid / 64; i < kPairWindow && I0 + i < nb; i += 4) {  // wave-uniform bounds
+    int key = 63 - d - 64;  // past the last block: below every valid candidate
+    if (I0 + i + 1 + d < nb) {  // then row i+1+d < rows
+      const uint32_t* a = bits + i * rs;
+      const uint32_t* b = bits + (i + 1 + d) * rs;
+      int c = 0;
+      for (int w = 0; w < words; ++w) c += __popc(a[w] & b[w]);
+      key = (c << 6) | (63 - d);
+    }
+    int rank = 0;  // keys are distinct: the ranks are a permutation of 0..63
+#pragma unroll
+    for (int o = 0; o < 64; ++o) rank += __builtin_amdgcn_readlane(key, o) > key;
+    out[rank * kPairWindow + i] = (uint8_t)d;
+  }
+}
+
+// Greedy pairing, one wave per head: query blocks are visited in ascending order; a block not yet
+// taken is paired with the untaken block among its next 64 that it ranks first, or stays alone
+// when none is left. A block is only ever taken by one of the 63 blocks before it, so block I+64
+// is always free when I is visited: every block but possibly the last gets a partner, which makes
+// exactly ceil(nb / 2) groups. pairs[head][g] = I | J << 16 (J = nb: no partner), in the order the
+// groups are formed. Lane k holds the k-th choices of a chunk's 64 blocks (64 bytes in registers,
+// the next chunk loading meanwhile); a step is a ballot over the lanes whose choice is still free
+// and a find-first-set. The table is gathered in LDS and written out at the end, so no store
+// shares the memory counter with the chunk loads.
+constexpr int kMaxPairGroups = 2032;  // ceil(4064 / 2): the most query blocks pairing serves
+__global__ __launch_bounds__(64) void pair_greedy_kernel(int nb, int ngroups, int nchunks,
+                                                         const uint8_t* __restrict__ pref,
+                                                         int32_t* __restrict__ pairs) {
+  __shared__ int32_t tbl[kMaxPairGroups];
+  const long head = blockIdx.x;
+  const int lane = threadIdx.x;
+  const uint4* src = reinterpret_cast<const uint4*>(pref + head * nchunks * (long)(kPairWindow * kPairWindow));
+  int32_t* out = pairs + head * ngroups;
+  uint4 cur[4], nxt[4];
+  auto fetch = [&](int c, uint4 (&r)[4]) {  // lane k: the 64 bytes of choice k, chunk c
+#pragma unroll
+    for (int j = 0; j < 4; ++j) r[j] = src[(long)c * 256 + lane * 4 + j];
+  };
+  fetch(0, cur);
+  uint64_t taken = 0;  // bit k: block I+k already has a partner
+  int g = 0;
+  for (int c = 0; c < nchunks; ++c) {
+    fetch(min(c + 1, nchunks - 1), nxt);  // unconditional: a fixed count of loads in flight
+    const uint32_t w[16] = {cur[0].x, cur[0].y, cur[0].z, cur[0].w, cur[1].x, cur[1].y,
+                            cur[1].z, cur[1].w, cur[2].x, cur[2].y, cur[2].z, cur[2].w,
+                            cur[3].x, cur[3].y, cur[3].z, cur[3].w};
+#pragma unroll
+    for (int r = 0; r < kPairWindow; ++r) {
+      const int I = c * kPairWindow + r;
+      if (I < nb) {
+        if (taken & 1) {
+          taken >>= 1;
+        } else {
+          const int d = (w[r / 4] >> (8 * (r % 4))) & 0xFF;  // this lane's choice
+          const bool free_d = I + 1 + d < nb && !(((taken >> d) >> 1) & 1);
+          const uint64_t m = __ballot(free_d);
+          taken >>= 1;
+          int partner = nb;
+          if (m) {
+            const int dd = __builtin_amdgcn_readlane(d, (int)__builtin_ctzll(m));
+            partner = I + 1 + dd;
+            taken |= 1ull << dd;
+          }
+          if (g < ngroups) tbl[g] = I | (partner << 16);  // every lane stores the same value
+          ++g;
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) cur[j] = nxt[j];
+  }
+  __syncthreads();
+  for (int i = lane; i < ngroups; i += 64) out[i] = tbl[i];
+}
+
+// G query blocks share a workgroup of the attention kernel: G consecutive ones, or with G = 2 and
+// a pair table the two that pair_greedy_kernel matched. For each (b, h, group) this writes the
+// entry count and then the ascending union of the G block lists, each entry
 // J | (bit i: query block i of the group selected J) << 16. Built through bitmaps, so the lists may
 // come in any order; out-of-range entries are dropped, as the attention skips them.
 template <int G>
 __global__ __launch_bounds__(256) void group_union_kernel(int nb, int keep, int ngroups, int stride,
                                                           const int32_t* __restrict__ idx,
+                                                          const int32_t* __restrict__ pairs,
                                                           int32_t* __restrict__ out) {
   extern __shared__ uint32_t sh[];
   const int words = (nb + 31) >> 5;
@@ -70,8 +189,11 @@ __global__ __launch_bounds__(256) void group_union_kernel(int nb, int keep, int 
   const int tid = threadIdx.x;
   for (int w = tid; w < G * words; w += 256) bits[w] = 0u;
   __syncthreads();
-  for (int b = 0; b < G && I0 + b < nb; ++b) {
-    const int32_t* sel = idx + (head * nb + I0 + b) * (long)keep;
+  const int pr = G == 2 && pairs ? pairs[gp] : 0;
+  for (int b = 0; b < G; ++b) {
+    const int Ib = G == 2 && pairs ? (b ? pr >> 16 : pr & 0xFFFF) : I0 + b;
+    if (Ib >= nb) break;
+    const int32_t* sel = idx + (head * nb + Ib) * (long)keep;
     for (int i = tid; i < keep; i += 256) {
       const int J = sel[i];
       if ((unsigned)J < (unsigned)nb) atomicOr(&bits[b * words + (J >> 5)], 1u << (J & 31));
@@ -111,15 +233,25 @@ __global__ __launch_bounds__(256) void group_union_kernel(int nb, int keep, int 
   }
 }
 
-// bf16 attention kernel: one workgroup per (b, h, G consecutive query blocks); see the file comment.
+// Query block qb of group grp: from the pair table when there is one (G = 2), else grp*G + qb.
+template <int G>
+__device__ __forceinline__ int group_block(const int32_t* pairs, long entry, int grp, int qb) {
+  if (G != 2 || !pairs) return grp * G + qb;
+  typedef const __attribute__((address_space(4))) int32_t* const_i32;
+  const int pr = ((const_i32)pairs)[entry];
+  return qb ? pr >> 16 : pr & 0xFFFF;
+}
+
+// bf16 attention kernel: one workgroup per (b, h, G query blocks); see the file comment.
 // lists: G = 1: the block lists [B, H, nb, list_stride] (list_len entries used); G > 1:
 //        group_union_kernel output, list_stride ints per (b, h, group); nullptr: every key block in
 //        order for all query blocks of the group (list_len = nb).
 template <int BLK, int G, int NBUF, int TAB>
 __global__ __launch_bounds__(G * BLK * 2, 2) void sparse_attn_kernel(
     int N, int nb, int ngroups, int total, const int32_t* __restrict__ lists, int list_len,
-    int list_stride, float scale_log2, const bf16* __restrict__ Q, const bf16* __restrict__ K,
-    const bf16* __restrict__ V, bf16* __restrict__ O) {
+    int list_stride, const int32_t* __restrict__ pairs, float scale_log2,
+    const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
+    bf16* __restrict__ O) {
   static_assert(G == 1 || G == 2 || G == 4, "one, two or four query blocks per workgroup");
   static_assert(NBUF >= 3, "loads of later sub-tiles stay in flight during a step");
   constexpr int D = 128, WPB = BLK / 32, NW = G * WPB;
@@ -137,7 +269,7 @@ __global__ __launch_bounds__(G * BLK * 2, 2) void sparse_attn_kernel(
   const int tid = threadIdx.x, lane = tid % 64, hh = lane / 32;
   const int wave = wave_uniform(tid / 64);   // wave-uniform: LDS DMA bases in SGPRs
   const int qb = wave / WPB;                 // which of the group's query blocks this wave serves
-  const int I = grp * G + qb;                // its index (== nb for a missing second block)
+  const int I = group_block<G>(pairs, head * ngroups + grp, grp, qb);  // nb: missing second block
   const int q = I * BLK + (wave % WPB) * 32 + lane % 32;  // this lane's query (column of S^T, O^T)
   const bool qvalid = I < nb && q < N;
   const int mybit = 1 << qb;
@@ -393,8 +525,9 @@ __global__ __launch_bounds__(G * BLK * 2, 2) void sparse_attn_kernel(
 template <int BLK, int G, int NBUF, int TAB>
 __global__ __launch_bounds__(G * BLK * 4) void sparse_attn16_kernel(
     int N, int nb, int ngroups, int total, const int32_t* __restrict__ lists, int list_len,
-    int list_stride, float scale_log2, const bf16* __restrict__ Q, const bf16* __restrict__ K,
-    const bf16* __restrict__ V, bf16* __restrict__ O) {
+    int list_stride, const int32_t* __restrict__ pairs, float scale_log2,
+    const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
+    bf16* __restrict__ O) {
   static_assert(G == 1 || G == 2 || G == 4, "one, two or four query blocks per workgroup");
   static_assert(NBUF >= 3, "loads of later sub-tiles stay in flight during a step");
   constexpr int D = 128, WPB = BLK / 16, NW = G * WPB, NT = NW * 64;
@@ -413,7 +546,7 @@ __global__ __launch_bounds__(G * BLK * 4) void sparse_attn16_kernel(
   const int tid = threadIdx.x, lane = tid % 64, lr = lane % 16, g = lane / 16;
   const int wave = wave_uniform(tid / 64);
   const int qb = wave / WPB;
-  const int I = grp * G + qb;
+  const int I = group_block<G>(pairs, head * ngroups + grp, grp, qb);
   const int q = I * BLK + (wave % WPB) * 16 + lr;  // this lane's query (column of S^T, O^T)
   const bool qvalid = I < nb && q < N;
   const int mybit = 1 << qb;
@@ -668,19 +801,19 @@ __global__ __launch_bounds__(128) void sparse_simple_kernel(int N, int block, in
 
 template <int WAVE_Q, int BLK, int G, int NBUF, int TAB>
 hipError_t launch_bf16_tab(const Shape& s, const void* Qr, const void* Kr, const void* V,
-                           const int32_t* lists, int list_len, int list_stride, float scale,
-                           void* Os, hipStream_t st) {
+                           const int32_t* lists, int list_len, int list_stride,
+                           const int32_t* pairs, float scale, void* Os, hipStream_t st) {
   const int nb = num_blocks(s.N, BLK);
   const int ngroups = (nb + G - 1) / G;
   const int total = ngroups * s.H * s.B;
   const float sl = scale * 1.4426950408889634f;
   if constexpr (WAVE_Q == 32)
     hipLaunchKernelGGL((sparse_attn_kernel<BLK, G, NBUF, TAB>), dim3(total), dim3(G * BLK * 2), 0,
-                       st, s.N, nb, ngroups, total, lists, list_len, list_stride, sl,
+                       st, s.N, nb, ngroups, total, lists, list_len, list_stride, pairs, sl,
                        (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V, (bf16*)Os);
   else
     hipLaunchKernelGGL((sparse_attn16_kernel<BLK, G, NBUF, TAB>), dim3(total), dim3(G * BLK * 4),
-                       0, st, s.N, nb, ngroups, total, lists, list_len, list_stride, sl,
+                       0, st, s.N, nb, ngroups, total, lists, list_len, list_stride, pairs, sl,
                        (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V, (bf16*)Os);
   return hipGetLastError();
 }
@@ -690,13 +823,13 @@ constexpr int kTable = 1024;
 template <int WAVE_Q, int BLK, int G, int NBUF>
 hipError_t launch_bf16(const Shape& s, const void* Qr, const void* Kr, const void* V,
                        const int32_t* lists, int list_len, int list_stride, float scale, void* Os,
-                       hipStream_t st) {
+                       hipStream_t st, const int32_t* pairs = nullptr) {
   const int max_len = G > 1 ? list_stride - 1 : list_len;
   if (lists && max_len <= kTable)
     return launch_bf16_tab<WAVE_Q, BLK, G, NBUF, kTable>(s, Qr, Kr, V, lists, list_len, list_stride,
-                                                         scale, Os, st);
-  return launch_bf16_tab<WAVE_Q, BLK, G, NBUF, 0>(s, Qr, Kr, V, lists, list_len, list_stride, scale,
-                                                  Os, st);
+                                                         pairs, scale, Os, st);
+  return launch_bf16_tab<WAVE_Q, BLK, G, NBUF, 0>(s, Qr, Kr, V, lists, list_len, list_stride, pairs,
+                                                  scale, Os, st);
 }
 
 template <typename T, int D>
@@ -711,13 +844,37 @@ hipError_t launch_simple(const Shape& s, const void* Qr, const void* Kr, const v
 // Query blocks per workgroup when a workspace for the merged lists is given.
 int group_of(const Shape& s, int block) { return s.bf16 && block == 64 ? ROLA_B64_GROUP : 1; }
 
+// Pairs are matched by overlap when G = 2 and one overlap workgroup's bitmaps fit in 64 KB of LDS
+// (up to 4064 query blocks); otherwise the pairs are adjacent blocks.
+bool pairing_on(int G, int nb) {
+  return ROLA_B64_PAIRING && G == 2 && kPairRows * pair_row_stride(nb) * 4 <= 65536 &&
+         (nb + 1) / 2 <= kMaxPairGroups;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Workspace: [pair table: int32 per group, when pairing][union lists, which the candidate ranks
+// (kPairWindow bytes per query block, whole chunks) occupy before the lists are written].
+struct SparseWs {
+  size_t pair_bytes, list_bytes;
+};
+SparseWs sparse_ws_layout(const Shape& s, int block, int keep) {
+  const int G = group_of(s, block);
+  if (G == 1) return {0, 0};
+  const int nb = num_blocks(s.N, block);
+  const size_t heads = (size_t)s.B * s.H, ngroups = (nb + G - 1) / G;
+  size_t lists = heads * ngroups * ((size_t)G * keep + 1) * sizeof(int32_t);
+  if (!pairing_on(G, nb)) return {0, lists};
+  const size_t nchunks = (nb + kPairWindow - 1) / kPairWindow;
+  lists = std::max(lists, heads * nchunks * kPairWindow * kPairWindow);
+  return {align256(heads * ngroups * sizeof(int32_t)), lists};
+}
+
 }  // namespace
 
 size_t sparse_workspace_bytes(const Shape& s, int block, int keep) {
-  const int G = group_of(s, block);
-  if (G == 1) return 0;
-  const long ngroups = (num_blocks(s.N, block) + G - 1) / G;
-  return (size_t)s.B * s.H * ngroups * ((size_t)G * keep + 1) * sizeof(int32_t);
+  const SparseWs w = sparse_ws_layout(s, block, keep);
+  return w.pair_bytes + w.list_bytes;
 }
 
 hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, const void* V,
@@ -730,14 +887,25 @@ hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, co
       if (!idx) return launch_bf16<32, 64, 2, 3>(s, Qr, Kr, V, nullptr, nb, 0, scale, Os, st);
       if (ws && G > 1) {
         const int ngroups = (nb + G - 1) / G, stride = G * keep + 1;
-        const int words = (nb + 31) / 32;
-        hipLaunchKernelGGL(group_union_kernel<G>, dim3(ngroups * s.H * s.B), dim3(256),
+        const int words = (nb + 31) / 32, heads = s.B * s.H;
+        const SparseWs lay = sparse_ws_layout(s, 64, keep);
+        int32_t* pairs = lay.pair_bytes ? (int32_t*)ws : nullptr;
+        int32_t* lists = (int32_t*)((char*)ws + lay.pair_bytes);
+        if (pairs) {
+          const int nchunks = (nb + kPairWindow - 1) / kPairWindow;
+          hipLaunchKernelGGL(pair_rank_kernel, dim3(nchunks * heads), dim3(256),
+                             kPairRows * pair_row_stride(nb) * sizeof(uint32_t), st, nb, keep,
+                             nchunks, idx, (uint8_t*)lists);
+          hipLaunchKernelGGL(pair_greedy_kernel, dim3(heads), dim3(64), 0, st, nb, ngroups,
+                             nchunks, (const uint8_t*)lists, pairs);
+        }
+        hipLaunchKernelGGL(group_union_kernel<G>, dim3(ngroups * heads), dim3(256),
                            (G * words + 256) * sizeof(uint32_t), st, nb, keep, ngroups, stride, idx,
-                           (int32_t*)ws);
+                           (const int32_t*)pairs, lists);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
-        return launch_bf16<ROLA_B64_WAVE_Q, 64, G, ROLA_B64_NBUF>(s, Qr, Kr, V, (const int32_t*)ws,
-                                                                  0, stride, scale, Os, st);
+        return launch_bf16<ROLA_B64_WAVE_Q, 64, G, ROLA_B64_NBUF>(s, Qr, Kr, V, lists, 0, stride,
+                                                                  scale, Os, st, pairs);
       }
       return launch_bf16<32, 64, 1, 3>(s, Qr, Kr, V, idx, keep, keep, scale, Os, st);
     }

@@ -183,6 +183,71 @@ def test_sparse_shared_loads(grid, s):
             T.assert_close(T.to_np(single[0, h]), want, w.dtype, f"single {order} h{h}")
 
 
+def _greedy_pairs(lists, nb, window=64):
+    """Pairing of query blocks by list overlap: blocks in ascending order; a block without a partner
+    yet takes the free block among its next `window` that shares the most entries (the nearest on
+    ties), or stays alone. Entries I | J << 16, J = nb for no partner."""
+    sets = [set(int(j) for j in row if 0 <= j < nb) for row in lists]
+    taken = np.zeros(nb, bool)
+    out = []
+    for i in range(nb):
+        if taken[i]:
+            continue
+        best, bj = -1, nb
+        for j in range(i + 1, min(nb, i + window + 1)):
+            if not taken[j] and len(sets[i] & sets[j]) > best:
+                best, bj = len(sets[i] & sets[j]), j
+        if bj < nb:
+            taken[bj] = True
+        out.append(i | (bj << 16))
+    return np.array(out, np.int64)
+
+
+@pytest.mark.parametrize("lists_kind,s", [("selected", 0.8), ("far-partner", 0.85), ("keep-all", 0.0)])
+def test_overlap_pairing(lists_kind, s):
+    """Query blocks share a workgroup by list overlap: the pair table in the workspace equals the
+    greedy matching computed here, covers every block once, and the attention output is bitwise
+    that of one query block per workgroup. 135 query blocks (three 64-block chunks, ragged last
+    block, odd count), two batch entries of two heads."""
+    w = synth.WAN_1_3B_480P.replace(grid=(7, 30, 41), B=2, H=2, sparsity=s)
+    inp, _ = _inputs(w, seed=8)
+    g = w.grid
+    prob = R.problem(w.B, w.H, w.N, w.d_h, g, w.dtype)
+    cos, sin = R.rola_rope_tables(prob, w.split)
+    qr = R.rola_rope_apply(inp["Qn"], cos, sin, g)
+    kr = R.rola_rope_apply(inp["Kn"], cos, sin, g)
+    nb = O.num_blocks(w.N, 64)
+    keep = O.keep_blocks(nb, s)
+    assert nb == 135
+    if lists_kind == "selected":
+        idx = R.rola_block_select(qr, kr, g, 64, s)
+    else:  # block I selects the keep blocks from (I * m) % nb on: its best partners sit far away
+        def lists_for(m):
+            start = (np.arange(nb) * m) % nb
+            return np.sort((start[:, None] + np.arange(keep)[None, :]) % nb, axis=1)
+        full = np.stack([np.stack([lists_for(37 + 16 * (b * w.H + h)) for h in range(w.H)])
+                         for b in range(w.B)])
+        idx = torch.from_numpy(full.astype(np.int32)).cuda()
+    need = R.sparse_workspace_bytes(prob, 64, s)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    shared = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, s, idx, ws=ws)
+    single = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, s, idx, share=False)
+    torch.cuda.synchronize()
+    ngroups = (nb + 1) // 2
+    table = ws[: w.B * w.H * ngroups * 4].view(torch.int32).cpu().numpy().reshape(w.B, w.H, ngroups)
+    idx_np = idx.cpu().numpy()
+    for b in range(w.B):
+        for h in range(w.H):
+            want = _greedy_pairs(idx_np[b, h], nb)
+            got = table[b, h].astype(np.int64)
+            assert np.array_equal(got, want), (b, h, np.nonzero(got != want)[0][:8])
+            members = np.concatenate([got & 0xFFFF, got >> 16])
+            assert np.array_equal(np.sort(members[members < nb]), np.arange(nb))
+    _report("overlap pairing", kind=lists_kind, adjacent=int(sum(
+        ((table[0, 0] >> 16) - (table[0, 0] & 0xFFFF)) == 1)), groups=ngroups)
+    assert torch.equal(shared, single)
+
+
 def test_exact_ties_go_to_lower_block():
     """Identical key blocks tie exactly: every row must keep the lowest block indices."""
     w = synth.WAN_1_3B_480P.replace(grid=(2, 8, 16), H=2)
