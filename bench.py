@@ -203,6 +203,32 @@ def sweep(reps: int) -> None:
             del inp, C, z, ws, olr, out
     print()
 
+    # feature-map variants of the low-rank branch at the 14B shape (Sec. 5.1, Sec. 5.3)
+    print("## Low-rank feature variants, H40 d128 N75600 r32 bf16 (warm cache)\n")
+    print("| phi | rotation | summary ms | summary GB/s | readout+combine ms | readout+combine GB/s |")
+    print("|---|---|---|---|---|---|", flush=True)
+    w = synth.lowrank_sweep(75600, 32)
+    g = w.grid
+    inp = synth.make_inputs(w, 0, device=dev)
+    prob = R.problem(w.B, w.H, w.N, w.d_h, g, w.dtype)
+    cos, sin = R.rola_rope_tables(prob, w.split, w.base)
+    tensor = w.B * w.H * w.N * w.d_h * 2
+    tables = 2 * w.N * 16 * 4
+    ws = torch.empty(R.summary_workspace_bytes(prob, 32), dtype=torch.uint8, device=dev)
+    C, z = R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], 32, cos, sin, g)
+    out = torch.empty_like(inp["Qn"])
+    for phi, order in (("silu", "outside"), ("identity", "outside"), ("tanh", "outside"),
+                       ("relu", "outside"), ("gelu", "outside"), ("silu", "inside"), ("silu", "none")):
+        sm = time_call(lambda: R.rola_lowrank_summary_ex(inp["Kn"], inp["V"], inp["Pk"], 32, cos, sin,
+                                                         g, phi, order, C=C, z=z, ws=ws), reps)[0]
+        rm = time_call(lambda: R.rola_lowrank_readout_combine_ex(
+            inp["Qn"], inp["Pq"], 32, cos, sin, C, inp["V"], inp["logits"], g, phi, order, out=out),
+            reps)[0]
+        print(f"| {phi} | {order} | {sm:.4f} | {(2 * tensor + tables) / sm / 1e6:.0f} | {rm:.4f} | "
+              f"{(3 * tensor + tables) / rm / 1e6:.0f} |", flush=True)
+    del inp, C, z, ws, out
+    print()
+
     # sparse branch: sparsity x block, dense reference
     print("## Sparse branch, H40 d128 N75600 bf16 (MFMA roofline 2.5 PFLOP/s)\n")
     print("| block | sparsity | keep | select ms | sparse ms | TFLOP/s performed | % of peak | "

@@ -148,6 +148,47 @@ rola_status rola_lowrank_readout(const rola_problem* p, const void* Qn, const vo
                                  const float* cos_tab, const float* sin_tab, int32_t rope_ld,
                                  const float* C, float eps_lr, void* Olr, hipStream_t stream);
 
+/* ---- low-rank feature variants (Sec. 5.1 "Mechanism-Level Validation", Sec. 5.3 "Ablation
+ * Study", Tab. abl_activation; Prop. inside) ----------------------------------------------------
+ * The functions above use the paper's design, SiLU with the rotation outside it. The *_ex forms take
+ * the feature map phi and the place of the rotation: outside (R_r(p) phi(P x), the paper's design),
+ * inside (phi(R_r(p) P x), Prop. inside) or none (phi(P x), position-blind). Everything else is as in
+ * the plain forms; phi = ROLA_PHI_SILU with ROLA_ROPE_OUTSIDE gives bitwise their results. An
+ * unknown phi or order is ROLA_ERR_INVALID_ARGUMENT. */
+typedef enum {
+  ROLA_PHI_SILU = 0,      /* x / (1 + e^-x) */
+  ROLA_PHI_IDENTITY = 1,  /* x */
+  ROLA_PHI_TANH = 2,      /* tanh x */
+  ROLA_PHI_RELU = 3,      /* max(x, 0) */
+  ROLA_PHI_GELU = 4       /* x Phi(x), Phi the standard normal CDF (erf form) */
+} rola_phi;
+typedef enum { ROLA_ROPE_OUTSIDE = 0, ROLA_ROPE_INSIDE = 1, ROLA_ROPE_NONE = 2 } rola_rope_order;
+
+rola_status rola_lowrank_summary_ex(const rola_problem* p, const void* Kn, const void* V,
+                                    const void* Pk, int32_t r, const float* cos_tab,
+                                    const float* sin_tab, int32_t rope_ld, int32_t phi,
+                                    int32_t rope_order, float* C, float* z, void* ws,
+                                    size_t ws_bytes, hipStream_t stream);
+rola_status rola_lowrank_readout_ex(const rola_problem* p, const void* Qn, const void* Pq, int32_t r,
+                                    const float* cos_tab, const float* sin_tab, int32_t rope_ld,
+                                    int32_t phi, int32_t rope_order, const float* C, float eps_lr,
+                                    void* Olr, hipStream_t stream);
+rola_status rola_lowrank_readout_combine_ex(const rola_problem* p, const void* Qn, const void* Pq,
+                                            int32_t r, const float* cos_tab, const float* sin_tab,
+                                            int32_t rope_ld, int32_t phi, int32_t rope_order,
+                                            const float* C, float eps_lr, const void* Os,
+                                            const float* gate_logits, float eps, void* O,
+                                            hipStream_t stream);
+
+/* The low-rank features themselves, F[b, h, n, :] = the r-vector x~_n of X[b, h, n, :] under
+ * projection P ([H, r, d_h], P_q or P_k), phi and rope_order, pairs (2j, 2j+1) interleaved; fp32
+ * [B, H, N, r], fp32 projection. Not a step of the module: it exposes q~ and k~ so that the
+ * pre-RMSNorm low-rank logit s(p, q) = q~_p . k~_q of Sec. 5.1 (its dependence on the offset p - q
+ * and its shift residual |s(p + d, q + d) - s(p, q)|) can be measured. */
+rola_status rola_lowrank_features(const rola_problem* p, const void* X, const void* P, int32_t r,
+                                  const float* cos_tab, const float* sin_tab, int32_t rope_ld,
+                                  int32_t phi, int32_t rope_order, float* F, hipStream_t stream);
+
 /* ---- gated fusion (Sec. 4.4, eq. gate; Algorithm steps 8-10) --------------------------------- */
 
 /* O_p = (O^s_p / r_p + g_p O^lr_p) r_p, r_p = sqrt(mean_i (O^s_{p,i})^2 + eps), g_p =

@@ -30,6 +30,9 @@ Points where the paper is silent are fixed by these readings (each also listed i
   R8  the fused output uses eps = 1e-6 and one gate per token shared by all heads.
   R9  Q^r, K^r are the backbone's rotated tensors in the working precision: R(Q^n) rounded once
       (round-to-nearest-even) to the input dtype.
+  R10 the activation ablation's GELU is the exact form x * Phi(x) (Phi the standard normal CDF);
+      "rotation inside the activation" is phi(R_r(p) P x), as Prop. inside defines it; "no RoPE" is
+      phi(P x). Everything else in the branch is unchanged by these variants.
 """
 
 from __future__ import annotations
@@ -43,7 +46,8 @@ __all__ = [
     "num_blocks", "keep_blocks", "pool_blocks", "block_scores", "select_blocks",
     "sparse_attention", "sparse_attention_rows", "silu", "lowrank_features", "lowrank_summary",
     "lowrank_readout_u", "rms_normalize", "lowrank_readout", "gate", "combine", "forward_head",
-    "forward", "inside_features", "norope_features", "lowrank_logit", "flop_counts",
+    "forward", "inside_features", "norope_features", "lowrank_logit", "flop_counts", "activation",
+    "features",
 ]
 
 # --------------------------------------------------------------------------------------------------
@@ -215,22 +219,59 @@ def silu(x: np.ndarray) -> np.ndarray:
     return out
 
 
-def lowrank_features(x: np.ndarray, P: np.ndarray, cos, sin) -> np.ndarray:
+_erf = np.vectorize(math.erf, otypes=[np.float64])
+
+
+def activation(x: np.ndarray, phi: str = "silu") -> np.ndarray:
+    """Feature map of the low-rank branch: SiLU (eq. qklr), or one of the alternatives of the
+    activation ablation (Sec. 5.3, Tab. abl_activation): identity, tanh, ReLU, and GELU in its exact
+    form x * Phi(x), Phi the standard normal CDF (reading R10)."""
+    x = np.asarray(x, dtype=np.float64)
+    if phi == "silu":
+        return silu(x)
+    if phi == "identity":
+        return x.copy()
+    if phi == "tanh":
+        return np.tanh(x)
+    if phi == "relu":
+        return np.maximum(x, 0.0)
+    if phi == "gelu":
+        return x * 0.5 * (1.0 + _erf(x / math.sqrt(2.0)))
+    raise ValueError(f"unknown feature map {phi!r}")
+
+
+def features(x: np.ndarray, P: np.ndarray, cos, sin, phi: str = "silu",
+             ordering: str = "outside") -> np.ndarray:
+    """Low-rank features of every token under a feature map and a place of the rotation: outside,
+    R_r(p) phi(P x_p) (eq. qklr, Sec. 4.3, the paper's design); inside, phi(R_r(p) P x_p) (Prop.
+    inside); none, phi(P x_p) (position-blind). x: [N, d_h], P: [r, d_h] -> [N, r]."""
+    y = x @ P.T
+    if ordering == "outside":
+        return rotate(activation(y, phi), cos, sin)
+    if ordering == "inside":
+        return activation(rotate(y, cos, sin), phi)
+    if ordering == "none":
+        return activation(y, phi)
+    raise ValueError(f"unknown rotation order {ordering!r}")
+
+
+def lowrank_features(x: np.ndarray, P: np.ndarray, cos, sin, phi: str = "silu",
+                     ordering: str = "outside") -> np.ndarray:
     """Rotary low-rank features R_r(p) SiLU(P x_p) of every token (eq. qklr; RoPE outside the
-    activation, Sec. 4.3). x: [N, d_h], P: [r, d_h] -> [N, r]."""
-    return rotate(silu(x @ P.T), cos, sin)
+    activation, Sec. 4.3), or a variant (see features). x: [N, d_h], P: [r, d_h] -> [N, r]."""
+    return features(x, P, cos, sin, phi, ordering)
 
 
-def lowrank_summary(kn, v, Pk, cos, sin):
+def lowrank_summary(kn, v, Pk, cos, sin, phi: str = "silu", ordering: str = "outside"):
     """Global context C = sum_q k~_q v_q^T in R^{r x d_h} (eq. ctx; computed once per head) and the
     feature sum z = sum_q k~_q (reading R7). v is not rotated."""
-    kt = lowrank_features(kn, Pk, cos, sin)
+    kt = lowrank_features(kn, Pk, cos, sin, phi, ordering)
     return kt.T @ v, kt.sum(axis=0)
 
 
-def lowrank_readout_u(qn, Pq, cos, sin, C) -> np.ndarray:
+def lowrank_readout_u(qn, Pq, cos, sin, C, phi: str = "silu", ordering: str = "outside") -> np.ndarray:
     """Pre-normalisation readout u_p = q~_p^T C for every token (eq. ctx)."""
-    return lowrank_features(qn, Pq, cos, sin) @ C
+    return lowrank_features(qn, Pq, cos, sin, phi, ordering) @ C
 
 
 def rms_normalize(u: np.ndarray, eps: float) -> np.ndarray:
@@ -238,9 +279,10 @@ def rms_normalize(u: np.ndarray, eps: float) -> np.ndarray:
     return u / np.sqrt(np.mean(u * u, axis=-1, keepdims=True) + eps)
 
 
-def lowrank_readout(qn, Pq, cos, sin, C, eps_lr: float = 1e-6) -> np.ndarray:
+def lowrank_readout(qn, Pq, cos, sin, C, eps_lr: float = 1e-6, phi: str = "silu",
+                    ordering: str = "outside") -> np.ndarray:
     """O^lr_p = RMSNorm(q~_p^T C) (eq. ctx)."""
-    return rms_normalize(lowrank_readout_u(qn, Pq, cos, sin, C), eps_lr)
+    return rms_normalize(lowrank_readout_u(qn, Pq, cos, sin, C, phi, ordering), eps_lr)
 
 
 # --------------------------------------------------------------------------------------------------
@@ -340,7 +382,8 @@ def norope_features(x, P, cos=None, sin=None) -> np.ndarray:
     return silu(x @ P.T)
 
 
-def lowrank_logit(qn_p, kn_q, Pq, Pk, pos_p, pos_q, split, base=10000.0, ordering="outside"):
+def lowrank_logit(qn_p, kn_q, Pq, Pk, pos_p, pos_q, split, base=10000.0, ordering="outside",
+                  phi="silu"):
     """Pre-RMSNorm low-rank logit s(p, q) = q~_p . k~_q of one query/key pair placed at explicit
     positions (the quantity whose shift residual |s(p+d, q+d) - s(p, q)| Sec. 5.1 measures)."""
     r = Pq.shape[0]
@@ -350,9 +393,8 @@ def lowrank_logit(qn_p, kn_q, Pq, Pk, pos_p, pos_q, split, base=10000.0, orderin
         return np.cos(ang)[None, :], np.sin(ang)[None, :]
     cp, sp = table(pos_p)
     cq, sq = table(pos_q)
-    fn = {"outside": lowrank_features, "inside": inside_features, "none": norope_features}[ordering]
-    a = fn(qn_p[None, :], Pq, cp, sp)[0]
-    b = fn(kn_q[None, :], Pk, cq, sq)[0]
+    a = features(qn_p[None, :], Pq, cp, sp, phi, ordering)[0]
+    b = features(kn_q[None, :], Pk, cq, sq, phi, ordering)[0]
     assert a.shape == (r,)
     return float(a @ b)
 

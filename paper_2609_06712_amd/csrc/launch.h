@@ -38,14 +38,20 @@ hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, co
 // lowrank.hip
 int summary_chunks(const Shape& s, int r);
 size_t summary_workspace_bytes(const Shape& s, int r);
+// feat: feature map phi | rotation order << 8 (the ROLA_PHI_* / ROLA_ROPE_* values; 0 = SiLU with
+// the rotation outside, the paper's design).
 hipError_t launch_lowrank_summary(const Shape& s, const void* Kn, const void* V, const void* Pk,
                                   int r, const float* cos_tab, const float* sin_tab, int ld,
-                                  float* C, float* z, void* ws, hipStream_t st);
+                                  int feat, float* C, float* z, void* ws, hipStream_t st);
 // Os == nullptr: plain readout into Out; otherwise readout fused with the gated combine.
 hipError_t launch_lowrank_readout(const Shape& s, const void* Qn, const void* Pq, int r,
-                                  const float* cos_tab, const float* sin_tab, int ld,
+                                  const float* cos_tab, const float* sin_tab, int ld, int feat,
                                   const float* C, float eps_lr, const void* Os,
                                   const float* logits, float eps, void* Out, hipStream_t st);
+// Features of every token, fp32 [B, H, N, r].
+hipError_t launch_lowrank_features(const Shape& s, const void* X, const void* P, int r,
+                                   const float* cos_tab, const float* sin_tab, int ld, int feat,
+                                   float* F, hipStream_t st);
 hipError_t launch_combine(const Shape& s, const void* Os, const void* Olr, const float* logits,
                           float eps, void* O, hipStream_t st);
 

@@ -33,6 +33,51 @@ __device__ __forceinline__ f32x4 mfma16x16x32(const bf16x8& a, const bf16x8& b, 
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+// Feature map of the low-rank branch. The paper's design is SiLU with the rotation applied outside
+// it (eq. qklr); its ablations replace SiLU by Identity, Tanh, ReLU or GELU and move the rotation
+// inside the activation or drop it (Sec. 5.1 RoPE placement, Prop. inside). feat = phi | order << 8
+// with the ROLA_PHI_* / ROLA_ROPE_* values of the ABI. Every phi maps 0 to 0, so zero rows (padding
+// tokens, padding pairs) keep zero features under every variant.
+constexpr int kPhiSilu = 0, kPhiIdentity = 1, kPhiTanh = 2, kPhiRelu = 3, kPhiGelu = 4;
+constexpr int kRopeOutside = 0, kRopeInside = 1, kRopeNone = 2;
+
+__device__ __forceinline__ float feature_act(float x, int phi) {
+  switch (phi) {
+    case kPhiIdentity: return x;
+    case kPhiTanh: return tanhf(x);
+    case kPhiRelu: return fmaxf(x, 0.f);
+    case kPhiGelu: return 0.5f * x * (1.f + erff(x * 0.70710678118654752f));  // exact (erf) GELU
+    default: return silu(x);
+  }
+}
+
+// Features of one rotary pair from its two projections (e, o) = (P_2j x, P_2j+1 x) at a position
+// with rotation (c, s). GENERIC = false is the paper's design, SiLU then the rotation; GENERIC =
+// true applies feat at run time (the default feat gives the same arithmetic).
+template <bool GENERIC>
+__device__ __forceinline__ void feature_pair(float& e, float& o, float c, float s, int feat) {
+  if (!GENERIC) {
+    const float a = silu(e), b = silu(o);
+    e = a * c - b * s;
+    o = a * s + b * c;
+    return;
+  }
+  const int phi = feat & 0xFF, order = feat >> 8;
+  if (order == kRopeInside) {
+    const float a = e * c - o * s, b = e * s + o * c;
+    e = a;
+    o = b;
+  }
+  const float a = feature_act(e, phi), b = feature_act(o, phi);
+  if (order == kRopeOutside) {
+    e = a * c - b * s;
+    o = a * s + b * c;
+  } else {
+    e = a;
+    o = b;
+  }
+}
+
 int summary_chunk_len(const Shape& s) {
   const long heads = (long)s.B * s.H;
   // About 2048 workgroups: several full rounds over the chip, so the last partial round is short.
@@ -45,9 +90,9 @@ int summary_chunk_len(const Shape& s) {
 // ------------------------------------------------------------------------------------------------
 // bf16 summary
 // ------------------------------------------------------------------------------------------------
-template <int JT>
+template <int JT, bool GENERIC>
 __global__ __launch_bounds__(256, JT == 1 ? 2 : 1) void summary_mfma_kernel(
-    int N, int H, int r, int chunk_len, int n_chunks, int total, int ld,
+    int N, int H, int r, int chunk_len, int n_chunks, int total, int ld, int feat,
     const bf16* __restrict__ Kn, const bf16* __restrict__ V, const bf16* __restrict__ Pk,
     const float* __restrict__ cos_tab, const float* __restrict__ sin_tab,
     float* __restrict__ part) {
@@ -181,8 +226,8 @@ __global__ __launch_bounds__(256, JT == 1 ? 2 : 1) void summary_mfma_kernel(
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const float c = tc[jt][tt][v], s = ts[jt][tt][v];
-          const float a = silu(ye[v]), b = silu(yo[v]);
-          const float ke = a * c - b * s, ko = a * s + b * c;
+          float ke = ye[v], ko = yo[v];
+          feature_pair<GENERIC>(ke, ko, c, s, feat);
           ze[jt] += ke;
           zo[jt] += ko;
           be[4 * tt + v] = (bf16)ke;
@@ -274,7 +319,7 @@ __global__ __launch_bounds__(256, JT == 1 ? 2 : 1) void summary_mfma_kernel(
 // ------------------------------------------------------------------------------------------------
 template <typename T, int D>
 __global__ __launch_bounds__(256) void summary_simple_kernel(
-    int N, int H, int r, int chunk_len, int n_chunks, int ld, const T* __restrict__ Kn,
+    int N, int H, int r, int chunk_len, int n_chunks, int ld, int feat, const T* __restrict__ Kn,
     const T* __restrict__ V, const T* __restrict__ Pk, const float* __restrict__ cos_tab,
     const float* __restrict__ sin_tab, float* __restrict__ part) {
   constexpr int TT = 32, MAXR = 128;
@@ -309,11 +354,11 @@ __global__ __launch_bounds__(256) void summary_simple_kernel(
         ae = fmaf(to_f32(Ph[(long)(2 * j) * D + c]), Ks[tr][c], ae);
         ao = fmaf(to_f32(Ph[(long)(2 * j + 1) * D + c]), Ks[tr][c], ao);
       }
-      const float a = silu(ae), b = silu(ao);
       float cs = 1.f, sn = 0.f;
       if (tok < t1) { cs = cos_tab[(long)tok * ld + j]; sn = sin_tab[(long)tok * ld + j]; }
-      kt[tr][2 * j] = a * cs - b * sn;
-      kt[tr][2 * j + 1] = a * sn + b * cs;
+      feature_pair<true>(ae, ao, cs, sn, feat);
+      kt[tr][2 * j] = ae;
+      kt[tr][2 * j + 1] = ao;
     }
     __syncthreads();
 #pragma unroll
@@ -359,9 +404,9 @@ __global__ __launch_bounds__(256) void summary_reduce_kernel(int rd, int r, int 
 // ------------------------------------------------------------------------------------------------
 constexpr int kReadoutTilesPerWave = 4;  // 16-token tiles per wave per workgroup
 
-template <int JT, bool COMBINE>
+template <int JT, bool COMBINE, bool GENERIC>
 __global__ __launch_bounds__(256) void readout_mfma_kernel(
-    int N, int H, int r, int n_groups, int total, int ld, const bf16* __restrict__ Qn,
+    int N, int H, int r, int n_groups, int total, int ld, int feat, const bf16* __restrict__ Qn,
     const bf16* __restrict__ Pq, const float* __restrict__ cos_tab,
     const float* __restrict__ sin_tab, const float* __restrict__ C, float eps_lr,
     const bf16* Os, const float* __restrict__ logits, float eps, bf16* Out) {
@@ -471,8 +516,8 @@ __global__ __launch_bounds__(256) void readout_mfma_kernel(
         bf16x8 bq, bl;  // q~ = hi + lo
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const float a = silu(ye[v]), bb = silu(yo[v]);
-          const float qe = a * cc[v] - bb * ss[v], qo = a * ss[v] + bb * cc[v];
+          float qe = ye[v], qo = yo[v];
+          feature_pair<GENERIC>(qe, qo, cc[v], ss[v], feat);
           bq[v] = (bf16)qe;
           bq[4 + v] = (bf16)qo;
           bl[v] = (bf16)(qe - (float)bq[v]);
@@ -537,7 +582,7 @@ __global__ __launch_bounds__(256) void readout_mfma_kernel(
 // ------------------------------------------------------------------------------------------------
 template <typename T, int D, bool COMBINE>
 __global__ __launch_bounds__(256) void readout_simple_kernel(
-    int N, int H, int r, int ld, const T* __restrict__ Qn, const T* __restrict__ Pq,
+    int N, int H, int r, int ld, int feat, const T* __restrict__ Qn, const T* __restrict__ Pq,
     const float* __restrict__ cos_tab, const float* __restrict__ sin_tab,
     const float* __restrict__ C, float eps_lr, const T* Os, const float* __restrict__ logits,
     float eps, T* Out) {
@@ -564,11 +609,11 @@ __global__ __launch_bounds__(256) void readout_simple_kernel(
       ae = fmaf(to_f32(Ph[(long)(2 * j) * D + c]), Qs[tr][c], ae);
       ao = fmaf(to_f32(Ph[(long)(2 * j + 1) * D + c]), Qs[tr][c], ao);
     }
-    const float a = silu(ae), bb = silu(ao);
     float cs = 1.f, sn = 0.f;
     if (tok < N) { cs = cos_tab[(long)tok * ld + j]; sn = sin_tab[(long)tok * ld + j]; }
-    ft[tr][2 * j] = a * cs - bb * sn;
-    ft[tr][2 * j + 1] = a * sn + bb * cs;
+    feature_pair<true>(ae, ao, cs, sn, feat);
+    ft[tr][2 * j] = ae;
+    ft[tr][2 * j + 1] = ao;
   }
   __syncthreads();
   const int tr = threadIdx.x / 8, sub = threadIdx.x % 8, tok = tok0 + tr;
@@ -648,49 +693,106 @@ __global__ __launch_bounds__(256) void combine_kernel(long rows, int N, int H, i
   store8(O + row * d + sub * 8, o);
 }
 
-template <int JT>
+// ------------------------------------------------------------------------------------------------
+// Features q~ (or k~) of every token, fp32 [B, H, N, r], pairs interleaved: one thread per (token,
+// pair), fp32 projection, then feature_pair. Not on the module's path: it exposes the features for
+// checks and for the positional metrics of the RoPE-placement study (Sec. 5.1).
+// ------------------------------------------------------------------------------------------------
+template <typename T, int D>
+__global__ __launch_bounds__(256) void features_kernel(long total, int N, int H, int r, int ld,
+                                                       int feat, const T* __restrict__ X,
+                                                       const T* __restrict__ P,
+                                                       const float* __restrict__ cos_tab,
+                                                       const float* __restrict__ sin_tab,
+                                                       float* __restrict__ F) {
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= total) return;
+  const int half = r / 2;
+  const int j = (int)(i % half);
+  const long row = i / half;  // (b, h, token)
+  const int tok = (int)(row % N), h = (int)((row / N) % H);
+  const T* x = X + row * D;
+  const T* pe = P + ((long)h * r + 2 * j) * D;
+  const T* po = pe + D;
+  float e = 0.f, o = 0.f;
+  for (int c = 0; c < D; ++c) {
+    const float xc = to_f32(x[c]);
+    e = fmaf(to_f32(pe[c]), xc, e);
+    o = fmaf(to_f32(po[c]), xc, o);
+  }
+  feature_pair<true>(e, o, cos_tab[(long)tok * ld + j], sin_tab[(long)tok * ld + j], feat);
+  F[row * r + 2 * j] = e;
+  F[row * r + 2 * j + 1] = o;
+}
+
+template <int JT, bool GENERIC>
 hipError_t summary_mfma(const Shape& s, const void* Kn, const void* V, const void* Pk, int r,
-                        const float* ct, const float* st_, int ld, float* part, int chunk_len,
-                        int n_chunks, hipStream_t st) {
+                        const float* ct, const float* st_, int ld, int feat, float* part,
+                        int chunk_len, int n_chunks, hipStream_t st) {
   const int total = s.B * s.H * n_chunks;
-  hipLaunchKernelGGL((summary_mfma_kernel<JT>), dim3(total), dim3(256), 0, st, s.N, s.H, r,
-                     chunk_len, n_chunks, total, ld, (const bf16*)Kn, (const bf16*)V,
+  hipLaunchKernelGGL((summary_mfma_kernel<JT, GENERIC>), dim3(total), dim3(256), 0, st, s.N, s.H,
+                     r, chunk_len, n_chunks, total, ld, feat, (const bf16*)Kn, (const bf16*)V,
                      (const bf16*)Pk, ct, st_, part);
   return hipGetLastError();
 }
 
-template <int JT, bool COMBINE>
+template <int JT>
+hipError_t summary_mfma_feat(const Shape& s, const void* Kn, const void* V, const void* Pk, int r,
+                             const float* ct, const float* st_, int ld, int feat, float* part,
+                             int chunk_len, int n_chunks, hipStream_t st) {
+  if (feat == 0)
+    return summary_mfma<JT, false>(s, Kn, V, Pk, r, ct, st_, ld, feat, part, chunk_len, n_chunks, st);
+  return summary_mfma<JT, true>(s, Kn, V, Pk, r, ct, st_, ld, feat, part, chunk_len, n_chunks, st);
+}
+
+template <int JT, bool COMBINE, bool GENERIC>
 hipError_t readout_mfma(const Shape& s, const void* Qn, const void* Pq, int r, const float* ct,
-                        const float* st_, int ld, const float* C, float eps_lr, const void* Os,
-                        const float* logits, float eps, void* Out, hipStream_t st) {
+                        const float* st_, int ld, int feat, const float* C, float eps_lr,
+                        const void* Os, const float* logits, float eps, void* Out, hipStream_t st) {
   const int per_group = 4 * kReadoutTilesPerWave * 16;
   const int n_groups = (s.N + per_group - 1) / per_group;
   const int total = s.B * s.H * n_groups;
-  hipLaunchKernelGGL((readout_mfma_kernel<JT, COMBINE>), dim3(total), dim3(256), 0, st, s.N, s.H,
-                     r, n_groups, total, ld, (const bf16*)Qn, (const bf16*)Pq, ct, st_, C, eps_lr,
-                     (const bf16*)Os, logits, eps, (bf16*)Out);
+  hipLaunchKernelGGL((readout_mfma_kernel<JT, COMBINE, GENERIC>), dim3(total), dim3(256), 0, st,
+                     s.N, s.H, r, n_groups, total, ld, feat, (const bf16*)Qn, (const bf16*)Pq, ct,
+                     st_, C, eps_lr, (const bf16*)Os, logits, eps, (bf16*)Out);
   return hipGetLastError();
+}
+
+template <int JT, bool COMBINE>
+hipError_t readout_mfma_feat(const Shape& s, const void* Qn, const void* Pq, int r,
+                             const float* ct, const float* st_, int ld, int feat, const float* C,
+                             float eps_lr, const void* Os, const float* logits, float eps,
+                             void* Out, hipStream_t st) {
+  if (feat == 0)
+    return readout_mfma<JT, COMBINE, false>(s, Qn, Pq, r, ct, st_, ld, feat, C, eps_lr, Os, logits,
+                                            eps, Out, st);
+  return readout_mfma<JT, COMBINE, true>(s, Qn, Pq, r, ct, st_, ld, feat, C, eps_lr, Os, logits,
+                                         eps, Out, st);
 }
 
 template <bool COMBINE>
 hipError_t readout_dispatch(const Shape& s, const void* Qn, const void* Pq, int r, const float* ct,
-                            const float* st_, int ld, const float* C, float eps_lr, const void* Os,
-                            const float* logits, float eps, void* Out, hipStream_t st) {
+                            const float* st_, int ld, int feat, const float* C, float eps_lr,
+                            const void* Os, const float* logits, float eps, void* Out,
+                            hipStream_t st) {
   if (s.bf16) {
     if (r <= 32)
-      return readout_mfma<1, COMBINE>(s, Qn, Pq, r, ct, st_, ld, C, eps_lr, Os, logits, eps, Out, st);
+      return readout_mfma_feat<1, COMBINE>(s, Qn, Pq, r, ct, st_, ld, feat, C, eps_lr, Os, logits,
+                                           eps, Out, st);
     if (r <= 64)
-      return readout_mfma<2, COMBINE>(s, Qn, Pq, r, ct, st_, ld, C, eps_lr, Os, logits, eps, Out, st);
-    return readout_mfma<4, COMBINE>(s, Qn, Pq, r, ct, st_, ld, C, eps_lr, Os, logits, eps, Out, st);
+      return readout_mfma_feat<2, COMBINE>(s, Qn, Pq, r, ct, st_, ld, feat, C, eps_lr, Os, logits,
+                                           eps, Out, st);
+    return readout_mfma_feat<4, COMBINE>(s, Qn, Pq, r, ct, st_, ld, feat, C, eps_lr, Os, logits,
+                                         eps, Out, st);
   }
   const dim3 grid((s.N + 31) / 32, s.H, s.B);
   if (s.d == 64)
     hipLaunchKernelGGL((readout_simple_kernel<float, 64, COMBINE>), grid, dim3(256), 0, st, s.N,
-                       s.H, r, ld, (const float*)Qn, (const float*)Pq, ct, st_, C, eps_lr,
+                       s.H, r, ld, feat, (const float*)Qn, (const float*)Pq, ct, st_, C, eps_lr,
                        (const float*)Os, logits, eps, (float*)Out);
   else
     hipLaunchKernelGGL((readout_simple_kernel<float, 128, COMBINE>), grid, dim3(256), 0, st, s.N,
-                       s.H, r, ld, (const float*)Qn, (const float*)Pq, ct, st_, C, eps_lr,
+                       s.H, r, ld, feat, (const float*)Qn, (const float*)Pq, ct, st_, C, eps_lr,
                        (const float*)Os, logits, eps, (float*)Out);
   return hipGetLastError();
 }
@@ -709,24 +811,30 @@ size_t summary_workspace_bytes(const Shape& s, int r) {
 
 hipError_t launch_lowrank_summary(const Shape& s, const void* Kn, const void* V, const void* Pk,
                                   int r, const float* cos_tab, const float* sin_tab, int ld,
-                                  float* C, float* z, void* ws, hipStream_t st) {
+                                  int feat, float* C, float* z, void* ws, hipStream_t st) {
   const int chunk_len = summary_chunk_len(s);
   const int n_chunks = (s.N + chunk_len - 1) / chunk_len;
   float* part = (float*)ws;
   hipError_t e;
   if (s.bf16) {
-    if (r <= 32) e = summary_mfma<1>(s, Kn, V, Pk, r, cos_tab, sin_tab, ld, part, chunk_len, n_chunks, st);
-    else if (r <= 64) e = summary_mfma<2>(s, Kn, V, Pk, r, cos_tab, sin_tab, ld, part, chunk_len, n_chunks, st);
-    else e = summary_mfma<4>(s, Kn, V, Pk, r, cos_tab, sin_tab, ld, part, chunk_len, n_chunks, st);
+    if (r <= 32)
+      e = summary_mfma_feat<1>(s, Kn, V, Pk, r, cos_tab, sin_tab, ld, feat, part, chunk_len,
+                               n_chunks, st);
+    else if (r <= 64)
+      e = summary_mfma_feat<2>(s, Kn, V, Pk, r, cos_tab, sin_tab, ld, feat, part, chunk_len,
+                               n_chunks, st);
+    else
+      e = summary_mfma_feat<4>(s, Kn, V, Pk, r, cos_tab, sin_tab, ld, feat, part, chunk_len,
+                               n_chunks, st);
   } else {
     const dim3 grid(n_chunks, s.H, s.B);
     if (s.d == 64)
       hipLaunchKernelGGL((summary_simple_kernel<float, 64>), grid, dim3(256), 0, st, s.N, s.H, r,
-                         chunk_len, n_chunks, ld, (const float*)Kn, (const float*)V,
+                         chunk_len, n_chunks, ld, feat, (const float*)Kn, (const float*)V,
                          (const float*)Pk, cos_tab, sin_tab, part);
     else
       hipLaunchKernelGGL((summary_simple_kernel<float, 128>), grid, dim3(256), 0, st, s.N, s.H, r,
-                         chunk_len, n_chunks, ld, (const float*)Kn, (const float*)V,
+                         chunk_len, n_chunks, ld, feat, (const float*)Kn, (const float*)V,
                          (const float*)Pk, cos_tab, sin_tab, part);
     e = hipGetLastError();
   }
@@ -738,14 +846,37 @@ hipError_t launch_lowrank_summary(const Shape& s, const void* Kn, const void* V,
 }
 
 hipError_t launch_lowrank_readout(const Shape& s, const void* Qn, const void* Pq, int r,
-                                  const float* cos_tab, const float* sin_tab, int ld,
+                                  const float* cos_tab, const float* sin_tab, int ld, int feat,
                                   const float* C, float eps_lr, const void* Os,
                                   const float* logits, float eps, void* Out, hipStream_t st) {
   if (Os)
-    return readout_dispatch<true>(s, Qn, Pq, r, cos_tab, sin_tab, ld, C, eps_lr, Os, logits, eps,
-                                  Out, st);
-  return readout_dispatch<false>(s, Qn, Pq, r, cos_tab, sin_tab, ld, C, eps_lr, nullptr, nullptr,
-                                 0.f, Out, st);
+    return readout_dispatch<true>(s, Qn, Pq, r, cos_tab, sin_tab, ld, feat, C, eps_lr, Os, logits,
+                                  eps, Out, st);
+  return readout_dispatch<false>(s, Qn, Pq, r, cos_tab, sin_tab, ld, feat, C, eps_lr, nullptr,
+                                 nullptr, 0.f, Out, st);
+}
+
+hipError_t launch_lowrank_features(const Shape& s, const void* X, const void* P, int r,
+                                   const float* cos_tab, const float* sin_tab, int ld, int feat,
+                                   float* F, hipStream_t st) {
+  const long total = (long)s.B * s.H * s.N * (r / 2);
+  const dim3 grid((unsigned)((total + 255) / 256));
+  if (s.bf16) {
+    if (s.d == 64)
+      hipLaunchKernelGGL((features_kernel<bf16, 64>), grid, dim3(256), 0, st, total, s.N, s.H, r,
+                         ld, feat, (const bf16*)X, (const bf16*)P, cos_tab, sin_tab, F);
+    else
+      hipLaunchKernelGGL((features_kernel<bf16, 128>), grid, dim3(256), 0, st, total, s.N, s.H, r,
+                         ld, feat, (const bf16*)X, (const bf16*)P, cos_tab, sin_tab, F);
+  } else {
+    if (s.d == 64)
+      hipLaunchKernelGGL((features_kernel<float, 64>), grid, dim3(256), 0, st, total, s.N, s.H, r,
+                         ld, feat, (const float*)X, (const float*)P, cos_tab, sin_tab, F);
+    else
+      hipLaunchKernelGGL((features_kernel<float, 128>), grid, dim3(256), 0, st, total, s.N, s.H, r,
+                         ld, feat, (const float*)X, (const float*)P, cos_tab, sin_tab, F);
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_combine(const Shape& s, const void* Os, const void* Olr, const float* logits,

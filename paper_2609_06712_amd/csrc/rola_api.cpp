@@ -78,6 +78,15 @@ rola_status check_rank(const rola::Shape& s, int32_t r, const char* fn) {
   return ROLA_OK;
 }
 
+rola_status check_feature(int32_t phi, int32_t order, const char* fn, int* feat) {
+  if (phi < ROLA_PHI_SILU || phi > ROLA_PHI_GELU)
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: unknown feature map phi = %d", fn, (int)phi);
+  if (order < ROLA_ROPE_OUTSIDE || order > ROLA_ROPE_NONE)
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: unknown rotation order %d", fn, (int)order);
+  *feat = phi | order << 8;  // the kernels' encoding
+  return ROLA_OK;
+}
+
 rola_status check_tables(const float* c, const float* s, int32_t ld, int32_t need, const char* fn) {
   if (!aligned(c) || !aligned(s))
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: rotary tables null or not 16-byte aligned", fn);
@@ -237,13 +246,16 @@ rola_status rola_dense_attn(const rola_problem* p, const void* Qr, const void* K
                                              nullptr, stream), __func__);
 }
 
-rola_status rola_lowrank_summary(const rola_problem* p, const void* Kn, const void* V,
-                                 const void* Pk, int32_t r, const float* cos_tab,
-                                 const float* sin_tab, int32_t rope_ld, float* C, float* z,
-                                 void* ws, size_t ws_bytes, hipStream_t stream) {
+rola_status rola_lowrank_summary_ex(const rola_problem* p, const void* Kn, const void* V,
+                                    const void* Pk, int32_t r, const float* cos_tab,
+                                    const float* sin_tab, int32_t rope_ld, int32_t phi,
+                                    int32_t rope_order, float* C, float* z, void* ws,
+                                    size_t ws_bytes, hipStream_t stream) {
   rola::Shape s;
+  int feat = 0;
   TRY(check_problem(p, __func__, &s));
   TRY(check_rank(s, r, __func__));
+  TRY(check_feature(phi, rope_order, __func__, &feat));
   REQUIRE_PTR(Kn);
   REQUIRE_PTR(V);
   REQUIRE_PTR(Pk);
@@ -255,16 +267,27 @@ rola_status rola_lowrank_summary(const rola_problem* p, const void* Kn, const vo
   const size_t need = rola::summary_workspace_bytes(s, r);
   if (ws_bytes < need)
     return fail(ROLA_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", __func__, ws_bytes, need);
-  return hip_status(rola::launch_lowrank_summary(s, Kn, V, Pk, r, cos_tab, sin_tab, rope_ld, C, z,
-                                                 ws, stream), __func__);
+  return hip_status(rola::launch_lowrank_summary(s, Kn, V, Pk, r, cos_tab, sin_tab, rope_ld, feat,
+                                                 C, z, ws, stream), __func__);
 }
 
-rola_status rola_lowrank_readout(const rola_problem* p, const void* Qn, const void* Pq, int32_t r,
-                                 const float* cos_tab, const float* sin_tab, int32_t rope_ld,
-                                 const float* C, float eps_lr, void* Olr, hipStream_t stream) {
+rola_status rola_lowrank_summary(const rola_problem* p, const void* Kn, const void* V,
+                                 const void* Pk, int32_t r, const float* cos_tab,
+                                 const float* sin_tab, int32_t rope_ld, float* C, float* z,
+                                 void* ws, size_t ws_bytes, hipStream_t stream) {
+  return rola_lowrank_summary_ex(p, Kn, V, Pk, r, cos_tab, sin_tab, rope_ld, ROLA_PHI_SILU,
+                                 ROLA_ROPE_OUTSIDE, C, z, ws, ws_bytes, stream);
+}
+
+rola_status rola_lowrank_readout_ex(const rola_problem* p, const void* Qn, const void* Pq, int32_t r,
+                                    const float* cos_tab, const float* sin_tab, int32_t rope_ld,
+                                    int32_t phi, int32_t rope_order, const float* C, float eps_lr,
+                                    void* Olr, hipStream_t stream) {
   rola::Shape s;
+  int feat = 0;
   TRY(check_problem(p, __func__, &s));
   TRY(check_rank(s, r, __func__));
+  TRY(check_feature(phi, rope_order, __func__, &feat));
   REQUIRE_PTR(Qn);
   REQUIRE_PTR(Pq);
   REQUIRE_PTR(C);
@@ -272,8 +295,32 @@ rola_status rola_lowrank_readout(const rola_problem* p, const void* Qn, const vo
   TRY(check_tables(cos_tab, sin_tab, rope_ld, r / 2, __func__));
   if (!(eps_lr >= 0.f) || !isfinite(eps_lr))
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: eps_lr must be finite and >= 0", __func__);
-  return hip_status(rola::launch_lowrank_readout(s, Qn, Pq, r, cos_tab, sin_tab, rope_ld, C, eps_lr,
-                                                 nullptr, nullptr, 0.f, Olr, stream), __func__);
+  return hip_status(rola::launch_lowrank_readout(s, Qn, Pq, r, cos_tab, sin_tab, rope_ld, feat, C,
+                                                 eps_lr, nullptr, nullptr, 0.f, Olr, stream),
+                    __func__);
+}
+
+rola_status rola_lowrank_readout(const rola_problem* p, const void* Qn, const void* Pq, int32_t r,
+                                 const float* cos_tab, const float* sin_tab, int32_t rope_ld,
+                                 const float* C, float eps_lr, void* Olr, hipStream_t stream) {
+  return rola_lowrank_readout_ex(p, Qn, Pq, r, cos_tab, sin_tab, rope_ld, ROLA_PHI_SILU,
+                                 ROLA_ROPE_OUTSIDE, C, eps_lr, Olr, stream);
+}
+
+rola_status rola_lowrank_features(const rola_problem* p, const void* X, const void* P, int32_t r,
+                                  const float* cos_tab, const float* sin_tab, int32_t rope_ld,
+                                  int32_t phi, int32_t rope_order, float* F, hipStream_t stream) {
+  rola::Shape s;
+  int feat = 0;
+  TRY(check_problem(p, __func__, &s));
+  TRY(check_rank(s, r, __func__));
+  TRY(check_feature(phi, rope_order, __func__, &feat));
+  REQUIRE_PTR(X);
+  REQUIRE_PTR(P);
+  REQUIRE_PTR(F);
+  TRY(check_tables(cos_tab, sin_tab, rope_ld, r / 2, __func__));
+  return hip_status(rola::launch_lowrank_features(s, X, P, r, cos_tab, sin_tab, rope_ld, feat, F,
+                                                  stream), __func__);
 }
 
 rola_status rola_combine(const rola_problem* p, const void* Os, const void* Olr,
@@ -290,14 +337,17 @@ rola_status rola_combine(const rola_problem* p, const void* Os, const void* Olr,
   return hip_status(rola::launch_combine(s, Os, Olr, gate_logits, eps, O, stream), __func__);
 }
 
-rola_status rola_lowrank_readout_combine(const rola_problem* p, const void* Qn, const void* Pq,
-                                         int32_t r, const float* cos_tab, const float* sin_tab,
-                                         int32_t rope_ld, const float* C, float eps_lr,
-                                         const void* Os, const float* gate_logits, float eps,
-                                         void* O, hipStream_t stream) {
+rola_status rola_lowrank_readout_combine_ex(const rola_problem* p, const void* Qn, const void* Pq,
+                                            int32_t r, const float* cos_tab, const float* sin_tab,
+                                            int32_t rope_ld, int32_t phi, int32_t rope_order,
+                                            const float* C, float eps_lr, const void* Os,
+                                            const float* gate_logits, float eps, void* O,
+                                            hipStream_t stream) {
   rola::Shape s;
+  int feat = 0;
   TRY(check_problem(p, __func__, &s));
   TRY(check_rank(s, r, __func__));
+  TRY(check_feature(phi, rope_order, __func__, &feat));
   REQUIRE_PTR(Qn);
   REQUIRE_PTR(Pq);
   REQUIRE_PTR(C);
@@ -307,8 +357,19 @@ rola_status rola_lowrank_readout_combine(const rola_problem* p, const void* Qn, 
   TRY(check_tables(cos_tab, sin_tab, rope_ld, r / 2, __func__));
   if (!(eps_lr >= 0.f) || !isfinite(eps_lr) || !(eps >= 0.f) || !isfinite(eps))
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: eps values must be finite and >= 0", __func__);
-  return hip_status(rola::launch_lowrank_readout(s, Qn, Pq, r, cos_tab, sin_tab, rope_ld, C, eps_lr,
-                                                 Os, gate_logits, eps, O, stream), __func__);
+  return hip_status(rola::launch_lowrank_readout(s, Qn, Pq, r, cos_tab, sin_tab, rope_ld, feat, C,
+                                                 eps_lr, Os, gate_logits, eps, O, stream),
+                    __func__);
+}
+
+rola_status rola_lowrank_readout_combine(const rola_problem* p, const void* Qn, const void* Pq,
+                                         int32_t r, const float* cos_tab, const float* sin_tab,
+                                         int32_t rope_ld, const float* C, float eps_lr,
+                                         const void* Os, const float* gate_logits, float eps,
+                                         void* O, hipStream_t stream) {
+  return rola_lowrank_readout_combine_ex(p, Qn, Pq, r, cos_tab, sin_tab, rope_ld, ROLA_PHI_SILU,
+                                         ROLA_ROPE_OUTSIDE, C, eps_lr, Os, gate_logits, eps, O,
+                                         stream);
 }
 
 }  // extern "C"

@@ -47,7 +47,22 @@ SIGNATURES = {
     "rola_combine": (_i32, [_PP, _p, _p, _p, _f32, _p, _p]),
     "rola_lowrank_readout_combine": (_i32, [_PP, _p, _p, _i32, _p, _p, _i32, _p, _f32, _p, _p, _f32,
                                             _p, _p]),
+    "rola_lowrank_summary_ex": (_i32, [_PP, _p, _p, _p, _i32, _p, _p, _i32, _i32, _i32, _p, _p, _p,
+                                       _sz, _p]),
+    "rola_lowrank_readout_ex": (_i32, [_PP, _p, _p, _i32, _p, _p, _i32, _i32, _i32, _p, _f32, _p,
+                                       _p]),
+    "rola_lowrank_readout_combine_ex": (_i32, [_PP, _p, _p, _i32, _p, _p, _i32, _i32, _i32, _p, _f32,
+                                               _p, _p, _f32, _p, _p]),
+    "rola_lowrank_features": (_i32, [_PP, _p, _p, _i32, _p, _p, _i32, _i32, _i32, _p, _p]),
 }
+
+# Feature map and rotation order of the low-rank branch (rola_phi, rola_rope_order).
+PHI = {"silu": 0, "identity": 1, "tanh": 2, "relu": 3, "gelu": 4}
+ROPE_ORDER = {"outside": 0, "inside": 1, "none": 2}
+
+
+def _code(table, v):
+    return table[v] if isinstance(v, str) else int(v)
 
 
 def _load():
@@ -233,4 +248,61 @@ def rola_lowrank_readout_combine(Qn, Pq, r, cos, sin, C, Os, logits, grid, eps_l
                                             _ptr(sin), cos.stride(0), _ptr(C), eps_lr, _ptr(Os),
                                             _ptr(logits), eps, _ptr(out), _stream(stream)),
            "rola_lowrank_readout_combine")
+    return out
+
+
+def rola_lowrank_summary_ex(Kn, V, Pk, r, cos, sin, grid, phi="silu", rope_order="outside", C=None,
+                            z=None, ws=None, stream=None, want_z=True):
+    _act(Kn, "Kn")
+    prob = problem_of(Kn, grid)
+    if C is None:
+        C = torch.empty((prob.B, prob.H, r, prob.d_h), dtype=torch.float32, device=Kn.device)
+    if z is None and want_z:
+        z = torch.empty((prob.B, prob.H, r), dtype=torch.float32, device=Kn.device)
+    need = summary_workspace_bytes(prob, r)
+    if ws is None:
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=Kn.device)
+    _check(LIB.rola_lowrank_summary_ex(ctypes.byref(prob), _ptr(Kn), _ptr(V), _ptr(Pk), r, _ptr(cos),
+                                       _ptr(sin), cos.stride(0), _code(PHI, phi),
+                                       _code(ROPE_ORDER, rope_order), _ptr(C), _ptr(z), _ptr(ws),
+                                       ws.numel(), _stream(stream)), "rola_lowrank_summary_ex")
+    return C, z
+
+
+def rola_lowrank_readout_ex(Qn, Pq, r, cos, sin, C, grid, phi="silu", rope_order="outside",
+                            eps_lr=1e-6, out=None, stream=None):
+    _act(Qn, "Qn")
+    prob = problem_of(Qn, grid)
+    out = torch.empty_like(Qn) if out is None else out
+    _check(LIB.rola_lowrank_readout_ex(ctypes.byref(prob), _ptr(Qn), _ptr(Pq), r, _ptr(cos),
+                                       _ptr(sin), cos.stride(0), _code(PHI, phi),
+                                       _code(ROPE_ORDER, rope_order), _ptr(C), eps_lr, _ptr(out),
+                                       _stream(stream)), "rola_lowrank_readout_ex")
+    return out
+
+
+def rola_lowrank_readout_combine_ex(Qn, Pq, r, cos, sin, C, Os, logits, grid, phi="silu",
+                                    rope_order="outside", eps_lr=1e-6, eps=1e-6, out=None,
+                                    stream=None):
+    _act(Qn, "Qn")
+    prob = problem_of(Qn, grid)
+    out = torch.empty_like(Os) if out is None else out
+    _check(LIB.rola_lowrank_readout_combine_ex(ctypes.byref(prob), _ptr(Qn), _ptr(Pq), r, _ptr(cos),
+                                               _ptr(sin), cos.stride(0), _code(PHI, phi),
+                                               _code(ROPE_ORDER, rope_order), _ptr(C), eps_lr,
+                                               _ptr(Os), _ptr(logits), eps, _ptr(out),
+                                               _stream(stream)), "rola_lowrank_readout_combine_ex")
+    return out
+
+
+def rola_lowrank_features(X, P, r, cos, sin, grid, phi="silu", rope_order="outside", out=None,
+                          stream=None):
+    """q~ (X = Q^n, P = P_q) or k~ (X = K^n, P = P_k) of every token: fp32 [B, H, N, r]."""
+    _act(X, "X")
+    prob = problem_of(X, grid)
+    if out is None:
+        out = torch.empty((prob.B, prob.H, prob.N, r), dtype=torch.float32, device=X.device)
+    _check(LIB.rola_lowrank_features(ctypes.byref(prob), _ptr(X), _ptr(P), r, _ptr(cos), _ptr(sin),
+                                     cos.stride(0), _code(PHI, phi), _code(ROPE_ORDER, rope_order),
+                                     _ptr(out), _stream(stream)), "rola_lowrank_features")
     return out

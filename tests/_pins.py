@@ -60,3 +60,22 @@ def sdpa_f64(q, k, v):
 
 def silu_ref(x):
     return x * (1.0 / (1.0 + np.exp(-x)))
+
+
+def activation_ref(x, phi):
+    """The ablation's feature maps written independently of the oracle: tanh through exponentials,
+    ReLU as (x + |x|) / 2, GELU through scipy's normal CDF."""
+    from scipy.stats import norm
+    x = np.asarray(x, dtype=np.float64)
+    if phi == "silu":
+        return silu_ref(x)
+    if phi == "identity":
+        return x
+    if phi == "tanh":
+        e = np.exp(-2.0 * np.abs(x))
+        return np.sign(x) * (1.0 - e) / (1.0 + e)
+    if phi == "relu":
+        return 0.5 * (x + np.abs(x))
+    if phi == "gelu":
+        return x * norm.cdf(x)
+    raise ValueError(phi)

@@ -127,6 +127,21 @@ def test_invalid_arguments_are_rejected_before_launch():
         (R.ROLA_ERR_INVALID_ARGUMENT, "rola_rope_apply", P(ok), FAKE, FAKE, FAKE, 64, FAKE, None),
         (R.ROLA_ERR_INVALID_ARGUMENT, "rola_lowrank_readout_combine", P(ok), FAKE, FAKE, 32, FAKE, FAKE,
          64, FAKE, 1e-6, None, FAKE, 1e-6, FAKE, None),
+        # feature-map variants: unknown phi or rotation order
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_lowrank_summary_ex", P(ok), FAKE, FAKE, FAKE, 32, FAKE,
+         FAKE, 64, 5, 0, FAKE, None, FAKE, 1 << 40, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_lowrank_summary_ex", P(ok), FAKE, FAKE, FAKE, 32, FAKE,
+         FAKE, 64, 0, 3, FAKE, None, FAKE, 1 << 40, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_lowrank_readout_ex", P(ok), FAKE, FAKE, 32, FAKE, FAKE, 64,
+         -1, 0, FAKE, 1e-6, FAKE, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_lowrank_readout_combine_ex", P(ok), FAKE, FAKE, 32, FAKE,
+         FAKE, 64, 0, 7, FAKE, 1e-6, FAKE, FAKE, 1e-6, FAKE, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_lowrank_features", P(ok), FAKE, FAKE, 32, FAKE, FAKE, 64,
+         9, 0, FAKE, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_lowrank_features", P(ok), FAKE, FAKE, 32, FAKE, FAKE, 64,
+         0, 0, None, None),
+        (R.ROLA_ERR_UNSUPPORTED, "rola_lowrank_features", P(ok), FAKE, FAKE, 48, FAKE, FAKE, 64, 0, 0,
+         FAKE, None),
     ]
     for want, name, *args in cases:
         got = _call(name, *args)

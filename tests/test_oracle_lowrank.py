@@ -216,3 +216,93 @@ def test_flop_accounting_matches_simplified_forms():
         f = O.flop_counts(B, H, L, d, r, S)
         assert abs(f["eta"] - (2 * r + 0.5) / (L * (1 - S))) < 1e-12 * f["eta"]
         assert abs(f["lowrank"] / (4.0 * B * H * L * d * d) - 2.0 * r / d) < 1e-15
+
+
+# ---- feature-map and rotation-order variants (Sec. 5.1 RoPE placement, Sec. 5.3 activation
+# ablation, Prop. exact, Prop. inside) -------------------------------------------------------------
+
+PHIS = ("silu", "identity", "tanh", "relu", "gelu")
+
+
+def test_activation_golden_values():
+    """Each feature map at points whose value is fixed by its definition (tests/golden)."""
+    for phi, x, want in _golden("activations.txt"):
+        got = O.activation(np.array([float(x)]), phi)[0]
+        assert got == pytest.approx(float(want), abs=1e-14), (phi, x)
+
+
+def test_activation_odd_parts():
+    """sigma(x) + sigma(-x) = 1 and Phi(x) + Phi(-x) = 1 give f(x) - f(-x) = x for SiLU and GELU; ReLU
+    also gives x; tanh is odd; identity gives 2x. Checks signs and dropped terms on a grid."""
+    x = np.linspace(-6, 6, 241)
+    odd = {"silu": x, "gelu": x, "relu": x, "identity": 2 * x, "tanh": 0 * x}
+    for phi in PHIS:
+        f = O.activation(x, phi)
+        np.testing.assert_allclose(f - O.activation(-x, phi) if phi != "tanh" else f + O.activation(-x, phi),
+                                   odd[phi], atol=1e-13, err_msg=phi)
+        np.testing.assert_allclose(f, P.activation_ref(x, phi), atol=1e-13, err_msg=phi)
+
+
+@pytest.mark.parametrize("phi", PHIS)
+def test_variant_readout_equals_relative_bruteforce(phi):
+    """Prop. exact holds for any position-free feature map: with the rotation outside, the
+    summary-then-readout path equals the O(N^2) relative form sum_q phi(P_q q_p)^T R_r(q - p)
+    phi(P_k k_q) v_q (explicit rotations, activation written independently)."""
+    grid, split, r = (2, 3, 4), (28, 18, 18), 16
+    N, d = int(np.prod(grid)), sum(split)
+    qn, kn, v, Pq, Pk = _content(N, d, r, 5)
+    cos, sin = O.rope_tables(*grid, split)
+    C, _ = O.lowrank_summary(kn, v, Pk, cos, sin, phi=phi)
+    got = O.lowrank_readout_u(qn, Pq, cos, sin, C, phi=phi)
+    fq, fk = P.activation_ref(qn @ Pq.T, phi), P.activation_ref(kn @ Pk.T, phi)
+    pos = P.positions(grid)
+    want = np.zeros((N, d))
+    for p in range(N):
+        for q in range(N):
+            want[p] += (fq[p] @ P.rotation(split, pos[q] - pos[p], r=r) @ fk[q]) * v[q]
+    np.testing.assert_allclose(got, want, atol=1e-10)
+
+
+def test_inside_and_none_orderings_closed_forms():
+    """Inside: phi(R_r(p) P x) written with explicit rotation matrices. Identity commutes with the
+    rotation, so inside and outside coincide for it. None: phi(P x) with no position at all."""
+    grid, split, r = (2, 3, 4), (28, 18, 18), 16
+    N, d = int(np.prod(grid)), sum(split)
+    x, _, _, Pm, _ = _content(N, d, r, 6)
+    cos, sin = O.rope_tables(*grid, split)
+    pos = P.positions(grid)
+    for phi in PHIS:
+        want = np.stack([P.activation_ref(P.rotation(split, pos[n], r=r) @ (Pm @ x[n]), phi)
+                         for n in range(N)])
+        np.testing.assert_allclose(O.features(x, Pm, cos, sin, phi, "inside"), want, atol=1e-12)
+        np.testing.assert_allclose(O.features(x, Pm, cos, sin, phi, "none"),
+                                   P.activation_ref(x @ Pm.T, phi), atol=1e-12)
+    np.testing.assert_allclose(O.features(x, Pm, cos, sin, "identity", "inside"),
+                               O.features(x, Pm, cos, sin, "identity", "outside"), atol=1e-12)
+
+
+def test_shift_residual_by_phi_and_ordering():
+    """The Sec. 5.1 criterion for every feature map: with the rotation outside the logit depends on
+    the offset only (shift residual ~ 0, offset range > 0, Prop. exact); inside, every nonlinear map
+    leaks absolute position (Prop. inside) while the identity map does not; without rotation the
+    logit is position-blind (both exactly 0)."""
+    rng = np.random.default_rng(7)
+    split, r = (44, 42, 42), 32
+    Pq, Pk = (rng.standard_normal((r, 128)) / math.sqrt(128) for _ in range(2))
+    qv, kv = rng.standard_normal(128), rng.standard_normal(128)
+    p, q = np.array([2.0, 10, 20]), np.array([7.0, 10, 20])
+    for phi in PHIS:
+        for ordering in ("outside", "inside", "none"):
+            s0 = O.lowrank_logit(qv, kv, Pq, Pk, p, q, split, ordering=ordering, phi=phi)
+            res = max(abs(O.lowrank_logit(qv, kv, Pq, Pk, p + dl, q + dl, split, ordering=ordering,
+                                          phi=phi) - s0)
+                      for dl in (np.array([5.0, 0, 0]), np.array([11.0, 0, 0])))
+            offs = [O.lowrank_logit(qv, kv, Pq, Pk, p, p + np.array([dt, 0, 0]), split,
+                                    ordering=ordering, phi=phi) for dt in range(-8, 9)]
+            span = max(offs) - min(offs)
+            if ordering == "none":
+                assert res == 0.0 and span == 0.0, phi
+            elif ordering == "outside" or phi == "identity":
+                assert res < 1e-10 and span > 1e-3, (phi, ordering, res, span)
+            else:
+                assert res > 1e-4 and span > 1e-3, (phi, ordering, res, span)
