@@ -229,6 +229,22 @@ def sweep(reps: int) -> None:
     del inp, C, z, ws, out
     print()
 
+    # gate logits X W_g + b_g (Sec. 4.4; Algorithm step 8) at the 14B 720p shape
+    print("## Gate logits X W_g + b_g, N 75600, d_model 5120 bf16 (HBM roofline 8 TB/s)\n")
+    print("| bytes (MB) | warm ms | warm GB/s | cold ms | cold GB/s | cold % of 8 TB/s |")
+    print("|---|---|---|---|---|---|", flush=True)
+    gen = torch.Generator(device=dev).manual_seed(5)
+    X = torch.randn((1, 75600, 5120), generator=gen, device=dev).to(torch.bfloat16)
+    Wg = (torch.randn((5120,), generator=gen, device=dev) / 5120 ** 0.5).to(torch.bfloat16)
+    lg = torch.empty((1, 75600), dtype=torch.float32, device=dev)
+    nbytes = X.numel() * 2 + lg.numel() * 4
+    fn = lambda: R.rola_gate_logits(X, Wg, -1.946, (21, 45, 80), out=lg)  # noqa: E731
+    wm = time_call(fn, reps)[0]
+    cm = time_call(fn, reps, cold=evict)[0]
+    print(f"| {nbytes / 1e6:.0f} | {wm:.4f} | {nbytes / wm / 1e6:.0f} | {cm:.4f} | {nbytes / cm / 1e6:.0f} | "
+          f"{100 * nbytes / cm / 1e6 / PEAK_HBM_GBS:.1f} |\n", flush=True)
+    del X, Wg, lg
+
     # sparse branch: sparsity x block, dense reference
     print("## Sparse branch, H40 d128 N75600 bf16 (MFMA roofline 2.5 PFLOP/s)\n")
     print("| block | sparsity | keep | select ms | sparse ms | TFLOP/s performed | % of peak | "

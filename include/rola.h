@@ -191,6 +191,14 @@ rola_status rola_lowrank_features(const rola_problem* p, const void* X, const vo
 
 /* ---- gated fusion (Sec. 4.4, eq. gate; Algorithm steps 8-10) --------------------------------- */
 
+/* Gate logits of the token-wise gate g = sigmoid(X W_g + b_g) (Sec. 4.4; Algorithm step 8):
+ * logits[b, n] = sum_i X[b, n, i] W_g[i] + b_g, fp32 accumulation, fp32 [B, N]; rola_combine and
+ * rola_lowrank_readout_combine take these logits and apply the sigmoid. X: the attention block's
+ * input hidden states [B, N, d_model] in p->dtype (p->H and p->d_h are not used); W_g: [d_model] in
+ * p->dtype; d_model a multiple of 8, at most 16384 (else ROLA_ERR_UNSUPPORTED). */
+rola_status rola_gate_logits(const rola_problem* p, const void* X, int32_t d_model, const void* Wg,
+                             float bg, float* logits, hipStream_t stream);
+
 /* O_p = (O^s_p / r_p + g_p O^lr_p) r_p, r_p = sqrt(mean_i (O^s_{p,i})^2 + eps), g_p =
  * 1/(1 + exp(-logit_{b,p})). O may alias Os (in place); it must not overlap Olr otherwise. */
 rola_status rola_combine(const rola_problem* p, const void* Os, const void* Olr,

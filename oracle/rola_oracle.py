@@ -47,7 +47,7 @@ __all__ = [
     "sparse_attention", "sparse_attention_rows", "silu", "lowrank_features", "lowrank_summary",
     "lowrank_readout_u", "rms_normalize", "lowrank_readout", "gate", "combine", "forward_head",
     "forward", "inside_features", "norope_features", "lowrank_logit", "flop_counts", "activation",
-    "features",
+    "features", "gate_logits",
 ]
 
 # --------------------------------------------------------------------------------------------------
@@ -288,6 +288,12 @@ def lowrank_readout(qn, Pq, cos, sin, C, eps_lr: float = 1e-6, phi: str = "silu"
 # --------------------------------------------------------------------------------------------------
 # Gated fusion  (Sec. 4.4, eq. gate; Algorithm, steps 8-10)
 # --------------------------------------------------------------------------------------------------
+
+
+def gate_logits(X: np.ndarray, Wg: np.ndarray, bg: float) -> np.ndarray:
+    """The gate's pre-activation X W_g + b_g over the block's input hidden states (Sec. 4.4;
+    Algorithm step 8). X: [..., d_model], W_g: [d_model] -> [...]."""
+    return np.asarray(X, np.float64) @ np.asarray(Wg, np.float64) + float(bg)
 
 
 def gate(logits: np.ndarray) -> np.ndarray:

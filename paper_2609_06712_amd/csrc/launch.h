@@ -55,4 +55,9 @@ hipError_t launch_lowrank_features(const Shape& s, const void* X, const void* P,
 hipError_t launch_combine(const Shape& s, const void* Os, const void* Olr, const float* logits,
                           float eps, void* O, hipStream_t st);
 
+// gate.hip: logits [B, N] = X [B, N, d_model] . Wg + bg (d_model % 8 == 0, <= gate_max_model()).
+hipError_t launch_gate_logits(const Shape& s, const void* X, int d_model, const void* Wg, float bg,
+                              float* logits, hipStream_t st);
+int gate_max_model();
+
 }  // namespace rola

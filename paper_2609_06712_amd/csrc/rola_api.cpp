@@ -323,6 +323,23 @@ rola_status rola_lowrank_features(const rola_problem* p, const void* X, const vo
                                                   stream), __func__);
 }
 
+rola_status rola_gate_logits(const rola_problem* p, const void* X, int32_t d_model, const void* Wg,
+                             float bg, float* logits, hipStream_t stream) {
+  rola::Shape s;
+  TRY(check_problem(p, __func__, &s));
+  REQUIRE_PTR(X);
+  REQUIRE_PTR(Wg);
+  REQUIRE_PTR(logits);
+  if (d_model <= 0 || (d_model % 8) != 0)
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: d_model=%d must be a positive multiple of 8", __func__,
+                (int)d_model);
+  if (d_model > rola::gate_max_model())
+    return fail(ROLA_ERR_UNSUPPORTED, "%s: d_model=%d above %d", __func__, (int)d_model,
+                rola::gate_max_model());
+  if (!isfinite(bg)) return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: b_g must be finite", __func__);
+  return hip_status(rola::launch_gate_logits(s, X, d_model, Wg, bg, logits, stream), __func__);
+}
+
 rola_status rola_combine(const rola_problem* p, const void* Os, const void* Olr,
                          const float* gate_logits, float eps, void* O, hipStream_t stream) {
   rola::Shape s;

@@ -54,6 +54,7 @@ SIGNATURES = {
     "rola_lowrank_readout_combine_ex": (_i32, [_PP, _p, _p, _i32, _p, _p, _i32, _i32, _i32, _p, _f32,
                                                _p, _p, _f32, _p, _p]),
     "rola_lowrank_features": (_i32, [_PP, _p, _p, _i32, _p, _p, _i32, _i32, _i32, _p, _p]),
+    "rola_gate_logits": (_i32, [_PP, _p, _i32, _p, _f32, _p, _p]),
 }
 
 # Feature map and rotation order of the low-rank branch (rola_phi, rola_rope_order).
@@ -305,4 +306,17 @@ def rola_lowrank_features(X, P, r, cos, sin, grid, phi="silu", rope_order="outsi
     _check(LIB.rola_lowrank_features(ctypes.byref(prob), _ptr(X), _ptr(P), r, _ptr(cos), _ptr(sin),
                                      cos.stride(0), _code(PHI, phi), _code(ROPE_ORDER, rope_order),
                                      _ptr(out), _stream(stream)), "rola_lowrank_features")
+    return out
+
+
+def rola_gate_logits(X, Wg, bg, grid, H=1, d_h=128, out=None, stream=None):
+    """Gate logits X W_g + b_g of every token: X [B, N, d_model], W_g [d_model] -> fp32 [B, N]."""
+    if not (X.is_cuda and X.dim() == 3 and X.is_contiguous()):
+        raise ValueError("X must be a contiguous [B, N, d_model] device tensor")
+    B, N, dm = X.shape
+    prob = problem(B, H, N, d_h, grid, X.dtype)
+    if out is None:
+        out = torch.empty((B, N), dtype=torch.float32, device=X.device)
+    _check(LIB.rola_gate_logits(ctypes.byref(prob), _ptr(X), dm, _ptr(Wg), bg, _ptr(out),
+                                _stream(stream)), "rola_gate_logits")
     return out

@@ -142,6 +142,12 @@ def test_invalid_arguments_are_rejected_before_launch():
          0, 0, None, None),
         (R.ROLA_ERR_UNSUPPORTED, "rola_lowrank_features", P(ok), FAKE, FAKE, 48, FAKE, FAKE, 64, 0, 0,
          FAKE, None),
+        # gate logits: d_model not a multiple of 8, too large, non-finite bias, null output
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_gate_logits", P(ok), FAKE, 5124, FAKE, -1.9, FAKE, None),
+        (R.ROLA_ERR_UNSUPPORTED, "rola_gate_logits", P(ok), FAKE, 16392, FAKE, -1.9, FAKE, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_gate_logits", P(ok), FAKE, 5120, FAKE, float("inf"), FAKE,
+         None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_gate_logits", P(ok), FAKE, 5120, FAKE, -1.9, None, None),
     ]
     for want, name, *args in cases:
         got = _call(name, *args)

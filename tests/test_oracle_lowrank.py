@@ -306,3 +306,20 @@ def test_shift_residual_by_phi_and_ordering():
                 assert res < 1e-10 and span > 1e-3, (phi, ordering, res, span)
             else:
                 assert res > 1e-4 and span > 1e-3, (phi, ordering, res, span)
+
+
+def test_gate_logits_closed_forms():
+    """Sec. 4.4 / Algorithm step 8: X W_g + b_g. One-hot hidden states pick one weight; constant
+    states give c * sum(W_g) + b_g; at the paper's initialisation (W_g = 0, b_g = b_0 = -1.946 of Tab.
+    hyper) every logit is b_0 and the gate is sigma(b_0) = 0.125 (b_0 = -ln 7 to four digits)."""
+    rng = np.random.default_rng(8)
+    dm = 24
+    Wg = rng.standard_normal(dm)
+    eye = np.eye(dm)
+    np.testing.assert_allclose(O.gate_logits(eye, Wg, 0.5), Wg + 0.5, atol=1e-15)
+    np.testing.assert_allclose(O.gate_logits(np.full((3, dm), 2.0), Wg, -1.0), 2.0 * Wg.sum() - 1.0,
+                               atol=1e-12)
+    X = rng.standard_normal((5, 7, dm))
+    b0 = -1.946
+    np.testing.assert_array_equal(O.gate_logits(X, np.zeros(dm), b0), np.full((5, 7), b0))
+    assert O.gate(np.array([b0]))[0] == pytest.approx(0.125, abs=1e-5)
