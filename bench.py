@@ -68,11 +68,10 @@ def sparse_flops_performed(idx: torch.Tensor, N: int, block: int, d: int) -> flo
     return float(4.0 * d * (keys * sizes).sum())
 
 
-def lowrank_bytes(w) -> float:
-    """HBM bytes the low-rank branch + fused combine must move: summary reads K^n, V; the fused
-    readout reads Q^n, O^s and writes O (2-byte elements), plus the rotary-table columns it uses."""
-    per_token_head = 5 * w.d_h * 2
-    return float(w.B * w.H * w.N * per_token_head + 2 * w.N * (w.r // 2) * 4)
+def summary_bytes(w) -> float:
+    """HBM bytes the low-rank summary must move: K^n and V (2-byte elements) plus the rotary-table
+    columns it uses."""
+    return float(w.B * w.H * w.N * 2 * w.d_h * 2 + 2 * w.N * (w.r // 2) * 4)
 
 
 def cpu_baseline(w, inp_cpu_head0: dict, budget_s: float) -> dict:
@@ -151,16 +150,16 @@ def sweep(reps: int) -> None:
     cos, sin = R.rola_rope_tables(prob, w.split, w.base)
     qr = R.rola_rope_apply(inp["Qn"], cos, sin, g)
     kr = R.rola_rope_apply(inp["Kn"], cos, sin, g)
-    ws_sp = torch.empty(max(R.sparse_workspace_bytes(prob, w.block, w.sparsity), 16), dtype=torch.uint8,
-                        device=dev)
+    ws_sp = torch.empty(R.sparse_combine_workspace_bytes(prob, w.block, w.sparsity, w.r),
+                        dtype=torch.uint8, device=dev)
     idx = R.rola_block_select(qr, kr, g, w.block, w.sparsity)
     o_s = torch.empty_like(qr)
 
     def layer():
         R.rola_block_select(qr, kr, g, w.block, w.sparsity, out=idx)
-        R.rola_sparse_attn(qr, kr, inp["V"], g, w.block, w.sparsity, idx, out=o_s, ws=ws_sp)
         C, _ = R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], w.r, cos, sin, g)
-        R.rola_lowrank_readout_combine(inp["Qn"], inp["Pq"], w.r, cos, sin, C, o_s, inp["logits"], g)
+        R.rola_sparse_attn_combine(qr, kr, inp["V"], g, w.block, w.sparsity, idx, inp["Qn"], inp["Pq"],
+                                   w.r, cos, sin, C, inp["logits"], out=o_s, ws=ws_sp)
     ms, lo, hi = time_call(layer, reps)
     f = sparse_flops_performed(idx, w.N, w.block, w.d_h) + 8.0 * w.B * w.H * w.N * w.d_h * w.r
     print(f"## Layer, {w.name}\n\n| ms (median) | p10 | p90 | eff. TFLOP/s |\n|---|---|---|---|")
@@ -319,14 +318,15 @@ def main():
     idx = torch.empty((w.B, w.H, nb, keep), dtype=torch.int32, device=dev)
     ws_sel = torch.empty(R.select_workspace_bytes(prob, w.block), dtype=torch.uint8, device=dev)
     ws_sum = torch.empty(R.summary_workspace_bytes(prob, w.r), dtype=torch.uint8, device=dev)
-    ws_sp = torch.empty(R.sparse_workspace_bytes(prob, w.block, w.sparsity), dtype=torch.uint8,
-                        device=dev)
-    o_s = torch.empty_like(inp["Qn"])
+    ws_sp = torch.empty(R.sparse_combine_workspace_bytes(prob, w.block, w.sparsity, w.r),
+                        dtype=torch.uint8, device=dev)
     out = torch.empty_like(inp["Qn"])
     C = torch.empty((w.B, w.H, w.r, w.d_h), dtype=torch.float32, device=dev)
     z = torch.empty((w.B, w.H, w.r), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
-    names = ["select", "sparse", "summary", "readout_combine"]
+    # the layer: selection, low-rank summary, then the sparse attention with the low-rank readout
+    # and the gated combine in its epilogue (O^s and O^lr never reach memory)
+    names = ["select", "summary", "sparse_readout_combine"]
 
     def step(ev=None):
         def mark(i):
@@ -335,13 +335,11 @@ def main():
         mark(0)
         R.rola_block_select(qr, kr, g, w.block, w.sparsity, out=idx, ws=ws_sel)
         mark(1)
-        R.rola_sparse_attn(qr, kr, inp["V"], g, w.block, w.sparsity, idx, out=o_s, ws=ws_sp)
-        mark(2)
         R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], w.r, cos, sin, g, C=C, z=z, ws=ws_sum)
+        mark(2)
+        R.rola_sparse_attn_combine(qr, kr, inp["V"], g, w.block, w.sparsity, idx, inp["Qn"],
+                                   inp["Pq"], w.r, cos, sin, C, inp["logits"], out=out, ws=ws_sp)
         mark(3)
-        R.rola_lowrank_readout_combine(inp["Qn"], inp["Pq"], w.r, cos, sin, C, o_s, inp["logits"], g,
-                                       out=out)
-        mark(4)
 
     if args.calibration_copy:  # a plain copy of known size, for scaling FETCH_SIZE / WRITE_SIZE
         scratch = torch.empty_like(inp["V"])
@@ -351,7 +349,8 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
+              for _ in range(args.steps)]
     print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -369,9 +368,8 @@ def main():
     f_sparse = sparse_flops_performed(idx, w.N, w.block, w.d_h)
     f_lowrank = 8.0 * w.B * w.H * w.N * w.d_h * w.r
     eff = (f_sparse + f_lowrank) / (ms * 1e-3) / 1e12
-    achieved = f_sparse / (kern_ms["sparse"] * 1e-3) / 1e12
-    lr_ms = kern_ms["summary"] + kern_ms["readout_combine"]
-    lr_gbs = lowrank_bytes(w) / (lr_ms * 1e-3) / 1e9
+    achieved = f_sparse / (kern_ms["sparse_readout_combine"] * 1e-3) / 1e12
+    sum_gbs = summary_bytes(w) / (kern_ms["summary"] * 1e-3) / 1e9
 
     res = {
         "metric": METRIC, "value": round(eff, 2), "unit": "TFLOP/s", "n_gpus": 1,
@@ -381,13 +379,13 @@ def main():
         "config": {"workload": w.name, "B": w.B, "H": w.H, "N": w.N, "grid": list(g), "d_h": w.d_h,
                    "block": w.block, "sparsity": w.sparsity, "keep": keep, "r": w.r,
                    "parallelism": "single GPU"},
-        "roofline": {"bound": "mfma", "kernel": "rola_sparse_attn", "achieved": round(achieved, 2),
-                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+        "roofline": {"bound": "mfma", "kernel": "rola_sparse_attn_combine (block-sparse attention "
+                     "with the low-rank readout and gated combine in its epilogue)",
+                     "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": measured_traffic()},
-        "lowrank_roofline": {"bound": "hbm", "kernels": "rola_lowrank_summary + "
-                             "rola_lowrank_readout_combine", "achieved": round(lr_gbs, 1),
-                             "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                             "frac": round(lr_gbs / PEAK_HBM_GBS, 4)},
+        "summary_roofline": {"bound": "hbm", "kernels": "rola_lowrank_summary",
+                             "achieved": round(sum_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                             "frac": round(sum_gbs / PEAK_HBM_GBS, 4)},
         "kernels_ms": {k: round(v, 4) for k, v in kern_ms.items()},
         "flops": {"sparse_performed": f_sparse, "lowrank_paper": f_lowrank,
                   "sparse_paper_formula": 4.0 * w.B * w.H * w.N ** 2 * (1 - w.sparsity) * w.d_h},

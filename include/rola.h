@@ -126,6 +126,25 @@ rola_status rola_sparse_attn(const rola_problem* p, const void* Qr, const void* 
                              float softmax_scale, void* Os, void* ws, size_t ws_bytes,
                              hipStream_t stream);
 
+/* The sparse branch, the low-rank readout and the gated combine in one call (Algorithm steps 4 and
+ * 7-10): O = (O^s / r + g O^lr) r with O^s = rola_sparse_attn(...) and O^lr =
+ * rola_lowrank_readout(...) of the summary C, without writing O^s or O^lr to memory. Arguments as in
+ * those two calls and rola_combine; O: [B, H, N, d_h] in dtype (must not alias an input). ws:
+ * rola_sparse_combine_workspace_bytes(p, block, sparsity, r) bytes, required (the pair lists of
+ * rola_sparse_attn plus the C fragments of the epilogue). On the bf16 path with r in {16, 32, 64}
+ * the readout and combine run in the attention kernel's epilogue; otherwise the attention and the
+ * fused readout + combine run one after the other. Results agree with the separate calls to the
+ * module's tolerance (the epilogue combines O^s before its bf16 rounding). */
+size_t rola_sparse_combine_workspace_bytes(const rola_problem* p, int32_t block, double sparsity,
+                                           int32_t r);
+rola_status rola_sparse_attn_combine(const rola_problem* p, const void* Qr, const void* Kr,
+                                     const void* V, int32_t block, double sparsity,
+                                     const int32_t* blk_idx, float softmax_scale, const void* Qn,
+                                     const void* Pq, int32_t r, const float* cos_tab,
+                                     const float* sin_tab, int32_t rope_ld, const float* C,
+                                     float eps_lr, const float* gate_logits, float eps, void* O,
+                                     void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Dense softmax attention O = softmax(Q^r K^r^T * scale) V (Sec. 3, "Full attention"): the 0 %
  * sparsity reference, same kernel as rola_sparse_attn walking every key block in order. */
 rola_status rola_dense_attn(const rola_problem* p, const void* Qr, const void* Kr, const void* V,

@@ -31,9 +31,26 @@ hipError_t launch_block_select(const Shape& s, const void* Qr, const void* Kr, i
 // ws: sparse_workspace_bytes(s, block, keep) bytes, or nullptr (then no K/V loads are shared
 // between query blocks).
 size_t sparse_workspace_bytes(const Shape& s, int block, int keep);
+// The low-rank readout and gated combine fused into the attention epilogue (bf16, d 128, r 16-64):
+// Os then receives O = combine(O^s, RMSNorm(q~^T C), logits). fuse_ws: fuse_workspace_bytes(s, r).
+struct LowrankFuse {
+  const void* Qn;
+  const void* Pq;
+  int r;
+  const float* cos_tab;
+  const float* sin_tab;
+  int ld;
+  const float* C;
+  float eps_lr;
+  const float* logits;
+  float eps;
+};
+bool fuse_supported(const Shape& s, int r);
+size_t fuse_workspace_bytes(const Shape& s, int r);
 hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, const void* V,
                               int block, int keep, const int32_t* idx, float scale, void* Os,
-                              void* ws, hipStream_t st);
+                              void* ws, hipStream_t st, const LowrankFuse* lf = nullptr,
+                              void* fuse_ws = nullptr);
 
 // lowrank.hip
 int summary_chunks(const Shape& s, int r);

@@ -4,6 +4,8 @@
 #include "rola.h"
 
 #include <math.h>
+
+#include <algorithm>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -244,6 +246,65 @@ rola_status rola_dense_attn(const rola_problem* p, const void* Qr, const void* K
   const int nb = rola::num_blocks(s.N, block);
   return hip_status(rola::launch_sparse_attn(s, Qr, Kr, V, block, nb, nullptr, softmax_scale, O,
                                              nullptr, stream), __func__);
+}
+
+size_t rola_sparse_combine_workspace_bytes(const rola_problem* p, int32_t block, double sparsity,
+                                           int32_t r) {
+  rola::Shape s;
+  if (check_problem(p, __func__, &s) != ROLA_OK || check_block(s, block, __func__) != ROLA_OK ||
+      check_sparsity(sparsity, __func__) != ROLA_OK || check_rank(s, r, __func__) != ROLA_OK)
+    return 0;
+  const int keep = rola_keep_blocks(rola::num_blocks(s.N, block), sparsity);
+  const size_t sp = (rola::sparse_workspace_bytes(s, block, keep) + 255) & ~(size_t)255;
+  return sp + std::max<size_t>(rola::fuse_workspace_bytes(s, r), 16);
+}
+
+rola_status rola_sparse_attn_combine(const rola_problem* p, const void* Qr, const void* Kr,
+                                     const void* V, int32_t block, double sparsity,
+                                     const int32_t* blk_idx, float softmax_scale, const void* Qn,
+                                     const void* Pq, int32_t r, const float* cos_tab,
+                                     const float* sin_tab, int32_t rope_ld, const float* C,
+                                     float eps_lr, const float* gate_logits, float eps, void* O,
+                                     void* ws, size_t ws_bytes, hipStream_t stream) {
+  rola::Shape s;
+  TRY(check_problem(p, __func__, &s));
+  TRY(check_block(s, block, __func__));
+  TRY(check_sparsity(sparsity, __func__));
+  TRY(check_rank(s, r, __func__));
+  REQUIRE_PTR(Qr);
+  REQUIRE_PTR(Kr);
+  REQUIRE_PTR(V);
+  REQUIRE_PTR(blk_idx);
+  REQUIRE_PTR(Qn);
+  REQUIRE_PTR(Pq);
+  REQUIRE_PTR(C);
+  REQUIRE_PTR(gate_logits);
+  REQUIRE_PTR(O);
+  REQUIRE_PTR(ws);
+  TRY(check_tables(cos_tab, sin_tab, rope_ld, r / 2, __func__));
+  if (!(softmax_scale > 0.f) || !isfinite(softmax_scale))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: softmax_scale must be finite and positive", __func__);
+  if (!(eps_lr >= 0.f) || !isfinite(eps_lr) || !(eps >= 0.f) || !isfinite(eps))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: eps values must be finite and >= 0", __func__);
+  const size_t need = rola_sparse_combine_workspace_bytes(p, block, sparsity, r);
+  if (ws_bytes < need)
+    return fail(ROLA_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", __func__, ws_bytes, need);
+  const int keep = rola_keep_blocks(rola::num_blocks(s.N, block), sparsity);
+  const size_t sp = rola::sparse_workspace_bytes(s, block, keep);
+  void* fuse_ws = static_cast<char*>(ws) + ((sp + 255) & ~(size_t)255);
+  if (rola::fuse_supported(s, r)) {
+    const rola::LowrankFuse lf{Qn, Pq, r, cos_tab, sin_tab, rope_ld, C, eps_lr, gate_logits, eps};
+    return hip_status(rola::launch_sparse_attn(s, Qr, Kr, V, block, keep, blk_idx, softmax_scale, O,
+                                               sp > 0 ? ws : nullptr, stream, &lf, fuse_ws),
+                      __func__);
+  }
+  // other shapes: the attention into O, then the readout and combine in place
+  hipError_t e = rola::launch_sparse_attn(s, Qr, Kr, V, block, keep, blk_idx, softmax_scale, O,
+                                          sp > 0 ? ws : nullptr, stream);
+  if (e == hipSuccess)
+    e = rola::launch_lowrank_readout(s, Qn, Pq, r, cos_tab, sin_tab, rope_ld, 0, C, eps_lr, O,
+                                     gate_logits, eps, O, stream);
+  return hip_status(e, __func__);
 }
 
 rola_status rola_lowrank_summary_ex(const rola_problem* p, const void* Kn, const void* V,

@@ -35,9 +35,6 @@
 #ifndef ROLA_B64_PAIRING
 #define ROLA_B64_PAIRING 1  // pair query blocks by list overlap (1) or take adjacent pairs (0)
 #endif
-#ifndef ROLA_B64_WAVE_Q
-#define ROLA_B64_WAVE_Q 32  // queries per wave of that kernel: 32 (32x32 MFMA) or 16 (16x16 MFMA)
-#endif
 
 namespace rola {
 namespace {
@@ -233,6 +230,160 @@ __global__ __launch_bounds__(256) void group_union_kernel(int nb, int keep, int 
   }
 }
 
+// ---- fused low-rank readout + gated combine in the attention epilogue ------------------------------
+// (eq. ctx readout, eq. gate; Algorithm steps 7-10) for the 32 queries of a wave, whose O^s sits in
+// the accumulators: lane l holds query l%32 and channels 32w + 8j + 4(l/32) + i in acc[w][4j + i].
+//   Phi = P_q Q^n    on v_mfma_f32_32x32x16_bf16 per tile of 16 rotary pairs: A rows 0-15 = even
+//                    rows of P_q, rows 16-31 = odd rows, B = Q^n in the layout Q^r has in the main
+//                    loop, so both members of a pair land in one lane (c[4j+i] and c[4j+8+i]);
+//   q~ = R_r SiLU(Phi) in registers, split into bf16 hi + lo;
+//   u^T = C^T q~     A = C^T fragments prepared per head by cfrag_kernel (hi + lo), k ordered as the
+//                    lanes hold q~; three MFMAs per k-step (hi.hi, lo.hi, hi.lo) as in the standalone
+//                    readout, so the contraction is accurate to ~2^-16;
+//   O = O^s + (sigma(logit) r_s / rms(u)) u  with r_s, rms(u) over the 128 channels (in-lane sums
+//                    plus one permlane32 swap); O lands in the accumulators' layout.
+struct FuseArgs {
+  const bf16* Qn;        // [B, H, N, 128]
+  const bf16* Pq;        // [H, r, 128]
+  const float* cos_tab;  // [N, ld]
+  const float* sin_tab;
+  const uint4* cfrag;    // cfrag_kernel output
+  const float* logits;   // [B, N]
+  int H, r, ld;
+  float eps_lr, eps;
+};
+
+// C^T fragments: entry (head, w, t, s, lane) = {hi, lo} of the 8 values C[2J + s][32w + l%32],
+// J = 16t + 8(m/4) + 4(l/32) + m%4 for m = 0..7 (zero for J >= r/2).
+__global__ __launch_bounds__(256) void cfrag_kernel(long total, int r, int RJ,
+                                                    const float* __restrict__ C,
+                                                    uint4* __restrict__ out) {
+  const long e = (long)blockIdx.x * 256 + threadIdx.x;
+  if (e >= total) return;
+  const int lane = (int)(e % 64);
+  const int ts = (int)((e / 64) % (2 * RJ)), w = (int)((e / (64 * 2 * RJ)) % 4);
+  const long head = e / (64L * 2 * RJ * 4);
+  const int t = ts / 2, sd = ts % 2, half = r / 2;
+  const int c = 32 * w + lane % 32, h = lane / 32;
+  const float* Ch = C + head * (long)r * 128;
+  bf16x8 hi, lo;
+#pragma unroll
+  for (int m = 0; m < 8; ++m) {
+    const int J = 16 * t + 8 * (m / 4) + 4 * h + m % 4;
+    const float v = J < half ? Ch[(long)(2 * J + sd) * 128 + c] : 0.f;
+    hi[m] = (bf16)v;
+    lo[m] = (bf16)(v - (float)hi[m]);
+  }
+  out[2 * e] = *reinterpret_cast<const uint4*>(&hi);
+  out[2 * e + 1] = *reinterpret_cast<const uint4*>(&lo);
+}
+
+template <int RJ>
+__device__ __forceinline__ void fuse_epilogue(const FuseArgs& fz, f32x16 (&acc)[4], float l,
+                                              bool qvalid, long head, int N, int q, int lane,
+                                              bf16* __restrict__ O) {
+  constexpr int D = 128;
+  const int hh = lane / 32, half = fz.r / 2;
+  const int h = (int)(head % fz.H);
+  const long bidx = head / fz.H;
+  // O^s and its RMS
+  const float inv = qvalid ? 1.0f / l : 0.f;
+  float ss = 0.f;
+#pragma unroll
+  for (int w = 0; w < 4; ++w)
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      acc[w][k] *= inv;
+      ss = fmaf(acc[w][k], acc[w][k], ss);
+    }
+  {
+    const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(ss), __float_as_uint(ss), false, false);
+    ss = __uint_as_float(x[0]) + __uint_as_float(x[1]);
+  }
+  const float rs = sqrtf(ss * (1.0f / D) + fz.eps);
+  // Q^n operand (query q, d = 16s + 8(l/32) .. +7) and the token's gate logit
+  const bf16* Qq = fz.Qn + head * (long)N * D + (long)q * D;
+  bf16x8 qn[8];
+#pragma unroll
+  for (int s = 0; s < 8; ++s)
+    qn[s] = qvalid ? *reinterpret_cast<const bf16x8*>(Qq + 16 * s + 8 * hh) : bf16x8{};
+  const float lg = qvalid ? fz.logits[bidx * N + q] : 0.f;
+  f32x16 u[4];
+#pragma unroll
+  for (int w = 0; w < 4; ++w) u[w] = f32x16{};
+#pragma unroll
+  for (int t = 0; t < RJ; ++t) {
+    const int rho = lane % 32, pair = 16 * t + (rho & 15);
+    const bool pok = pair < half;
+    const bf16* Pr = fz.Pq + ((long)h * fz.r + 2 * pair + (rho >> 4)) * D + 8 * hh;
+    f32x16 ph = f32x16{};
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      const bf16x8 pa = pok ? *reinterpret_cast<const bf16x8*>(Pr + 16 * s) : bf16x8{};
+      ph = mfma32(pa, qn[s], ph);
+    }
+    // features of this lane's pairs J = 16t + 8jp + 4(l/32) + i: e in ph[4jp+i], o in ph[4jp+8+i]
+    bf16x8 beh, bel, boh, bol;
+#pragma unroll
+    for (int jp = 0; jp < 2; ++jp) {
+      const int J0 = 16 * t + 8 * jp + 4 * hh;  // half is a multiple of 8: 4 pairs valid or none
+      float4 c4 = {1.f, 1.f, 1.f, 1.f}, s4 = {0.f, 0.f, 0.f, 0.f};
+      if (qvalid && J0 < half) {
+        c4 = *reinterpret_cast<const float4*>(fz.cos_tab + (long)q * fz.ld + J0);
+        s4 = *reinterpret_cast<const float4*>(fz.sin_tab + (long)q * fz.ld + J0);
+      }
+      const float cc[4] = {c4.x, c4.y, c4.z, c4.w}, sn[4] = {s4.x, s4.y, s4.z, s4.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float a = silu(ph[4 * jp + i]), b = silu(ph[4 * jp + 8 + i]);
+        const float qe = a * cc[i] - b * sn[i], qo = a * sn[i] + b * cc[i];
+        beh[4 * jp + i] = (bf16)qe;
+        bel[4 * jp + i] = (bf16)(qe - (float)beh[4 * jp + i]);
+        boh[4 * jp + i] = (bf16)qo;
+        bol[4 * jp + i] = (bf16)(qo - (float)boh[4 * jp + i]);
+      }
+    }
+#pragma unroll
+    for (int w = 0; w < 4; ++w)
+#pragma unroll
+      for (int sd = 0; sd < 2; ++sd) {
+        const uint4* fr = fz.cfrag + ((((head * 4 + w) * (2 * RJ) + 2 * t + sd) * 64) + lane) * 2;
+        const uint4 fh = fr[0], fl = fr[1];
+        const bf16x8 ah = *reinterpret_cast<const bf16x8*>(&fh);
+        const bf16x8 al = *reinterpret_cast<const bf16x8*>(&fl);
+        const bf16x8& bh = sd ? boh : beh;
+        const bf16x8& bl = sd ? bol : bel;
+        u[w] = mfma32(ah, bh, u[w]);
+        u[w] = mfma32(al, bh, u[w]);
+        u[w] = mfma32(ah, bl, u[w]);
+      }
+  }
+  float su = 0.f;
+#pragma unroll
+  for (int w = 0; w < 4; ++w)
+#pragma unroll
+    for (int k = 0; k < 16; ++k) su = fmaf(u[w][k], u[w][k], su);
+  {
+    const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(su), __float_as_uint(su), false, false);
+    su = __uint_as_float(x[0]) + __uint_as_float(x[1]);
+  }
+  const float inv_u = rsqrtf(su * (1.0f / D) + fz.eps_lr);
+  // (O^s / r_s + g O^lr) r_s  ==  O^s + (g r_s / rms(u)) u
+  const float coef = sigmoid(lg) * rs * inv_u;
+  if (qvalid) {
+    bf16* Oq = O + head * (long)N * D + (long)q * D;
+#pragma unroll
+    for (int w = 0; w < 4; ++w)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        bf16x4 o;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = (bf16)fmaf(coef, u[w][4 * j + i], acc[w][4 * j + i]);
+        *reinterpret_cast<bf16x4*>(Oq + 32 * w + 8 * j + 4 * hh) = o;
+      }
+  }
+}
+
 // Query block qb of group grp: from the pair table when there is one (G = 2), else grp*G + qb.
 template <int G>
 __device__ __forceinline__ int group_block(const int32_t* pairs, long entry, int grp, int qb) {
@@ -246,12 +397,14 @@ __device__ __forceinline__ int group_block(const int32_t* pairs, long entry, int
 // lists: G = 1: the block lists [B, H, nb, list_stride] (list_len entries used); G > 1:
 //        group_union_kernel output, list_stride ints per (b, h, group); nullptr: every key block in
 //        order for all query blocks of the group (list_len = nb).
-template <int BLK, int G, int NBUF, int TAB>
+// RJ > 0: the epilogue also computes the low-rank readout (r <= 32 RJ) and the gated combine
+// (fuse_epilogue) and writes O instead of O^s.
+template <int BLK, int G, int NBUF, int TAB, int RJ>
 __global__ __launch_bounds__(G * BLK * 2, 2) void sparse_attn_kernel(
     int N, int nb, int ngroups, int total, const int32_t* __restrict__ lists, int list_len,
     int list_stride, const int32_t* __restrict__ pairs, float scale_log2,
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
-    bf16* __restrict__ O) {
+    bf16* __restrict__ O, FuseArgs fz) {
   static_assert(G == 1 || G == 2 || G == 4, "one, two or four query blocks per workgroup");
   static_assert(NBUF >= 3, "loads of later sub-tiles stay in flight during a step");
   constexpr int D = 128, WPB = BLK / 32, NW = G * WPB;
@@ -495,6 +648,10 @@ __global__ __launch_bounds__(G * BLK * 2, 2) void sparse_attn_kernel(
     const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(l), __float_as_uint(l), false, false);
     l = __uint_as_float(x[0]) + __uint_as_float(x[1]);
   }
+  if constexpr (RJ > 0) {
+    fuse_epilogue<RJ>(fz, acc, l, qvalid, head, N, q, lane, O);
+    return;
+  }
   if (qvalid) {
     const float inv = 1.0f / l;
     bf16* Oq = O + head * (long)N * D + (long)q * D;
@@ -510,227 +667,6 @@ __global__ __launch_bounds__(G * BLK * 2, 2) void sparse_attn_kernel(
   }
 }
 
-// bf16 attention kernel with 16-query waves (v_mfma_f32_16x16x32_bf16): one workgroup per (b, h,
-// G consecutive query blocks), BLK/16 waves per query block. A wave holds about a hundred VGPRs,
-// so sixteen waves share a CU; this makes groups of four query blocks (whose list union saves about
-// 45 % of the K/V bytes of single blocks) affordable although each wave computes on only about half
-// of the union. Per wave and 32-key sub-tile:
-//   S^T = K Q^T   two 16-key tiles x four 32-channel k-steps; lane (c = l%16, g = l/16) receives
-//                 keys 4g+v of each tile for query c, so a row max takes two permlane swaps;
-//   P = exp2(S^T * scale*log2e - m) in bf16, the B operand of O^T = V^T P^T (eight 16-channel
-//                 tiles; V^T through ds_read_b64_tr_b16 of row-major V, keys in the order S^T hands
-//                 them out), row sums from one more MFMA against ones.
-// K rows are stored with chunk ^ row%16 and V rows with chunk ^ 2(row%8), which makes the operand
-// reads (16 rows per pass) and the transposing reads (8 rows per pass) bank-conflict free.
-template <int BLK, int G, int NBUF, int TAB>
-__global__ __launch_bounds__(G * BLK * 4) void sparse_attn16_kernel(
-    int N, int nb, int ngroups, int total, const int32_t* __restrict__ lists, int list_len,
-    int list_stride, const int32_t* __restrict__ pairs, float scale_log2,
-    const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
-    bf16* __restrict__ O) {
-  static_assert(G == 1 || G == 2 || G == 4, "one, two or four query blocks per workgroup");
-  static_assert(NBUF >= 3, "loads of later sub-tiles stay in flight during a step");
-  constexpr int D = 128, WPB = BLK / 16, NW = G * WPB, NT = NW * 64;
-  constexpr int TILE = kSub * D * 2;   // 8 KB: K (or V) of one sub-tile
-  constexpr int STAGE = 2 * TILE;      // K then V
-  constexpr int SLOTS = STAGE / 1024;  // 1-KB direct loads per stage (K: 0-7, V: 8-15)
-  static_assert(SLOTS % NW == 0, "whole loads per wave");
-  constexpr int SPW = SLOTS / NW;      // loads per wave per sub-tile
-  constexpr int SUBS = BLK / kSub;     // sub-tiles per key block
-  __shared__ __attribute__((aligned(1024))) char lds[NBUF * STAGE];
-  __shared__ int tab[TAB > 0 ? TAB : 1];
-
-  const int L = xcd_remap(blockIdx.x, total);
-  const int grp = L % ngroups;
-  const long head = L / ngroups;
-  const int tid = threadIdx.x, lane = tid % 64, lr = lane % 16, g = lane / 16;
-  const int wave = wave_uniform(tid / 64);
-  const int qb = wave / WPB;
-  const int I = group_block<G>(pairs, head * ngroups + grp, grp, qb);
-  const int q = I * BLK + (wave % WPB) * 16 + lr;  // this lane's query (column of S^T, O^T)
-  const bool qvalid = I < nb && q < N;
-  const int mybit = 1 << qb;
-  const bf16* Qh = Q + head * (long)N * D;
-  const char* Kh = reinterpret_cast<const char*>(K + head * (long)N * D);
-  const char* Vh = reinterpret_cast<const char*>(V + head * (long)N * D);
-
-  // The block list (as in sparse_attn_kernel): LDS table read a step ahead, or scalar loads.
-  typedef const __attribute__((address_space(4))) int32_t* const_i32;
-  const int32_t* glist = nullptr;
-  int E = list_len;
-  if (lists && G > 1) {
-    glist = lists + (head * ngroups + grp) * (long)list_stride;
-    E = ((const_i32)glist)[0];
-    glist += 1;
-  } else if (lists) {
-    glist = lists + (head * nb + grp) * (long)list_stride;
-  }
-  const const_i32 slist = (const_i32)glist;
-  const int T = E * SUBS;
-  if (TAB > 0 && glist)
-    for (int i = tid; i < E; i += NT) tab[i] = glist[i];
-  struct Step {
-    int k0, mask;
-  };
-  auto raw = [&](int e) -> int {
-    if (!glist) return G > 1 ? (e | (((1 << G) - 1) << 16)) : e;  // dense: every block, all
-    const int i = min(e, max(E - 1, 0));
-    return TAB > 0 ? tab[i] : (int)slist[i];
-  };
-  auto step_of = [&](int v, int t) {
-    v = TAB > 0 ? wave_uniform(v) : v;
-    const int J = G > 1 ? (v & 0xFFFF) : v;
-    const int mask = G > 1 ? (v >> 16) : 1;
-    return Step{(unsigned)J < (unsigned)nb ? J * BLK + (t % SUBS) * kSub : -1, mask};
-  };
-  auto active = [&](const Step& s) { return (s.mask & mybit) && s.k0 >= 0 && s.k0 < N; };
-
-  bf16x8 qf[4];  // Q^T fragments of the four k-steps (d = 32kc + 8g .. +7)
-#pragma unroll
-  for (int kc = 0; kc < 4; ++kc)
-    qf[kc] = qvalid ? *reinterpret_cast<const bf16x8*>(Qh + (long)q * D + 32 * kc + 8 * g) : bf16x8{};
-  __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0): Q and the list are in registers
-  if (TAB > 0) __syncthreads();
-
-  f32x4 acc[8], accl = f32x4{0.f, 0.f, 0.f, 0.f};  // O^T tiles and the row sums
-  float m = -INFINITY;
-#pragma unroll
-  for (int w = 0; w < 8; ++w) acc[w] = f32x4{0.f, 0.f, 0.f, 0.f};
-  bf16x8 ones;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) ones[i] = (bf16)1.0f;
-
-  // DMA: slot s of a stage fills rows 4(s%8) .. +3 of K (s < 8) or V; lane l fills row
-  // 4(s%8) + l/16 at chunk position l%16 with source chunk (position ^ swizzle(row)).
-  uint32_t dsrc[SPW];
-#pragma unroll
-  for (int i = 0; i < SPW; ++i) {
-    const int slot = wave * SPW + i, row = 4 * (slot % 8) + lane / 16, pos = lane % 16;
-    const int sw = slot < 8 ? (row & 15) : ((row & 7) << 1);
-    dsrc[i] = row * D * 2 + ((pos ^ sw) << 4);
-  }
-  int ko[2][4];
-#pragma unroll
-  for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-    for (int kc = 0; kc < 4; ++kc) {
-      const int row = 16 * kt + lr;
-      ko[kt][kc] = row * 256 + (((4 * kc + g) ^ (row & 15)) << 4);
-    }
-  const int sp = lr >> 2, mp = lr & 3, vr = 4 * g + sp;
-  int vo[8];
-#pragma unroll
-  for (int w = 0; w < 8; ++w)
-    vo[w] = TILE + vr * 256 + (((2 * w + (mp >> 1)) ^ ((vr & 7) << 1)) << 4) + ((mp & 1) << 3);
-
-  const uint32_t lds0 = lds_address(lds);
-  auto issue = [&](const Step& s, int buf) {  // always SPW loads per wave (fixed vmcnt per step)
-    const int k0 = max(s.k0, 0);
-    const uint32_t dst = lds0 + buf * STAGE;
-#pragma unroll
-    for (int i = 0; i < SPW; ++i) {
-      const int slot = wave * SPW + i;
-      const char* base = slot < 8 ? Kh : Vh;
-      const uint32_t d = dst + (slot < 8 ? 0 : TILE) + (slot % 8) * 1024;
-      if (k0 + kSub <= N) {
-        dma16(base + (long)k0 * D * 2, dsrc[i], d);
-      } else {  // ragged tail: rows past N re-read row N-1 (a valid key; its probabilities are zeroed)
-        const int r = 4 * (slot % 8) + lane / 16;
-        dma16(base, (uint32_t)(min(k0 + r, N - 1) - r) * (D * 2) + dsrc[i], d);
-      }
-    }
-  };
-
-  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
-  auto compute = [&](const char* base, int k0) {
-    bf16x8 kf[4][2];
-#pragma unroll
-    for (int kc = 0; kc < 4; ++kc)
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) kf[kc][kt] = *reinterpret_cast<const bf16x8*>(base + ko[kt][kc]);
-    f32x4 s0 = f32x4{0.f, 0.f, 0.f, 0.f}, s1 = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kc = 0; kc < 4; ++kc) {
-      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kc][0], qf[kc], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kc][1], qf[kc], s1, 0, 0, 0);
-    }
-    const float mx = fmaxf(fmaxf(fmaxf(s0[0], s0[1]), fmaxf(s0[2], s0[3])),
-                           fmaxf(fmaxf(s1[0], s1[1]), fmaxf(s1[2], s1[3])));
-    const float mt = rows_max(mx) * scale_log2;
-    if (__any(mt > m + kRescaleTau)) {  // lazy rescale, exact (see sparse_attn_kernel)
-      const float mnew = fmaxf(m, mt);
-      const float alpha = __builtin_amdgcn_exp2f(m - mnew);
-      m = mnew;
-      accl *= alpha;
-#pragma unroll
-      for (int w = 0; w < 8; ++w) acc[w] *= alpha;
-    }
-    bf16x8 pb;
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      pb[v] = (bf16)__builtin_amdgcn_exp2f(fmaf(s0[v], scale_log2, -m));
-      pb[4 + v] = (bf16)__builtin_amdgcn_exp2f(fmaf(s1[v], scale_log2, -m));
-    }
-    if (k0 + kSub > N) {  // value 4kt + v holds key k0 + 16kt + 4g + v
-      const int lim = N - k0 - 4 * g;
-#pragma unroll
-      for (int k = 0; k < 8; ++k)
-        if (16 * (k / 4) + k % 4 >= lim) pb[k] = (bf16)0.f;
-    }
-    accl = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb, accl, 0, 0, 0);
-#pragma unroll
-    for (int w = 0; w < 8; ++w) {
-      const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(base + vo[w]));
-      const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(base + vo[w] + 16 * 256));
-      acc[w] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-          __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7), pb, acc[w], 0, 0, 0);
-    }
-  };
-
-  // Pipeline as in sparse_attn_kernel: wait for sub-tile t, barrier, issue t+NBUF-1, compute t.
-  int issued = 0;
-#pragma unroll
-  for (int j = 0; j < NBUF - 1; ++j)
-    if (j < T) {
-      issue(step_of(raw(j / SUBS), j), j);
-      ++issued;
-    }
-  int pi = raw(issued / SUBS), pc = raw(0);
-  for (int t = 0; t < T;) {
-#pragma unroll
-    for (int j = 0; j < NBUF; ++j) {
-      if (t >= T) break;
-      if (issued == t + NBUF - 1) {
-        constexpr int allowed = SPW * (NBUF - 2);
-        __builtin_amdgcn_s_waitcnt((allowed & 15) | ((allowed >> 4) << 14) | (7 << 4) | (15 << 8));
-      } else {
-        __builtin_amdgcn_s_waitcnt(0);
-      }
-      __syncthreads();
-      if (issued < T) {
-        issue(step_of(pi, issued), (j + NBUF - 1) % NBUF);
-        ++issued;
-      }
-      const Step cur = step_of(pc, t);
-      pi = raw(issued / SUBS);
-      pc = raw((t + 1) / SUBS);
-      if (active(cur)) compute(lds + j * STAGE, cur.k0);
-      ++t;
-    }
-  }
-
-  if (qvalid) {
-    const float inv = 1.0f / accl[0];
-    bf16* Oq = O + head * (long)N * D + (long)q * D;
-#pragma unroll
-    for (int w = 0; w < 8; ++w) {
-      bf16x4 o;
-#pragma unroll
-      for (int v = 0; v < 4; ++v) o[v] = (bf16)(acc[w][v] * inv);
-      *reinterpret_cast<bf16x4*>(Oq + 16 * w + 4 * g) = o;
-    }
-  }
-}
 
 // Plain kernel for the fp32 path: one thread per query, keys streamed through LDS 32 at a time.
 template <typename T, int D>
@@ -799,37 +735,49 @@ __global__ __launch_bounds__(128) void sparse_simple_kernel(int N, int block, in
   }
 }
 
-template <int WAVE_Q, int BLK, int G, int NBUF, int TAB>
+template <int BLK, int G, int NBUF, int TAB, int RJ>
 hipError_t launch_bf16_tab(const Shape& s, const void* Qr, const void* Kr, const void* V,
                            const int32_t* lists, int list_len, int list_stride,
-                           const int32_t* pairs, float scale, void* Os, hipStream_t st) {
+                           const int32_t* pairs, float scale, void* Os, const FuseArgs& fz,
+                           hipStream_t st) {
   const int nb = num_blocks(s.N, BLK);
   const int ngroups = (nb + G - 1) / G;
   const int total = ngroups * s.H * s.B;
   const float sl = scale * 1.4426950408889634f;
-  if constexpr (WAVE_Q == 32)
-    hipLaunchKernelGGL((sparse_attn_kernel<BLK, G, NBUF, TAB>), dim3(total), dim3(G * BLK * 2), 0,
-                       st, s.N, nb, ngroups, total, lists, list_len, list_stride, pairs, sl,
-                       (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V, (bf16*)Os);
-  else
-    hipLaunchKernelGGL((sparse_attn16_kernel<BLK, G, NBUF, TAB>), dim3(total), dim3(G * BLK * 4),
-                       0, st, s.N, nb, ngroups, total, lists, list_len, list_stride, pairs, sl,
-                       (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V, (bf16*)Os);
+  hipLaunchKernelGGL((sparse_attn_kernel<BLK, G, NBUF, TAB, RJ>), dim3(total), dim3(G * BLK * 2), 0,
+                     st, s.N, nb, ngroups, total, lists, list_len, list_stride, pairs, sl,
+                     (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V, (bf16*)Os, fz);
   return hipGetLastError();
 }
 
 // Lists of up to kTable entries go through the LDS table; longer ones through scalar loads.
 constexpr int kTable = 1024;
-template <int WAVE_Q, int BLK, int G, int NBUF>
-hipError_t launch_bf16(const Shape& s, const void* Qr, const void* Kr, const void* V,
-                       const int32_t* lists, int list_len, int list_stride, float scale, void* Os,
-                       hipStream_t st, const int32_t* pairs = nullptr) {
+template <int BLK, int G, int NBUF, int RJ>
+hipError_t launch_bf16_rj(const Shape& s, const void* Qr, const void* Kr, const void* V,
+                          const int32_t* lists, int list_len, int list_stride, float scale,
+                          void* Os, const int32_t* pairs, const FuseArgs& fz, hipStream_t st) {
   const int max_len = G > 1 ? list_stride - 1 : list_len;
   if (lists && max_len <= kTable)
-    return launch_bf16_tab<WAVE_Q, BLK, G, NBUF, kTable>(s, Qr, Kr, V, lists, list_len, list_stride,
-                                                         pairs, scale, Os, st);
-  return launch_bf16_tab<WAVE_Q, BLK, G, NBUF, 0>(s, Qr, Kr, V, lists, list_len, list_stride, pairs,
-                                                  scale, Os, st);
+    return launch_bf16_tab<BLK, G, NBUF, kTable, RJ>(s, Qr, Kr, V, lists, list_len, list_stride,
+                                                     pairs, scale, Os, fz, st);
+  return launch_bf16_tab<BLK, G, NBUF, 0, RJ>(s, Qr, Kr, V, lists, list_len, list_stride, pairs,
+                                              scale, Os, fz, st);
+}
+
+// fz.r == 0: plain attention (O^s); otherwise the fused epilogue with RJ = r / 32 tiles (r 16 -> 1).
+template <int BLK, int G, int NBUF>
+hipError_t launch_bf16(const Shape& s, const void* Qr, const void* Kr, const void* V,
+                       const int32_t* lists, int list_len, int list_stride, float scale, void* Os,
+                       hipStream_t st, const int32_t* pairs = nullptr, const FuseArgs* fz = nullptr) {
+  static const FuseArgs none{};
+  if (!fz || fz->r == 0)
+    return launch_bf16_rj<BLK, G, NBUF, 0>(s, Qr, Kr, V, lists, list_len, list_stride, scale, Os,
+                                           pairs, none, st);
+  if (fz->r <= 32)
+    return launch_bf16_rj<BLK, G, NBUF, 1>(s, Qr, Kr, V, lists, list_len, list_stride, scale, Os,
+                                           pairs, *fz, st);
+  return launch_bf16_rj<BLK, G, NBUF, 2>(s, Qr, Kr, V, lists, list_len, list_stride, scale, Os,
+                                         pairs, *fz, st);
 }
 
 template <typename T, int D>
@@ -877,14 +825,34 @@ size_t sparse_workspace_bytes(const Shape& s, int block, int keep) {
   return w.pair_bytes + w.list_bytes;
 }
 
+size_t fuse_workspace_bytes(const Shape& s, int r) {
+  if (!fuse_supported(s, r)) return 0;
+  const size_t RJ = r <= 32 ? 1 : 2;
+  return (size_t)s.B * s.H * 4 * 2 * RJ * 64 * 2 * sizeof(uint4);
+}
+
+bool fuse_supported(const Shape& s, int r) { return s.bf16 && s.d == 128 && r >= 16 && r <= 64; }
+
 hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, const void* V,
                               int block, int keep, const int32_t* idx, float scale, void* Os,
-                              void* ws, hipStream_t st) {
+                              void* ws, hipStream_t st, const LowrankFuse* lf, void* fuse_ws) {
+  FuseArgs fz{};
+  if (lf) {  // fused epilogue: C^T fragments first (fuse_ws: fuse_workspace_bytes)
+    const int RJ = lf->r <= 32 ? 1 : 2;
+    const long total = (long)s.B * s.H * 4 * 2 * RJ * 64;
+    hipLaunchKernelGGL(cfrag_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, total,
+                       lf->r, RJ, lf->C, (uint4*)fuse_ws);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    fz = FuseArgs{(const bf16*)lf->Qn, (const bf16*)lf->Pq, lf->cos_tab, lf->sin_tab,
+                  (const uint4*)fuse_ws, lf->logits, s.H, lf->r, lf->ld, lf->eps_lr, lf->eps};
+  }
+  const FuseArgs* fp = lf ? &fz : nullptr;
   if (s.bf16) {
     const int nb = num_blocks(s.N, block);
     if (block == 64) {
       constexpr int G = ROLA_B64_GROUP;
-      if (!idx) return launch_bf16<32, 64, 2, 3>(s, Qr, Kr, V, nullptr, nb, 0, scale, Os, st);
+      if (!idx) return launch_bf16<64, 2, 3>(s, Qr, Kr, V, nullptr, nb, 0, scale, Os, st, nullptr, fp);
       if (ws && G > 1) {
         const int ngroups = (nb + G - 1) / G, stride = G * keep + 1;
         const int words = (nb + 31) / 32, heads = s.B * s.H;
@@ -904,13 +872,13 @@ hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, co
                            (const int32_t*)pairs, lists);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
-        return launch_bf16<ROLA_B64_WAVE_Q, 64, G, ROLA_B64_NBUF>(s, Qr, Kr, V, lists, 0, stride,
-                                                                  scale, Os, st, pairs);
+        return launch_bf16<64, G, ROLA_B64_NBUF>(s, Qr, Kr, V, lists, 0, stride, scale, Os, st,
+                                                 pairs, fp);
       }
-      return launch_bf16<32, 64, 1, 3>(s, Qr, Kr, V, idx, keep, keep, scale, Os, st);
+      return launch_bf16<64, 1, 3>(s, Qr, Kr, V, idx, keep, keep, scale, Os, st, nullptr, fp);
     }
-    if (!idx) return launch_bf16<32, 128, 1, 3>(s, Qr, Kr, V, nullptr, nb, 0, scale, Os, st);
-    return launch_bf16<32, 128, 1, 3>(s, Qr, Kr, V, idx, keep, keep, scale, Os, st);
+    if (!idx) return launch_bf16<128, 1, 3>(s, Qr, Kr, V, nullptr, nb, 0, scale, Os, st, nullptr, fp);
+    return launch_bf16<128, 1, 3>(s, Qr, Kr, V, idx, keep, keep, scale, Os, st, nullptr, fp);
   }
   if (s.d == 64) return launch_simple<float, 64>(s, Qr, Kr, V, block, keep, idx, scale, Os, st);
   return launch_simple<float, 128>(s, Qr, Kr, V, block, keep, idx, scale, Os, st);

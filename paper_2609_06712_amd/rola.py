@@ -55,6 +55,9 @@ SIGNATURES = {
                                                _p, _p, _f32, _p, _p]),
     "rola_lowrank_features": (_i32, [_PP, _p, _p, _i32, _p, _p, _i32, _i32, _i32, _p, _p]),
     "rola_gate_logits": (_i32, [_PP, _p, _i32, _p, _f32, _p, _p]),
+    "rola_sparse_combine_workspace_bytes": (_sz, [_PP, _i32, _f64, _i32]),
+    "rola_sparse_attn_combine": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p, _i32, _p, _p,
+                                        _i32, _p, _f32, _p, _f32, _p, _p, _sz, _p]),
 }
 
 # Feature map and rotation order of the low-rank branch (rola_phi, rola_rope_order).
@@ -319,4 +322,27 @@ def rola_gate_logits(X, Wg, bg, grid, H=1, d_h=128, out=None, stream=None):
         out = torch.empty((B, N), dtype=torch.float32, device=X.device)
     _check(LIB.rola_gate_logits(ctypes.byref(prob), _ptr(X), dm, _ptr(Wg), bg, _ptr(out),
                                 _stream(stream)), "rola_gate_logits")
+    return out
+
+
+def sparse_combine_workspace_bytes(prob: Problem, block: int, sparsity: float, r: int) -> int:
+    return LIB.rola_sparse_combine_workspace_bytes(ctypes.byref(prob), block, sparsity, r)
+
+
+def rola_sparse_attn_combine(Qr, Kr, V, grid, block, sparsity, blk_idx, Qn, Pq, r, cos, sin, C,
+                             logits, scale=None, eps_lr=1e-6, eps=1e-6, out=None, ws=None,
+                             stream=None):
+    """O = combine(sparse attention, low-rank readout of C) in one call (fused epilogue)."""
+    _act(Qr, "Qr")
+    prob = problem_of(Qr, grid)
+    scale = prob.d_h ** -0.5 if scale is None else scale
+    out = torch.empty_like(Qr) if out is None else out
+    if ws is None:
+        need = sparse_combine_workspace_bytes(prob, block, sparsity, r)
+        ws = torch.empty(need, dtype=torch.uint8, device=Qr.device)
+    _check(LIB.rola_sparse_attn_combine(ctypes.byref(prob), _ptr(Qr), _ptr(Kr), _ptr(V), block,
+                                        sparsity, _ptr(blk_idx), scale, _ptr(Qn), _ptr(Pq), r,
+                                        _ptr(cos), _ptr(sin), cos.stride(0), _ptr(C), eps_lr,
+                                        _ptr(logits), eps, _ptr(out), _ptr(ws), ws.numel(),
+                                        _stream(stream)), "rola_sparse_attn_combine")
     return out

@@ -32,7 +32,11 @@ def run_gpu(w: synth.Workload, inp: dict, fused_only=False):
     C, z = R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], w.r, cos, sin, g)
     out_fused = R.rola_lowrank_readout_combine(inp["Qn"], inp["Pq"], w.r, cos, sin, C, o_s,
                                                inp["logits"], g)
-    res = dict(cos=cos, sin=sin, qr=qr, kr=kr, idx=idx, o_s=o_s, C=C, z=z, out_fused=out_fused)
+    # the whole tail in one call: attention with the readout and combine in its epilogue
+    out_epi = R.rola_sparse_attn_combine(qr, kr, inp["V"], g, w.block, w.sparsity, idx, inp["Qn"],
+                                         inp["Pq"], w.r, cos, sin, C, inp["logits"])
+    res = dict(cos=cos, sin=sin, qr=qr, kr=kr, idx=idx, o_s=o_s, C=C, z=z, out_fused=out_fused,
+               out_epi=out_epi)
     if not fused_only:
         o_lr = R.rola_lowrank_readout(inp["Qn"], inp["Pq"], w.r, cos, sin, C, g)
         res["o_lr"] = o_lr

@@ -72,6 +72,13 @@ def test_workspace_helpers():
     assert R.sparse_workspace_bytes(p, 128, 0.9) == 0    # 128-token blocks share nothing
     assert R.sparse_workspace_bytes(R.problem(1, 2, 256, 64, (1, 16, 16), "f32"), 64, 0.5) == 0
     assert R.sparse_workspace_bytes(bad, 64, 0.9) == 0
+    # attention + epilogue: the sparse workspace (rounded to 256 B) plus the C^T fragments,
+    # 4 channel tiles x 2 k-steps per 16 rotary pairs x 64 lanes x 32 B per head
+    sp = -(-R.sparse_workspace_bytes(p, 64, 0.9) // 256) * 256
+    assert R.sparse_combine_workspace_bytes(p, 64, 0.9, 32) == sp + 40 * 4 * 2 * 64 * 32
+    assert R.sparse_combine_workspace_bytes(p, 64, 0.9, 64) == sp + 40 * 4 * 4 * 64 * 32
+    assert R.sparse_combine_workspace_bytes(p, 64, 0.9, 128) == sp + 16  # standalone readout path
+    assert R.sparse_combine_workspace_bytes(p, 64, 0.9, 33) == 0
 
 
 def test_status_strings():
@@ -148,6 +155,13 @@ def test_invalid_arguments_are_rejected_before_launch():
         (R.ROLA_ERR_INVALID_ARGUMENT, "rola_gate_logits", P(ok), FAKE, 5120, FAKE, float("inf"), FAKE,
          None),
         (R.ROLA_ERR_INVALID_ARGUMENT, "rola_gate_logits", P(ok), FAKE, 5120, FAKE, -1.9, None, None),
+        # attention + readout + combine: no workspace, too small a workspace, odd rank
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn_combine", P(ok), FAKE, FAKE, FAKE, 64, 0.9,
+         FAKE, 0.1, FAKE, FAKE, 32, FAKE, FAKE, 64, FAKE, 1e-6, FAKE, 1e-6, FAKE, None, 0, None),
+        (R.ROLA_ERR_WORKSPACE, "rola_sparse_attn_combine", P(ok), FAKE, FAKE, FAKE, 64, 0.9, FAKE,
+         0.1, FAKE, FAKE, 32, FAKE, FAKE, 64, FAKE, 1e-6, FAKE, 1e-6, FAKE, FAKE, 64, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn_combine", P(ok), FAKE, FAKE, FAKE, 64, 0.9,
+         FAKE, 0.1, FAKE, FAKE, 31, FAKE, FAKE, 64, FAKE, 1e-6, FAKE, 1e-6, FAKE, FAKE, 1 << 40, None),
     ]
     for want, name, *args in cases:
         got = _call(name, *args)

@@ -48,6 +48,9 @@ def _compare_head(w, gpu, ora, b, h, dtype, check_fused=True, check_unfused=True
     if check_fused:
         res["out_fused"] = T.assert_close(T.to_np(gpu["out_fused"][b, h])[rows][keep_rows],
                                           ora["out"][keep_rows], dtype, "O fused")
+    if "out_epi" in gpu:
+        res["out_epi"] = T.assert_close(T.to_np(gpu["out_epi"][b, h])[rows][keep_rows],
+                                        ora["out"][keep_rows], dtype, "O attention epilogue")
     return res
 
 
@@ -110,7 +113,7 @@ def _sampled(w, heads, q_blocks):
         head_in = {k: inp[k][:, h:h + 1] for k in ("Qn", "Kn", "V")}
         head_in.update(Pq=inp["Pq"][h:h + 1], Pk=inp["Pk"][h:h + 1], logits=inp["logits"])
         ora = T.oracle_head(w, synth.to_f64(head_in), 0, 0, q_blocks=q_blocks)
-        sub = {k: gpu[k][:, h:h + 1] for k in ("idx", "o_s", "C", "z", "out_fused")}
+        sub = {k: gpu[k][:, h:h + 1] for k in ("idx", "o_s", "C", "z", "out_fused", "out_epi")}
         res = _compare_head(w, sub, ora, 0, 0, "bf16", check_unfused=False)
         _report(f"{w.name} h{h}", **res)
 
