@@ -277,6 +277,33 @@ def sweep(reps: int) -> None:
               f"{100 * f_dense / dense_ms / 1e9 / PEAK_BF16_TFLOPS:.1f} | 1 | 1 |", flush=True)
 
 
+def dit_bench(reps: int) -> None:
+    """Per-block time of a synthetic Wan-shaped DiT block (random weights) with the RoLA module or
+    the dense attention kernel as its self-attention, and the implied DiT time per denoising step
+    (blocks x block time, one forward, no CFG). Printed as markdown."""
+    from paper_2609_06712_amd import dit_block as DB
+    print("## Synthetic Wan-shaped DiT block (random weights), bf16\n")
+    print("| model | grid | attention | self-attention ms | block ms | blocks | DiT ms per step | "
+          "dense / RoLA per step |")
+    print("|---|---|---|---|---|---|---|---|", flush=True)
+    for shape in (DB.WAN_1_3B_480P, DB.WAN_14B_720P):
+        x, ctx = DB.inputs(shape)
+        res = {}
+        for attn in ("dense", "rola"):
+            blk = DB.DiTBlock(shape, attn=attn)
+            h = torch.randn_like(x)
+            sa = time_call(lambda: blk.self_attention(h), max(2, reps // 2 if attn == "dense" else reps))[0]
+            bm = time_call(lambda: blk.forward(x, ctx), max(2, reps // 2 if attn == "dense" else reps))[0]
+            res[attn] = bm
+            ratio = f"{res['dense'] / bm:.2f}" if attn == "rola" else "-"
+            print(f"| {shape.name} | {'x'.join(map(str, shape.grid))} | {attn} | {sa:.2f} | {bm:.2f} | "
+                  f"{shape.layers} | {bm * shape.layers:.0f} | {ratio} |", flush=True)
+            del blk, h
+            torch.cuda.empty_cache()
+        del x, ctx
+    print()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -288,6 +315,8 @@ def main():
                     help="print the measurement sweeps (1.3B layer, low-rank N x r, sparse S x block) "
                          "as markdown instead of the JSON line")
     ap.add_argument("--sweep-reps", type=int, default=10)
+    ap.add_argument("--dit", action="store_true",
+                    help="time a synthetic Wan-shaped DiT block with RoLA vs dense self-attention")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="one untimed device copy of one activation tensor (counter calibration)")
     args = ap.parse_args()
@@ -301,6 +330,9 @@ def main():
 
     if args.sweep:
         sweep(args.sweep_reps)
+        return
+    if args.dit:
+        dit_bench(args.sweep_reps)
         return
     from paper_2609_06712_amd import rola as R
 
