@@ -6,3 +6,4 @@ nothing in here imports the GPU library: the oracle is an independent restatemen
 """
 
 from .rola_oracle import *  # noqa: F401,F403
+from . import rola_grad  # noqa: E402,F401  gradients for fine-tuning (torch fp64 autograd)
