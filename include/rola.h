@@ -145,6 +145,27 @@ rola_status rola_sparse_attn_combine(const rola_problem* p, const void* Qr, cons
                                      float eps_lr, const float* gate_logits, float eps, void* O,
                                      void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* ---- backward of the sparse branch (fine-tuning, Sec. 4.5; Algorithm step 4) ------------------
+ * rola_sparse_attn_lse is rola_sparse_attn (without a workspace) that also writes, per query,
+ * lse[b, h, n] = log2 sum_k exp2(q^r_n . k^r_k * scale * log2 e) over its selected keys (fp32
+ * [B, H, N]), which the backward needs. rola_sparse_attn_backward returns the gradients of
+ * <dOs, O^s> with respect to Q^r, K^r and V (fp32 [B, H, N, d_h] each, fully overwritten) for the
+ * given (fixed) block lists: dQ^r = scale dS K^r, dK^r = scale dS^T Q^r, dV = P^T dO^s with
+ * P = softmax, dS = P (dO^s V^T - D), D_n = dO^s_n . O^s_n. Os and lse are the forward's outputs, dOs
+ * is bf16 [B, H, N, d_h]. ws: rola_sparse_backward_workspace_bytes(p, block, sparsity) bytes (the
+ * transposed block lists take 4 (n_b + 1) bytes per key block and head). bf16 path only
+ * (ROLA_ERR_UNSUPPORTED otherwise), block 64 or 128. */
+rola_status rola_sparse_attn_lse(const rola_problem* p, const void* Qr, const void* Kr,
+                                 const void* V, int32_t block, double sparsity,
+                                 const int32_t* blk_idx, float softmax_scale, void* Os, float* lse,
+                                 hipStream_t stream);
+size_t rola_sparse_backward_workspace_bytes(const rola_problem* p, int32_t block, double sparsity);
+rola_status rola_sparse_attn_backward(const rola_problem* p, const void* Qr, const void* Kr,
+                                      const void* V, int32_t block, double sparsity,
+                                      const int32_t* blk_idx, float softmax_scale, const void* Os,
+                                      const float* lse, const void* dOs, float* dQr, float* dKr,
+                                      float* dV, void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Dense softmax attention O = softmax(Q^r K^r^T * scale) V (Sec. 3, "Full attention"): the 0 %
  * sparsity reference, same kernel as rola_sparse_attn walking every key block in order. */
 rola_status rola_dense_attn(const rola_problem* p, const void* Qr, const void* Kr, const void* V,

@@ -47,10 +47,20 @@ struct LowrankFuse {
 };
 bool fuse_supported(const Shape& s, int r);
 size_t fuse_workspace_bytes(const Shape& s, int r);
+// lse (optional, bf16 path): [B, H, N] fp32, log2 of each query's softmax denominator of the
+// log2e-scaled scores, i.e. P = exp2(S * scale * log2e - lse).
 hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, const void* V,
                               int block, int keep, const int32_t* idx, float scale, void* Os,
                               void* ws, hipStream_t st, const LowrankFuse* lf = nullptr,
-                              void* fuse_ws = nullptr);
+                              void* fuse_ws = nullptr, float* lse = nullptr);
+
+// sparse_bwd.hip: gradients of the block-sparse attention (bf16, d 128, block 64 or 128); fp32
+// outputs; ws: sparse_backward_workspace_bytes(s, block).
+size_t sparse_backward_workspace_bytes(const Shape& s, int block);
+hipError_t launch_sparse_backward(const Shape& s, const void* Qr, const void* Kr, const void* V,
+                                  int block, int keep, const int32_t* idx, float scale,
+                                  const void* Os, const float* lse, const void* dOs, float* dQ,
+                                  float* dK, float* dV, void* ws, hipStream_t st);
 
 // lowrank.hip
 int summary_chunks(const Shape& s, int r);

@@ -248,6 +248,69 @@ rola_status rola_dense_attn(const rola_problem* p, const void* Qr, const void* K
                                              nullptr, stream), __func__);
 }
 
+rola_status rola_sparse_attn_lse(const rola_problem* p, const void* Qr, const void* Kr,
+                                 const void* V, int32_t block, double sparsity,
+                                 const int32_t* blk_idx, float softmax_scale, void* Os, float* lse,
+                                 hipStream_t stream) {
+  rola::Shape s;
+  TRY(check_problem(p, __func__, &s));
+  TRY(check_block(s, block, __func__));
+  TRY(check_sparsity(sparsity, __func__));
+  if (!s.bf16) return fail(ROLA_ERR_UNSUPPORTED, "%s: built for the bf16 path", __func__);
+  REQUIRE_PTR(Qr);
+  REQUIRE_PTR(Kr);
+  REQUIRE_PTR(V);
+  REQUIRE_PTR(blk_idx);
+  REQUIRE_PTR(Os);
+  REQUIRE_PTR(lse);
+  if (!(softmax_scale > 0.f) || !isfinite(softmax_scale))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: softmax_scale must be finite and positive", __func__);
+  const int keep = rola_keep_blocks(rola::num_blocks(s.N, block), sparsity);
+  return hip_status(rola::launch_sparse_attn(s, Qr, Kr, V, block, keep, blk_idx, softmax_scale, Os,
+                                             nullptr, stream, nullptr, nullptr, lse),
+                    __func__);
+}
+
+size_t rola_sparse_backward_workspace_bytes(const rola_problem* p, int32_t block, double sparsity) {
+  rola::Shape s;
+  if (check_problem(p, __func__, &s) != ROLA_OK || check_block(s, block, __func__) != ROLA_OK ||
+      check_sparsity(sparsity, __func__) != ROLA_OK)
+    return 0;
+  return rola::sparse_backward_workspace_bytes(s, block);
+}
+
+rola_status rola_sparse_attn_backward(const rola_problem* p, const void* Qr, const void* Kr,
+                                      const void* V, int32_t block, double sparsity,
+                                      const int32_t* blk_idx, float softmax_scale, const void* Os,
+                                      const float* lse, const void* dOs, float* dQr, float* dKr,
+                                      float* dV, void* ws, size_t ws_bytes, hipStream_t stream) {
+  rola::Shape s;
+  TRY(check_problem(p, __func__, &s));
+  TRY(check_block(s, block, __func__));
+  TRY(check_sparsity(sparsity, __func__));
+  if (!s.bf16) return fail(ROLA_ERR_UNSUPPORTED, "%s: built for the bf16 path", __func__);
+  REQUIRE_PTR(Qr);
+  REQUIRE_PTR(Kr);
+  REQUIRE_PTR(V);
+  REQUIRE_PTR(blk_idx);
+  REQUIRE_PTR(Os);
+  REQUIRE_PTR(lse);
+  REQUIRE_PTR(dOs);
+  REQUIRE_PTR(dQr);
+  REQUIRE_PTR(dKr);
+  REQUIRE_PTR(dV);
+  REQUIRE_PTR(ws);
+  if (!(softmax_scale > 0.f) || !isfinite(softmax_scale))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: softmax_scale must be finite and positive", __func__);
+  const size_t need = rola::sparse_backward_workspace_bytes(s, block);
+  if (ws_bytes < need)
+    return fail(ROLA_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", __func__, ws_bytes, need);
+  const int keep = rola_keep_blocks(rola::num_blocks(s.N, block), sparsity);
+  return hip_status(rola::launch_sparse_backward(s, Qr, Kr, V, block, keep, blk_idx, softmax_scale,
+                                                 Os, lse, dOs, dQr, dKr, dV, ws, stream),
+                    __func__);
+}
+
 size_t rola_sparse_combine_workspace_bytes(const rola_problem* p, int32_t block, double sparsity,
                                            int32_t r) {
   rola::Shape s;

@@ -251,6 +251,7 @@ struct FuseArgs {
   const float* logits;   // [B, N]
   int H, r, ld;
   float eps_lr, eps;
+  float* lse_out;        // optional [B, H, N]: log2 of the softmax denominator of the scaled scores
 };
 
 // C^T fragments: entry (head, w, t, s, lane) = {hi, lo} of the 8 values C[2J + s][32w + l%32],
@@ -648,6 +649,8 @@ __global__ __launch_bounds__(G * BLK * 2, 2) void sparse_attn_kernel(
     const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(l), __float_as_uint(l), false, false);
     l = __uint_as_float(x[0]) + __uint_as_float(x[1]);
   }
+  if (fz.lse_out && qvalid && hh == 0)  // sum_k exp2(x_k - m) = l: log2 sum exp2 x = m + log2 l
+    fz.lse_out[head * (long)N + q] = m + __log2f(l);
   if constexpr (RJ > 0) {
     fuse_epilogue<RJ>(fz, acc, l, qvalid, head, N, q, lane, O);
     return;
@@ -772,7 +775,7 @@ hipError_t launch_bf16(const Shape& s, const void* Qr, const void* Kr, const voi
   static const FuseArgs none{};
   if (!fz || fz->r == 0)
     return launch_bf16_rj<BLK, G, NBUF, 0>(s, Qr, Kr, V, lists, list_len, list_stride, scale, Os,
-                                           pairs, none, st);
+                                           pairs, fz ? *fz : none, st);
   if (fz->r <= 32)
     return launch_bf16_rj<BLK, G, NBUF, 1>(s, Qr, Kr, V, lists, list_len, list_stride, scale, Os,
                                            pairs, *fz, st);
@@ -835,8 +838,10 @@ bool fuse_supported(const Shape& s, int r) { return s.bf16 && s.d == 128 && r >=
 
 hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, const void* V,
                               int block, int keep, const int32_t* idx, float scale, void* Os,
-                              void* ws, hipStream_t st, const LowrankFuse* lf, void* fuse_ws) {
+                              void* ws, hipStream_t st, const LowrankFuse* lf, void* fuse_ws,
+                              float* lse) {
   FuseArgs fz{};
+  fz.lse_out = lse;
   if (lf) {  // fused epilogue: C^T fragments first (fuse_ws: fuse_workspace_bytes)
     const int RJ = lf->r <= 32 ? 1 : 2;
     const long total = (long)s.B * s.H * 4 * 2 * RJ * 64;
@@ -845,9 +850,9 @@ hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, co
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     fz = FuseArgs{(const bf16*)lf->Qn, (const bf16*)lf->Pq, lf->cos_tab, lf->sin_tab,
-                  (const uint4*)fuse_ws, lf->logits, s.H, lf->r, lf->ld, lf->eps_lr, lf->eps};
+                  (const uint4*)fuse_ws, lf->logits, s.H, lf->r, lf->ld, lf->eps_lr, lf->eps, lse};
   }
-  const FuseArgs* fp = lf ? &fz : nullptr;
+  const FuseArgs* fp = (lf || lse) ? &fz : nullptr;
   if (s.bf16) {
     const int nb = num_blocks(s.N, block);
     if (block == 64) {

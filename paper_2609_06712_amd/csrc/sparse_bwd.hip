@@ -1,0 +1,448 @@
+// Backward pass of the block-sparse attention (the sparse branch's part of fine-tuning, Sec. 4.5):
+// from dO^s, the saved O^s and the forward's log-sum-exp, the gradients dQ^r, dK^r, dV of
+// O^s = softmax(Q^r K^r^T * scale) V restricted to the selected key blocks (Algorithm step 4). The
+// block lists are constant (the selection is piecewise constant in Q^r, K^r).
+//
+// With P = exp(S*scale - lse) and D_q = sum_c dO^s_qc O^s_qc:  dP = dO V^T,  dS = P (dP - D),
+// dQ = scale dS K,  dK = scale dS^T Q,  dV = P^T dO.  Two kernels, each recomputing S and P:
+//   sparse_dq_kernel   per query block, walking its own list (as the forward): Q and dO of the wave's
+//                      32 queries in registers, K and V sub-tiles through three LDS stages;
+//   sparse_dkv_kernel  per key block, walking the query blocks that selected it (lists transposed by
+//                      bwd_reverse_kernel): K and V of the wave's 32 keys in registers, Q and dO
+//                      sub-tiles (and the queries' lse and D) through three LDS stages.
+// Products on v_mfma_f32_32x32x16_bf16. S and dP come out with one lane per key and the 32 queries
+// in its registers; the products that contract over keys (dQ) or queries (dK, dV) take their other
+// operand through the transposing LDS read ds_read_b64_tr_b16, in the order the registers hold the
+// contracted index (as the forward's P V). dQ needs dS with one lane per query: each wave passes its
+// dS tile through 2 KB of LDS. Tiles are stored with a swizzle that keeps both the row reads and the
+// transposing reads free of bank conflicts. Gradients are fp32.
+#include "common.h"
+#include "launch.h"
+
+namespace rola {
+namespace {
+
+constexpr int kBSub = 32;      // keys (dQ) or queries (dK, dV) per sub-tile
+constexpr int kLsePad = 128;  // zero entries after the packed lse/D array: a sub-tile of the last
+                              // query block reads up to block - 1 entries past the last query
+
+__device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// 16-byte chunk swizzle of a 256-byte tile row: a bijection on row%16 (16 consecutive rows of a
+// row read hit distinct chunks) whose bits 1-3 differ across every aligned group of four rows (the
+// four rows of a transposing read hit distinct 32-byte chunk pairs).
+__device__ __forceinline__ int bw_swizzle(int row) {
+  return ((row & 3) << 1) | ((row >> 2) & 1) | (row & 8);
+}
+
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+// A operand from a row-major [row][128] tile: the lane's row l%32 (+ row0), channels 16s + 8(l/32).
+__device__ __forceinline__ bf16x8 row_frag(const char* tile, int row, int s, int hh) {
+  return *reinterpret_cast<const bf16x8*>(tile + row * 256 + (((2 * s + hh) ^ bw_swizzle(row)) << 4));
+}
+
+// Transposed operand of a row-major [row][128] tile for channel tile w and the 16 rows of k-step u:
+// lane (channel 32w + 16((l/16)%2) + l%16) receives rows 16u + 4(l/32) + s and 16u + 8 + 4(l/32) + s,
+// s = 0..3 -- the order in which an MFMA output hands its rows to a lane.
+__device__ __forceinline__ bf16x8 tr_frag(const char* tile, int w, int u, int lane) {
+  const int i16 = lane % 16, hh = lane / 32, g1 = (lane / 16) & 1;
+  const int c = 2 * g1 + ((i16 & 3) >> 1);
+  bf16x4 part[2];
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    const int row = 16 * u + 8 * half + 4 * hh + i16 / 4;
+    const char* p = tile + row * 256 + (((4 * w + c) ^ bw_swizzle(row)) << 4) + 8 * (i16 & 1);
+    part[half] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p);
+  }
+  return __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// D_q = sum_c dO_qc O_qc and the forward's lse, packed per query: lseD[q] = {lse_q, D_q}. 16 lanes
+// per query row, 8 channels each. The array is padded by kLsePad zero entries (read past the end).
+__global__ __launch_bounds__(256) void bwd_rowdot_kernel(long rows, const bf16* __restrict__ O,
+                                                         const bf16* __restrict__ dO,
+                                                         const float* __restrict__ lse,
+                                                         float2* __restrict__ lseD) {
+  const long row = ((long)blockIdx.x * 256 + threadIdx.x) / 16;
+  const int part = threadIdx.x % 16;
+  float s = 0.f;
+  if (row < rows) {
+    float a[8], b[8];
+    load8(O + row * 128 + part * 8, a);
+    load8(dO + row * 128 + part * 8, b);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s = fmaf(a[i], b[i], s);
+  }
+#pragma unroll
+  for (int off = 8; off >= 1; off >>= 1) s += __shfl_xor(s, off, 16);
+  if (part == 0) {
+    if (row < rows) lseD[row] = make_float2(lse[row], s);
+    else if (row < rows + kLsePad) lseD[row] = make_float2(0.f, 0.f);
+  }
+}
+
+// Membership bitmaps of the block lists: bits[head][I][J / 32] bit J % 32 (cleared beforehand).
+__global__ __launch_bounds__(64) void bwd_bits_kernel(int nb, int keep, int words,
+                                                      const int32_t* __restrict__ idx,
+                                                      uint32_t* __restrict__ bits) {
+  const long row = blockIdx.x;  // head * nb + I
+  for (int k = threadIdx.x; k < keep; k += 64) {
+    const int J = idx[row * keep + k];
+    if ((unsigned)J < (unsigned)nb) atomicOr(&bits[row * words + (J >> 5)], 1u << (J & 31));
+  }
+}
+
+// Transposed lists: rev[head][J] = count, then the query blocks I that selected J, ascending.
+__global__ __launch_bounds__(256) void bwd_reverse_kernel(int nb, int words, long heads,
+                                                          const uint32_t* __restrict__ bits,
+                                                          int32_t* __restrict__ rev) {
+  const long e = (long)blockIdx.x * 256 + threadIdx.x;
+  if (e >= heads * nb) return;
+  const long head = e / nb;
+  const int J = (int)(e % nb);
+  const uint32_t* b = bits + head * nb * (long)words + (J >> 5);
+  int32_t* out = rev + e * (long)(nb + 1);
+  int cnt = 0;
+  for (int I = 0; I < nb; ++I)
+    if ((b[(long)I * words] >> (J & 31)) & 1u) out[1 + cnt++] = I;
+  out[0] = cnt;
+}
+
+// ---- dQ: one workgroup per (b, h, query block), BLK/32 waves of 32 queries -------------------------
+template <int BLK, int NBUF>
+__global__ __launch_bounds__(BLK * 2, 2) void sparse_dq_kernel(
+    int N, int nb, int total, const int32_t* __restrict__ lists, int keep, float scale_log2,
+    float scale, const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
+    const bf16* __restrict__ dO, const float2* __restrict__ lseD, float* __restrict__ dQ) {
+  constexpr int D = 128, NW = BLK / 32;
+  constexpr int TILE = kBSub * D * 2, STAGE = 2 * TILE;
+  constexpr int DMA_PER_WAVE = TILE / 1024 / NW, SUBS = BLK / kBSub;
+  constexpr int SPITCH = 72;  // bytes per row of the dS^T scratch tile (32 queries + 4 pad)
+  __shared__ __attribute__((aligned(1024))) char lds[NBUF * STAGE];
+  __shared__ __attribute__((aligned(16))) char scr[NW][kBSub * SPITCH];
+
+  const int L = xcd_remap(blockIdx.x, total);
+  const int I = L % nb;
+  const long head = L / nb;
+  const int tid = threadIdx.x, lane = tid % 64, hh = lane / 32;
+  const int wave = wave_uniform(tid / 64);
+  const int qrow0 = I * BLK + wave * 32;  // the wave's first query
+  const int q = qrow0 + lane % 32;        // A-operand row of this lane (and column of dQ^T)
+  const bool qvalid = q < N;
+  const long hoff = head * (long)N * D;
+  const char* Kh = reinterpret_cast<const char*>(K + hoff);
+  const char* Vh = reinterpret_cast<const char*>(V + hoff);
+  typedef const __attribute__((address_space(4))) int32_t* const_i32;
+  const const_i32 slist = (const_i32)(lists + (head * nb + I) * (long)keep);
+  const int T = keep * SUBS;
+
+  bf16x8 qf[8], df[8];
+#pragma unroll
+  for (int s = 0; s < 8; ++s) {
+    qf[s] = qvalid ? *reinterpret_cast<const bf16x8*>(Q + hoff + (long)q * D + 16 * s + 8 * hh) : bf16x8{};
+    df[s] = qvalid ? *reinterpret_cast<const bf16x8*>(dO + hoff + (long)q * D + 16 * s + 8 * hh) : bf16x8{};
+  }
+  // lse and D of the rows 8j + 4(l/32) + i the S tiles hand this lane; +inf lse for rows past N
+  float lse[16], dsum[16];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = qrow0 + 8 * j + 4 * hh + i;
+      const float2 v = r < N ? lseD[head * (long)N + r] : make_float2(INFINITY, 0.f);
+      lse[4 * j + i] = v.x;
+      dsum[4 * j + i] = v.y;
+    }
+  __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0): nothing of this waits in the loop
+
+  f32x16 acc[4];
+#pragma unroll
+  for (int w = 0; w < 4; ++w) acc[w] = f32x16{};
+
+  uint32_t dsrc[DMA_PER_WAVE];
+#pragma unroll
+  for (int i = 0; i < DMA_PER_WAVE; ++i) {
+    const int row = 4 * (wave * DMA_PER_WAVE + i) + lane / 16, pos = lane % 16;
+    dsrc[i] = row * D * 2 + ((pos ^ bw_swizzle(row)) << 4);
+  }
+  const uint32_t lds0 = lds_address(lds);
+  auto key0 = [&](int t) {
+    const int J = slist[t / SUBS];
+    return (unsigned)J < (unsigned)nb ? J * BLK + (t % SUBS) * kBSub : -1;
+  };
+  auto issue = [&](int k0, int buf) {  // 2 * DMA_PER_WAVE loads per wave, always
+    k0 = max(k0, 0);
+    const uint32_t dst = lds0 + buf * STAGE;
+#pragma unroll
+    for (int i = 0; i < DMA_PER_WAVE; ++i) {
+      const uint32_t slot = (wave * DMA_PER_WAVE + i) * 1024;
+      const int r = 4 * (wave * DMA_PER_WAVE + i) + lane / 16;
+      const uint32_t rowoff = (uint32_t)(min(k0 + r, N - 1) - r) * (D * 2);  // rows past N: N-1
+      dma16(Kh, rowoff + dsrc[i], dst + slot);
+      dma16(Vh, rowoff + dsrc[i], dst + TILE + slot);
+    }
+  };
+  char* sc = scr[wave];
+
+  constexpr int PER_STEP = 2 * DMA_PER_WAVE;
+  int issued = 0;
+#pragma unroll
+  for (int j = 0; j < NBUF - 1; ++j)
+    if (j < T) issue(key0(j), j), ++issued;
+  for (int t = 0; t < T;) {
+#pragma unroll
+    for (int b = 0; b < NBUF; ++b) {
+      if (t >= T) break;
+      if (issued == t + NBUF - 1) {
+        constexpr int allowed = PER_STEP * (NBUF - 2);
+        __builtin_amdgcn_s_waitcnt((allowed & 15) | ((allowed >> 4) << 14) | (7 << 4) | (15 << 8));
+      } else {
+        __builtin_amdgcn_s_waitcnt(0);
+      }
+      __syncthreads();
+      if (issued < T) issue(key0(issued), (b + NBUF - 1) % NBUF), ++issued;
+      const int k0 = key0(t);
+      if (k0 >= 0 && k0 < N) {
+        const char* Kt = lds + b * STAGE;
+        const char* Vt = Kt + TILE;
+        f32x16 S = f32x16{}, dP = f32x16{};
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+          S = mfma32(qf[s], row_frag(Kt, lane % 32, s, hh), S);
+          dP = mfma32(df[s], row_frag(Vt, lane % 32, s, hh), dP);
+        }
+        // dS with one lane per key (column l%32); rows 8j + 4(l/32) + i are queries
+        const bool kvalid = k0 + lane % 32 < N;
+        bf16x4 ds4[4];
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          const float p = kvalid ? __builtin_amdgcn_exp2f(fmaf(S[k], scale_log2, -lse[k])) : 0.f;
+          ds4[k / 4][k % 4] = (bf16)(p * (dP[k] - dsum[k]));
+        }
+        // dS^T row-major [key][query] in the wave's scratch, then read back transposed
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          *reinterpret_cast<bf16x4*>(sc + (lane % 32) * SPITCH + 2 * (8 * j + 4 * hh)) = ds4[j];
+        asm volatile("" ::: "memory");  // the reads below follow the writes (one wave, in order)
+        bf16x8 dsf[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int i16 = lane % 16, g1 = (lane / 16) & 1;
+          bf16x4 part[2];
+#pragma unroll
+          for (int half = 0; half < 2; ++half) {
+            const int row = 16 * u + 8 * half + 4 * hh + i16 / 4;
+            part[half] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                (lds_bf16x4*)(sc + row * SPITCH + 2 * (16 * g1 + 4 * (i16 & 3))));
+          }
+          dsf[u] = __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5, 6, 7);
+        }
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+#pragma unroll
+          for (int u = 0; u < 2; ++u) acc[w] = mfma32(tr_frag(Kt, w, u, lane), dsf[u], acc[w]);
+      }
+      ++t;
+    }
+  }
+  if (qvalid) {  // dQ^T: lane = query, rows = channels 32w + 8j + 4(l/32) + i
+    float* dq = dQ + hoff + (long)q * D;
+#pragma unroll
+    for (int w = 0; w < 4; ++w)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        *reinterpret_cast<float4*>(dq + 32 * w + 8 * j + 4 * hh) =
+            make_float4(acc[w][4 * j] * scale, acc[w][4 * j + 1] * scale, acc[w][4 * j + 2] * scale,
+                        acc[w][4 * j + 3] * scale);
+  }
+}
+
+// ---- dK, dV: one workgroup per (b, h, key block), BLK/32 waves of 32 keys --------------------------
+template <int BLK, int NBUF>
+__global__ __launch_bounds__(BLK * 2, 1) void sparse_dkv_kernel(
+    int N, int nb, int total, const int32_t* __restrict__ rev, float scale_log2, float scale,
+    const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
+    const bf16* __restrict__ dO, const float2* __restrict__ lseD, float* __restrict__ dK,
+    float* __restrict__ dV) {
+  constexpr int D = 128, NW = BLK / 32;
+  constexpr int TILE = kBSub * D * 2;
+  constexpr int STAGE = 2 * TILE + NW * 1024;  // Q, dO, then each wave's copy of the rows' lse/D
+  constexpr int DMA_PER_WAVE = TILE / 1024 / NW, SUBS = BLK / kBSub;
+  __shared__ __attribute__((aligned(1024))) char lds[NBUF * STAGE];
+
+  const int L = xcd_remap(blockIdx.x, total);
+  const int J = L % nb;
+  const long head = L / nb;
+  const int tid = threadIdx.x, lane = tid % 64, hh = lane / 32;
+  const int wave = wave_uniform(tid / 64);
+  const int key = J * BLK + wave * 32 + lane % 32;  // B-operand column of this lane
+  const bool kvalid = key < N;
+  const long hoff = head * (long)N * D;
+  const char* Qh = reinterpret_cast<const char*>(Q + hoff);
+  const char* dOh = reinterpret_cast<const char*>(dO + hoff);
+  typedef const __attribute__((address_space(4))) int32_t* const_i32;
+  const const_i32 rl = (const_i32)(rev + (head * nb + J) * (long)(nb + 1));
+  const int E = rl[0];
+  const int T = E * SUBS;
+
+  bf16x8 kf[8], vf[8];
+#pragma unroll
+  for (int s = 0; s < 8; ++s) {
+    kf[s] = kvalid ? *reinterpret_cast<const bf16x8*>(K + hoff + (long)key * D + 16 * s + 8 * hh) : bf16x8{};
+    vf[s] = kvalid ? *reinterpret_cast<const bf16x8*>(V + hoff + (long)key * D + 16 * s + 8 * hh) : bf16x8{};
+  }
+  __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
+
+  f32x16 aK[4], aV[4];
+#pragma unroll
+  for (int w = 0; w < 4; ++w) aK[w] = aV[w] = f32x16{};
+
+  uint32_t dsrc[DMA_PER_WAVE];
+#pragma unroll
+  for (int i = 0; i < DMA_PER_WAVE; ++i) {
+    const int row = 4 * (wave * DMA_PER_WAVE + i) + lane / 16, pos = lane % 16;
+    dsrc[i] = row * D * 2 + ((pos ^ bw_swizzle(row)) << 4);
+  }
+  const uint32_t lds0 = lds_address(lds);
+  const char* lsebase = reinterpret_cast<const char*>(lseD + head * (long)N);
+  auto query0 = [&](int t) { return rl[1 + t / SUBS] * BLK + (t % SUBS) * kBSub; };
+  auto issue = [&](int q0, int buf) {  // 2 * DMA_PER_WAVE + 1 loads per wave, always
+    const uint32_t dst = lds0 + buf * STAGE;
+#pragma unroll
+    for (int i = 0; i < DMA_PER_WAVE; ++i) {
+      const uint32_t slot = (wave * DMA_PER_WAVE + i) * 1024;
+      const int r = 4 * (wave * DMA_PER_WAVE + i) + lane / 16;
+      const uint32_t rowoff = (uint32_t)(min(q0 + r, N - 1) - r) * (D * 2);  // rows past N: N-1
+      dma16(Qh, rowoff + dsrc[i], dst + slot);
+      dma16(dOh, rowoff + dsrc[i], dst + TILE + slot);
+    }
+    // lse, D of the 32 queries (256 bytes, lanes 16-63 repeat lanes 0-15): the array is padded by
+    // kLsePad entries, and rows past N are masked below
+    dma16(lsebase, (uint32_t)(q0 * 8 + (lane % 16) * 16), dst + 2 * TILE + wave * 1024);
+  };
+
+  constexpr int PER_STEP = 2 * DMA_PER_WAVE + 1;
+  int issued = 0;
+#pragma unroll
+  for (int j = 0; j < NBUF - 1; ++j)
+    if (j < T) issue(query0(j), j), ++issued;
+  for (int t = 0; t < T;) {
+#pragma unroll
+    for (int b = 0; b < NBUF; ++b) {
+      if (t >= T) break;
+      if (issued == t + NBUF - 1) {
+        constexpr int allowed = PER_STEP * (NBUF - 2);
+        __builtin_amdgcn_s_waitcnt((allowed & 15) | ((allowed >> 4) << 14) | (7 << 4) | (15 << 8));
+      } else {
+        __builtin_amdgcn_s_waitcnt(0);
+      }
+      __syncthreads();
+      if (issued < T) issue(query0(issued), (b + NBUF - 1) % NBUF), ++issued;
+      const int q0 = query0(t);
+      const char* Qt = lds + b * STAGE;
+      const char* dOt = Qt + TILE;
+      const float2* lt = reinterpret_cast<const float2*>(Qt + 2 * TILE + wave * 1024);
+      f32x16 S = f32x16{}, dP = f32x16{};
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        S = mfma32(row_frag(Qt, lane % 32, s, hh), kf[s], S);
+        dP = mfma32(row_frag(dOt, lane % 32, s, hh), vf[s], dP);
+      }
+      // one lane per key; rows 8j + 4(l/32) + i are the queries q0 + row
+      bf16x8 pb[2], sb[2];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        const int row = 8 * (k / 4) + 4 * hh + k % 4;
+        const float2 ld = lt[row];
+        const float p = q0 + row < N ? __builtin_amdgcn_exp2f(fmaf(S[k], scale_log2, -ld.x)) : 0.f;
+        pb[k / 8][k % 8] = (bf16)p;
+        sb[k / 8][k % 8] = (bf16)(p * (dP[k] - ld.y));
+      }
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          aV[w] = mfma32(tr_frag(dOt, w, u, lane), pb[u], aV[w]);
+          aK[w] = mfma32(tr_frag(Qt, w, u, lane), sb[u], aK[w]);
+        }
+      ++t;
+    }
+  }
+  if (kvalid) {  // dK^T, dV^T: lane = key, rows = channels 32w + 8j + 4(l/32) + i
+    float* dk = dK + hoff + (long)key * D;
+    float* dv = dV + hoff + (long)key * D;
+#pragma unroll
+    for (int w = 0; w < 4; ++w)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int c = 32 * w + 8 * j + 4 * hh;
+        *reinterpret_cast<float4*>(dk + c) = make_float4(aK[w][4 * j] * scale, aK[w][4 * j + 1] * scale,
+                                                         aK[w][4 * j + 2] * scale, aK[w][4 * j + 3] * scale);
+        *reinterpret_cast<float4*>(dv + c) = make_float4(aV[w][4 * j], aV[w][4 * j + 1],
+                                                         aV[w][4 * j + 2], aV[w][4 * j + 3]);
+      }
+  }
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct BwdWs {
+  size_t lsed, bits, rev;
+};
+BwdWs bwd_layout(const Shape& s, int block) {
+  const size_t heads = (size_t)s.B * s.H, nb = num_blocks(s.N, block), words = (nb + 31) / 32;
+  return {align256((heads * s.N + kLsePad) * sizeof(float2)), align256(heads * nb * words * 4),
+          align256(heads * nb * (nb + 1) * 4)};
+}
+
+template <int BLK>
+hipError_t launch_bwd(const Shape& s, const void* Qr, const void* Kr, const void* V, int keep,
+                      const int32_t* idx, float scale, const void* Os, const float* lse,
+                      const void* dOs, float* dQ, float* dK, float* dV, void* ws, hipStream_t st) {
+  const int nb = num_blocks(s.N, BLK), words = (nb + 31) / 32;
+  const long heads = (long)s.B * s.H, rows = heads * s.N;
+  const BwdWs lay = bwd_layout(s, BLK);
+  float2* lseD = (float2*)ws;
+  uint32_t* bits = (uint32_t*)((char*)ws + lay.lsed);
+  int32_t* rev = (int32_t*)((char*)ws + lay.lsed + lay.bits);
+  const long rd_threads = (rows + kLsePad) * 16;
+  hipLaunchKernelGGL(bwd_rowdot_kernel, dim3((unsigned)((rd_threads + 255) / 256)), dim3(256), 0,
+                     st, rows, (const bf16*)Os, (const bf16*)dOs, lse, lseD);
+  hipError_t e = hipMemsetAsync(bits, 0, (size_t)heads * nb * words * 4, st);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(bwd_bits_kernel, dim3((unsigned)(heads * nb)), dim3(64), 0, st, nb, keep,
+                     words, idx, bits);
+  hipLaunchKernelGGL(bwd_reverse_kernel, dim3((unsigned)((heads * nb + 255) / 256)), dim3(256), 0,
+                     st, nb, words, heads, (const uint32_t*)bits, rev);
+  const int total = (int)(heads * nb);
+  const float sl = scale * 1.4426950408889634f;
+  hipLaunchKernelGGL((sparse_dq_kernel<BLK, 3>), dim3(total), dim3(BLK * 2), 0, st, s.N, nb, total,
+                     idx, keep, sl, scale, (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V,
+                     (const bf16*)dOs, (const float2*)lseD, dQ);
+  hipLaunchKernelGGL((sparse_dkv_kernel<BLK, 3>), dim3(total), dim3(BLK * 2), 0, st, s.N, nb, total,
+                     (const int32_t*)rev, sl, scale, (const bf16*)Qr, (const bf16*)Kr,
+                     (const bf16*)V, (const bf16*)dOs, (const float2*)lseD, dK, dV);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t sparse_backward_workspace_bytes(const Shape& s, int block) {
+  if (!s.bf16 || s.d != 128 || (block != 64 && block != 128)) return 0;
+  const BwdWs w = bwd_layout(s, block);
+  return w.lsed + w.bits + w.rev;
+}
+
+hipError_t launch_sparse_backward(const Shape& s, const void* Qr, const void* Kr, const void* V,
+                                  int block, int keep, const int32_t* idx, float scale,
+                                  const void* Os, const float* lse, const void* dOs, float* dQ,
+                                  float* dK, float* dV, void* ws, hipStream_t st) {
+  if (block == 64)
+    return launch_bwd<64>(s, Qr, Kr, V, keep, idx, scale, Os, lse, dOs, dQ, dK, dV, ws, st);
+  return launch_bwd<128>(s, Qr, Kr, V, keep, idx, scale, Os, lse, dOs, dQ, dK, dV, ws, st);
+}
+
+}  // namespace rola

@@ -56,6 +56,10 @@ SIGNATURES = {
     "rola_lowrank_features": (_i32, [_PP, _p, _p, _i32, _p, _p, _i32, _i32, _i32, _p, _p]),
     "rola_gate_logits": (_i32, [_PP, _p, _i32, _p, _f32, _p, _p]),
     "rola_sparse_combine_workspace_bytes": (_sz, [_PP, _i32, _f64, _i32]),
+    "rola_sparse_attn_lse": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p, _p]),
+    "rola_sparse_backward_workspace_bytes": (_sz, [_PP, _i32, _f64]),
+    "rola_sparse_attn_backward": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p, _p, _p, _p,
+                                         _p, _p, _sz, _p]),
     "rola_sparse_attn_combine": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p, _i32, _p, _p,
                                         _i32, _p, _f32, _p, _f32, _p, _p, _sz, _p]),
 }
@@ -346,3 +350,36 @@ def rola_sparse_attn_combine(Qr, Kr, V, grid, block, sparsity, blk_idx, Qn, Pq, 
                                         _ptr(logits), eps, _ptr(out), _ptr(ws), ws.numel(),
                                         _stream(stream)), "rola_sparse_attn_combine")
     return out
+
+
+def rola_sparse_attn_lse(Qr, Kr, V, grid, block, sparsity, blk_idx, scale=None, out=None, lse=None,
+                         stream=None):
+    """Sparse attention that also returns the per-query log2-sum-exp2 (fp32 [B, H, N])."""
+    _act(Qr, "Qr")
+    prob = problem_of(Qr, grid)
+    scale = prob.d_h ** -0.5 if scale is None else scale
+    out = torch.empty_like(Qr) if out is None else out
+    if lse is None:
+        lse = torch.empty(Qr.shape[:3], dtype=torch.float32, device=Qr.device)
+    _check(LIB.rola_sparse_attn_lse(ctypes.byref(prob), _ptr(Qr), _ptr(Kr), _ptr(V), block, sparsity,
+                                    _ptr(blk_idx), scale, _ptr(out), _ptr(lse), _stream(stream)),
+           "rola_sparse_attn_lse")
+    return out, lse
+
+
+def rola_sparse_attn_backward(Qr, Kr, V, grid, block, sparsity, blk_idx, Os, lse, dOs, scale=None,
+                              ws=None, stream=None):
+    """Gradients (dQ^r, dK^r, dV), fp32, of <dOs, O^s> for fixed block lists."""
+    _act(Qr, "Qr")
+    prob = problem_of(Qr, grid)
+    scale = prob.d_h ** -0.5 if scale is None else scale
+    dQ = torch.empty(Qr.shape, dtype=torch.float32, device=Qr.device)
+    dK, dV = torch.empty_like(dQ), torch.empty_like(dQ)
+    if ws is None:
+        need = LIB.rola_sparse_backward_workspace_bytes(ctypes.byref(prob), block, sparsity)
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=Qr.device)
+    _check(LIB.rola_sparse_attn_backward(ctypes.byref(prob), _ptr(Qr), _ptr(Kr), _ptr(V), block,
+                                         sparsity, _ptr(blk_idx), scale, _ptr(Os), _ptr(lse),
+                                         _ptr(dOs), _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(ws),
+                                         ws.numel(), _stream(stream)), "rola_sparse_attn_backward")
+    return dQ, dK, dV
