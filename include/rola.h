@@ -166,6 +166,31 @@ rola_status rola_sparse_attn_backward(const rola_problem* p, const void* Qr, con
                                       const float* lse, const void* dOs, float* dQr, float* dKr,
                                       float* dV, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* ---- backward of the low-rank branch, the fusion and the gate (fine-tuning, Sec. 4.5) ----------
+ * rola_lowrank_backward: gradients of <dO, O> with O = (O^s / r_s + sigma(logit) RMSNorm(q~^T C)) r_s
+ * (eq. gate, eq. ctx, eq. qklr; SiLU with the rotation outside) with respect to O^s (dOs, bf16
+ * [B, H, N, d_h], the input of rola_sparse_attn_backward), Q^n, K^n and V through the low-rank branch
+ * (dQn, dKn, dV: fp32 [B, H, N, d_h]; the sparse branch's shares come from rola_sparse_attn_backward),
+ * P_q and P_k (dPq, dPk: fp32 [H, r, d_h], summed over the batch) and the gate logits (dlogits: fp32
+ * [B, N], summed over the heads). C is the forward's summary, Os the forward's O^s. Reductions run in
+ * a fixed order (reproducible). ws: rola_lowrank_backward_workspace_bytes(p, r). bf16 path with
+ * r <= 64 (ROLA_ERR_UNSUPPORTED otherwise).
+ * rola_gate_logits_backward: for logits = X W_g + b_g, dX = dlogits W_g^T (fp32 [B, N, d_model];
+ * may be NULL), dWg = X^T dlogits (fp32 [d_model]) and dbg = sum dlogits (fp32, one device value).
+ * ws: rola_gate_backward_workspace_bytes(p, d_model). */
+size_t rola_lowrank_backward_workspace_bytes(const rola_problem* p, int32_t r);
+rola_status rola_lowrank_backward(const rola_problem* p, const void* Qn, const void* Kn,
+                                  const void* V, const void* Pq, const void* Pk, int32_t r,
+                                  const float* cos_tab, const float* sin_tab, int32_t rope_ld,
+                                  const float* C, const void* Os, const float* gate_logits,
+                                  float eps_lr, float eps, const void* dO, void* dOs, float* dQn,
+                                  float* dKn, float* dV, float* dPq, float* dPk, float* dlogits,
+                                  void* ws, size_t ws_bytes, hipStream_t stream);
+size_t rola_gate_backward_workspace_bytes(const rola_problem* p, int32_t d_model);
+rola_status rola_gate_logits_backward(const rola_problem* p, const void* X, int32_t d_model,
+                                      const void* Wg, const float* dlogits, float* dX, float* dWg,
+                                      float* dbg, void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Dense softmax attention O = softmax(Q^r K^r^T * scale) V (Sec. 3, "Full attention"): the 0 %
  * sparsity reference, same kernel as rola_sparse_attn walking every key block in order. */
 rola_status rola_dense_attn(const rola_problem* p, const void* Qr, const void* Kr, const void* V,

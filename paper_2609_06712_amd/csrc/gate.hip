@@ -62,7 +62,69 @@ __global__ __launch_bounds__(256) void gate_logits_kernel(long rows, int dm, con
   }
 }
 
+// Backward of the gate logits: dX[row] = dlogit[row] W_g (fp32), and per chunk of rows the partial
+// sums of dW_g = sum_row dlogit[row] X[row] and db_g = sum_row dlogit[row] (slot dm of the partial).
+template <typename T>
+__global__ __launch_bounds__(256) void gate_bwd_kernel(long rows, int dm, long chunk,
+                                                       const T* __restrict__ X,
+                                                       const T* __restrict__ W,
+                                                       const float* __restrict__ dlog,
+                                                       float* __restrict__ dX,
+                                                       float* __restrict__ part) {
+  const long r0 = blockIdx.x * chunk, r1 = min(rows, r0 + chunk);
+  for (int c = threadIdx.x; c <= dm; c += 256) {
+    const float w = c < dm ? to_f32(W[c]) : 0.f;
+    float acc = 0.f;
+    for (long r = r0; r < r1; ++r) {
+      const float g = dlog[r];
+      if (c < dm) {
+        acc = fmaf(g, to_f32(X[r * dm + c]), acc);
+        if (dX) dX[r * dm + c] = g * w;
+      } else {
+        acc += g;
+      }
+    }
+    part[blockIdx.x * (long)(dm + 1) + c] = acc;
+  }
+}
+
+__global__ __launch_bounds__(256) void gate_bwd_reduce_kernel(int n, int dm,
+                                                              const float* __restrict__ part,
+                                                              float* __restrict__ dW,
+                                                              float* __restrict__ db) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c > dm) return;
+  float s = 0.f;
+  for (int i = 0; i < n; ++i) s += part[(long)i * (dm + 1) + c];  // chunk order: reproducible
+  if (c < dm) dW[c] = s;
+  else *db = s;
+}
+
+constexpr int kGateBwdChunks = 1024;
+
 }  // namespace
+
+size_t gate_backward_workspace_bytes(int d_model) {
+  return (size_t)kGateBwdChunks * (d_model + 1) * sizeof(float);
+}
+
+hipError_t launch_gate_backward(const Shape& s, const void* X, int d_model, const void* Wg,
+                                const float* dlogits, float* dX, float* dWg, float* dbg, void* ws,
+                                hipStream_t st) {
+  const long rows = (long)s.B * s.N;
+  const long chunk = (rows + kGateBwdChunks - 1) / kGateBwdChunks;
+  const int n = (int)((rows + chunk - 1) / chunk);
+  float* part = (float*)ws;
+  if (s.bf16)
+    hipLaunchKernelGGL(gate_bwd_kernel<bf16>, dim3(n), dim3(256), 0, st, rows, d_model, chunk,
+                       (const bf16*)X, (const bf16*)Wg, dlogits, dX, part);
+  else
+    hipLaunchKernelGGL(gate_bwd_kernel<float>, dim3(n), dim3(256), 0, st, rows, d_model, chunk,
+                       (const float*)X, (const float*)Wg, dlogits, dX, part);
+  hipLaunchKernelGGL(gate_bwd_reduce_kernel, dim3((d_model + 1 + 255) / 256), dim3(256), 0, st, n,
+                     d_model, (const float*)part, dWg, dbg);
+  return hipGetLastError();
+}
 
 hipError_t launch_gate_logits(const Shape& s, const void* X, int d_model, const void* Wg, float bg,
                               float* logits, hipStream_t st) {

@@ -54,6 +54,17 @@ hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, co
                               void* ws, hipStream_t st, const LowrankFuse* lf = nullptr,
                               void* fuse_ws = nullptr, float* lse = nullptr);
 
+// lowrank_bwd.hip: gradients of the low-rank branch and the gated fusion (bf16, d 128, r <= 64, SiLU
+// with the rotation outside). dOs bf16; the other gradients fp32; dP_q, dP_k summed over the batch,
+// dlogits over the heads. ws: lowrank_backward_workspace_bytes(s, r).
+size_t lowrank_backward_workspace_bytes(const Shape& s, int r);
+hipError_t launch_lowrank_backward(const Shape& s, const void* Qn, const void* Kn, const void* V,
+                                   const void* Pq, const void* Pk, int r, const float* cos_tab,
+                                   const float* sin_tab, int ld, const float* C, const void* Os,
+                                   const float* logits, float eps_lr, float eps, const void* dO,
+                                   void* dOs, float* dQn, float* dKn, float* dV, float* dPq,
+                                   float* dPk, float* dlogits, void* ws, hipStream_t st);
+
 // sparse_bwd.hip: gradients of the block-sparse attention (bf16, d 128, block 64 or 128); fp32
 // outputs; ws: sparse_backward_workspace_bytes(s, block).
 size_t sparse_backward_workspace_bytes(const Shape& s, int block);
@@ -86,5 +97,11 @@ hipError_t launch_combine(const Shape& s, const void* Os, const void* Olr, const
 hipError_t launch_gate_logits(const Shape& s, const void* X, int d_model, const void* Wg, float bg,
                               float* logits, hipStream_t st);
 int gate_max_model();
+// Backward of the gate logits: dX (optional, fp32 [B, N, d_model]) = dlogits W_g; dWg (fp32 [d_model])
+// = sum dlogits X; dbg (fp32 scalar) = sum dlogits. ws: gate_backward_workspace_bytes(d_model).
+size_t gate_backward_workspace_bytes(int d_model);
+hipError_t launch_gate_backward(const Shape& s, const void* X, int d_model, const void* Wg,
+                                const float* dlogits, float* dX, float* dWg, float* dbg, void* ws,
+                                hipStream_t st);
 
 }  // namespace rola

@@ -464,6 +464,74 @@ rola_status rola_gate_logits(const rola_problem* p, const void* X, int32_t d_mod
   return hip_status(rola::launch_gate_logits(s, X, d_model, Wg, bg, logits, stream), __func__);
 }
 
+size_t rola_gate_backward_workspace_bytes(const rola_problem* p, int32_t d_model) {
+  rola::Shape s;
+  if (check_problem(p, __func__, &s) != ROLA_OK || d_model <= 0 || (d_model % 8) != 0 ||
+      d_model > rola::gate_max_model())
+    return 0;
+  return rola::gate_backward_workspace_bytes(d_model);
+}
+
+rola_status rola_gate_logits_backward(const rola_problem* p, const void* X, int32_t d_model,
+                                      const void* Wg, const float* dlogits, float* dX, float* dWg,
+                                      float* dbg, void* ws, size_t ws_bytes, hipStream_t stream) {
+  rola::Shape s;
+  TRY(check_problem(p, __func__, &s));
+  REQUIRE_PTR(X);
+  REQUIRE_PTR(Wg);
+  REQUIRE_PTR(dlogits);
+  REQUIRE_PTR(dWg);
+  REQUIRE_PTR(dbg);
+  REQUIRE_PTR(ws);
+  if (dX != nullptr && !aligned(dX))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: dX not 16-byte aligned", __func__);
+  if (d_model <= 0 || (d_model % 8) != 0)
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: d_model=%d must be a positive multiple of 8", __func__,
+                (int)d_model);
+  if (d_model > rola::gate_max_model())
+    return fail(ROLA_ERR_UNSUPPORTED, "%s: d_model=%d above %d", __func__, (int)d_model,
+                rola::gate_max_model());
+  const size_t need = rola::gate_backward_workspace_bytes(d_model);
+  if (ws_bytes < need)
+    return fail(ROLA_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", __func__, ws_bytes, need);
+  return hip_status(rola::launch_gate_backward(s, X, d_model, Wg, dlogits, dX, dWg, dbg, ws, stream),
+                    __func__);
+}
+
+size_t rola_lowrank_backward_workspace_bytes(const rola_problem* p, int32_t r) {
+  rola::Shape s;
+  if (check_problem(p, __func__, &s) != ROLA_OK || check_rank(s, r, __func__) != ROLA_OK) return 0;
+  return rola::lowrank_backward_workspace_bytes(s, r);
+}
+
+rola_status rola_lowrank_backward(const rola_problem* p, const void* Qn, const void* Kn,
+                                  const void* V, const void* Pq, const void* Pk, int32_t r,
+                                  const float* cos_tab, const float* sin_tab, int32_t rope_ld,
+                                  const float* C, const void* Os, const float* gate_logits,
+                                  float eps_lr, float eps, const void* dO, void* dOs, float* dQn,
+                                  float* dKn, float* dV, float* dPq, float* dPk, float* dlogits,
+                                  void* ws, size_t ws_bytes, hipStream_t stream) {
+  rola::Shape s;
+  TRY(check_problem(p, __func__, &s));
+  TRY(check_rank(s, r, __func__));
+  if (!s.bf16 || r > 64)
+    return fail(ROLA_ERR_UNSUPPORTED, "%s: built for the bf16 path with r <= 64", __func__);
+  const void* ptrs[] = {Qn, Kn, V, Pq, Pk, C, Os, gate_logits, dO, dOs, dQn, dKn, dV, dPq, dPk,
+                        dlogits, ws};
+  for (const void* q : ptrs)
+    if (!aligned(q)) return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: a pointer is null or not 16-byte aligned", __func__);
+  TRY(check_tables(cos_tab, sin_tab, rope_ld, r / 2, __func__));
+  if (!(eps_lr >= 0.f) || !isfinite(eps_lr) || !(eps >= 0.f) || !isfinite(eps))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: eps values must be finite and >= 0", __func__);
+  const size_t need = rola::lowrank_backward_workspace_bytes(s, r);
+  if (ws_bytes < need)
+    return fail(ROLA_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", __func__, ws_bytes, need);
+  return hip_status(rola::launch_lowrank_backward(s, Qn, Kn, V, Pq, Pk, r, cos_tab, sin_tab, rope_ld,
+                                                  C, Os, gate_logits, eps_lr, eps, dO, dOs, dQn,
+                                                  dKn, dV, dPq, dPk, dlogits, ws, stream),
+                    __func__);
+}
+
 rola_status rola_combine(const rola_problem* p, const void* Os, const void* Olr,
                          const float* gate_logits, float eps, void* O, hipStream_t stream) {
   rola::Shape s;

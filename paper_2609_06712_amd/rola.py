@@ -57,6 +57,11 @@ SIGNATURES = {
     "rola_gate_logits": (_i32, [_PP, _p, _i32, _p, _f32, _p, _p]),
     "rola_sparse_combine_workspace_bytes": (_sz, [_PP, _i32, _f64, _i32]),
     "rola_sparse_attn_lse": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p, _p]),
+    "rola_lowrank_backward_workspace_bytes": (_sz, [_PP, _i32]),
+    "rola_lowrank_backward": (_i32, [_PP, _p, _p, _p, _p, _p, _i32, _p, _p, _i32, _p, _p, _p, _f32,
+                                     _f32, _p, _p, _p, _p, _p, _p, _p, _p, _p, _sz, _p]),
+    "rola_gate_backward_workspace_bytes": (_sz, [_PP, _i32]),
+    "rola_gate_logits_backward": (_i32, [_PP, _p, _i32, _p, _p, _p, _p, _p, _p, _sz, _p]),
     "rola_sparse_backward_workspace_bytes": (_sz, [_PP, _i32, _f64]),
     "rola_sparse_attn_backward": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p, _p, _p, _p,
                                          _p, _p, _sz, _p]),
@@ -383,3 +388,42 @@ def rola_sparse_attn_backward(Qr, Kr, V, grid, block, sparsity, blk_idx, Os, lse
                                          _ptr(dOs), _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(ws),
                                          ws.numel(), _stream(stream)), "rola_sparse_attn_backward")
     return dQ, dK, dV
+
+
+def rola_lowrank_backward(Qn, Kn, V, Pq, Pk, r, cos, sin, C, Os, logits, dO, grid, eps_lr=1e-6,
+                          eps=1e-6, ws=None, stream=None):
+    """(dOs bf16, dQn, dKn, dV fp32 [B, H, N, d], dPq, dPk fp32 [H, r, d], dlogits fp32 [B, N])."""
+    _act(Qn, "Qn")
+    prob = problem_of(Qn, grid)
+    dOs = torch.empty_like(Qn)
+    f32 = dict(dtype=torch.float32, device=Qn.device)
+    dQn, dKn, dV = (torch.empty(Qn.shape, **f32) for _ in range(3))
+    dPq, dPk = torch.empty(Pq.shape, **f32), torch.empty(Pk.shape, **f32)
+    dlog = torch.empty(logits.shape, **f32)
+    if ws is None:
+        need = LIB.rola_lowrank_backward_workspace_bytes(ctypes.byref(prob), r)
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=Qn.device)
+    _check(LIB.rola_lowrank_backward(ctypes.byref(prob), _ptr(Qn), _ptr(Kn), _ptr(V), _ptr(Pq),
+                                     _ptr(Pk), r, _ptr(cos), _ptr(sin), cos.stride(0), _ptr(C),
+                                     _ptr(Os), _ptr(logits), eps_lr, eps, _ptr(dO), _ptr(dOs),
+                                     _ptr(dQn), _ptr(dKn), _ptr(dV), _ptr(dPq), _ptr(dPk),
+                                     _ptr(dlog), _ptr(ws), ws.numel(), _stream(stream)),
+           "rola_lowrank_backward")
+    return dOs, dQn, dKn, dV, dPq, dPk, dlog
+
+
+def rola_gate_logits_backward(X, Wg, dlogits, grid, H=1, d_h=128, want_dX=True, ws=None,
+                              stream=None):
+    """(dX fp32 [B, N, d_model] or None, dWg fp32 [d_model], dbg fp32 [1]) of X W_g + b_g."""
+    B, N, dm = X.shape
+    prob = problem(B, H, N, d_h, grid, X.dtype)
+    f32 = dict(dtype=torch.float32, device=X.device)
+    dX = torch.empty(X.shape, **f32) if want_dX else None
+    dWg, dbg = torch.empty(dm, **f32), torch.empty(4, **f32)
+    if ws is None:
+        need = LIB.rola_gate_backward_workspace_bytes(ctypes.byref(prob), dm)
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=X.device)
+    _check(LIB.rola_gate_logits_backward(ctypes.byref(prob), _ptr(X), dm, _ptr(Wg), _ptr(dlogits),
+                                         _ptr(dX), _ptr(dWg), _ptr(dbg), _ptr(ws), ws.numel(),
+                                         _stream(stream)), "rola_gate_logits_backward")
+    return dX, dWg, dbg[:1]

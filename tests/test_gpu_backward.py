@@ -75,3 +75,86 @@ def test_sparse_backward(grid, block, s, B):
             # shifting all keys leaves O^s unchanged: the key gradients sum to zero
             colsum = np.abs(_f64(dk[b, h]).sum(0)).max()
             assert colsum <= 1e-2 * np.abs(_f64(dk[b, h])).sum(0).max() + 1e-6
+
+
+@pytest.mark.parametrize("r,B", [(32, 1), (16, 2), (64, 1)])
+def test_lowrank_backward(r, B):
+    """The low-rank branch + fusion backward against the oracle, per head, from the GPU's own O^s."""
+    w = synth.WAN_1_3B_480P.replace(grid=(3, 10, 13), H=2, B=B, r=r)
+    inp = synth.make_inputs(w, 8)
+    d = {k: v.cuda() for k, v in inp.items()}
+    g = w.grid
+    prob = R.problem(w.B, w.H, w.N, w.d_h, g, w.dtype)
+    cos, sin = R.rola_rope_tables(prob, w.split)
+    C, _ = R.rola_lowrank_summary(d["Kn"], d["V"], d["Pk"], r, cos, sin, g)
+    gen = torch.Generator().manual_seed(5)
+    os_ = torch.randn(d["Qn"].shape, generator=gen).to(torch.bfloat16).cuda()
+    dO = torch.randn(d["Qn"].shape, generator=gen).to(torch.bfloat16).cuda()
+    dOs, dQn, dKn, dV, dPq, dPk, dlog = R.rola_lowrank_backward(
+        d["Qn"], d["Kn"], d["V"], d["Pq"], d["Pk"], r, cos, sin, C, os_, d["logits"], dO, g)
+    torch.cuda.synchronize()
+    ocos, osin = O.rope_tables(*g, w.split)
+    f = synth.to_f64(inp)
+    want = {(b, h): G.lowrank_combine_grads(f["Qn"][b, h], f["Kn"][b, h], f["V"][b, h], f["Pq"][h],
+                                            f["Pk"][h], _f64(os_[b, h]), f["logits"][b], ocos, osin,
+                                            _f64(dO[b, h]))
+            for b in range(w.B) for h in range(w.H)}
+    for (b, h), wt in want.items():
+        errs = {n: _rel(_f64(t[b, h]), wt[k]) for n, t, k in
+                (("dOs", dOs, "dos"), ("dQn", dQn, "dqn"), ("dKn", dKn, "dkn"), ("dV", dV, "dv"))}
+        print(f"[parity] lowrank backward r{r} b{b} h{h}: " +
+              ", ".join(f"{n} rel {e:.2e}" for n, e in errs.items()), flush=True)
+        for n, e in errs.items():
+            assert e <= 1e-2, (n, e)
+    # parameter gradients summed over the batch, gate-logit gradients over the heads
+    for name, k in (("dPq", dPq), ("dPk", dPk)):
+        ref = np.stack([sum(want[(b, h)][name] for b in range(w.B)) for h in range(w.H)])
+        assert _rel(_f64(k), ref) <= 1e-2, name
+    ref = np.stack([sum(want[(b, h)]["dlogits"] for h in range(w.H)) for b in range(w.B)])
+    assert _rel(_f64(dlog), ref) <= 1e-2
+
+
+def test_gate_backward():
+    gen = torch.Generator().manual_seed(6)
+    X = torch.randn((2, 300, 1536), generator=gen).to(torch.bfloat16)
+    Wg = (torch.randn((1536,), generator=gen) / 40).to(torch.bfloat16)
+    dl = torch.randn((2, 300), generator=gen)
+    dX, dWg, dbg = R.rola_gate_logits_backward(X.cuda(), Wg.cuda(), dl.cuda(), (300, 1, 1))
+    torch.cuda.synchronize()
+    want = G.gate_grads(X.double().numpy().reshape(-1, 1536), Wg.double().numpy(), dl.double().numpy().ravel())
+    assert _rel(_f64(dX).reshape(-1, 1536), want["dX"]) <= 1e-6
+    assert _rel(_f64(dWg), want["dWg"]) <= 1e-5
+    assert float(dbg.cpu()) == pytest.approx(want["dbg"], rel=1e-5)
+
+
+@pytest.mark.parametrize("grid,s", [((3, 10, 13), 0.5), ((4, 8, 16), 0.75)])
+def test_module_backward(grid, s):
+    """The composed backward (paper_2609_06712_amd.train) against fp64 autograd of the whole module,
+    per head, with the GPU's block lists."""
+    from paper_2609_06712_amd import train
+    w = synth.WAN_1_3B_480P.replace(grid=grid, H=2, sparsity=s)
+    inp = synth.make_inputs(w, 9)
+    d = {k: v.cuda() for k, v in inp.items()}
+    out, saved = train.forward(d["Qn"], d["Kn"], d["V"], d["Pq"], d["Pk"], d["logits"], w.grid,
+                               w.split, 64, s, w.r)
+    gen = torch.Generator().manual_seed(7)
+    dO = torch.randn(out.shape, generator=gen).to(torch.bfloat16).cuda()
+    gr = train.backward(d["Qn"], d["Kn"], d["V"], d["Pq"], d["Pk"], d["logits"], saved, dO)
+    torch.cuda.synchronize()
+    f = synth.to_f64(inp)
+    ocos, osin = O.rope_tables(*w.grid, w.split)
+    tot = {"dPq": 0, "dPk": 0, "dlogits": 0}
+    for h in range(w.H):
+        want = G.module_grads(f["Qn"][0, h], f["Kn"][0, h], f["V"][0, h], f["Pq"][h], f["Pk"][h],
+                              f["logits"][0], ocos, osin, saved["idx"][0, h].cpu().numpy(), 64,
+                              _f64(dO[0, h]))
+        errs = {n: _rel(_f64(gr[n][0, h]), want[k]) for n, k in
+                (("dQn", "dqn"), ("dKn", "dkn"), ("dV", "dv"))}
+        errs["dPq"] = _rel(_f64(gr["dPq"][h]), want["dPq"])
+        errs["dPk"] = _rel(_f64(gr["dPk"][h]), want["dPk"])
+        tot["dlogits"] = tot["dlogits"] + want["dlogits"]
+        print(f"[parity] module backward {grid} s{s} h{h}: " +
+              ", ".join(f"{n} rel {e:.2e}" for n, e in errs.items()), flush=True)
+        for n, e in errs.items():
+            assert e <= 2e-2, (n, e)
+    assert _rel(_f64(gr["dlogits"][0]), tot["dlogits"]) <= 2e-2
