@@ -15,6 +15,7 @@ oracle timed on a bounded sample of the same layer.
 from __future__ import annotations
 
 import argparse
+import ctypes
 import json
 import os
 import sys
@@ -277,6 +278,51 @@ def sweep(reps: int) -> None:
               f"{100 * f_dense / dense_ms / 1e9 / PEAK_BF16_TFLOPS:.1f} | 1 | 1 |", flush=True)
 
 
+def train_bench(reps: int) -> None:
+    """Forward (keeping what the backward needs) and backward of the module at the 14B 720p shape,
+    per entry point, printed as markdown."""
+    from paper_2609_06712_amd import rola as R
+    w = synth.WAN_14B_720P
+    g = w.grid
+    dev = torch.device("cuda:0")
+    inp = synth.make_inputs(w, 0, device=dev)
+    prob = R.problem(w.B, w.H, w.N, w.d_h, g, w.dtype)
+    cos, sin = R.rola_rope_tables(prob, w.split, w.base)
+    qr = R.rola_rope_apply(inp["Qn"], cos, sin, g)
+    kr = R.rola_rope_apply(inp["Kn"], cos, sin, g)
+    idx = R.rola_block_select(qr, kr, g, w.block, w.sparsity)
+    os_, lse = R.rola_sparse_attn_lse(qr, kr, inp["V"], g, w.block, w.sparsity, idx)
+    C, _ = R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], w.r, cos, sin, g)
+    dO = torch.randn_like(os_)
+    f_fwd = sparse_flops_performed(idx, w.N, w.block, w.d_h)
+    ws_sp = torch.empty(R.LIB.rola_sparse_backward_workspace_bytes(ctypes.byref(prob), w.block,
+                                                                    w.sparsity), dtype=torch.uint8,
+                        device=dev)
+    ws_lr = torch.empty(R.LIB.rola_lowrank_backward_workspace_bytes(ctypes.byref(prob), w.r),
+                        dtype=torch.uint8, device=dev)
+    dOs = R.rola_lowrank_backward(inp["Qn"], inp["Kn"], inp["V"], inp["Pq"], inp["Pk"], w.r, cos, sin,
+                                  C, os_, inp["logits"], dO, g, ws=ws_lr)[0]
+    rows = [
+        ("sparse forward with lse", lambda: R.rola_sparse_attn_lse(qr, kr, inp["V"], g, w.block,
+                                                                   w.sparsity, idx, out=os_, lse=lse),
+         f_fwd),
+        ("low-rank + fusion backward", lambda: R.rola_lowrank_backward(
+            inp["Qn"], inp["Kn"], inp["V"], inp["Pq"], inp["Pk"], w.r, cos, sin, C, os_,
+            inp["logits"], dO, g, ws=ws_lr), None),
+        ("sparse attention backward", lambda: R.rola_sparse_attn_backward(
+            qr, kr, inp["V"], g, w.block, w.sparsity, idx, os_, lse, dOs, ws=ws_sp), 2.5 * f_fwd),
+    ]
+    print("## Fine-tuning pass of the module, " + w.name + "\n")
+    print("| step | ms (median) | TFLOP/s (algorithmic) | % of bf16 peak |")
+    print("|---|---|---|---|", flush=True)
+    for name, fn, flops in rows:
+        ms = time_call(fn, reps)[0]
+        tf = f"{flops / ms / 1e9:.1f}" if flops else "-"
+        pc = f"{100 * flops / ms / 1e9 / PEAK_BF16_TFLOPS:.1f}" if flops else "-"
+        print(f"| {name} | {ms:.3f} | {tf} | {pc} |", flush=True)
+    print()
+
+
 def dit_bench(reps: int) -> None:
     """Per-block time of a synthetic Wan-shaped DiT block (random weights) with the RoLA module or
     the dense attention kernel as its self-attention, and the implied DiT time per denoising step
@@ -315,6 +361,8 @@ def main():
                     help="print the measurement sweeps (1.3B layer, low-rank N x r, sparse S x block) "
                          "as markdown instead of the JSON line")
     ap.add_argument("--sweep-reps", type=int, default=10)
+    ap.add_argument("--train", action="store_true",
+                    help="time the module's fine-tuning forward and backward at the 14B shape")
     ap.add_argument("--dit", action="store_true",
                     help="time a synthetic Wan-shaped DiT block with RoLA vs dense self-attention")
     ap.add_argument("--calibration-copy", action="store_true",
@@ -333,6 +381,9 @@ def main():
         return
     if args.dit:
         dit_bench(args.sweep_reps)
+        return
+    if args.train:
+        train_bench(args.sweep_reps)
         return
     from paper_2609_06712_amd import rola as R
 

@@ -11,7 +11,7 @@
 //   dk~ = dC v,  dv = dC^T k~,  dpsi = R_r^T dk~,  dy = dpsi * SiLU'(y),  dk^n = P_k^T dy,
 //   dP_k = sum_k dy_k k^n_k^T.
 // One workgroup per (b, h, chunk of tokens), four waves each on its own token: the per-token vectors
-// use one lane per rotary coordinate (r <= 64) or two channels per lane; the outer products dC,
+// use one lane per rotary coordinate (r <= 64) or channels l and l + 64; the outer products dC,
 // dP_q, dP_k accumulate per thread over the chunk and are summed over chunks (and batch) in a fixed
 // order afterwards, so every gradient is reproducible. fp32 arithmetic, bf16 inputs.
 #include "common.h"
@@ -21,6 +21,7 @@ namespace rola {
 namespace {
 
 constexpr int kD = 128, kMaxR = 64, kWaves = 4;
+constexpr int kLd = kD + 1;  // LDS row pitch of P and C (floats): lane-strided row reads hit distinct banks
 constexpr int kOuterPer = kMaxR * kD / 256;  // outer-product elements per thread (r <= 64)
 
 __device__ __forceinline__ float wsum(float x) {  // sum over the 64 lanes
@@ -44,7 +45,7 @@ __device__ __forceinline__ Feat features(const float* xs, const float* Ps, int r
                                          float c, float s) {
   float y = 0.f;
   if (lane < r)
-    for (int k = 0; k < kD; ++k) y = fmaf(Ps[lane * kD + k], xs[k], y);
+    for (int k = 0; k < kD; ++k) y = fmaf(Ps[lane * kLd + k], xs[k], y);
   const float a = silu(y);
   const float b = __shfl_xor(a, 1);  // the pair partner's activation
   const float f = (lane & 1) ? b * s + a * c : a * c - b * s;
@@ -66,7 +67,7 @@ __global__ __launch_bounds__(256) void lr_bwd_q_kernel(
     const float* __restrict__ logits, float eps_lr, float eps, const bf16* __restrict__ dO,
     bf16* __restrict__ dOs, float* __restrict__ dQn, float* __restrict__ dlog_h,
     float* __restrict__ part_dC, float* __restrict__ part_dPq) {
-  __shared__ float Cs[kMaxR * kD], Ps[kMaxR * kD];
+  __shared__ float Cs[kMaxR * kLd], Ps[kMaxR * kLd];
   __shared__ float xq[kWaves][kD], vt[kWaves][kD];     // q^n and du of each wave's token
   __shared__ float ft[kWaves][kMaxR], dyt[kWaves][kMaxR];  // q~ and dy of each wave's token
   const long head = blockIdx.x / n_chunks;
@@ -74,8 +75,8 @@ __global__ __launch_bounds__(256) void lr_bwd_q_kernel(
   const long b = head / H;
   const int tid = threadIdx.x, lane = tid % 64, wave = tid / 64;
   for (int e = tid; e < r * kD; e += 256) {
-    Cs[e] = C[head * r * kD + e];
-    Ps[e] = to_f32(Pq[(long)h * r * kD + e]);
+    Cs[(e / kD) * kLd + e % kD] = C[head * r * kD + e];
+    Ps[(e / kD) * kLd + e % kD] = to_f32(Pq[(long)h * r * kD + e]);
   }
   float accC[kOuterPer], accP[kOuterPer];
 #pragma unroll
@@ -88,11 +89,11 @@ __global__ __launch_bounds__(256) void lr_bwd_q_kernel(
     if (valid) {
       const long row = (head * N + tok) * kD;
       float2 qv, ov, dv;
-      qv = make_float2(to_f32(Qn[row + 2 * lane]), to_f32(Qn[row + 2 * lane + 1]));
-      ov = make_float2(to_f32(Os[row + 2 * lane]), to_f32(Os[row + 2 * lane + 1]));
-      dv = make_float2(to_f32(dO[row + 2 * lane]), to_f32(dO[row + 2 * lane + 1]));
-      xq[wave][2 * lane] = qv.x;
-      xq[wave][2 * lane + 1] = qv.y;
+      qv = make_float2(to_f32(Qn[row + lane]), to_f32(Qn[row + lane + 64]));
+      ov = make_float2(to_f32(Os[row + lane]), to_f32(Os[row + lane + 64]));
+      dv = make_float2(to_f32(dO[row + lane]), to_f32(dO[row + lane + 64]));
+      xq[wave][lane] = qv.x;
+      xq[wave][lane + 64] = qv.y;
       const int j = lane / 2;
       const float c = lane < r ? cos_tab[(long)tok * ld + j] : 1.f;
       const float s = lane < r ? sin_tab[(long)tok * ld + j] : 0.f;
@@ -104,8 +105,8 @@ __global__ __launch_bounds__(256) void lr_bwd_q_kernel(
       float u0 = 0.f, u1 = 0.f;
       for (int k = 0; k < r; ++k) {
         const float fk = ft[wave][k];
-        u0 = fmaf(fk, Cs[k * kD + 2 * lane], u0);
-        u1 = fmaf(fk, Cs[k * kD + 2 * lane + 1], u1);
+        u0 = fmaf(fk, Cs[k * kLd + lane], u0);
+        u1 = fmaf(fk, Cs[k * kLd + lane + 64], u1);
       }
       const float su = wsum(u0 * u0 + u1 * u1), so = wsum(ov.x * ov.x + ov.y * ov.y);
       const float t = wsum(dv.x * u0 + dv.y * u1);
@@ -113,18 +114,18 @@ __global__ __launch_bounds__(256) void lr_bwd_q_kernel(
       const float g = sigmoid(logits[b * N + tok]);
       const float a = g * rs / rho;
       const float kos = g * t / (rho * kD * rs);
-      dOs[row + 2 * lane] = (bf16)fmaf(kos, ov.x, dv.x);
-      dOs[row + 2 * lane + 1] = (bf16)fmaf(kos, ov.y, dv.y);
+      dOs[row + lane] = (bf16)fmaf(kos, ov.x, dv.x);
+      dOs[row + lane + 64] = (bf16)fmaf(kos, ov.y, dv.y);
       if (lane == 0) dlog_h[head * N + tok] = rs * t / rho * g * (1.f - g);
       const float kdu = a * t / (kD * rho * rho);
       const float du0 = a * dv.x - kdu * u0, du1 = a * dv.y - kdu * u1;
-      vt[wave][2 * lane] = du0;
-      vt[wave][2 * lane + 1] = du1;
+      vt[wave][lane] = du0;
+      vt[wave][lane + 64] = du1;
       __builtin_amdgcn_wave_barrier();
       // dq~ = C du (lane k < r), then dy
       float dq = 0.f;
       if (lane < r)
-        for (int cc = 0; cc < kD; ++cc) dq = fmaf(Cs[lane * kD + cc], vt[wave][cc], dq);
+        for (int cc = 0; cc < kD; ++cc) dq = fmaf(Cs[lane * kLd + cc], vt[wave][cc], dq);
       const float dy = feature_grad(dq, fq.y, r, lane, c, s);
       dyt[wave][lane] = dy;
       __builtin_amdgcn_wave_barrier();
@@ -132,10 +133,11 @@ __global__ __launch_bounds__(256) void lr_bwd_q_kernel(
       float d0 = 0.f, d1 = 0.f;
       for (int k = 0; k < r; ++k) {
         const float dk = dyt[wave][k];
-        d0 = fmaf(Ps[k * kD + 2 * lane], dk, d0);
-        d1 = fmaf(Ps[k * kD + 2 * lane + 1], dk, d1);
+        d0 = fmaf(Ps[k * kLd + lane], dk, d0);
+        d1 = fmaf(Ps[k * kLd + lane + 64], dk, d1);
       }
-      *reinterpret_cast<float2*>(dQn + row + 2 * lane) = make_float2(d0, d1);
+      dQn[row + lane] = d0;
+      dQn[row + lane + 64] = d1;
     } else {
       for (int e = lane; e < kD; e += 64) xq[wave][e] = vt[wave][e] = 0.f;
       ft[wave][lane] = dyt[wave][lane] = 0.f;
@@ -194,15 +196,15 @@ __global__ __launch_bounds__(256) void lr_bwd_k_kernel(
     const bf16* __restrict__ V, const bf16* __restrict__ Pk, const float* __restrict__ cos_tab,
     const float* __restrict__ sin_tab, const float* __restrict__ dC, float* __restrict__ dKn,
     float* __restrict__ dV, float* __restrict__ part_dPk) {
-  __shared__ float Gs[kMaxR * kD], Ps[kMaxR * kD];
+  __shared__ float Gs[kMaxR * kLd], Ps[kMaxR * kLd];
   __shared__ float xk[kWaves][kD], vv[kWaves][kD];
   __shared__ float ft[kWaves][kMaxR], dyt[kWaves][kMaxR];
   const long head = blockIdx.x / n_chunks;
   const int chunk = blockIdx.x % n_chunks, h = (int)(head % H);
   const int tid = threadIdx.x, lane = tid % 64, wave = tid / 64;
   for (int e = tid; e < r * kD; e += 256) {
-    Gs[e] = dC[head * r * kD + e];
-    Ps[e] = to_f32(Pk[(long)h * r * kD + e]);
+    Gs[(e / kD) * kLd + e % kD] = dC[head * r * kD + e];
+    Ps[(e / kD) * kLd + e % kD] = to_f32(Pk[(long)h * r * kD + e]);
   }
   float accP[kOuterPer];
 #pragma unroll
@@ -214,11 +216,11 @@ __global__ __launch_bounds__(256) void lr_bwd_k_kernel(
     __syncthreads();
     if (valid) {
       const long row = (head * N + tok) * kD;
-      xk[wave][2 * lane] = to_f32(Kn[row + 2 * lane]);
-      xk[wave][2 * lane + 1] = to_f32(Kn[row + 2 * lane + 1]);
-      const float v0 = to_f32(V[row + 2 * lane]), v1 = to_f32(V[row + 2 * lane + 1]);
-      vv[wave][2 * lane] = v0;
-      vv[wave][2 * lane + 1] = v1;
+      xk[wave][lane] = to_f32(Kn[row + lane]);
+      xk[wave][lane + 64] = to_f32(Kn[row + lane + 64]);
+      const float v0 = to_f32(V[row + lane]), v1 = to_f32(V[row + lane + 64]);
+      vv[wave][lane] = v0;
+      vv[wave][lane + 64] = v1;
       const int j = lane / 2;
       const float c = lane < r ? cos_tab[(long)tok * ld + j] : 1.f;
       const float s = lane < r ? sin_tab[(long)tok * ld + j] : 0.f;
@@ -229,24 +231,26 @@ __global__ __launch_bounds__(256) void lr_bwd_k_kernel(
       // dk~ = dC v (lane k < r); dv = dC^T k~ (two channels per lane)
       float dk = 0.f;
       if (lane < r)
-        for (int cc = 0; cc < kD; ++cc) dk = fmaf(Gs[lane * kD + cc], vv[wave][cc], dk);
+        for (int cc = 0; cc < kD; ++cc) dk = fmaf(Gs[lane * kLd + cc], vv[wave][cc], dk);
       float w0 = 0.f, w1 = 0.f;
       for (int k = 0; k < r; ++k) {
         const float fkk = ft[wave][k];
-        w0 = fmaf(Gs[k * kD + 2 * lane], fkk, w0);
-        w1 = fmaf(Gs[k * kD + 2 * lane + 1], fkk, w1);
+        w0 = fmaf(Gs[k * kLd + lane], fkk, w0);
+        w1 = fmaf(Gs[k * kLd + lane + 64], fkk, w1);
       }
-      *reinterpret_cast<float2*>(dV + row + 2 * lane) = make_float2(w0, w1);
+      dV[row + lane] = w0;
+      dV[row + lane + 64] = w1;
       const float dy = feature_grad(dk, fk.y, r, lane, c, s);
       dyt[wave][lane] = dy;
       __builtin_amdgcn_wave_barrier();
       float d0 = 0.f, d1 = 0.f;
       for (int k = 0; k < r; ++k) {
         const float dyk = dyt[wave][k];
-        d0 = fmaf(Ps[k * kD + 2 * lane], dyk, d0);
-        d1 = fmaf(Ps[k * kD + 2 * lane + 1], dyk, d1);
+        d0 = fmaf(Ps[k * kLd + lane], dyk, d0);
+        d1 = fmaf(Ps[k * kLd + lane + 64], dyk, d1);
       }
-      *reinterpret_cast<float2*>(dKn + row + 2 * lane) = make_float2(d0, d1);
+      dKn[row + lane] = d0;
+      dKn[row + lane + 64] = d1;
     } else {
       for (int e = lane; e < kD; e += 64) xk[wave][e] = 0.f;
       dyt[wave][lane] = 0.f;
