@@ -100,15 +100,4 @@ __device__ __forceinline__ int xcd_remap(int wg, int total) {
   return (xcd < rem ? xcd * (q + 1) : rem * (q + 1) + (xcd - rem) * q) + local;
 }
 
-// Bijective remap in which the 8 XCDs take interleaved chunks of `c` consecutive logical ids: at any
-// moment every XCD works on its own run of c neighbours, and together they cover 8c consecutive
-// ids (for the attention grid: one head's query blocks, so that head's K/V is what the shared
-// Infinity Cache holds). Ids past the last full group of 8c keep their dispatch position.
-__device__ __forceinline__ int xcd_chunk_remap(int wg, int total, int c) {
-  const int full = total / (kNumXcd * c) * (kNumXcd * c);
-  if (wg >= full) return wg;
-  const int xcd = wg % kNumXcd, k = wg / kNumXcd;
-  return (k / c) * (kNumXcd * c) + xcd * c + k % c;
-}
-
 }  // namespace rola
