@@ -100,4 +100,30 @@ __device__ __forceinline__ int xcd_remap(int wg, int total) {
   return (xcd < rem ? xcd * (q + 1) : rem * (q + 1) + (xcd - rem) * q) + local;
 }
 
+// The XCD the calling wave runs on (hardware register XCC_ID).
+__device__ __forceinline__ int xcd_id() {
+  unsigned v;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(v));
+  return (int)(v % kNumXcd);
+}
+
+// Work queue over the same XCD ranges as xcd_remap, for a grid of resident workgroups: XCD x
+// hands out its range [begin(x), begin(x) + len(x)) in ascending order through counter[x] (zero
+// at launch), and a workgroup whose XCD's range is used up takes ids from the other ranges. The
+// dies of one chip do not run equally fast (their finishing times under a static split differ by
+// up to a fifth, and which die is slow changes from chip to chip), so the kernel then ends when
+// the work ends, not when the slowest die's share does. Returns -1 once all ranges are used up;
+// every call ends after at most kNumXcd atomics, as the counters only grow.
+__device__ inline int xcd_queue_claim(int* counter, int xcd, int total) {
+  const int q = total / kNumXcd, rem = total % kNumXcd;
+  for (int k = 0; k < kNumXcd; ++k) {
+    const int y = (xcd + k) % kNumXcd;
+    const int len = q + (y < rem);
+    if (__hip_atomic_load(counter + y, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= len) continue;
+    const int i = atomicAdd(counter + y, 1);
+    if (i < len) return (y < rem ? y * (q + 1) : rem * (q + 1) + (y - rem) * q) + i;
+  }
+  return -1;
+}
+
 }  // namespace rola

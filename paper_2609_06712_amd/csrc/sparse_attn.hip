@@ -21,6 +21,7 @@
 // wave overlaps that of the others. O is rescaled only when a sub-tile raises a row max by more
 // than 2^8: the softmax ratio does not depend on the reference max, so this is exact.
 #include <algorithm>
+#include <atomic>
 #include <climits>
 
 #include "common.h"
@@ -34,6 +35,9 @@
 #endif
 #ifndef ROLA_B64_PAIRING
 #define ROLA_B64_PAIRING 1  // pair query blocks by list overlap (1) or take adjacent pairs (0)
+#endif
+#ifndef ROLA_B64_QUEUE
+#define ROLA_B64_QUEUE 1  // resident workgroups claim groups from per-XCD queues (1) or a static grid (0)
 #endif
 
 namespace rola {
@@ -175,7 +179,8 @@ template <int G>
 __global__ __launch_bounds__(256) void group_union_kernel(int nb, int keep, int ngroups, int stride,
                                                           const int32_t* __restrict__ idx,
                                                           const int32_t* __restrict__ pairs,
-                                                          int32_t* __restrict__ out) {
+                                                          int32_t* __restrict__ out,
+                                                          int* __restrict__ queue) {
   extern __shared__ uint32_t sh[];
   const int words = (nb + 31) >> 5;
   uint32_t* bits = sh;                                 // [G][words]: membership of each list
@@ -184,6 +189,7 @@ __global__ __launch_bounds__(256) void group_union_kernel(int nb, int keep, int 
   const long head = gp / ngroups;
   const int I0 = G * (int)(gp % ngroups);
   const int tid = threadIdx.x;
+  if (queue && gp == 0 && tid < kNumXcd) queue[tid] = 0;  // the attention kernel's work queue
   for (int w = tid; w < G * words; w += 256) bits[w] = 0u;
   __syncthreads();
   const int pr = G == 2 && pairs ? pairs[gp] : 0;
@@ -400,12 +406,23 @@ __device__ __forceinline__ int group_block(const int32_t* pairs, long entry, int
 //        order for all query blocks of the group (list_len = nb).
 // RJ > 0: the epilogue also computes the low-rank readout (r <= 32 RJ) and the gated combine
 // (fuse_epilogue) and writes O instead of O^s.
-template <int BLK, int G, int NBUF, int TAB, int RJ>
-__global__ __launch_bounds__(G * BLK * 2, 2) void sparse_attn_kernel(
-    int N, int nb, int ngroups, int total, const int32_t* __restrict__ lists, int list_len,
-    int list_stride, const int32_t* __restrict__ pairs, float scale_log2,
-    const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
-    bf16* __restrict__ O, FuseArgs fz) {
+struct AttnArgs {
+  int N, nb, ngroups, total;  // total = B * H * ngroups groups
+  const int32_t* lists;
+  int list_len, list_stride;
+  const int32_t* pairs;
+  float scale_log2;
+  const bf16* Q;
+  const bf16* K;
+  const bf16* V;
+  bf16* O;
+  FuseArgs fz;
+  int* queue;  // QUEUE: kNumXcd counters, zero at launch
+};
+
+template <int BLK, int G, int NBUF, int TAB, int RJ, bool QUEUE>
+__global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 ? 3 : 2) void sparse_attn_kernel(
+    const AttnArgs args) {
   static_assert(G == 1 || G == 2 || G == 4, "one, two or four query blocks per workgroup");
   static_assert(NBUF >= 3, "loads of later sub-tiles stay in flight during a step");
   constexpr int D = 128, WPB = BLK / 32, NW = G * WPB;
@@ -417,256 +434,297 @@ __global__ __launch_bounds__(G * BLK * 2, 2) void sparse_attn_kernel(
   __shared__ __attribute__((aligned(1024))) char lds[NBUF * STAGE];
   __shared__ int tab[TAB > 0 ? TAB : 1];  // the workgroup's block list (TAB > 0)
 
-  const int L = xcd_remap(blockIdx.x, total);
-  const int grp = L % ngroups;
-  const long head = L / ngroups;
-  const int tid = threadIdx.x, lane = tid % 64, hh = lane / 32;
-  const int wave = wave_uniform(tid / 64);   // wave-uniform: LDS DMA bases in SGPRs
-  const int qb = wave / WPB;                 // which of the group's query blocks this wave serves
-  const int I = group_block<G>(pairs, head * ngroups + grp, grp, qb);  // nb: missing second block
-  const int q = I * BLK + (wave % WPB) * 32 + lane % 32;  // this lane's query (column of S^T, O^T)
-  const bool qvalid = I < nb && q < N;
-  const int mybit = 1 << qb;
-  const bf16* Qh = Q + head * (long)N * D;
-  const char* Kh = reinterpret_cast<const char*>(K + head * (long)N * D);
-  const char* Vh = reinterpret_cast<const char*>(V + head * (long)N * D);
+  const int wave = wave_uniform(threadIdx.x / 64);  // wave-uniform: LDS DMA bases in SGPRs
 
-  // The workgroup's block list: with TAB > 0 it is copied into LDS once (E <= TAB) and each step
-  // reads the entries of the next step, which the barrier of that step finds complete, so list reads
-  // never stall a step; otherwise entries come through uniform scalar loads.
-  typedef const __attribute__((address_space(4))) int32_t* const_i32;
-  const int32_t* glist = nullptr;
-  int E = list_len;
-  if (lists && G > 1) {
-    glist = lists + (head * ngroups + grp) * (long)list_stride;
-    E = ((const_i32)glist)[0];
-    glist += 1;
-  } else if (lists) {
-    glist = lists + (head * nb + grp) * (long)list_stride;
-  }
-  const const_i32 slist = (const_i32)glist;
-  const int T = E * SUBS;  // sub-tiles the workgroup walks
-  if (TAB > 0 && glist) {
-    for (int i = tid; i < E; i += NW * 64) tab[i] = glist[i];
-  }
-  struct Step {
-    int k0;    // first key, -1 if the block index is out of range
-    int mask;  // query blocks of the group that selected the block
-  };
-  // raw(e): entry e of the list (in a VGPR when it comes from the LDS table); step_of decodes the
-  // entry of sub-tile t.
-  auto raw = [&](int e) -> int {
-    if (!glist) return G > 1 ? (e | (((1 << G) - 1) << 16)) : e;  // dense: every block, all
-    const int i = min(e, max(E - 1, 0));
-    return TAB > 0 ? tab[i] : (int)slist[i];
-  };
-  auto step_of = [&](int v, int t) {
-    v = TAB > 0 ? wave_uniform(v) : v;
-    const int J = G > 1 ? (v & 0xFFFF) : v;
-    const int mask = G > 1 ? (v >> 16) : 1;
-    return Step{(unsigned)J < (unsigned)nb ? J * BLK + (t % SUBS) * kSub : -1, mask};
-  };
-  auto active = [&](const Step& s) { return (s.mask & mybit) && s.k0 >= 0 && s.k0 < N; };
+  // One group (b, h, G query blocks), logical id L in [0, total). With the work queue the
+  // arguments and the lane index are re-derived per group through opaque values: otherwise the
+  // compiler hoists everything derived from them out of the group loop, and the kernel, already at
+  // the SGPR limit, spills them into VGPRs and loses a workgroup per CU.
+  auto run = [&](const int L) {
+    typedef const __attribute__((address_space(4))) AttnArgs* args_ptr;
+    // the only explicit argument, at offset 0 of the kernel-argument segment
+    args_ptr ap = (args_ptr)__builtin_amdgcn_kernarg_segment_ptr();
+    int lane;
+    if constexpr (QUEUE) {
+      asm volatile("" : "+s"(ap));
+      asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lane));
+    } else {
+      lane = threadIdx.x % 64;
+    }
+    const int tid = wave * 64 + lane;
+    const int N = ap->N, nb = ap->nb, ngroups = ap->ngroups;
+    const int list_len = ap->list_len, list_stride = ap->list_stride;
+    const int32_t* __restrict__ lists = ap->lists;
+    const int32_t* __restrict__ pairs = ap->pairs;
+    const float scale_log2 = ap->scale_log2;
+    const bf16* __restrict__ Q = ap->Q;
+    const bf16* __restrict__ K = ap->K;
+    const bf16* __restrict__ V = ap->V;
+    bf16* __restrict__ O = ap->O;
+    const FuseArgs& fz = *(const FuseArgs*)&ap->fz;
+    const int hh = lane / 32;
+    const int qb = wave / WPB;  // which of the group's query blocks this wave serves
+    // Per-lane LDS offsets. DMA: lane l of 1-KB slot s fills row 4s + l/16 at chunk position l%16
+    // with source chunk (position ^ swizzle(row)). K operand of k-step s: row l%32, chunk 2s + l/32.
+    // V^T operand of channel tile w: the lane supplies row 4(l/32) + (l%16)/4 (plus 16u + 8 for the
+    // second four keys of k-step u) and channels 32w + 16((l/16)%2) + 4(l%4) .. +3.
+    uint32_t dk[DMA_PER_WAVE], dv[DMA_PER_WAVE];
+#pragma unroll
+    for (int i = 0; i < DMA_PER_WAVE; ++i) {
+      const int row = 4 * (wave * DMA_PER_WAVE + i) + lane / 16, pos = lane % 16;
+      dk[i] = row * D * 2 + ((pos ^ k_swizzle(row)) << 4);
+      dv[i] = row * D * 2 + ((pos ^ v_swizzle(row)) << 4);
+    }
+    int ko[8];
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      const int row = lane % 32;
+      ko[s] = row * 256 + (((2 * s + hh) ^ k_swizzle(row)) << 4);
+    }
+    int vo[4];
+    {
+      const int i16 = lane % 16, row = 4 * hh + i16 / 4;
+      const int c = 2 * ((lane / 16) & 1) + ((i16 & 3) >> 1);
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+        vo[w] = TILE + row * 256 + (((4 * w + c) ^ v_swizzle(row)) << 4) + 8 * (i16 & 1);
+    }
+    const uint32_t lds0 = lds_address(lds);
+    const int grp = L % ngroups;
+    const long head = L / ngroups;
+    const int I = group_block<G>(pairs, head * ngroups + grp, grp, qb);  // nb: missing second block
+    const int q = I * BLK + (wave % WPB) * 32 + lane % 32;  // this lane's query (column of S^T, O^T)
+    const bool qvalid = I < nb && q < N;
+    const int mybit = 1 << qb;
+    const bf16* Qh = Q + head * (long)N * D;
+    const char* Kh = reinterpret_cast<const char*>(K + head * (long)N * D);
+    const char* Vh = reinterpret_cast<const char*>(V + head * (long)N * D);
 
-  // Q^T fragments of the 8 k-steps (d = 16s + 8(l/32) .. +7) stay in registers. They are complete
-  // before the first K/V load is issued: a wait for them inside the loop would also drain the
-  // K/V loads in flight.
-  bf16x8 qf[8];
-#pragma unroll
-  for (int s = 0; s < 8; ++s)
-    qf[s] = qvalid ? *reinterpret_cast<const bf16x8*>(Qh + (long)q * D + 16 * s + 8 * hh) : bf16x8{};
-  __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
-  if (TAB > 0) __syncthreads();  // the list table is complete
+    // The workgroup's block list: with TAB > 0 it is copied into LDS once (E <= TAB) and each step
+    // reads the entries of the next step, which the barrier of that step finds complete, so list reads
+    // never stall a step; otherwise entries come through uniform scalar loads.
+    typedef const __attribute__((address_space(4))) int32_t* const_i32;
+    const int32_t* glist = nullptr;
+    int E = list_len;
+    if (lists && G > 1) {
+      glist = lists + (head * ngroups + grp) * (long)list_stride;
+      E = ((const_i32)glist)[0];
+      glist += 1;
+    } else if (lists) {
+      glist = lists + (head * nb + grp) * (long)list_stride;
+    }
+    const const_i32 slist = (const_i32)glist;
+    const int T = E * SUBS;  // sub-tiles the workgroup walks
+    if (TAB > 0 && glist) {
+      for (int i = tid; i < E; i += NW * 64) tab[i] = glist[i];
+    }
+    struct Step {
+      int k0;    // first key, -1 if the block index is out of range
+      int mask;  // query blocks of the group that selected the block
+    };
+    // raw(e): entry e of the list (in a VGPR when it comes from the LDS table); step_of decodes the
+    // entry of sub-tile t.
+    auto raw = [&](int e) -> int {
+      if (!glist) return G > 1 ? (e | (((1 << G) - 1) << 16)) : e;  // dense: every block, all
+      const int i = min(e, max(E - 1, 0));
+      return TAB > 0 ? tab[i] : (int)slist[i];
+    };
+    auto step_of = [&](int v, int t) {
+      v = TAB > 0 ? wave_uniform(v) : v;
+      const int J = G > 1 ? (v & 0xFFFF) : v;
+      const int mask = G > 1 ? (v >> 16) : 1;
+      return Step{(unsigned)J < (unsigned)nb ? J * BLK + (t % SUBS) * kSub : -1, mask};
+    };
+    auto active = [&](const Step& s) { return (s.mask & mybit) && s.k0 >= 0 && s.k0 < N; };
 
-  f32x16 acc[4];        // O^T channel tiles 32w .. 32w+31
-  float m = -INFINITY;  // running reference max (log2 units) of this lane's query
-  float l = 0.f;        // running sum of this lane's 16 keys per sub-tile (the other 16: lane l^32)
+    // Q^T fragments of the 8 k-steps (d = 16s + 8(l/32) .. +7) stay in registers. They are complete
+    // before the first K/V load is issued: a wait for them inside the loop would also drain the
+    // K/V loads in flight.
+    bf16x8 qf[8];
 #pragma unroll
-  for (int w = 0; w < 4; ++w) acc[w] = f32x16{};
+    for (int s = 0; s < 8; ++s)
+      qf[s] = qvalid ? *reinterpret_cast<const bf16x8*>(Qh + (long)q * D + 16 * s + 8 * hh) : bf16x8{};
+    __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
+    if (TAB > 0) __syncthreads();  // the list table is complete
 
-  // Per-lane LDS offsets. DMA: lane l of 1-KB slot s fills row 4s + l/16 at chunk position l%16
-  // with source chunk (position ^ swizzle(row)). K operand of k-step s: row l%32, chunk 2s + l/32.
-  // V^T operand of channel tile w: the lane supplies row 4(l/32) + (l%16)/4 (plus 16u + 8 for the
-  // second four keys of k-step u) and channels 32w + 16((l/16)%2) + 4(l%4) .. +3.
-  uint32_t dk[DMA_PER_WAVE], dv[DMA_PER_WAVE];
+    f32x16 acc[4];        // O^T channel tiles 32w .. 32w+31
+    float m = -INFINITY;  // running reference max (log2 units) of this lane's query
+    float l = 0.f;        // running sum of this lane's 16 keys per sub-tile (the other 16: lane l^32)
 #pragma unroll
-  for (int i = 0; i < DMA_PER_WAVE; ++i) {
-    const int row = 4 * (wave * DMA_PER_WAVE + i) + lane / 16, pos = lane % 16;
-    dk[i] = row * D * 2 + ((pos ^ k_swizzle(row)) << 4);
-    dv[i] = row * D * 2 + ((pos ^ v_swizzle(row)) << 4);
-  }
-  int ko[8];
-#pragma unroll
-  for (int s = 0; s < 8; ++s) {
-    const int row = lane % 32;
-    ko[s] = row * 256 + (((2 * s + hh) ^ k_swizzle(row)) << 4);
-  }
-  int vo[4];
-  {
-    const int i16 = lane % 16, row = 4 * hh + i16 / 4;
-    const int c = 2 * ((lane / 16) & 1) + ((i16 & 3) >> 1);
-#pragma unroll
-    for (int w = 0; w < 4; ++w)
-      vo[w] = TILE + row * 256 + (((4 * w + c) ^ v_swizzle(row)) << 4) + 8 * (i16 & 1);
-  }
+    for (int w = 0; w < 4; ++w) acc[w] = f32x16{};
 
-  const uint32_t lds0 = lds_address(lds);
-  auto issue = [&](const Step& s, int buf) {  // always 2 * DMA_PER_WAVE loads (fixed vmcnt per step)
-    const int k0 = max(s.k0, 0);
-    const uint32_t dst = lds0 + buf * STAGE;
-    if (k0 + kSub <= N) {
-      const char* kb = Kh + (long)k0 * D * 2;
-      const char* vb = Vh + (long)k0 * D * 2;
+    auto issue = [&](const Step& s, int buf) {  // always 2 * DMA_PER_WAVE loads (fixed vmcnt per step)
+      const int k0 = max(s.k0, 0);
+      const uint32_t dst = lds0 + buf * STAGE;
+      if (k0 + kSub <= N) {
+        const char* kb = Kh + (long)k0 * D * 2;
+        const char* vb = Vh + (long)k0 * D * 2;
 #pragma unroll
-      for (int i = 0; i < DMA_PER_WAVE; ++i) {
-        const uint32_t slot = (wave * DMA_PER_WAVE + i) * 1024;
-        dma16(kb, dk[i], dst + slot);
-        dma16(vb, dv[i], dst + TILE + slot);
+        for (int i = 0; i < DMA_PER_WAVE; ++i) {
+          const uint32_t slot = (wave * DMA_PER_WAVE + i) * 1024;
+          dma16(kb, dk[i], dst + slot);
+          dma16(vb, dv[i], dst + TILE + slot);
+        }
+      } else {  // ragged tail: rows past N re-read row N-1 (a valid key, see mask_tail)
+#pragma unroll
+        for (int i = 0; i < DMA_PER_WAVE; ++i) {
+          const uint32_t slot = (wave * DMA_PER_WAVE + i) * 1024;
+          const int r = 4 * (wave * DMA_PER_WAVE + i) + lane / 16;
+          const uint32_t row = (uint32_t)(min(k0 + r, N - 1) - r) * (D * 2);
+          dma16(Kh, row + dk[i], dst + slot);
+          dma16(Vh, row + dv[i], dst + TILE + slot);
+        }
       }
-    } else {  // ragged tail: rows past N re-read row N-1 (a valid key, see mask_tail)
-#pragma unroll
-      for (int i = 0; i < DMA_PER_WAVE; ++i) {
-        const uint32_t slot = (wave * DMA_PER_WAVE + i) * 1024;
-        const int r = 4 * (wave * DMA_PER_WAVE + i) + lane / 16;
-        const uint32_t row = (uint32_t)(min(k0 + r, N - 1) - r) * (D * 2);
-        dma16(Kh, row + dk[i], dst + slot);
-        dma16(Vh, row + dv[i], dst + TILE + slot);
-      }
-    }
-  };
+    };
 
-  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
-  auto load_k = [&](int buf, int s0, bf16x8 (&kf)[4]) {  // K operands of k-steps s0 .. s0+3
+    typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+    auto load_k = [&](int buf, int s0, bf16x8 (&kf)[4]) {  // K operands of k-steps s0 .. s0+3
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
-      kf[s] = *reinterpret_cast<const bf16x8*>(lds + buf * STAGE + ko[s0 + s]);
-  };
-  auto load_v = [&](int buf, int u, bf16x8 (&vf)[4]) {  // V^T operands of key k-step u
+      for (int s = 0; s < 4; ++s)
+        kf[s] = *reinterpret_cast<const bf16x8*>(lds + buf * STAGE + ko[s0 + s]);
+    };
+    auto load_v = [&](int buf, int u, bf16x8 (&vf)[4]) {  // V^T operands of key k-step u
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const char* p = lds + buf * STAGE + vo[w] + 16 * u * 256;
-      const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p);
-      const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p + 8 * 256));
-      vf[w] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-    }
-  };
-  // Softmax pieces on S^T of one sub-tile (16 keys of this lane's query; the other 16 in lane l^32).
-  auto row_max = [&](const f32x16& s) {
-    float mx = s[0];
+      for (int w = 0; w < 4; ++w) {
+        const char* p = lds + buf * STAGE + vo[w] + 16 * u * 256;
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p);
+        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p + 8 * 256));
+        vf[w] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      }
+    };
+    // Softmax pieces on S^T of one sub-tile (16 keys of this lane's query; the other 16 in lane l^32).
+    auto row_max = [&](const f32x16& s) {
+      float mx = s[0];
 #pragma unroll
-    for (int k = 1; k < 16; ++k) mx = fmaxf(mx, s[k]);
-    const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
-    return fmaxf(__uint_as_float(x[0]), __uint_as_float(x[1])) * scale_log2;
-  };
-  auto rescale = [&](float mt) {  // lazy: only when the max grew by more than 2^tau
-    if (__any(mt > m + kRescaleTau)) {
-      const float mnew = fmaxf(m, mt);
-      const float alpha = __builtin_amdgcn_exp2f(m - mnew);
-      m = mnew;
-      l *= alpha;
+      for (int k = 1; k < 16; ++k) mx = fmaxf(mx, s[k]);
+      const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+      return fmaxf(__uint_as_float(x[0]), __uint_as_float(x[1])) * scale_log2;
+    };
+    auto rescale = [&](float mt) {  // lazy: only when the max grew by more than 2^tau
+      if (__any(mt > m + kRescaleTau)) {
+        const float mnew = fmaxf(m, mt);
+        const float alpha = __builtin_amdgcn_exp2f(m - mnew);
+        m = mnew;
+        l *= alpha;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) acc[w] *= alpha;
-    }
-  };
-  // Rows of a ragged last sub-tile repeat key N-1, whose score is a valid one: they leave the row
-  // max unchanged and only their probabilities are zeroed. The row sum adds exactly the bf16
-  // probabilities that enter P V (v_dot2 against (1, 1), fp32 accumulation).
-  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-  auto probs = [&](const f32x16& s, int k0, bf16x8 (&pb)[2]) {
-#pragma unroll
-    for (int k = 0; k < 16; ++k)
-      pb[k / 8][k % 8] = (bf16)__builtin_amdgcn_exp2f(fmaf(s[k], scale_log2, -m));
-    if (k0 + kSub > N) {  // value k holds key k0 + 8(k/4) + 4(l/32) + k%4
-      const int lim = N - k0 - 4 * hh;
+        for (int w = 0; w < 4; ++w) acc[w] *= alpha;
+      }
+    };
+    // Rows of a ragged last sub-tile repeat key N-1, whose score is a valid one: they leave the row
+    // max unchanged and only their probabilities are zeroed. The row sum adds exactly the bf16
+    // probabilities that enter P V (v_dot2 against (1, 1), fp32 accumulation).
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    auto probs = [&](const f32x16& s, int k0, bf16x8 (&pb)[2]) {
 #pragma unroll
       for (int k = 0; k < 16; ++k)
-        if (8 * (k / 4) + k % 4 >= lim) pb[k / 8][k % 8] = (bf16)0.f;
-    }
-    const bf16x2 one2 = {(bf16)1.0f, (bf16)1.0f};
+        pb[k / 8][k % 8] = (bf16)__builtin_amdgcn_exp2f(fmaf(s[k], scale_log2, -m));
+      if (k0 + kSub > N) {  // value k holds key k0 + 8(k/4) + 4(l/32) + k%4
+        const int lim = N - k0 - 4 * hh;
 #pragma unroll
-    for (int k = 0; k < 16; k += 2)
-      l = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[k / 8][k % 8], pb[k / 8][k % 8 + 1]}, one2, l, false);
-  };
-  auto pv = [&](int u, const bf16x8 (&vf)[4], const bf16x8 (&pb)[2]) {
-#pragma unroll
-    for (int w = 0; w < 4; ++w) acc[w] = mfma32(vf[w], pb[u], acc[w]);
-  };
-  auto qk = [&](int s0, const bf16x8* kf, f32x16& sacc, int n) {  // k-steps s0 .. s0+n-1
-#pragma unroll
-    for (int s = 0; s < n; ++s) sacc = mfma32(kf[s], qf[s0 + s], sacc);
-  };
-
-  // Pipeline: step t waits for the loads of sub-tile t and a barrier, issues the loads of sub-tile
-  // t+NBUF-1 into the buffer sub-tile t-1 has released, then S = QK(t), softmax, O += P V(t). The
-  // second wave on each SIMD overlaps its matrix and vector work with this one's. Unrolled by NBUF
-  // so each buffer is a compile-time offset.
-  constexpr int PER_STEP = 2 * DMA_PER_WAVE;  // vector-memory instructions per wave per sub-tile
-  int issued = 0;
-#pragma unroll
-  for (int j = 0; j < NBUF - 1; ++j)
-    if (j < T) {
-      issue(step_of(raw(j / SUBS), j), j);
-      ++issued;
-    }
-  int pi = raw(issued / SUBS), pc = raw(0);  // entries the next step decodes
-  for (int t = 0; t < T;) {
-#pragma unroll
-    for (int j = 0; j < NBUF; ++j) {
-      if (t >= T) break;
-      if (issued == t + NBUF - 1) {  // loads of t+1 .. t+NBUF-2 may stay in flight
-        constexpr int allowed = PER_STEP * (NBUF - 2);
-        __builtin_amdgcn_s_waitcnt((allowed & 15) | ((allowed >> 4) << 14) | (7 << 4) | (15 << 8));
-      } else {
-        __builtin_amdgcn_s_waitcnt(0);
+        for (int k = 0; k < 16; ++k)
+          if (8 * (k / 4) + k % 4 >= lim) pb[k / 8][k % 8] = (bf16)0.f;
       }
-      __syncthreads();  // sub-tile t landed for every wave; every wave is done with sub-tile t-1
-      if (issued < T) {
-        issue(step_of(pi, issued), (j + NBUF - 1) % NBUF);
+      const bf16x2 one2 = {(bf16)1.0f, (bf16)1.0f};
+#pragma unroll
+      for (int k = 0; k < 16; k += 2)
+        l = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[k / 8][k % 8], pb[k / 8][k % 8 + 1]}, one2, l, false);
+    };
+    auto pv = [&](int u, const bf16x8 (&vf)[4], const bf16x8 (&pb)[2]) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w) acc[w] = mfma32(vf[w], pb[u], acc[w]);
+    };
+    auto qk = [&](int s0, const bf16x8* kf, f32x16& sacc, int n) {  // k-steps s0 .. s0+n-1
+#pragma unroll
+      for (int s = 0; s < n; ++s) sacc = mfma32(kf[s], qf[s0 + s], sacc);
+    };
+
+    // Pipeline: step t waits for the loads of sub-tile t and a barrier, issues the loads of sub-tile
+    // t+NBUF-1 into the buffer sub-tile t-1 has released, then S = QK(t), softmax, O += P V(t). The
+    // second wave on each SIMD overlaps its matrix and vector work with this one's. Unrolled by NBUF
+    // so each buffer is a compile-time offset.
+    constexpr int PER_STEP = 2 * DMA_PER_WAVE;  // vector-memory instructions per wave per sub-tile
+    int issued = 0;
+#pragma unroll
+    for (int j = 0; j < NBUF - 1; ++j)
+      if (j < T) {
+        issue(step_of(raw(j / SUBS), j), j);
         ++issued;
       }
-      const Step cur = step_of(pc, t);
-      pi = raw(issued / SUBS);
-      pc = raw((t + 1) / SUBS);
-      if (active(cur)) {
-        bf16x8 kf[4], kg[4], vf[4], pb[2];
-        load_k(j, 0, kf);
-        load_k(j, 4, kg);
-        f32x16 sc = mfma32(kf[0], qf[0], f32x16{});
-        qk(1, kf + 1, sc, 3);
-        qk(4, kg, sc, 4);
-        load_v(j, 0, vf);
-        rescale(row_max(sc));
-        probs(sc, cur.k0, pb);
-        pv(0, vf, pb);
-        load_v(j, 1, vf);
-        pv(1, vf, pb);
+    int pi = raw(issued / SUBS), pc = raw(0);  // entries the next step decodes
+    for (int t = 0; t < T;) {
+#pragma unroll
+      for (int j = 0; j < NBUF; ++j) {
+        if (t >= T) break;
+        if (issued == t + NBUF - 1) {  // loads of t+1 .. t+NBUF-2 may stay in flight
+          constexpr int allowed = PER_STEP * (NBUF - 2);
+          __builtin_amdgcn_s_waitcnt((allowed & 15) | ((allowed >> 4) << 14) | (7 << 4) | (15 << 8));
+        } else {
+          __builtin_amdgcn_s_waitcnt(0);
+        }
+        __syncthreads();  // sub-tile t landed for every wave; every wave is done with sub-tile t-1
+        if (issued < T) {
+          issue(step_of(pi, issued), (j + NBUF - 1) % NBUF);
+          ++issued;
+        }
+        const Step cur = step_of(pc, t);
+        pi = raw(issued / SUBS);
+        pc = raw((t + 1) / SUBS);
+        if (active(cur)) {
+          bf16x8 kf[4], kg[4], vf[4], pb[2];
+          load_k(j, 0, kf);
+          load_k(j, 4, kg);
+          f32x16 sc = mfma32(kf[0], qf[0], f32x16{});
+          qk(1, kf + 1, sc, 3);
+          qk(4, kg, sc, 4);
+          load_v(j, 0, vf);
+          rescale(row_max(sc));
+          probs(sc, cur.k0, pb);
+          pv(0, vf, pb);
+          load_v(j, 1, vf);
+          pv(1, vf, pb);
+        }
+        ++t;
       }
-      ++t;
     }
-  }
 
-  {
-    const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(l), __float_as_uint(l), false, false);
-    l = __uint_as_float(x[0]) + __uint_as_float(x[1]);
-  }
-  if (fz.lse_out && qvalid && hh == 0)  // sum_k exp2(x_k - m) = l: log2 sum exp2 x = m + log2 l
-    fz.lse_out[head * (long)N + q] = m + __log2f(l);
-  if constexpr (RJ > 0) {
-    fuse_epilogue<RJ>(fz, acc, l, qvalid, head, N, q, lane, O);
-    return;
-  }
-  if (qvalid) {
-    const float inv = 1.0f / l;
-    bf16* Oq = O + head * (long)N * D + (long)q * D;
+    {
+      const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(l), __float_as_uint(l), false, false);
+      l = __uint_as_float(x[0]) + __uint_as_float(x[1]);
+    }
+    if (fz.lse_out && qvalid && hh == 0)  // sum_k exp2(x_k - m) = l: log2 sum exp2 x = m + log2 l
+      fz.lse_out[head * (long)N + q] = m + __log2f(l);
+    if constexpr (RJ > 0) {
+      fuse_epilogue<RJ>(fz, acc, l, qvalid, head, N, q, lane, O);
+      return;
+    }
+    if (qvalid) {
+      const float inv = 1.0f / l;
+      bf16* Oq = O + head * (long)N * D + (long)q * D;
 #pragma unroll
-    for (int w = 0; w < 4; ++w)
+      for (int w = 0; w < 4; ++w)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        bf16x4 o;
+        for (int j = 0; j < 4; ++j) {
+          bf16x4 o;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) o[i] = (bf16)(acc[w][4 * j + i] * inv);
-        *reinterpret_cast<bf16x4*>(Oq + 32 * w + 8 * j + 4 * hh) = o;
-      }
+          for (int i = 0; i < 4; ++i) o[i] = (bf16)(acc[w][4 * j + i] * inv);
+          *reinterpret_cast<bf16x4*>(Oq + 32 * w + 8 * j + 4 * hh) = o;
+        }
+    }
+  };
+
+  if constexpr (!QUEUE) {  // static grid: one group per workgroup, XCD-ordered
+    run(xcd_remap(blockIdx.x, args.total));
+  } else {  // a grid of resident workgroups claims groups until none are left (xcd_queue_claim)
+    __shared__ int next_group;
+    const int xcd = xcd_id();
+    for (;;) {
+      __syncthreads();  // every wave is done with the previous group's LDS stages, table and id
+      if (threadIdx.x == 0) next_group = xcd_queue_claim(args.queue, xcd, args.total);
+      __syncthreads();
+      const int L = wave_uniform(next_group);
+      if (L < 0) break;
+      run(L);
+    }
   }
 }
 
@@ -738,18 +796,49 @@ __global__ __launch_bounds__(128) void sparse_simple_kernel(int N, int block, in
   }
 }
 
+// Workgroups of `kernel` (threads each) that the current device holds at once, cached per device.
+template <typename Kernel>
+int resident_workgroups(Kernel kernel, int threads) {
+  constexpr int kMaxDevices = 64;
+  static std::atomic<int> cache[kMaxDevices];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) dev = -1;
+  if (dev >= 0) {
+    const int c = cache[dev].load(std::memory_order_relaxed);
+    if (c > 0) return c;
+  }
+  int cus = 0, per_cu = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev < 0 ? 0 : dev) != hipSuccess)
+    cus = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess)
+    per_cu = 0;
+  (void)hipGetLastError();
+  const int n = std::max(1, cus) * std::max(1, per_cu);
+  if (dev >= 0) cache[dev].store(n, std::memory_order_relaxed);
+  return n;
+}
+
+// queue: kNumXcd zeroed counters, or nullptr for the static grid of one workgroup per group.
 template <int BLK, int G, int NBUF, int TAB, int RJ>
 hipError_t launch_bf16_tab(const Shape& s, const void* Qr, const void* Kr, const void* V,
                            const int32_t* lists, int list_len, int list_stride,
                            const int32_t* pairs, float scale, void* Os, const FuseArgs& fz,
-                           hipStream_t st) {
+                           int* queue, hipStream_t st) {
   const int nb = num_blocks(s.N, BLK);
   const int ngroups = (nb + G - 1) / G;
   const int total = ngroups * s.H * s.B;
   const float sl = scale * 1.4426950408889634f;
-  hipLaunchKernelGGL((sparse_attn_kernel<BLK, G, NBUF, TAB, RJ>), dim3(total), dim3(G * BLK * 2), 0,
-                     st, s.N, nb, ngroups, total, lists, list_len, list_stride, pairs, sl,
-                     (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V, (bf16*)Os, fz);
+  const int threads = G * BLK * 2;
+  const AttnArgs a{s.N, nb, ngroups, total, lists, list_len, list_stride, pairs, sl,
+                   (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V, (bf16*)Os, fz, queue};
+  if (queue) {
+    const auto kernel = sparse_attn_kernel<BLK, G, NBUF, TAB, RJ, true>;
+    const int grid = std::min(total, resident_workgroups(kernel, threads));
+    hipLaunchKernelGGL(kernel, dim3(grid), dim3(threads), 0, st, a);
+  } else {
+    hipLaunchKernelGGL((sparse_attn_kernel<BLK, G, NBUF, TAB, RJ, false>), dim3(total), dim3(threads),
+                       0, st, a);
+  }
   return hipGetLastError();
 }
 
@@ -758,29 +847,31 @@ constexpr int kTable = 1024;
 template <int BLK, int G, int NBUF, int RJ>
 hipError_t launch_bf16_rj(const Shape& s, const void* Qr, const void* Kr, const void* V,
                           const int32_t* lists, int list_len, int list_stride, float scale,
-                          void* Os, const int32_t* pairs, const FuseArgs& fz, hipStream_t st) {
+                          void* Os, const int32_t* pairs, const FuseArgs& fz, int* queue,
+                          hipStream_t st) {
   const int max_len = G > 1 ? list_stride - 1 : list_len;
   if (lists && max_len <= kTable)
     return launch_bf16_tab<BLK, G, NBUF, kTable, RJ>(s, Qr, Kr, V, lists, list_len, list_stride,
-                                                     pairs, scale, Os, fz, st);
+                                                     pairs, scale, Os, fz, queue, st);
   return launch_bf16_tab<BLK, G, NBUF, 0, RJ>(s, Qr, Kr, V, lists, list_len, list_stride, pairs,
-                                              scale, Os, fz, st);
+                                              scale, Os, fz, queue, st);
 }
 
 // fz.r == 0: plain attention (O^s); otherwise the fused epilogue with RJ = r / 32 tiles (r 16 -> 1).
 template <int BLK, int G, int NBUF>
 hipError_t launch_bf16(const Shape& s, const void* Qr, const void* Kr, const void* V,
                        const int32_t* lists, int list_len, int list_stride, float scale, void* Os,
-                       hipStream_t st, const int32_t* pairs = nullptr, const FuseArgs* fz = nullptr) {
+                       hipStream_t st, const int32_t* pairs = nullptr, const FuseArgs* fz = nullptr,
+                       int* queue = nullptr) {
   static const FuseArgs none{};
   if (!fz || fz->r == 0)
     return launch_bf16_rj<BLK, G, NBUF, 0>(s, Qr, Kr, V, lists, list_len, list_stride, scale, Os,
-                                           pairs, fz ? *fz : none, st);
+                                           pairs, fz ? *fz : none, queue, st);
   if (fz->r <= 32)
     return launch_bf16_rj<BLK, G, NBUF, 1>(s, Qr, Kr, V, lists, list_len, list_stride, scale, Os,
-                                           pairs, *fz, st);
+                                           pairs, *fz, queue, st);
   return launch_bf16_rj<BLK, G, NBUF, 2>(s, Qr, Kr, V, lists, list_len, list_stride, scale, Os,
-                                         pairs, *fz, st);
+                                         pairs, *fz, queue, st);
 }
 
 template <typename T, int D>
@@ -804,28 +895,30 @@ bool pairing_on(int G, int nb) {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Workspace: [pair table: int32 per group, when pairing][union lists, which the candidate ranks
-// (kPairWindow bytes per query block, whole chunks) occupy before the lists are written].
+// Workspace: [work-queue counters: kNumXcd ints in 256 bytes][pair table: int32 per group, when
+// pairing][union lists, which the candidate ranks (kPairWindow bytes per query block, whole
+// chunks) occupy before the lists are written].
+constexpr size_t kQueueBytes = 256;
 struct SparseWs {
-  size_t pair_bytes, list_bytes;
+  size_t queue_bytes, pair_bytes, list_bytes;
 };
 SparseWs sparse_ws_layout(const Shape& s, int block, int keep) {
   const int G = group_of(s, block);
-  if (G == 1) return {0, 0};
+  if (G == 1) return {0, 0, 0};
   const int nb = num_blocks(s.N, block);
   const size_t heads = (size_t)s.B * s.H, ngroups = (nb + G - 1) / G;
   size_t lists = heads * ngroups * ((size_t)G * keep + 1) * sizeof(int32_t);
-  if (!pairing_on(G, nb)) return {0, lists};
+  if (!pairing_on(G, nb)) return {kQueueBytes, 0, lists};
   const size_t nchunks = (nb + kPairWindow - 1) / kPairWindow;
   lists = std::max(lists, heads * nchunks * kPairWindow * kPairWindow);
-  return {align256(heads * ngroups * sizeof(int32_t)), lists};
+  return {kQueueBytes, align256(heads * ngroups * sizeof(int32_t)), lists};
 }
 
 }  // namespace
 
 size_t sparse_workspace_bytes(const Shape& s, int block, int keep) {
   const SparseWs w = sparse_ws_layout(s, block, keep);
-  return w.pair_bytes + w.list_bytes;
+  return w.queue_bytes + w.pair_bytes + w.list_bytes;
 }
 
 size_t fuse_workspace_bytes(const Shape& s, int r) {
@@ -862,8 +955,9 @@ hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, co
         const int ngroups = (nb + G - 1) / G, stride = G * keep + 1;
         const int words = (nb + 31) / 32, heads = s.B * s.H;
         const SparseWs lay = sparse_ws_layout(s, 64, keep);
-        int32_t* pairs = lay.pair_bytes ? (int32_t*)ws : nullptr;
-        int32_t* lists = (int32_t*)((char*)ws + lay.pair_bytes);
+        int* queue = ROLA_B64_QUEUE ? (int*)ws : nullptr;
+        int32_t* pairs = lay.pair_bytes ? (int32_t*)((char*)ws + lay.queue_bytes) : nullptr;
+        int32_t* lists = (int32_t*)((char*)ws + lay.queue_bytes + lay.pair_bytes);
         if (pairs) {
           const int nchunks = (nb + kPairWindow - 1) / kPairWindow;
           hipLaunchKernelGGL(pair_rank_kernel, dim3(nchunks * heads), dim3(256),
@@ -874,11 +968,11 @@ hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, co
         }
         hipLaunchKernelGGL(group_union_kernel<G>, dim3(ngroups * heads), dim3(256),
                            (G * words + 256) * sizeof(uint32_t), st, nb, keep, ngroups, stride, idx,
-                           (const int32_t*)pairs, lists);
+                           (const int32_t*)pairs, lists, queue);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         return launch_bf16<64, G, ROLA_B64_NBUF>(s, Qr, Kr, V, lists, 0, stride, scale, Os, st,
-                                                 pairs, fp);
+                                                 pairs, fp, queue);
       }
       return launch_bf16<64, 1, 3>(s, Qr, Kr, V, idx, keep, keep, scale, Os, st, nullptr, fp);
     }

@@ -55,20 +55,21 @@ def test_workspace_helpers():
     assert R.summary_workspace_bytes(p, 33) == 0         # odd rank
     bad = R.problem(1, 40, 75601, 128, (21, 45, 80), "bf16")
     assert R.select_workspace_bytes(bad, 64) == 0
-    # pair table (one int32 per pair of query blocks, padded to 256 B), then the pair-union lists:
-    # per (b, h, pair) a count and at most 2 * keep entries; the region first holds the candidate
-    # ranks of every query block (64 bytes each, whole chunks of 64 blocks)
+    # 256 B of work-queue counters, the pair table (one int32 per pair of query blocks, padded to
+    # 256 B), then the pair-union lists: per (b, h, pair) a count and at most 2 * keep entries; the
+    # region first holds the candidate ranks of every query block (64 bytes each, whole chunks of 64)
     keep = O.keep_blocks(nb, 0.9)
+    queue = 256
     table = -(-4 * 40 * ((nb + 1) // 2) // 256) * 256
     ranks = 40 * -(-nb // 64) * 64 * 64
     lists = max(4 * 40 * ((nb + 1) // 2) * (2 * keep + 1), ranks)
-    assert R.sparse_workspace_bytes(p, 64, 0.9) == table + lists
+    assert R.sparse_workspace_bytes(p, 64, 0.9) == queue + table + lists
     keep1 = O.keep_blocks(nb, 0.99)  # short lists: the ranks set the size
     assert 4 * 40 * ((nb + 1) // 2) * (2 * keep1 + 1) < ranks
-    assert R.sparse_workspace_bytes(p, 64, 0.99) == table + ranks
+    assert R.sparse_workspace_bytes(p, 64, 0.99) == queue + table + ranks
     # more than 4064 query blocks: adjacent pairs, no table
     long = R.problem(1, 2, 64 * 4100, 128, (41, 80, 80), "bf16")
-    assert R.sparse_workspace_bytes(long, 64, 0.9) == 4 * 2 * 2050 * (2 * O.keep_blocks(4100, 0.9) + 1)
+    assert R.sparse_workspace_bytes(long, 64, 0.9) == queue + 4 * 2 * 2050 * (2 * O.keep_blocks(4100, 0.9) + 1)
     assert R.sparse_workspace_bytes(p, 128, 0.9) == 0    # 128-token blocks share nothing
     assert R.sparse_workspace_bytes(R.problem(1, 2, 256, 64, (1, 16, 16), "f32"), 64, 0.5) == 0
     assert R.sparse_workspace_bytes(bad, 64, 0.9) == 0

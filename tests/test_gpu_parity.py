@@ -237,7 +237,8 @@ def test_overlap_pairing(lists_kind, s):
     single = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, s, idx, share=False)
     torch.cuda.synchronize()
     ngroups = (nb + 1) // 2
-    table = ws[: w.B * w.H * ngroups * 4].view(torch.int32).cpu().numpy().reshape(w.B, w.H, ngroups)
+    # the workspace starts with 256 bytes of work-queue counters, then the pair table
+    table = ws[256: 256 + w.B * w.H * ngroups * 4].view(torch.int32).cpu().numpy().reshape(w.B, w.H, ngroups)
     idx_np = idx.cpu().numpy()
     for b in range(w.B):
         for h in range(w.H):
@@ -249,6 +250,36 @@ def test_overlap_pairing(lists_kind, s):
     _report("overlap pairing", kind=lists_kind, adjacent=int(sum(
         ((table[0, 0] >> 16) - (table[0, 0] & 0xFFFF)) == 1)), groups=ngroups)
     assert torch.equal(shared, single)
+
+
+def test_work_queue_full_size():
+    """At the 14B 720p size the attention kernel runs as resident workgroups that claim (head,
+    pair) groups from per-XCD counters: 23640 groups, far more than the chip holds at once, so
+    workgroups loop and XCDs that finish early take groups from the others. Every group must be
+    done exactly once: starting from stale counters (the list-merge kernel clears them), all
+    counters end past their ranges and the whole output is bitwise that of the path with one
+    query block per workgroup (a static grid); a second call on the same workspace agrees."""
+    w = synth.WAN_14B_720P
+    inp = synth.make_inputs(w, 0, device="cuda")
+    g = w.grid
+    prob = R.problem(w.B, w.H, w.N, w.d_h, g, w.dtype)
+    cos, sin = R.rola_rope_tables(prob, w.split)
+    qr = R.rola_rope_apply(inp["Qn"], cos, sin, g)
+    kr = R.rola_rope_apply(inp["Kn"], cos, sin, g)
+    idx = R.rola_block_select(qr, kr, g, 64, w.sparsity)
+    ws = torch.empty(R.sparse_workspace_bytes(prob, 64, w.sparsity), dtype=torch.uint8, device="cuda")
+    ws[:256].fill_(0x7F)
+    shared = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, w.sparsity, idx, ws=ws)
+    counters = ws[:32].view(torch.int32).cpu().numpy()
+    again = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, w.sparsity, idx, ws=ws)
+    single = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, w.sparsity, idx, share=False)
+    torch.cuda.synchronize()
+    total = w.B * w.H * ((O.num_blocks(w.N, 64) + 1) // 2)
+    q, rem = divmod(total, 8)
+    _report("work queue", groups=total, counters=counters.tolist())
+    assert all(counters[x] >= q + (x < rem) for x in range(8)), counters
+    assert torch.equal(shared, single)
+    assert torch.equal(again, single)
 
 
 def test_exact_ties_go_to_lower_block():
