@@ -113,5 +113,17 @@ def assert_frob(got, want, dtype, what):
     return rel
 
 
+def walk_order(idx: torch.Tensor, nb: int) -> torch.Tensor:
+    """Each row of a block list in the order the merged-list attention walks key blocks: by
+    increasing bit-reversed index over the smallest power of two >= nb. The one-block-per-workgroup
+    path walks a list in the order given, so on lists in this order both paths sum every query's
+    keys in the same order."""
+    k = max(1, (nb - 1).bit_length())
+    key = np.array([int(format(j, f"0{k}b")[::-1], 2) for j in range(1 << k)])
+    a = idx.cpu().numpy()
+    order = np.argsort(key[np.clip(a, 0, (1 << k) - 1)], axis=-1, kind="stable")
+    return torch.from_numpy(np.take_along_axis(a, order, axis=-1).copy()).to(idx.device)
+
+
 def to_np(t: torch.Tensor) -> np.ndarray:
     return t.detach().to("cpu", torch.float64).numpy()

@@ -153,10 +153,11 @@ def test_dense_reference_kernel(dtype, grid, block):
 @pytest.mark.parametrize("grid,s", [((3, 10, 13), 0.5), ((2, 9, 20), 0.7), ((4, 8, 16), 0.0)],
                          ids=["odd-nb", "batchlike", "keep-all"])
 def test_sparse_shared_loads(grid, s):
-    """The path in which adjacent query blocks share K/V loads (merged block lists) against the
-    one-block-per-workgroup path and the oracle, on random block lists: ascending lists visit the
-    same blocks in the same order on both paths (bitwise equal results); shuffled lists are valid
-    input too (any order) and must still match the oracle."""
+    """The path in which paired query blocks share K/V loads (merged block lists) against the
+    one-block-per-workgroup path and the oracle, on random block lists: given the lists in the
+    merged lists' walk order, the one-block path visits the same blocks in the same order (bitwise
+    equal results); ascending and shuffled lists are valid input too (any order) and must still
+    match the oracle."""
     w = synth.WAN_1_3B_480P.replace(grid=grid, H=2, sparsity=s)
     inp, f64 = _inputs(w, seed=6)
     g = w.grid
@@ -175,9 +176,9 @@ def test_sparse_shared_loads(grid, s):
         idx = torch.from_numpy(idx_np.astype(np.int32)).cuda()
         shared = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, s, idx, share=True)
         single = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, s, idx, share=False)
+        walked = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, s, T.walk_order(idx, nb), share=False)
         torch.cuda.synchronize()
-        if order == "ascending":
-            assert torch.equal(shared, single)
+        assert torch.equal(shared, walked)
         for h in range(w.H):
             q = O.round_to(O.rotate(f64["Qn"][0, h], ocos, osin), w.dtype)
             k = O.round_to(O.rotate(f64["Kn"][0, h], ocos, osin), w.dtype)
@@ -210,8 +211,8 @@ def _greedy_pairs(lists, nb, window=64):
 def test_overlap_pairing(lists_kind, s):
     """Query blocks share a workgroup by list overlap: the pair table in the workspace equals the
     greedy matching computed here, covers every block once, and the attention output is bitwise
-    that of one query block per workgroup. 135 query blocks (three 64-block chunks, ragged last
-    block, odd count), two batch entries of two heads."""
+    that of one query block per workgroup walking the lists in the same order. 135 query blocks
+    (three 64-block chunks, ragged last block, odd count), two batch entries of two heads."""
     w = synth.WAN_1_3B_480P.replace(grid=(7, 30, 41), B=2, H=2, sparsity=s)
     inp, _ = _inputs(w, seed=8)
     g = w.grid
@@ -234,7 +235,7 @@ def test_overlap_pairing(lists_kind, s):
     need = R.sparse_workspace_bytes(prob, 64, s)
     ws = torch.empty(need, dtype=torch.uint8, device="cuda")
     shared = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, s, idx, ws=ws)
-    single = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, s, idx, share=False)
+    single = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, s, T.walk_order(idx, nb), share=False)
     torch.cuda.synchronize()
     ngroups = (nb + 1) // 2
     # the workspace starts with 256 bytes of work-queue counters, then the pair table
@@ -258,7 +259,8 @@ def test_work_queue_full_size():
     workgroups loop and XCDs that finish early take groups from the others. Every group must be
     done exactly once: starting from stale counters (the list-merge kernel clears them), all
     counters end past their ranges and the whole output is bitwise that of the path with one
-    query block per workgroup (a static grid); a second call on the same workspace agrees."""
+    query block per workgroup (a static grid, lists in the same walk order); a second call on the
+    same workspace agrees."""
     w = synth.WAN_14B_720P
     inp = synth.make_inputs(w, 0, device="cuda")
     g = w.grid
@@ -272,9 +274,10 @@ def test_work_queue_full_size():
     shared = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, w.sparsity, idx, ws=ws)
     counters = ws[:32].view(torch.int32).cpu().numpy()
     again = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, w.sparsity, idx, ws=ws)
-    single = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, w.sparsity, idx, share=False)
+    nb = O.num_blocks(w.N, 64)
+    single = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, w.sparsity, T.walk_order(idx, nb), share=False)
     torch.cuda.synchronize()
-    total = w.B * w.H * ((O.num_blocks(w.N, 64) + 1) // 2)
+    total = w.B * w.H * ((nb + 1) // 2)
     q, rem = divmod(total, 8)
     _report("work queue", groups=total, counters=counters.tolist())
     assert all(counters[x] >= q + (x < rem) for x in range(8)), counters
