@@ -146,7 +146,8 @@ rola_status rola_sparse_attn_combine(const rola_problem* p, const void* Qr, cons
                                      void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ---- backward of the sparse branch (fine-tuning, Sec. 4.5; Algorithm step 4) ------------------
- * rola_sparse_attn_lse is rola_sparse_attn (without a workspace) that also writes, per query,
+ * rola_sparse_attn_lse is rola_sparse_attn (same workspace rule: ws NULL or ws_bytes >=
+ * rola_sparse_workspace_bytes) that also writes, per query,
  * lse[b, h, n] = log2 sum_k exp2(q^r_n . k^r_k * scale * log2 e) over its selected keys (fp32
  * [B, H, N]), which the backward needs. rola_sparse_attn_backward returns the gradients of
  * <dOs, O^s> with respect to Q^r, K^r and V (fp32 [B, H, N, d_h] each, fully overwritten) for the
@@ -158,7 +159,7 @@ rola_status rola_sparse_attn_combine(const rola_problem* p, const void* Qr, cons
 rola_status rola_sparse_attn_lse(const rola_problem* p, const void* Qr, const void* Kr,
                                  const void* V, int32_t block, double sparsity,
                                  const int32_t* blk_idx, float softmax_scale, void* Os, float* lse,
-                                 hipStream_t stream);
+                                 void* ws, size_t ws_bytes, hipStream_t stream);
 size_t rola_sparse_backward_workspace_bytes(const rola_problem* p, int32_t block, double sparsity);
 rola_status rola_sparse_attn_backward(const rola_problem* p, const void* Qr, const void* Kr,
                                       const void* V, int32_t block, double sparsity,

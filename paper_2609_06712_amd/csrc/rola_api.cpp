@@ -251,7 +251,7 @@ rola_status rola_dense_attn(const rola_problem* p, const void* Qr, const void* K
 rola_status rola_sparse_attn_lse(const rola_problem* p, const void* Qr, const void* Kr,
                                  const void* V, int32_t block, double sparsity,
                                  const int32_t* blk_idx, float softmax_scale, void* Os, float* lse,
-                                 hipStream_t stream) {
+                                 void* ws, size_t ws_bytes, hipStream_t stream) {
   rola::Shape s;
   TRY(check_problem(p, __func__, &s));
   TRY(check_block(s, block, __func__));
@@ -266,8 +266,15 @@ rola_status rola_sparse_attn_lse(const rola_problem* p, const void* Qr, const vo
   if (!(softmax_scale > 0.f) || !isfinite(softmax_scale))
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: softmax_scale must be finite and positive", __func__);
   const int keep = rola_keep_blocks(rola::num_blocks(s.N, block), sparsity);
+  const size_t need = rola::sparse_workspace_bytes(s, block, keep);
+  if (ws && need > 0) {
+    if (reinterpret_cast<uintptr_t>(ws) % 16)
+      return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: ws must be 16-byte aligned", __func__);
+    if (ws_bytes < need)
+      return fail(ROLA_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", __func__, ws_bytes, need);
+  }
   return hip_status(rola::launch_sparse_attn(s, Qr, Kr, V, block, keep, blk_idx, softmax_scale, Os,
-                                             nullptr, stream, nullptr, nullptr, lse),
+                                             need > 0 ? ws : nullptr, stream, nullptr, nullptr, lse),
                     __func__);
 }
 

@@ -56,7 +56,7 @@ SIGNATURES = {
     "rola_lowrank_features": (_i32, [_PP, _p, _p, _i32, _p, _p, _i32, _i32, _i32, _p, _p]),
     "rola_gate_logits": (_i32, [_PP, _p, _i32, _p, _f32, _p, _p]),
     "rola_sparse_combine_workspace_bytes": (_sz, [_PP, _i32, _f64, _i32]),
-    "rola_sparse_attn_lse": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p, _p]),
+    "rola_sparse_attn_lse": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p, _p, _sz, _p]),
     "rola_lowrank_backward_workspace_bytes": (_sz, [_PP, _i32]),
     "rola_lowrank_backward": (_i32, [_PP, _p, _p, _p, _p, _p, _i32, _p, _p, _i32, _p, _p, _p, _f32,
                                      _f32, _p, _p, _p, _p, _p, _p, _p, _p, _p, _sz, _p]),
@@ -358,16 +358,22 @@ def rola_sparse_attn_combine(Qr, Kr, V, grid, block, sparsity, blk_idx, Qn, Pq, 
 
 
 def rola_sparse_attn_lse(Qr, Kr, V, grid, block, sparsity, blk_idx, scale=None, out=None, lse=None,
-                         stream=None):
-    """Sparse attention that also returns the per-query log2-sum-exp2 (fp32 [B, H, N])."""
+                         ws=None, stream=None, share=True):
+    """Sparse attention that also returns the per-query log2-sum-exp2 (fp32 [B, H, N]); share=False
+    passes no workspace (one query block per workgroup)."""
     _act(Qr, "Qr")
     prob = problem_of(Qr, grid)
     scale = prob.d_h ** -0.5 if scale is None else scale
     out = torch.empty_like(Qr) if out is None else out
     if lse is None:
         lse = torch.empty(Qr.shape[:3], dtype=torch.float32, device=Qr.device)
+    if ws is None and share:
+        need = sparse_workspace_bytes(prob, block, sparsity)
+        ws = torch.empty(need, dtype=torch.uint8, device=Qr.device) if need else None
     _check(LIB.rola_sparse_attn_lse(ctypes.byref(prob), _ptr(Qr), _ptr(Kr), _ptr(V), block, sparsity,
-                                    _ptr(blk_idx), scale, _ptr(out), _ptr(lse), _stream(stream)),
+                                    _ptr(blk_idx), scale, _ptr(out), _ptr(lse),
+                                    _ptr(ws) if ws is not None else None,
+                                    ws.numel() if ws is not None else 0, _stream(stream)),
            "rola_sparse_attn_lse")
     return out, lse
 

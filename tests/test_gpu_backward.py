@@ -43,7 +43,7 @@ def test_sparse_backward(grid, block, s, B):
     kr = R.rola_rope_apply(d["Kn"], cos, sin, g)
     idx = R.rola_block_select(qr, kr, g, block, s)
     os_, lse = R.rola_sparse_attn_lse(qr, kr, d["V"], g, block, s, idx)
-    ref_os = R.rola_sparse_attn(qr, kr, d["V"], g, block, s, idx, share=False)
+    ref_os = R.rola_sparse_attn(qr, kr, d["V"], g, block, s, idx)
     gen = torch.Generator().manual_seed(3)
     dos = torch.randn(qr.shape, generator=gen).to(torch.bfloat16).cuda()
     dq, dk, dv = R.rola_sparse_attn_backward(qr, kr, d["V"], g, block, s, idx, os_, lse, dos)
