@@ -114,6 +114,38 @@ def test_lowrank_backward(r, B):
     assert _rel(_f64(dlog), ref) <= 1e-2
 
 
+def test_lowrank_backward_multistep():
+    """40 heads of 7800 tokens: every chunk of the low-rank backward then spans two 64-token steps
+    (the last one ragged), so the outer products accumulate across steps. Sampled heads against
+    the oracle; dP summed over the batch (B = 1: the head's own)."""
+    w = synth.WAN_1_3B_480P.replace(grid=(5, 30, 52), H=40, B=1, r=32)
+    inp = synth.make_inputs(w, 11)
+    d = {k: v.cuda() for k, v in inp.items()}
+    g = w.grid
+    prob = R.problem(w.B, w.H, w.N, w.d_h, g, w.dtype)
+    cos, sin = R.rola_rope_tables(prob, w.split)
+    C, _ = R.rola_lowrank_summary(d["Kn"], d["V"], d["Pk"], w.r, cos, sin, g)
+    gen = torch.Generator().manual_seed(6)
+    os_ = torch.randn(d["Qn"].shape, generator=gen).to(torch.bfloat16).cuda()
+    dO = torch.randn(d["Qn"].shape, generator=gen).to(torch.bfloat16).cuda()
+    dOs, dQn, dKn, dV, dPq, dPk, _ = R.rola_lowrank_backward(
+        d["Qn"], d["Kn"], d["V"], d["Pq"], d["Pk"], w.r, cos, sin, C, os_, d["logits"], dO, g)
+    torch.cuda.synchronize()
+    ocos, osin = O.rope_tables(*g, w.split)
+    f = synth.to_f64(inp)
+    for h in (0, 21, 39):
+        wt = G.lowrank_combine_grads(f["Qn"][0, h], f["Kn"][0, h], f["V"][0, h], f["Pq"][h],
+                                     f["Pk"][h], _f64(os_[0, h]), f["logits"][0], ocos, osin,
+                                     _f64(dO[0, h]))
+        errs = {n: _rel(_f64(t), wt[k]) for n, t, k in
+                (("dOs", dOs[0, h], "dos"), ("dQn", dQn[0, h], "dqn"), ("dKn", dKn[0, h], "dkn"),
+                 ("dV", dV[0, h], "dv"), ("dPq", dPq[h], "dPq"), ("dPk", dPk[h], "dPk"))}
+        print(f"[parity] lowrank backward 40 heads x 7800 tokens h{h}: " +
+              ", ".join(f"{n} rel {e:.2e}" for n, e in errs.items()), flush=True)
+        for n, e in errs.items():
+            assert e <= 1e-2, (n, e)
+
+
 def test_gate_backward():
     gen = torch.Generator().manual_seed(6)
     X = torch.randn((2, 300, 1536), generator=gen).to(torch.bfloat16)
