@@ -219,7 +219,8 @@ __global__ __launch_bounds__(BLK * 2, 2) void sparse_dq_kernel(
         bf16x4 ds4[4];
 #pragma unroll
         for (int k = 0; k < 16; ++k) {
-          const float p = kvalid ? __builtin_amdgcn_exp2f(fmaf(S[k], scale_log2, -lse[k])) : 0.f;
+          const float e = __builtin_amdgcn_exp2f(fmaf(S[k], scale_log2, -lse[k]));
+          const float p = kvalid ? e : 0.f;
           ds4[k / 4][k % 4] = (bf16)(p * (dP[k] - dsum[k]));
         }
         // dS^T row-major [key][query] in the wave's scratch, then read back transposed
@@ -262,7 +263,7 @@ __global__ __launch_bounds__(BLK * 2, 2) void sparse_dq_kernel(
 
 // ---- dK, dV: one workgroup per (b, h, key block), BLK/32 waves of 32 keys --------------------------
 #ifndef ROLA_DKV_NBUF
-#define ROLA_DKV_NBUF 3  // LDS stages of sparse_dkv_kernel
+#define ROLA_DKV_NBUF 2  // LDS stages (34 KB each) of sparse_dkv_kernel
 #endif
 #ifndef ROLA_DKV_WAVES_PER_EU
 #define ROLA_DKV_WAVES_PER_EU 1  // waves per SIMD the register budget of sparse_dkv_kernel targets
@@ -274,10 +275,14 @@ void sparse_dkv_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
     const bf16* __restrict__ dO, const float2* __restrict__ lseD, float* __restrict__ dK,
     float* __restrict__ dV) {
-  constexpr int D = 128, NW = BLK / 32;
-  constexpr int TILE = kBSub * D * 2;
+  // A step takes 64 queries as two independent 32-query halves: one wave per SIMD (the dK, dV
+  // accumulators and the K, V operands hold most of the registers), so the second half's S and dP
+  // products are what overlaps the first half's softmax.
+  constexpr int D = 128, NW = BLK / 32, QS = 2 * kBSub;
+  constexpr int TILE = QS * D * 2;
   constexpr int STAGE = 2 * TILE + NW * 1024;  // Q, dO, then each wave's copy of the rows' lse/D
-  constexpr int DMA_PER_WAVE = TILE / 1024 / NW, SUBS = BLK / kBSub;
+  constexpr int DMA_PER_WAVE = TILE / 1024 / NW, SUBS = BLK / QS;
+  static_assert(SUBS >= 1 && DMA_PER_WAVE >= 1, "64- or 128-query blocks");
   __shared__ __attribute__((aligned(1024))) char lds[NBUF * STAGE];
 
   const int L = xcd_remap(blockIdx.x, total);
@@ -315,7 +320,7 @@ void sparse_dkv_kernel(
   }
   const uint32_t lds0 = lds_address(lds);
   const char* lsebase = reinterpret_cast<const char*>(lseD + head * (long)N);
-  auto query0 = [&](int t) { return rl[1 + t / SUBS] * BLK + (t % SUBS) * kBSub; };
+  auto query0 = [&](int t) { return rl[1 + t / SUBS] * BLK + (t % SUBS) * QS; };
   auto issue = [&](int q0, int buf) {  // 2 * DMA_PER_WAVE + 1 loads per wave, always
     const uint32_t dst = lds0 + buf * STAGE;
 #pragma unroll
@@ -326,9 +331,9 @@ void sparse_dkv_kernel(
       dma16(Qh, rowoff + dsrc[i], dst + slot);
       dma16(dOh, rowoff + dsrc[i], dst + TILE + slot);
     }
-    // lse, D of the 32 queries (256 bytes, lanes 16-63 repeat lanes 0-15): the array is padded by
+    // lse, D of the 64 queries (512 bytes, lanes 32-63 repeat lanes 0-31): the array is padded by
     // kLsePad entries, and rows past N are masked below
-    dma16(lsebase, (uint32_t)(q0 * 8 + (lane % 16) * 16), dst + 2 * TILE + wave * 1024);
+    dma16(lsebase, (uint32_t)(q0 * 8 + (lane % 32) * 16), dst + 2 * TILE + wave * 1024);
   };
 
   constexpr int PER_STEP = 2 * DMA_PER_WAVE + 1;
@@ -352,29 +357,62 @@ void sparse_dkv_kernel(
       const char* Qt = lds + b * STAGE;
       const char* dOt = Qt + TILE;
       const float2* lt = reinterpret_cast<const float2*>(Qt + 2 * TILE + wave * 1024);
-      f32x16 S = f32x16{}, dP = f32x16{};
+      // Phases, each kept apart by a scheduling barrier so that operand reads are not all hoisted
+      // to the top (which overflows the register file): S, dP of half 0; S, dP of half 1 beside
+      // the softmax of half 0; the dV, dK products of half 0 beside the softmax of half 1; the
+      // products of half 1.
+      auto scores = [&](int h, f32x16& S, f32x16& dP) {
+        S = f32x16{};
+        dP = f32x16{};
 #pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        S = mfma32(row_frag(Qt, lane % 32, s, hh), kf[s], S);
-        dP = mfma32(row_frag(dOt, lane % 32, s, hh), vf[s], dP);
-      }
-      // one lane per key; rows 8j + 4(l/32) + i are the queries q0 + row
-      bf16x8 pb[2], sb[2];
-#pragma unroll
-      for (int k = 0; k < 16; ++k) {
-        const int row = 8 * (k / 4) + 4 * hh + k % 4;
-        const float2 ld = lt[row];
-        const float p = q0 + row < N ? __builtin_amdgcn_exp2f(fmaf(S[k], scale_log2, -ld.x)) : 0.f;
-        pb[k / 8][k % 8] = (bf16)p;
-        sb[k / 8][k % 8] = (bf16)(p * (dP[k] - ld.y));
-      }
-#pragma unroll
-      for (int w = 0; w < 4; ++w)
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          aV[w] = mfma32(tr_frag(dOt, w, u, lane), pb[u], aV[w]);
-          aK[w] = mfma32(tr_frag(Qt, w, u, lane), sb[u], aK[w]);
+        for (int s = 0; s < 8; ++s) {
+          S = mfma32(row_frag(Qt, 32 * h + lane % 32, s, hh), kf[s], S);
+          dP = mfma32(row_frag(dOt, 32 * h + lane % 32, s, hh), vf[s], dP);
         }
+      };
+      // one lane per key; rows 32h + 8j + 4(l/32) + i are the queries q0 + row
+      // The exponentials are computed unconditionally and rows past N zeroed in one uniform branch:
+      // a per-element condition around them splits the step into a basic block per element,
+      // across which no matrix instruction can be scheduled.
+      auto softmax = [&](int h, const f32x16& S, const f32x16& dP, bf16x8 (&pb)[2], bf16x8 (&sb)[2]) {
+        float p[16], dd[16];
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          const float2 ld = lt[32 * h + 8 * (k / 4) + 4 * hh + k % 4];
+          p[k] = __builtin_amdgcn_exp2f(fmaf(S[k], scale_log2, -ld.x));
+          dd[k] = dP[k] - ld.y;
+        }
+        if (q0 + QS > N) {  // ragged last query block (uniform)
+#pragma unroll
+          for (int k = 0; k < 16; ++k)
+            p[k] = q0 + 32 * h + 8 * (k / 4) + 4 * hh + k % 4 < N ? p[k] : 0.f;
+        }
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          pb[k / 8][k % 8] = (bf16)p[k];
+          sb[k / 8][k % 8] = (bf16)(p[k] * dd[k]);
+        }
+      };
+      auto grads = [&](int h, const bf16x8 (&pb)[2], const bf16x8 (&sb)[2]) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+#pragma unroll
+          for (int u = 0; u < 2; ++u) {
+            aV[w] = mfma32(tr_frag(dOt + h * (TILE / 2), w, u, lane), pb[u], aV[w]);
+            aK[w] = mfma32(tr_frag(Qt + h * (TILE / 2), w, u, lane), sb[u], aK[w]);
+          }
+      };
+      f32x16 S0, dP0, S1, dP1;
+      bf16x8 pb0[2], sb0[2], pb1[2], sb1[2];
+      scores(0, S0, dP0);
+      __builtin_amdgcn_sched_barrier(0);
+      scores(1, S1, dP1);
+      softmax(0, S0, dP0, pb0, sb0);
+      __builtin_amdgcn_sched_barrier(0);
+      grads(0, pb0, sb0);
+      softmax(1, S1, dP1, pb1, sb1);
+      __builtin_amdgcn_sched_barrier(0);
+      grads(1, pb1, sb1);
       ++t;
     }
   }
