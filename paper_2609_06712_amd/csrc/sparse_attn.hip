@@ -823,11 +823,11 @@ __global__ __launch_bounds__(128) void sparse_simple_kernel(int N, int block, in
   }
 }
 
-// Workgroups of `kernel` (threads each) that the current device holds at once, cached per device.
+// Workgroups of `kernel` (threads each) that the current device holds at once, cached per device
+// in `cache` (one per kernel: every variant has the same function type).
+constexpr int kMaxDevices = 64;
 template <typename Kernel>
-int resident_workgroups(Kernel kernel, int threads) {
-  constexpr int kMaxDevices = 64;
-  static std::atomic<int> cache[kMaxDevices];
+int resident_workgroups(Kernel kernel, int threads, std::atomic<int> (&cache)[kMaxDevices]) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) dev = -1;
   if (dev >= 0) {
@@ -859,8 +859,9 @@ hipError_t launch_bf16_tab(const Shape& s, const void* Qr, const void* Kr, const
   const AttnArgs a{s.N, nb, ngroups, total, lists, list_len, list_stride, pairs, sl,
                    (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V, (bf16*)Os, fz, queue};
   if (queue) {
+    static std::atomic<int> resident[kMaxDevices];
     const auto kernel = sparse_attn_kernel<BLK, G, NBUF, TAB, RJ, true>;
-    const int grid = std::min(total, resident_workgroups(kernel, threads));
+    const int grid = std::min(total, resident_workgroups(kernel, threads, resident));
     hipLaunchKernelGGL(kernel, dim3(grid), dim3(threads), 0, st, a);
   } else {
     hipLaunchKernelGGL((sparse_attn_kernel<BLK, G, NBUF, TAB, RJ, false>), dim3(total), dim3(threads),

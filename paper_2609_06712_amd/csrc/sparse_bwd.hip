@@ -84,15 +84,21 @@ __global__ __launch_bounds__(256) void bwd_rowdot_kernel(long rows, const bf16* 
   }
 }
 
-// Membership bitmaps of the block lists: bits[head][I][J / 32] bit J % 32 (cleared beforehand).
+// Membership bitmaps of the block lists: bits[head][I][J / 32] bit J % 32. Each row is built in
+// LDS (words * 4 bytes of dynamic shared memory) and written whole, so no clearing pass is needed.
 __global__ __launch_bounds__(64) void bwd_bits_kernel(int nb, int keep, int words,
                                                       const int32_t* __restrict__ idx,
                                                       uint32_t* __restrict__ bits) {
+  extern __shared__ uint32_t row_bits[];
   const long row = blockIdx.x;  // head * nb + I
+  for (int w = threadIdx.x; w < words; w += 64) row_bits[w] = 0u;
+  __syncthreads();
   for (int k = threadIdx.x; k < keep; k += 64) {
     const int J = idx[row * keep + k];
-    if ((unsigned)J < (unsigned)nb) atomicOr(&bits[row * words + (J >> 5)], 1u << (J & 31));
+    if ((unsigned)J < (unsigned)nb) atomicOr(&row_bits[J >> 5], 1u << (J & 31));
   }
+  __syncthreads();
+  for (int w = threadIdx.x; w < words; w += 64) bits[row * words + w] = row_bits[w];
 }
 
 // Transposed lists: rev[head][J] = count, then the query blocks I that selected J, ascending.
@@ -456,10 +462,8 @@ hipError_t launch_bwd(const Shape& s, const void* Qr, const void* Kr, const void
   const long rd_threads = (rows + kLsePad) * 16;
   hipLaunchKernelGGL(bwd_rowdot_kernel, dim3((unsigned)((rd_threads + 255) / 256)), dim3(256), 0,
                      st, rows, (const bf16*)Os, (const bf16*)dOs, lse, lseD);
-  hipError_t e = hipMemsetAsync(bits, 0, (size_t)heads * nb * words * 4, st);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(bwd_bits_kernel, dim3((unsigned)(heads * nb)), dim3(64), 0, st, nb, keep,
-                     words, idx, bits);
+  hipLaunchKernelGGL(bwd_bits_kernel, dim3((unsigned)(heads * nb)), dim3(64), words * sizeof(uint32_t),
+                     st, nb, keep, words, idx, bits);
   hipLaunchKernelGGL(bwd_reverse_kernel, dim3((unsigned)((heads * nb + 255) / 256)), dim3(256), 0,
                      st, nb, words, heads, (const uint32_t*)bits, rev);
   const int total = (int)(heads * nb);
