@@ -285,6 +285,25 @@ def test_work_queue_full_size():
     assert torch.equal(again, single)
 
 
+@pytest.mark.parametrize("grid", [(21, 45, 80), (21, 45, 104), (21, 45, 160)],
+                         ids=["1182-blocks", "1536-blocks", "2363-blocks"])
+def test_block_select_rows(grid):
+    """Top-k over score rows of 1182 to 2363 key blocks (the radix select keeps a row's keys in
+    LDS). One head, every row against the oracle (pooling, fp64 scores, top-k with ties to the
+    lower block)."""
+    w = synth.WAN_1_3B_480P.replace(grid=grid, H=1, B=1, sparsity=0.9)
+    gen = torch.Generator().manual_seed(12)
+    qr = torch.randn((1, 1, w.N, 128), generator=gen).to(torch.bfloat16)
+    kr = torch.randn((1, 1, w.N, 128), generator=gen).to(torch.bfloat16)
+    idx = R.rola_block_select(qr.cuda(), kr.cuda(), w.grid, 64, w.sparsity).cpu().numpy()[0, 0]
+    nb = O.num_blocks(w.N, 64)
+    keep = O.keep_blocks(nb, w.sparsity)
+    scores = O.block_scores(O.pool_blocks(qr[0, 0].double().numpy(), 64),
+                            O.pool_blocks(kr[0, 0].double().numpy(), 64))
+    ties, differ = T.check_selection(scores, idx, O.select_blocks(scores, keep), keep)
+    _report("block select", n_b=nb, keep=keep, tie_rows=ties, differing=len(differ))
+
+
 def test_exact_ties_go_to_lower_block():
     """Identical key blocks tie exactly: every row must keep the lowest block indices."""
     w = synth.WAN_1_3B_480P.replace(grid=(2, 8, 16), H=2)
