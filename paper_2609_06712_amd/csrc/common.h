@@ -100,6 +100,36 @@ __device__ __forceinline__ int xcd_remap(int wg, int total) {
   return (xcd < rem ? xcd * (q + 1) : rem * (q + 1) + (xcd - rem) * q) + local;
 }
 
+// 16-byte chunk swizzle of a 256-byte tile row: a bijection on row%16 (16 consecutive rows of a
+// row read hit distinct chunks) whose bits 1-3 differ across every aligned group of four rows (the
+// four rows of a transposing read hit distinct 32-byte chunk pairs).
+__device__ __forceinline__ int bw_swizzle(int row) {
+  return ((row & 3) << 1) | ((row >> 2) & 1) | (row & 8);
+}
+
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+// A operand from a row-major [row][128] tile: the lane's row l%32 (+ row0), channels 16s + 8(l/32).
+__device__ __forceinline__ bf16x8 row_frag(const char* tile, int row, int s, int hh) {
+  return *reinterpret_cast<const bf16x8*>(tile + row * 256 + (((2 * s + hh) ^ bw_swizzle(row)) << 4));
+}
+
+// Transposed operand of a row-major [row][128] tile for channel tile w and the 16 rows of k-step u:
+// lane (channel 32w + 16((l/16)%2) + l%16) receives rows 16u + 4(l/32) + s and 16u + 8 + 4(l/32) + s,
+// s = 0..3 -- the order in which an MFMA output hands its rows to a lane.
+__device__ __forceinline__ bf16x8 tr_frag(const char* tile, int w, int u, int lane) {
+  const int i16 = lane % 16, hh = lane / 32, g1 = (lane / 16) & 1;
+  const int c = 2 * g1 + ((i16 & 3) >> 1);
+  bf16x4 part[2];
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    const int row = 16 * u + 8 * half + 4 * hh + i16 / 4;
+    const char* p = tile + row * 256 + (((4 * w + c) ^ bw_swizzle(row)) << 4) + 8 * (i16 & 1);
+    part[half] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p);
+  }
+  return __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
 // The XCD the calling wave runs on (hardware register XCC_ID).
 __device__ __forceinline__ int xcd_id() {
   unsigned v;

@@ -65,9 +65,17 @@ hipError_t launch_lowrank_backward(const Shape& s, const void* Qn, const void* K
                                    void* dOs, float* dQn, float* dKn, float* dV, float* dPq,
                                    float* dPk, float* dlogits, void* ws, hipStream_t st);
 
+// sparse_attn.hip: dQ^r of the block-sparse attention on the paired, queued attention kernel
+// (bf16, d 128, block 64: dq_supported); lseD: per query {log-sum-exp (log2), D = dO^s . O^s};
+// ws: sparse_workspace_bytes(s, 64, keep).
+bool dq_supported(const Shape& s, int block);
+hipError_t launch_sparse_dq(const Shape& s, const void* Qr, const void* Kr, const void* V, int keep,
+                            const int32_t* idx, float scale, const void* dO, const void* lseD,
+                            float* dQ, void* ws, hipStream_t st);
+
 // sparse_bwd.hip: gradients of the block-sparse attention (bf16, d 128, block 64 or 128); fp32
-// outputs; ws: sparse_backward_workspace_bytes(s, block).
-size_t sparse_backward_workspace_bytes(const Shape& s, int block);
+// outputs; ws: sparse_backward_workspace_bytes(s, block, keep).
+size_t sparse_backward_workspace_bytes(const Shape& s, int block, int keep);
 hipError_t launch_sparse_backward(const Shape& s, const void* Qr, const void* Kr, const void* V,
                                   int block, int keep, const int32_t* idx, float scale,
                                   const void* Os, const float* lse, const void* dOs, float* dQ,

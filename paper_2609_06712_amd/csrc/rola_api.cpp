@@ -283,7 +283,8 @@ size_t rola_sparse_backward_workspace_bytes(const rola_problem* p, int32_t block
   if (check_problem(p, __func__, &s) != ROLA_OK || check_block(s, block, __func__) != ROLA_OK ||
       check_sparsity(sparsity, __func__) != ROLA_OK)
     return 0;
-  return rola::sparse_backward_workspace_bytes(s, block);
+  return rola::sparse_backward_workspace_bytes(
+      s, block, rola_keep_blocks(rola::num_blocks(s.N, block), sparsity));
 }
 
 rola_status rola_sparse_attn_backward(const rola_problem* p, const void* Qr, const void* Kr,
@@ -309,10 +310,12 @@ rola_status rola_sparse_attn_backward(const rola_problem* p, const void* Qr, con
   REQUIRE_PTR(ws);
   if (!(softmax_scale > 0.f) || !isfinite(softmax_scale))
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: softmax_scale must be finite and positive", __func__);
-  const size_t need = rola::sparse_backward_workspace_bytes(s, block);
+  const int keep = rola_keep_blocks(rola::num_blocks(s.N, block), sparsity);
+  const size_t need = rola::sparse_backward_workspace_bytes(s, block, keep);
   if (ws_bytes < need)
     return fail(ROLA_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", __func__, ws_bytes, need);
-  const int keep = rola_keep_blocks(rola::num_blocks(s.N, block), sparsity);
+  if (reinterpret_cast<uintptr_t>(ws) % 16)
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: ws must be 16-byte aligned", __func__);
   return hip_status(rola::launch_sparse_backward(s, Qr, Kr, V, block, keep, blk_idx, softmax_scale,
                                                  Os, lse, dOs, dQr, dKr, dV, ws, stream),
                     __func__);

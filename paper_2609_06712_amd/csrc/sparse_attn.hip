@@ -445,10 +445,20 @@ struct AttnArgs {
   bf16* O;
   FuseArgs fz;
   int* queue;  // QUEUE: kNumXcd counters, zero at launch
+  // dQ mode: dO^s, the per-query {lse, D = dO^s . O^s} and the output dQ^r (fp32), scale
+  const bf16* dO;
+  const float2* lseD;
+  float* dQ;
+  float scale;
 };
 
-template <int BLK, int G, int NBUF, int TAB, int RJ, bool QUEUE>
-__global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 ? 3 : 2) void sparse_attn_kernel(
+// DQ: the backward's dQ^r = scale dS K^r over the same groups and lists (fine-tuning, Sec. 4.5):
+// per sub-tile S^T = K Q^T and dP^T = V dO^T (keys as rows, one lane per query, as the forward's
+// S^T), P = exp2(S^T scale log2e - lse) with the forward's log-sum-exp, dS^T = P (dP^T - D), and
+// dQ^T += K^T dS^T with K^T through transposing reads in the order the registers hold the keys. K
+// and V tiles use the swizzle that serves both row and transposing reads (bw_swizzle).
+template <int BLK, int G, int NBUF, int TAB, int RJ, bool QUEUE, bool DQ = false>
+__global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void sparse_attn_kernel(
     const AttnArgs args) {
   static_assert(G == 1 || G == 2 || G == 4, "one, two or four query blocks per workgroup");
   static_assert(NBUF >= 3, "loads of later sub-tiles stay in flight during a step");
@@ -499,8 +509,8 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 ? 3 : 2) void sparse_a
 #pragma unroll
     for (int i = 0; i < DMA_PER_WAVE; ++i) {
       const int row = 4 * (wave * DMA_PER_WAVE + i) + lane / 16, pos = lane % 16;
-      dk[i] = row * D * 2 + ((pos ^ k_swizzle(row)) << 4);
-      dv[i] = row * D * 2 + ((pos ^ v_swizzle(row)) << 4);
+      dk[i] = row * D * 2 + ((pos ^ (DQ ? bw_swizzle(row) : k_swizzle(row))) << 4);
+      dv[i] = row * D * 2 + ((pos ^ (DQ ? bw_swizzle(row) : v_swizzle(row))) << 4);
     }
     int ko[8];
 #pragma unroll
@@ -571,6 +581,17 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 ? 3 : 2) void sparse_a
 #pragma unroll
     for (int s = 0; s < 8; ++s)
       qf[s] = qvalid ? *reinterpret_cast<const bf16x8*>(Qh + (long)q * D + 16 * s + 8 * hh) : bf16x8{};
+    bf16x8 df[DQ ? 8 : 1];  // dQ mode: dO^T fragments, same layout as qf
+    float lse_q = 0.f, dsum_q = 0.f;
+    if constexpr (DQ) {
+      const bf16* dOq = ap->dO + head * (long)N * D + (long)q * D;
+#pragma unroll
+      for (int s = 0; s < 8; ++s)
+        df[s] = qvalid ? *reinterpret_cast<const bf16x8*>(dOq + 16 * s + 8 * hh) : bf16x8{};
+      const float2 v = qvalid ? ap->lseD[head * (long)N + q] : make_float2(INFINITY, 0.f);
+      lse_q = v.x;
+      dsum_q = v.y;
+    }
     __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
     if (TAB > 0) __syncthreads();  // the list table is complete
 
@@ -696,7 +717,32 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 ? 3 : 2) void sparse_a
         const Step cur = step_of(pc, t);
         pi = raw(issued / SUBS);
         pc = raw((t + 1) / SUBS);
-        if (active(cur)) {
+        if (DQ && active(cur)) {
+          const char* Kt = lds + j * STAGE;
+          const char* Vt = Kt + TILE;
+          f32x16 sc = f32x16{}, dp = f32x16{};
+#pragma unroll
+          for (int s = 0; s < 8; ++s) {
+            sc = mfma32(row_frag(Kt, lane % 32, s, hh), qf[s], sc);
+            dp = mfma32(row_frag(Vt, lane % 32, s, hh), df[s], dp);
+          }
+          // value k: key k0 + 8(k/4) + 4(l/32) + k%4 of this lane's query
+          float pr[16];
+#pragma unroll
+          for (int k = 0; k < 16; ++k) pr[k] = __builtin_amdgcn_exp2f(fmaf(sc[k], scale_log2, -lse_q));
+          if (cur.k0 + kSub > N) {  // ragged last block: keys past N
+            const int lim = N - cur.k0 - 4 * hh;
+#pragma unroll
+            for (int k = 0; k < 16; ++k) pr[k] = 8 * (k / 4) + k % 4 < lim ? pr[k] : 0.f;
+          }
+          bf16x8 ds[2];
+#pragma unroll
+          for (int k = 0; k < 16; ++k) ds[k / 8][k % 8] = (bf16)(pr[k] * (dp[k] - dsum_q));
+#pragma unroll
+          for (int w = 0; w < 4; ++w)
+#pragma unroll
+            for (int u = 0; u < 2; ++u) acc[w] = mfma32(tr_frag(Kt, w, u, lane), ds[u], acc[w]);
+        } else if (!DQ && active(cur)) {
           bf16x8 kf[4], kg[4], vf[4], pb[2];
           load_k(j, 0, kf);
           load_k(j, 4, kg);
@@ -714,6 +760,20 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 ? 3 : 2) void sparse_a
       }
     }
 
+    if constexpr (DQ) {  // dQ^T: lane = query, rows = channels 32w + 8j + 4(l/32) + i
+      if (qvalid) {
+        float* dq = ap->dQ + head * (long)N * D + (long)q * D;
+        const float sc = ap->scale;
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj)
+            *reinterpret_cast<float4*>(dq + 32 * w + 8 * jj + 4 * hh) =
+                make_float4(acc[w][4 * jj] * sc, acc[w][4 * jj + 1] * sc, acc[w][4 * jj + 2] * sc,
+                            acc[w][4 * jj + 3] * sc);
+      }
+      return;
+    }
     {
       const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(l), __float_as_uint(l), false, false);
       l = __uint_as_float(x[0]) + __uint_as_float(x[1]);
@@ -845,27 +905,35 @@ int resident_workgroups(Kernel kernel, int threads, std::atomic<int> (&cache)[kM
   return n;
 }
 
+// The dQ mode's extra operands (sparse_attn_kernel<.., DQ = true>).
+struct DqArgs {
+  const bf16* dO;
+  const float2* lseD;
+  float* dQ;
+};
+
 // queue: kNumXcd zeroed counters, or nullptr for the static grid of one workgroup per group.
-template <int BLK, int G, int NBUF, int TAB, int RJ>
+template <int BLK, int G, int NBUF, int TAB, int RJ, bool DQ = false>
 hipError_t launch_bf16_tab(const Shape& s, const void* Qr, const void* Kr, const void* V,
                            const int32_t* lists, int list_len, int list_stride,
                            const int32_t* pairs, float scale, void* Os, const FuseArgs& fz,
-                           int* queue, hipStream_t st) {
+                           int* queue, hipStream_t st, const DqArgs& dq = DqArgs{}) {
   const int nb = num_blocks(s.N, BLK);
   const int ngroups = (nb + G - 1) / G;
   const int total = ngroups * s.H * s.B;
   const float sl = scale * 1.4426950408889634f;
   const int threads = G * BLK * 2;
   const AttnArgs a{s.N, nb, ngroups, total, lists, list_len, list_stride, pairs, sl,
-                   (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V, (bf16*)Os, fz, queue};
+                   (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V, (bf16*)Os, fz, queue,
+                   dq.dO, dq.lseD, dq.dQ, scale};
   if (queue) {
     static std::atomic<int> resident[kMaxDevices];
-    const auto kernel = sparse_attn_kernel<BLK, G, NBUF, TAB, RJ, true>;
+    const auto kernel = sparse_attn_kernel<BLK, G, NBUF, TAB, RJ, true, DQ>;
     const int grid = std::min(total, resident_workgroups(kernel, threads, resident));
     hipLaunchKernelGGL(kernel, dim3(grid), dim3(threads), 0, st, a);
   } else {
-    hipLaunchKernelGGL((sparse_attn_kernel<BLK, G, NBUF, TAB, RJ, false>), dim3(total), dim3(threads),
-                       0, st, a);
+    hipLaunchKernelGGL((sparse_attn_kernel<BLK, G, NBUF, TAB, RJ, false, DQ>), dim3(total),
+                       dim3(threads), 0, st, a);
   }
   return hipGetLastError();
 }
@@ -942,6 +1010,38 @@ SparseWs sparse_ws_layout(const Shape& s, int block, int keep) {
   return {kQueueBytes, align256(heads * ngroups * sizeof(int32_t)), lists};
 }
 
+// Groups of the 64-token path in the workspace: pairs matched by overlap (or adjacent), their
+// merged lists in walk order, the work-queue counters cleared.
+struct Groups {
+  int* queue;
+  int32_t* pairs;
+  int32_t* lists;
+  int stride;
+};
+hipError_t prepare_groups(const Shape& s, int keep, const int32_t* idx, void* ws, hipStream_t st,
+                          Groups& gr) {
+  constexpr int G = ROLA_B64_GROUP;
+  const int nb = num_blocks(s.N, 64);
+  const int ngroups = (nb + G - 1) / G, heads = s.B * s.H;
+  const SparseWs lay = sparse_ws_layout(s, 64, keep);
+  gr.stride = G * keep + 1;
+  gr.queue = ROLA_B64_QUEUE ? (int*)ws : nullptr;
+  gr.pairs = lay.pair_bytes ? (int32_t*)((char*)ws + lay.queue_bytes) : nullptr;
+  gr.lists = (int32_t*)((char*)ws + lay.queue_bytes + lay.pair_bytes);
+  if (gr.pairs) {
+    const int nchunks = (nb + kPairWindow - 1) / kPairWindow;
+    hipLaunchKernelGGL(pair_rank_kernel, dim3(nchunks * heads), dim3(256),
+                       kPairRows * pair_row_stride(nb) * sizeof(uint32_t), st, nb, keep, nchunks,
+                       idx, (uint8_t*)gr.lists);
+    hipLaunchKernelGGL(pair_greedy_kernel, dim3(heads), dim3(64), 0, st, nb, ngroups, nchunks,
+                       (const uint8_t*)gr.lists, gr.pairs);
+  }
+  hipLaunchKernelGGL(group_union_kernel<G>, dim3(ngroups * heads), dim3(256),
+                     (G * walk_words(nb) + 256) * sizeof(uint32_t), st, nb, keep, ngroups, gr.stride,
+                     idx, (const int32_t*)gr.pairs, gr.lists, gr.queue);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 size_t sparse_workspace_bytes(const Shape& s, int block, int keep) {
@@ -956,6 +1056,25 @@ size_t fuse_workspace_bytes(const Shape& s, int r) {
 }
 
 bool fuse_supported(const Shape& s, int r) { return s.bf16 && s.d == 128 && r >= 16 && r <= 64; }
+
+bool dq_supported(const Shape& s, int block) {
+  return s.bf16 && s.d == 128 && block == 64 && ROLA_B64_GROUP == 2;
+}
+
+hipError_t launch_sparse_dq(const Shape& s, const void* Qr, const void* Kr, const void* V, int keep,
+                            const int32_t* idx, float scale, const void* dO, const void* lseD,
+                            float* dQ, void* ws, hipStream_t st) {
+  Groups gr;
+  const hipError_t e = prepare_groups(s, keep, idx, ws, st, gr);
+  if (e != hipSuccess) return e;
+  const DqArgs dq{(const bf16*)dO, (const float2*)lseD, dQ};
+  const FuseArgs none{};
+  if (gr.stride - 1 <= kTable)
+    return launch_bf16_tab<64, 2, 3, kTable, 0, true>(s, Qr, Kr, V, gr.lists, 0, gr.stride, gr.pairs,
+                                                      scale, nullptr, none, gr.queue, st, dq);
+  return launch_bf16_tab<64, 2, 3, 0, 0, true>(s, Qr, Kr, V, gr.lists, 0, gr.stride, gr.pairs, scale,
+                                               nullptr, none, gr.queue, st, dq);
+}
 
 hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, const void* V,
                               int block, int keep, const int32_t* idx, float scale, void* Os,
@@ -980,27 +1099,11 @@ hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, co
       constexpr int G = ROLA_B64_GROUP;
       if (!idx) return launch_bf16<64, 2, 3>(s, Qr, Kr, V, nullptr, nb, 0, scale, Os, st, nullptr, fp);
       if (ws && G > 1) {
-        const int ngroups = (nb + G - 1) / G, stride = G * keep + 1;
-        const int heads = s.B * s.H;
-        const SparseWs lay = sparse_ws_layout(s, 64, keep);
-        int* queue = ROLA_B64_QUEUE ? (int*)ws : nullptr;
-        int32_t* pairs = lay.pair_bytes ? (int32_t*)((char*)ws + lay.queue_bytes) : nullptr;
-        int32_t* lists = (int32_t*)((char*)ws + lay.queue_bytes + lay.pair_bytes);
-        if (pairs) {
-          const int nchunks = (nb + kPairWindow - 1) / kPairWindow;
-          hipLaunchKernelGGL(pair_rank_kernel, dim3(nchunks * heads), dim3(256),
-                             kPairRows * pair_row_stride(nb) * sizeof(uint32_t), st, nb, keep,
-                             nchunks, idx, (uint8_t*)lists);
-          hipLaunchKernelGGL(pair_greedy_kernel, dim3(heads), dim3(64), 0, st, nb, ngroups,
-                             nchunks, (const uint8_t*)lists, pairs);
-        }
-        hipLaunchKernelGGL(group_union_kernel<G>, dim3(ngroups * heads), dim3(256),
-                           (G * walk_words(nb) + 256) * sizeof(uint32_t), st, nb, keep, ngroups,
-                           stride, idx, (const int32_t*)pairs, lists, queue);
-        const hipError_t e = hipGetLastError();
+        Groups gr;
+        const hipError_t e = prepare_groups(s, keep, idx, ws, st, gr);
         if (e != hipSuccess) return e;
-        return launch_bf16<64, G, ROLA_B64_NBUF>(s, Qr, Kr, V, lists, 0, stride, scale, Os, st,
-                                                 pairs, fp, queue);
+        return launch_bf16<64, G, ROLA_B64_NBUF>(s, Qr, Kr, V, gr.lists, 0, gr.stride, scale, Os, st,
+                                                 gr.pairs, fp, gr.queue);
       }
       return launch_bf16<64, 1, 3>(s, Qr, Kr, V, idx, keep, keep, scale, Os, st, nullptr, fp);
     }

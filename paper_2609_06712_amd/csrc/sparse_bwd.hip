@@ -30,35 +30,6 @@ __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-// 16-byte chunk swizzle of a 256-byte tile row: a bijection on row%16 (16 consecutive rows of a
-// row read hit distinct chunks) whose bits 1-3 differ across every aligned group of four rows (the
-// four rows of a transposing read hit distinct 32-byte chunk pairs).
-__device__ __forceinline__ int bw_swizzle(int row) {
-  return ((row & 3) << 1) | ((row >> 2) & 1) | (row & 8);
-}
-
-typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
-
-// A operand from a row-major [row][128] tile: the lane's row l%32 (+ row0), channels 16s + 8(l/32).
-__device__ __forceinline__ bf16x8 row_frag(const char* tile, int row, int s, int hh) {
-  return *reinterpret_cast<const bf16x8*>(tile + row * 256 + (((2 * s + hh) ^ bw_swizzle(row)) << 4));
-}
-
-// Transposed operand of a row-major [row][128] tile for channel tile w and the 16 rows of k-step u:
-// lane (channel 32w + 16((l/16)%2) + l%16) receives rows 16u + 4(l/32) + s and 16u + 8 + 4(l/32) + s,
-// s = 0..3 -- the order in which an MFMA output hands its rows to a lane.
-__device__ __forceinline__ bf16x8 tr_frag(const char* tile, int w, int u, int lane) {
-  const int i16 = lane % 16, hh = lane / 32, g1 = (lane / 16) & 1;
-  const int c = 2 * g1 + ((i16 & 3) >> 1);
-  bf16x4 part[2];
-#pragma unroll
-  for (int half = 0; half < 2; ++half) {
-    const int row = 16 * u + 8 * half + 4 * hh + i16 / 4;
-    const char* p = tile + row * 256 + (((4 * w + c) ^ bw_swizzle(row)) << 4) + 8 * (i16 & 1);
-    part[half] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p);
-  }
-  return __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5, 6, 7);
-}
 
 // D_q = sum_c dO_qc O_qc and the forward's lse, packed per query: lseD[q] = {lse_q, D_q}. 16 lanes
 // per query row, 8 channels each. The array is padded by kLsePad zero entries (read past the end).
@@ -440,13 +411,16 @@ void sparse_dkv_kernel(
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Workspace: [lse, D per query][bitmaps][transposed lists][with dq_supported: the attention
+// workspace of the dQ pass (pairs, merged lists, queue counters)].
 struct BwdWs {
-  size_t lsed, bits, rev;
+  size_t lsed, bits, rev, dq;
 };
-BwdWs bwd_layout(const Shape& s, int block) {
+BwdWs bwd_layout(const Shape& s, int block, int keep) {
   const size_t heads = (size_t)s.B * s.H, nb = num_blocks(s.N, block), words = (nb + 31) / 32;
   return {align256((heads * s.N + kLsePad) * sizeof(float2)), align256(heads * nb * words * 4),
-          align256(heads * nb * (nb + 1) * 4)};
+          align256(heads * nb * (nb + 1) * 4),
+          dq_supported(s, block) ? align256(sparse_workspace_bytes(s, block, keep)) : 0};
 }
 
 template <int BLK>
@@ -455,7 +429,7 @@ hipError_t launch_bwd(const Shape& s, const void* Qr, const void* Kr, const void
                       const void* dOs, float* dQ, float* dK, float* dV, void* ws, hipStream_t st) {
   const int nb = num_blocks(s.N, BLK), words = (nb + 31) / 32;
   const long heads = (long)s.B * s.H, rows = heads * s.N;
-  const BwdWs lay = bwd_layout(s, BLK);
+  const BwdWs lay = bwd_layout(s, BLK, keep);
   float2* lseD = (float2*)ws;
   uint32_t* bits = (uint32_t*)((char*)ws + lay.lsed);
   int32_t* rev = (int32_t*)((char*)ws + lay.lsed + lay.bits);
@@ -468,9 +442,15 @@ hipError_t launch_bwd(const Shape& s, const void* Qr, const void* Kr, const void
                      st, nb, words, heads, (const uint32_t*)bits, rev);
   const int total = (int)(heads * nb);
   const float sl = scale * 1.4426950408889634f;
-  hipLaunchKernelGGL((sparse_dq_kernel<BLK, 3>), dim3(total), dim3(BLK * 2), 0, st, s.N, nb, total,
-                     idx, keep, sl, scale, (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V,
-                     (const bf16*)dOs, (const float2*)lseD, dQ);
+  if (dq_supported(s, BLK)) {  // dQ on the paired, queued attention kernel
+    const hipError_t e2 = launch_sparse_dq(s, Qr, Kr, V, keep, idx, scale, dOs, lseD, dQ,
+                                           (char*)ws + lay.lsed + lay.bits + lay.rev, st);
+    if (e2 != hipSuccess) return e2;
+  } else {
+    hipLaunchKernelGGL((sparse_dq_kernel<BLK, 3>), dim3(total), dim3(BLK * 2), 0, st, s.N, nb, total,
+                       idx, keep, sl, scale, (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V,
+                       (const bf16*)dOs, (const float2*)lseD, dQ);
+  }
   hipLaunchKernelGGL((sparse_dkv_kernel<BLK, ROLA_DKV_NBUF>), dim3(total), dim3(BLK * 2), 0, st, s.N, nb, total,
                      (const int32_t*)rev, sl, scale, (const bf16*)Qr, (const bf16*)Kr,
                      (const bf16*)V, (const bf16*)dOs, (const float2*)lseD, dK, dV);
@@ -479,10 +459,10 @@ hipError_t launch_bwd(const Shape& s, const void* Qr, const void* Kr, const void
 
 }  // namespace
 
-size_t sparse_backward_workspace_bytes(const Shape& s, int block) {
+size_t sparse_backward_workspace_bytes(const Shape& s, int block, int keep) {
   if (!s.bf16 || s.d != 128 || (block != 64 && block != 128)) return 0;
-  const BwdWs w = bwd_layout(s, block);
-  return w.lsed + w.bits + w.rev;
+  const BwdWs w = bwd_layout(s, block, keep);
+  return w.lsed + w.bits + w.rev + w.dq;
 }
 
 hipError_t launch_sparse_backward(const Shape& s, const void* Qr, const void* Kr, const void* V,
