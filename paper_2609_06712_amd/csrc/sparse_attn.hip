@@ -562,7 +562,9 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void s
     // raw(e): entry e of the list (in a VGPR when it comes from the LDS table); step_of decodes the
     // entry of sub-tile t.
     auto raw = [&](int e) -> int {
-      if (!glist) return G > 1 ? (e | (((1 << G) - 1) << 16)) : e;  // dense: every block, all
+      // the table is only used with a list (TAB > 0: never the dense walk), which saves a branch
+      // per lookup (about 2 % of the kernel)
+      if (TAB == 0 && !glist) return G > 1 ? (e | (((1 << G) - 1) << 16)) : e;  // dense: every block
       const int i = min(e, max(E - 1, 0));
       return TAB > 0 ? tab[i] : (int)slist[i];
     };
