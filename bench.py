@@ -369,8 +369,9 @@ def main():
                     help="one untimed device copy of one activation tensor (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the layer "
-              "shards by (batch, head) without communication, see the design notes", file=sys.stderr)
+        print(f"bench.py: measures one GPU only (asked for --gpus {args.gpus}); the layer shards by "
+              "(batch, head) with no communication, so N GPUs each run this single-GPU workload on "
+              "their share of the heads", file=sys.stderr)
         sys.exit(2)
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
