@@ -128,6 +128,15 @@ def test_bf16_wan14b_720p_sampled():
     _sampled(w, heads=[0, 13, 26, 39], q_blocks=[0, 590, 1181])
 
 
+def test_bf16_long_merged_lists_sampled():
+    """50 % sparsity on the 14B grid (keep 591 of 1182 blocks): the merged lists of a pair run past
+    the 1024 entries the LDS table holds, so the attention reads them through scalar loads. Two
+    heads, sampled query blocks against the oracle."""
+    w = synth.WAN_14B_720P.replace(name="14B grid H2 s0.5 (lists past the LDS table)", H=2,
+                                   sparsity=0.5)
+    _sampled(w, heads=[0, 1], q_blocks=[0, 591, 1181])
+
+
 @pytest.mark.parametrize("dtype,grid,block", [("bf16", (3, 10, 13), 64), ("bf16", (3, 10, 13), 128),
                                               ("f32", (4, 8, 8), 32)])
 def test_dense_reference_kernel(dtype, grid, block):
