@@ -25,6 +25,9 @@
  *  - C: fp32 [B, H, r, d_h]; z: fp32 [B, H, r]; block index list: int32 [B, H, n_blocks, keep].
  *  - Every pointer except the problem struct is a device pointer owned by the caller, 16-byte
  *    aligned. The library allocates nothing: scratch comes from the caller (see *_workspace_bytes).
+ *    A workspace holds the state of the call it is passed to (lists, partial sums, work-queue
+ *    counters) until that call's kernels finish: calls that may run at the same time, e.g. on
+ *    different streams, need workspaces of their own.
  *    Inputs are never written; outputs are fully overwritten; outputs must not overlap inputs unless
  *    stated.
  *  - Every call validates all arguments first and launches nothing when one is invalid. It then
@@ -116,10 +119,13 @@ rola_status rola_block_select(const rola_problem* p, const void* Qr, const void*
  * 1/sqrt(d_h) (Sec. 3). Os: [B, H, N, d_h] in dtype.
  * ws: rola_sparse_workspace_bytes(p, block, sparsity) bytes of device scratch, in which the bf16
  * path with 64-token blocks pairs query blocks (each with the block among its next 64 whose list
- * it shares most, up to 4064 query blocks; adjacent blocks beyond) and merges the lists of each
- * pair so that the two share their K/V loads; ws may be NULL (ws_bytes 0), which gives the same
- * results without that sharing (bitwise the same when every list is ascending). A non-NULL ws
- * smaller than needed is ROLA_ERR_WORKSPACE. */
+ * it shares most, up to 4064 query blocks; adjacent blocks beyond), merges the lists of each pair
+ * so that the two share their K/V loads, and keeps the counters of the per-XCD work queues the
+ * attention kernel's resident workgroups take pairs from. The merged lists are walked by
+ * increasing bit-reversed block index. ws may be NULL (ws_bytes 0): one query block per
+ * workgroup, its list walked in the order given. The two agree up to the order in which each
+ * query sums its keys (bitwise on lists given in bit-reversed order). A non-NULL ws smaller than
+ * needed is ROLA_ERR_WORKSPACE. */
 size_t rola_sparse_workspace_bytes(const rola_problem* p, int32_t block, double sparsity);
 rola_status rola_sparse_attn(const rola_problem* p, const void* Qr, const void* Kr, const void* V,
                              int32_t block, double sparsity, const int32_t* blk_idx,
@@ -154,8 +160,9 @@ rola_status rola_sparse_attn_combine(const rola_problem* p, const void* Qr, cons
  * given (fixed) block lists: dQ^r = scale dS K^r, dK^r = scale dS^T Q^r, dV = P^T dO^s with
  * P = softmax, dS = P (dO^s V^T - D), D_n = dO^s_n . O^s_n. Os and lse are the forward's outputs, dOs
  * is bf16 [B, H, N, d_h]. ws: rola_sparse_backward_workspace_bytes(p, block, sparsity) bytes (the
- * transposed block lists take 4 (n_b + 1) bytes per key block and head). bf16 path only
- * (ROLA_ERR_UNSUPPORTED otherwise), block 64 or 128. */
+ * transposed block lists take 4 (n_b + 1) bytes per key block and head; with 64-token blocks the
+ * dQ pass also keeps the pairs, merged lists and queue counters of rola_sparse_attn there). bf16
+ * path only (ROLA_ERR_UNSUPPORTED otherwise), block 64 or 128. */
 rola_status rola_sparse_attn_lse(const rola_problem* p, const void* Qr, const void* Kr,
                                  const void* V, int32_t block, double sparsity,
                                  const int32_t* blk_idx, float softmax_scale, void* Os, float* lse,
