@@ -144,13 +144,18 @@ __device__ __forceinline__ int xcd_id() {
 // up to a fifth, and which die is slow changes from chip to chip), so the kernel then ends when
 // the work ends, not when the slowest die's share does. Returns -1 once all ranges are used up;
 // every call ends after at most kNumXcd atomics, as the counters only grow.
+// Counter x sits at counter[x * kQueueStride]: each in a 256-byte slot of its own, because
+// atomics on one cache line serialise (with the eight counters in one line, the claims of the
+// whole chip queued behind each other: about 1 ms per launch at 23640 claims).
+constexpr int kQueueStride = 64;
 __device__ inline int xcd_queue_claim(int* counter, int xcd, int total) {
   const int q = total / kNumXcd, rem = total % kNumXcd;
   for (int k = 0; k < kNumXcd; ++k) {
     const int y = (xcd + k) % kNumXcd;
     const int len = q + (y < rem);
-    if (__hip_atomic_load(counter + y, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= len) continue;
-    const int i = atomicAdd(counter + y, 1);
+    int* c = counter + y * kQueueStride;
+    if (__hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= len) continue;
+    const int i = atomicAdd(c, 1);
     if (i < len) return (y < rem ? y * (q + 1) : rem * (q + 1) + (y - rem) * q) + i;
   }
   return -1;

@@ -213,7 +213,7 @@ __global__ __launch_bounds__(256) void group_union_kernel(int nb, int keep, int 
   const long head = gp / ngroups;
   const int I0 = G * (int)(gp % ngroups);
   const int tid = threadIdx.x;
-  if (queue && gp == 0 && tid < kNumXcd) queue[tid] = 0;  // the attention kernel's work queue
+  if (queue && gp == 0 && tid < kNumXcd) queue[tid * kQueueStride] = 0;  // the attention kernel's queue
   for (int w = tid; w < G * words; w += 256) bits[w] = 0u;
   __syncthreads();
   const int pr = G == 2 && pairs ? pairs[gp] : 0;
@@ -993,10 +993,10 @@ bool pairing_on(int G, int nb) {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Workspace: [work-queue counters: kNumXcd ints in 256 bytes][pair table: int32 per group, when
+// Workspace: [work-queue counters: kNumXcd ints, 256 bytes apart][pair table: int32 per group, when
 // pairing][union lists, which the candidate ranks (kPairWindow bytes per query block, whole
 // chunks) occupy before the lists are written].
-constexpr size_t kQueueBytes = 256;
+constexpr size_t kQueueBytes = kNumXcd * kQueueStride * sizeof(int);  // a 256-byte slot per counter
 struct SparseWs {
   size_t queue_bytes, pair_bytes, list_bytes;
 };

@@ -55,11 +55,12 @@ def test_workspace_helpers():
     assert R.summary_workspace_bytes(p, 33) == 0         # odd rank
     bad = R.problem(1, 40, 75601, 128, (21, 45, 80), "bf16")
     assert R.select_workspace_bytes(bad, 64) == 0
-    # 256 B of work-queue counters, the pair table (one int32 per pair of query blocks, padded to
-    # 256 B), then the pair-union lists: per (b, h, pair) a count and at most 2 * keep entries; the
-    # region first holds the candidate ranks of every query block (64 bytes each, whole chunks of 64)
+    # the work-queue counters (8, each in a 256-byte slot), the pair table (one int32 per pair of
+    # query blocks, padded to 256 B), then the pair-union lists: per (b, h, pair) a count and at most
+    # 2 * keep entries; the region first holds the candidate ranks of every query block (64 bytes
+    # each, whole chunks of 64)
     keep = O.keep_blocks(nb, 0.9)
-    queue = 256
+    queue = 8 * 256
     table = -(-4 * 40 * ((nb + 1) // 2) // 256) * 256
     ranks = 40 * -(-nb // 64) * 64 * 64
     lists = max(4 * 40 * ((nb + 1) // 2) * (2 * keep + 1), ranks)

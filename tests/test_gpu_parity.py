@@ -247,8 +247,9 @@ def test_overlap_pairing(lists_kind, s):
     single = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, s, T.walk_order(idx, nb), share=False)
     torch.cuda.synchronize()
     ngroups = (nb + 1) // 2
-    # the workspace starts with 256 bytes of work-queue counters, then the pair table
-    table = ws[256: 256 + w.B * w.H * ngroups * 4].view(torch.int32).cpu().numpy().reshape(w.B, w.H, ngroups)
+    # the workspace starts with the work-queue counters (8 slots of 256 bytes), then the pair table
+    q = 8 * 256
+    table = ws[q: q + w.B * w.H * ngroups * 4].view(torch.int32).cpu().numpy().reshape(w.B, w.H, ngroups)
     idx_np = idx.cpu().numpy()
     for b in range(w.B):
         for h in range(w.H):
@@ -279,9 +280,9 @@ def test_work_queue_full_size():
     kr = R.rola_rope_apply(inp["Kn"], cos, sin, g)
     idx = R.rola_block_select(qr, kr, g, 64, w.sparsity)
     ws = torch.empty(R.sparse_workspace_bytes(prob, 64, w.sparsity), dtype=torch.uint8, device="cuda")
-    ws[:256].fill_(0x7F)
+    ws[:8 * 256].fill_(0x7F)
     shared = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, w.sparsity, idx, ws=ws)
-    counters = ws[:32].view(torch.int32).cpu().numpy()
+    counters = ws[:8 * 256].view(torch.int32).cpu().numpy()[::64]  # one int per 256-byte slot
     again = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, w.sparsity, idx, ws=ws)
     nb = O.num_blocks(w.N, 64)
     single = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, w.sparsity, T.walk_order(idx, nb), share=False)
