@@ -122,10 +122,12 @@ rola_status rola_block_select(const rola_problem* p, const void* Qr, const void*
  * it shares most, up to 4064 query blocks; adjacent blocks beyond), merges the lists of each pair
  * so that the two share their K/V loads, and keeps the counters of the per-XCD work queues the
  * attention kernel's resident workgroups take pairs from. The merged lists are walked by
- * increasing bit-reversed block index. ws may be NULL (ws_bytes 0): one query block per
+ * increasing bit-reversed block index, each from a start phase set by the pair's place in its
+ * work queue (a fixed function of the pair and the device's resident workgroup count), so
+ * results are deterministic on a given device. ws may be NULL (ws_bytes 0): one query block per
  * workgroup, its list walked in the order given. The two agree up to the order in which each
- * query sums its keys (bitwise on lists given in bit-reversed order). A non-NULL ws smaller than
- * needed is ROLA_ERR_WORKSPACE. */
+ * query sums its keys (bitwise on lists given in the order the merged lists walk them). A
+ * non-NULL ws smaller than needed is ROLA_ERR_WORKSPACE. */
 size_t rola_sparse_workspace_bytes(const rola_problem* p, int32_t block, double sparsity);
 rola_status rola_sparse_attn(const rola_problem* p, const void* Qr, const void* Kr, const void* V,
                              int32_t block, double sparsity, const int32_t* blk_idx,

@@ -62,9 +62,9 @@ __device__ __forceinline__ int v_swizzle(int row) { return 2 * ((0x6530 >> (4 * 
 
 // Data-adaptive pairing of query blocks (G = 2). Query blocks whose lists overlap most are put in
 // one workgroup; neighbours share about half of their selections, the best partner among the
-// following 64 blocks often shares more. The pairing changes only which query blocks share K/V
-// loads: each query block still walks its own selections in ascending order, so results are
-// bitwise those of any other pairing.
+// following 64 blocks often shares more. The pairing changes which query blocks share K/V loads
+// and where each group's walk starts (walk_start); each query block sums its own selections only,
+// bitwise as the one-block path does when given them in the same order.
 constexpr int kPairWindow = 64;  // candidate partners of a query block: the next 64 blocks
 constexpr int kPairRows = 128;   // bitmap rows one overlap workgroup holds (64 blocks + window)
 
@@ -192,18 +192,33 @@ __device__ __forceinline__ int walk_pos(int J, int kb) {
   return ROLA_B64_WALK ? (int)(__brev((unsigned)J) >> (32 - kb)) : J;
 }
 
+// Start phase of a merged list (period > 0): the work queue hands group L out as entry i of its
+// XCD's range (xcd_queue_claim), and in the steady state the XCD's `period` resident workgroups
+// claim about `period` groups per group duration, so i / period tracks the time at which L
+// starts. Walking L's list cyclically from the fraction (i mod period) / period of it puts all
+// groups that run at once at about the same fraction of their walks, i.e. (walk order above) on
+// about the same key blocks: the XCD's working set shrinks to a window of the head's K/V (14B
+// layer: 22 % fewer bytes fetched beyond L2, about 2 % less time). Returns the first entry of a
+// list of E entries.
+__host__ __device__ inline int walk_start(int L, int total, int period, int E) {
+  if (period <= 0 || E <= 0) return 0;
+  const int q = total / kNumXcd, rem = total % kNumXcd;
+  const int i = L < rem * (q + 1) ? L % (q + 1) : (L - rem * (q + 1)) % q;
+  return (int)((long long)(i % period) * E / period);
+}
+
 // G query blocks share a workgroup of the attention kernel: G consecutive ones, or with G = 2 and
 // a pair table the two that pair_greedy_kernel matched. For each (b, h, group) this writes the
-// entry count and then the union of the G block lists in walk order (above), each entry
-// J | (bit i: query block i of the group selected J) << 16. Built through bitmaps indexed by walk
-// position, so the lists may come in any order; out-of-range entries are dropped, as the
-// attention skips them.
+// entry count and then the union of the G block lists in walk order (above), rotated to start at
+// walk_start, each entry J | (bit i: query block i of the group selected J) << 16. Built through
+// bitmaps indexed by walk position, so the lists may come in any order; out-of-range entries are
+// dropped, as the attention skips them.
 template <int G>
 __global__ __launch_bounds__(256) void group_union_kernel(int nb, int keep, int ngroups, int stride,
                                                           const int32_t* __restrict__ idx,
                                                           const int32_t* __restrict__ pairs,
                                                           int32_t* __restrict__ out,
-                                                          int* __restrict__ queue) {
+                                                          int* __restrict__ queue, int period) {
   extern __shared__ uint32_t sh[];
   const int kb = walk_bits(nb);
   const int words = walk_words(nb);
@@ -247,8 +262,11 @@ __global__ __launch_bounds__(256) void group_union_kernel(int nb, int keep, int 
     __syncthreads();
   }
   int32_t* o = out + gp * (long)stride;
-  if (tid == 255) o[0] = scan[255];
-  int pos = 1 + scan[tid] - cnt;
+  const int E = scan[255];
+  if (tid == 255) o[0] = E;
+  const int e0 = walk_start((int)gp, (int)gridDim.x, period, E);
+  int pos = scan[tid] - cnt - e0;  // rotated position of this thread's first entry
+  if (pos < 0) pos += E;
   for (int w = w0; w < w1; ++w) {
     uint32_t m[G], u = 0;
 #pragma unroll
@@ -258,7 +276,8 @@ __global__ __launch_bounds__(256) void group_union_kernel(int nb, int keep, int 
       uint32_t mask = 0;
 #pragma unroll
       for (int b = 0; b < G; ++b) mask |= ((m[b] >> bit) & 1u) << b;
-      o[pos++] = walk_pos(w * 32 + bit, kb) | (int)(mask << 16);  // the reversal is its own inverse
+      o[1 + pos] = walk_pos(w * 32 + bit, kb) | (int)(mask << 16);  // the reversal is its own inverse
+      if (++pos == E) pos = 0;
     }
   }
 }
@@ -914,6 +933,13 @@ struct DqArgs {
   float* dQ;
 };
 
+// Resident workgroups of the work-queue variant of sparse_attn_kernel (a cache per variant).
+template <int BLK, int G, int NBUF, int TAB, int RJ, bool DQ>
+int queue_resident() {
+  static std::atomic<int> cache[kMaxDevices];
+  return resident_workgroups(sparse_attn_kernel<BLK, G, NBUF, TAB, RJ, true, DQ>, G * BLK * 2, cache);
+}
+
 // queue: kNumXcd zeroed counters, or nullptr for the static grid of one workgroup per group.
 template <int BLK, int G, int NBUF, int TAB, int RJ, bool DQ = false>
 hipError_t launch_bf16_tab(const Shape& s, const void* Qr, const void* Kr, const void* V,
@@ -929,10 +955,9 @@ hipError_t launch_bf16_tab(const Shape& s, const void* Qr, const void* Kr, const
                    (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V, (bf16*)Os, fz, queue,
                    dq.dO, dq.lseD, dq.dQ, scale};
   if (queue) {
-    static std::atomic<int> resident[kMaxDevices];
-    const auto kernel = sparse_attn_kernel<BLK, G, NBUF, TAB, RJ, true, DQ>;
-    const int grid = std::min(total, resident_workgroups(kernel, threads, resident));
-    hipLaunchKernelGGL(kernel, dim3(grid), dim3(threads), 0, st, a);
+    const int grid = std::min(total, queue_resident<BLK, G, NBUF, TAB, RJ, DQ>());
+    hipLaunchKernelGGL((sparse_attn_kernel<BLK, G, NBUF, TAB, RJ, true, DQ>), dim3(grid),
+                       dim3(threads), 0, st, a);
   } else {
     hipLaunchKernelGGL((sparse_attn_kernel<BLK, G, NBUF, TAB, RJ, false, DQ>), dim3(total),
                        dim3(threads), 0, st, a);
@@ -1012,16 +1037,40 @@ SparseWs sparse_ws_layout(const Shape& s, int block, int keep) {
   return {kQueueBytes, align256(heads * ngroups * sizeof(int32_t)), lists};
 }
 
+// Period of walk_start for the merged lists of the 64-token path: resident workgroups per XCD of
+// the work-queue variant that will walk them (the table and epilogue variant launch_bf16_rj picks
+// for lists of stride - 1 entries and rank r; the dQ mode has no epilogue).
+template <int NBUF, bool DQ>
+int walk_period(int stride, int r) {
+  constexpr int G = ROLA_B64_GROUP;
+  int n;
+  if constexpr (DQ) {
+    n = stride - 1 <= kTable ? queue_resident<64, G, NBUF, kTable, 0, true>()
+                             : queue_resident<64, G, NBUF, 0, 0, true>();
+  } else if (stride - 1 <= kTable) {
+    n = r == 0    ? queue_resident<64, G, NBUF, kTable, 0, false>()
+        : r <= 32 ? queue_resident<64, G, NBUF, kTable, 1, false>()
+                  : queue_resident<64, G, NBUF, kTable, 2, false>();
+  } else {
+    n = r == 0    ? queue_resident<64, G, NBUF, 0, 0, false>()
+        : r <= 32 ? queue_resident<64, G, NBUF, 0, 1, false>()
+                  : queue_resident<64, G, NBUF, 0, 2, false>();
+  }
+  return n / kNumXcd;
+}
+
 // Groups of the 64-token path in the workspace: pairs matched by overlap (or adjacent), their
-// merged lists in walk order, the work-queue counters cleared.
+// merged lists in walk order rotated to their start phases (walk_start), the work-queue counters
+// cleared. r: rank of the fused epilogue (0: none); DQ: the lists are for the dQ mode.
 struct Groups {
   int* queue;
   int32_t* pairs;
   int32_t* lists;
   int stride;
 };
-hipError_t prepare_groups(const Shape& s, int keep, const int32_t* idx, void* ws, hipStream_t st,
-                          Groups& gr) {
+template <bool DQ>
+hipError_t prepare_groups(const Shape& s, int keep, const int32_t* idx, void* ws, int r,
+                          hipStream_t st, Groups& gr) {
   constexpr int G = ROLA_B64_GROUP;
   const int nb = num_blocks(s.N, 64);
   const int ngroups = (nb + G - 1) / G, heads = s.B * s.H;
@@ -1038,9 +1087,10 @@ hipError_t prepare_groups(const Shape& s, int keep, const int32_t* idx, void* ws
     hipLaunchKernelGGL(pair_greedy_kernel, dim3(heads), dim3(64), 0, st, nb, ngroups, nchunks,
                        (const uint8_t*)gr.lists, gr.pairs);
   }
+  const int period = gr.queue ? walk_period<DQ ? 3 : ROLA_B64_NBUF, DQ>(gr.stride, r) : 0;
   hipLaunchKernelGGL(group_union_kernel<G>, dim3(ngroups * heads), dim3(256),
                      (G * walk_words(nb) + 256) * sizeof(uint32_t), st, nb, keep, ngroups, gr.stride,
-                     idx, (const int32_t*)gr.pairs, gr.lists, gr.queue);
+                     idx, (const int32_t*)gr.pairs, gr.lists, gr.queue, period);
   return hipGetLastError();
 }
 
@@ -1067,7 +1117,7 @@ hipError_t launch_sparse_dq(const Shape& s, const void* Qr, const void* Kr, cons
                             const int32_t* idx, float scale, const void* dO, const void* lseD,
                             float* dQ, void* ws, hipStream_t st) {
   Groups gr;
-  const hipError_t e = prepare_groups(s, keep, idx, ws, st, gr);
+  const hipError_t e = prepare_groups<true>(s, keep, idx, ws, 0, st, gr);
   if (e != hipSuccess) return e;
   const DqArgs dq{(const bf16*)dO, (const float2*)lseD, dQ};
   const FuseArgs none{};
@@ -1102,7 +1152,7 @@ hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, co
       if (!idx) return launch_bf16<64, 2, 3>(s, Qr, Kr, V, nullptr, nb, 0, scale, Os, st, nullptr, fp);
       if (ws && G > 1) {
         Groups gr;
-        const hipError_t e = prepare_groups(s, keep, idx, ws, st, gr);
+        const hipError_t e = prepare_groups<false>(s, keep, idx, ws, lf ? lf->r : 0, st, gr);
         if (e != hipSuccess) return e;
         return launch_bf16<64, G, ROLA_B64_NBUF>(s, Qr, Kr, V, gr.lists, 0, gr.stride, scale, Os, st,
                                                  gr.pairs, fp, gr.queue);

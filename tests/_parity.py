@@ -113,16 +113,43 @@ def assert_frob(got, want, dtype, what):
     return rel
 
 
-def walk_order(idx: torch.Tensor, nb: int) -> torch.Tensor:
-    """Each row of a block list in the order the merged-list attention walks key blocks: by
-    increasing bit-reversed index over the smallest power of two >= nb. The one-block-per-workgroup
-    path walks a list in the order given, so on lists in this order both paths sum every query's
-    keys in the same order."""
+def walked_lists(ws: torch.Tensor, B: int, H: int, nb: int, keep: int, paired: bool = True) -> torch.Tensor:
+    """Each query block's selections in the order the work-queue attention walks them, read back
+    from its workspace: [queue counters: 8 slots of 256 bytes][pair table I0 | I1 << 16 per group,
+    padded to 256 bytes, when paired][per group: entry count E, then 2 keep entries J | members << 16].
+    Checks on the way that every merged list is the union in walk order (by increasing
+    bit-reversed key block index over the smallest power of two >= nb), rotated to some start, and that each member holds all keep of its entries. The one-block path walks a
+    list in the order given, so on these lists both paths sum every query's keys alike."""
+    heads, ng, stride = B * H, (nb + 1) // 2, 2 * keep + 1
+    off = 8 * 256
+    if paired:
+        table = ws[off: off + heads * ng * 4].view(torch.int32).cpu().numpy().reshape(heads, ng)
+        off += (heads * ng * 4 + 255) // 256 * 256
+    else:
+        g = np.arange(ng)
+        table = np.broadcast_to(2 * g | (2 * g + 1) << 16, (heads, ng))
+    table = table.astype(np.int64)
+    lists = ws[off: off + heads * ng * stride * 4].view(torch.int32).cpu().numpy()
+    lists = lists.reshape(heads, ng, stride).astype(np.int64)
+    E, ent = lists[..., 0], lists[..., 1:]
+    valid = np.arange(2 * keep)[None, None, :] < E[..., None]
     k = max(1, (nb - 1).bit_length())
     key = np.array([int(format(j, f"0{k}b")[::-1], 2) for j in range(1 << k)])
-    a = idx.cpu().numpy()
-    order = np.argsort(key[np.clip(a, 0, (1 << k) - 1)], axis=-1, kind="stable")
-    return torch.from_numpy(np.take_along_axis(a, order, axis=-1).copy()).to(idx.device)
+    pos = np.where(valid, key[np.clip(ent & 0xFFFF, 0, (1 << k) - 1)], -1)
+    desc = np.sum(valid[..., 1:] & (pos[..., 1:] < pos[..., :-1]), axis=-1)
+    last = np.take_along_axis(pos, np.maximum(E - 1, 0)[..., None], -1)[..., 0]
+    assert np.all(desc <= 1) and np.all((desc == 0) | (last < pos[..., 0])), "not a rotated walk"
+    out = np.full((heads, nb, keep), -1, np.int64)
+    for b in range(2):
+        I = table >> (16 * b) & 0xFFFF
+        sel = valid & ((ent >> (16 + b)) & 1).astype(bool)
+        hh, gg = np.nonzero(I < nb)
+        assert np.all(sel.sum(-1)[hh, gg] == keep)
+        order = np.argsort(~sel, axis=-1, kind="stable")[..., :keep]
+        J = np.take_along_axis(ent & 0xFFFF, order, -1)
+        out[hh, I[hh, gg]] = J[hh, gg]
+    assert np.all(out >= 0)
+    return torch.from_numpy(out.reshape(B, H, nb, keep).astype(np.int32)).to(ws.device)
 
 
 def to_np(t: torch.Tensor) -> np.ndarray:

@@ -163,10 +163,10 @@ def test_dense_reference_kernel(dtype, grid, block):
                          ids=["odd-nb", "batchlike", "keep-all"])
 def test_sparse_shared_loads(grid, s):
     """The path in which paired query blocks share K/V loads (merged block lists) against the
-    one-block-per-workgroup path and the oracle, on random block lists: given the lists in the
-    merged lists' walk order, the one-block path visits the same blocks in the same order (bitwise
-    equal results); ascending and shuffled lists are valid input too (any order) and must still
-    match the oracle."""
+    one-block-per-workgroup path and the oracle, on random block lists: given each block's list in
+    the order the merged lists walk it (read back from the workspace), the one-block path visits
+    the same blocks in the same order (bitwise equal results); ascending and shuffled lists are
+    valid input too (any order) and must still match the oracle."""
     w = synth.WAN_1_3B_480P.replace(grid=grid, H=2, sparsity=s)
     inp, f64 = _inputs(w, seed=6)
     g = w.grid
@@ -183,9 +183,11 @@ def test_sparse_shared_loads(grid, s):
     for order in ("ascending", "shuffled"):
         idx_np = np.sort(lists, axis=-1) if order == "ascending" else lists
         idx = torch.from_numpy(idx_np.astype(np.int32)).cuda()
-        shared = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, s, idx, share=True)
+        ws = torch.empty(R.sparse_workspace_bytes(prob, 64, s), dtype=torch.uint8, device="cuda")
+        shared = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, s, idx, ws=ws, share=True)
         single = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, s, idx, share=False)
-        walked = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, s, T.walk_order(idx, nb), share=False)
+        walked = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, s,
+                                    T.walked_lists(ws, w.B, w.H, nb, keep), share=False)
         torch.cuda.synchronize()
         assert torch.equal(shared, walked)
         for h in range(w.H):
@@ -220,7 +222,7 @@ def _greedy_pairs(lists, nb, window=64):
 def test_overlap_pairing(lists_kind, s):
     """Query blocks share a workgroup by list overlap: the pair table in the workspace equals the
     greedy matching computed here, covers every block once, and the attention output is bitwise
-    that of one query block per workgroup walking the lists in the same order. 135 query blocks
+    that of one query block per workgroup walking the lists in the order the merged lists do. 135 query blocks
     (three 64-block chunks, ragged last block, odd count), two batch entries of two heads."""
     w = synth.WAN_1_3B_480P.replace(grid=(7, 30, 41), B=2, H=2, sparsity=s)
     inp, _ = _inputs(w, seed=8)
@@ -244,7 +246,8 @@ def test_overlap_pairing(lists_kind, s):
     need = R.sparse_workspace_bytes(prob, 64, s)
     ws = torch.empty(need, dtype=torch.uint8, device="cuda")
     shared = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, s, idx, ws=ws)
-    single = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, s, T.walk_order(idx, nb), share=False)
+    single = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, s, T.walked_lists(ws, w.B, w.H, nb, keep),
+                                share=False)
     torch.cuda.synchronize()
     ngroups = (nb + 1) // 2
     # the workspace starts with the work-queue counters (8 slots of 256 bytes), then the pair table
@@ -269,8 +272,8 @@ def test_work_queue_full_size():
     workgroups loop and XCDs that finish early take groups from the others. Every group must be
     done exactly once: starting from stale counters (the list-merge kernel clears them), all
     counters end past their ranges and the whole output is bitwise that of the path with one
-    query block per workgroup (a static grid, lists in the same walk order); a second call on the
-    same workspace agrees."""
+    query block per workgroup (a static grid, each list in the order the merged lists walk it);
+    a second call on the same workspace agrees."""
     w = synth.WAN_14B_720P
     inp = synth.make_inputs(w, 0, device="cuda")
     g = w.grid
@@ -285,7 +288,9 @@ def test_work_queue_full_size():
     counters = ws[:8 * 256].view(torch.int32).cpu().numpy()[::64]  # one int per 256-byte slot
     again = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, w.sparsity, idx, ws=ws)
     nb = O.num_blocks(w.N, 64)
-    single = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, w.sparsity, T.walk_order(idx, nb), share=False)
+    keep = O.keep_blocks(nb, w.sparsity)
+    single = R.rola_sparse_attn(qr, kr, inp["V"], g, 64, w.sparsity,
+                                T.walked_lists(ws, w.B, w.H, nb, keep), share=False)
     torch.cuda.synchronize()
     total = w.B * w.H * ((nb + 1) // 2)
     q, rem = divmod(total, 8)
