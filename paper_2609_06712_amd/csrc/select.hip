@@ -107,7 +107,10 @@ __device__ __forceinline__ uint32_t order_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);  // larger float -> larger key
 }
 
-// One 64-lane workgroup per score row; dynamic LDS holds the row's nb keys.
+// One 64-lane workgroup per score row; dynamic LDS holds the row's nb keys. Every loop over the
+// row takes kBatch elements per lane at a time, loads first: one memory (or LDS) latency per batch
+// instead of one per element.
+constexpr int kBatch = 8;
 __global__ __launch_bounds__(64) void topk_kernel(int nb, int keep, const float* __restrict__ S,
                                                   int32_t* __restrict__ idx) {
   extern __shared__ uint32_t keys[];
@@ -121,15 +124,36 @@ __global__ __launch_bounds__(64) void topk_kernel(int nb, int keep, const float*
     for (int j = lane; j < nb; j += 64) out[j] = j;
     return;
   }
-  for (int j = lane; j < nb; j += 64) keys[j] = order_key(s[j]);
+  for (int base = 0; base < nb; base += 64 * kBatch) {
+    float v[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int j = base + 64 * u + lane;
+      v[u] = j < nb ? s[j] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int j = base + 64 * u + lane;
+      if (j < nb) keys[j] = order_key(v[u]);
+    }
+  }
   uint32_t prefix = 0, mask = 0;
   uint32_t remaining = (uint32_t)keep;
   for (int shift = 24; shift >= 0; shift -= 8) {
     for (int i = lane; i < 256; i += 64) hist[i] = 0;
     __syncthreads();
-    for (int j = lane; j < nb; j += 64) {
-      const uint32_t k = keys[j];
-      if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1u);
+    for (int base = 0; base < nb; base += 64 * kBatch) {
+      uint32_t k[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int j = base + 64 * u + lane;
+        k[u] = j < nb ? keys[j] : 0u;
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int j = base + 64 * u + lane;
+        if (j < nb && (k[u] & mask) == prefix) atomicAdd(&hist[(k[u] >> shift) & 255u], 1u);
+      }
     }
     __syncthreads();
     uint32_t c[4];
@@ -159,19 +183,28 @@ __global__ __launch_bounds__(64) void topk_kernel(int nb, int keep, const float*
   // Keys > prefix are all kept; of the keys == prefix, the `remaining` lowest indices are kept.
   uint32_t written = 0, eq_seen = 0;
   const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  for (int base = 0; base < nb; base += 64) {
-    const int j = base + lane;
-    const uint32_t k = j < nb ? keys[j] : 0u;
-    const bool gt = j < nb && k > prefix;
-    const bool eq = j < nb && k == prefix;
-    const uint64_t eqm = __ballot(eq);
-    const uint32_t eq_rank = eq_seen + (uint32_t)__popcll(eqm & below);
-    const bool sel = gt || (eq && eq_rank < remaining);
-    const uint64_t selm = __ballot(sel);
-    const uint32_t pos = written + (uint32_t)__popcll(selm & below);
-    if (sel && pos < (uint32_t)keep) out[pos] = j;
-    written += (uint32_t)__popcll(selm);
-    eq_seen += (uint32_t)__popcll(eqm);
+  for (int base0 = 0; base0 < nb; base0 += 64 * kBatch) {
+    uint32_t kk[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int j = base0 + 64 * u + lane;
+      kk[u] = j < nb ? keys[j] : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int j = base0 + 64 * u + lane;
+      const uint32_t k = kk[u];
+      const bool gt = j < nb && k > prefix;
+      const bool eq = j < nb && k == prefix;
+      const uint64_t eqm = __ballot(eq);
+      const uint32_t eq_rank = eq_seen + (uint32_t)__popcll(eqm & below);
+      const bool sel = gt || (eq && eq_rank < remaining);
+      const uint64_t selm = __ballot(sel);
+      const uint32_t pos = written + (uint32_t)__popcll(selm & below);
+      if (sel && pos < (uint32_t)keep) out[pos] = j;
+      written += (uint32_t)__popcll(selm);
+      eq_seen += (uint32_t)__popcll(eqm);
+    }
   }
 }
 
