@@ -3,9 +3,10 @@
 // softmax with fp32 running max / sum / accumulators. With no index list every key block is walked
 // in order, which is dense softmax attention (the 0 % sparsity reference).
 //
-// bf16 path (d_h = 128). A workgroup serves G = 1 or 2 consecutive query blocks of BLK tokens, with
-// BLK/32 waves of 32 queries per query block. With G = 2 it walks the ascending union of the two
-// blocks' lists (built by group_union_kernel): a key block both hold is fetched into LDS once, and
+// bf16 path (d_h = 128). A workgroup serves G = 1 or 2 query blocks of BLK tokens, with BLK/32
+// waves of 32 queries per query block. With G = 2 (a pair: neighbours, or matched by list overlap)
+// it walks the union of the two blocks' lists (built by group_union_kernel, in the walk order and
+// from the start phase described there): a key block both hold is fetched into LDS once, and
 // each wave computes only on the blocks its own query block selected. Adjacent query blocks share
 // about half of their selections, so this cuts the K/V bytes that cross L2 by about a quarter.
 // Keys stream in 32-key sub-tiles through NBUF LDS stages filled by direct global-to-LDS loads.
