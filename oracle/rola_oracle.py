@@ -44,9 +44,9 @@ import numpy as np
 __all__ = [
     "token_positions", "pair_schedule", "rope_tables", "rotate", "round_to", "round_bf16",
     "num_blocks", "keep_blocks", "pool_blocks", "block_scores", "select_blocks",
-    "sparse_attention", "sparse_attention_rows", "silu", "lowrank_features", "lowrank_summary",
-    "lowrank_readout_u", "rms_normalize", "lowrank_readout", "gate", "combine", "forward_head",
-    "forward", "inside_features", "norope_features", "lowrank_logit", "flop_counts", "activation",
+    "sparse_attention", "sparse_attention_rows", "sparse_attention_blocks", "silu",
+    "lowrank_features", "lowrank_summary", "lowrank_readout_u", "rms_normalize", "lowrank_readout",
+    "gate", "combine", "forward_head", "forward", "lowrank_logit", "flop_counts", "activation",
     "features", "gate_logits",
 ]
 
@@ -201,6 +201,20 @@ def sparse_attention(qr, kr, v, idx, block: int, scale: float) -> np.ndarray:
         w = np.exp(s - s.max(axis=1, keepdims=True))
         out[q_rows] = (w / w.sum(axis=1, keepdims=True)) @ v[keys]
     return out
+
+
+def sparse_attention_blocks(qr, kr, v, idx, block: int, scale: float, blocks) -> np.ndarray:
+    """O^s for the tokens of the given query blocks (in the order given), the same direct softmax as
+    sparse_attention; idx holds the lists of every query block [n_blocks, keep]."""
+    N = qr.shape[0]
+    out = []
+    for I in blocks:
+        q_rows = _block_tokens(int(I), block, N)
+        keys = np.concatenate([_block_tokens(J, block, N) for J in idx[int(I)]])
+        s = (qr[q_rows] @ kr[keys].T) * scale
+        w = np.exp(s - s.max(axis=1, keepdims=True))
+        out.append((w / w.sum(axis=1, keepdims=True)) @ v[keys])
+    return np.concatenate(out, axis=0)
 
 
 # --------------------------------------------------------------------------------------------------
@@ -376,16 +390,6 @@ def forward(Qn, Kn, V, Pq, Pk, logits, *, grid, split, block, sparsity, base=100
 # --------------------------------------------------------------------------------------------------
 # Negative controls and the mechanism metric  (Sec. 4.3; Prop. inside; Sec. 5.1 RoPE placement)
 # --------------------------------------------------------------------------------------------------
-
-
-def inside_features(x, P, cos, sin) -> np.ndarray:
-    """Inside-activation ordering SiLU(R_r(p) P x_p) of Prop. inside (not shift-invariant)."""
-    return silu(rotate(x @ P.T, cos, sin))
-
-
-def norope_features(x, P, cos=None, sin=None) -> np.ndarray:
-    """Low-rank features without any rotation (position-blind)."""
-    return silu(x @ P.T)
 
 
 def lowrank_logit(qn_p, kn_q, Pq, Pk, pos_p, pos_q, split, base=10000.0, ordering="outside",

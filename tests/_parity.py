@@ -46,8 +46,9 @@ def run_gpu(w: synth.Workload, inp: dict, fused_only=False):
 
 
 def oracle_head(w: synth.Workload, f64: dict, b: int, h: int, q_blocks=None):
-    """Oracle results for one (b, h). With q_blocks given, O^s / O^lr / O only for the rows of those
-    query blocks (selection rows likewise); C, z always over the whole head."""
+    """Oracle results for one (b, h). Block scores and selections cover every query block. With
+    q_blocks given, O^s / O^lr / O only for the rows of those query blocks (ascending); C, z always
+    over the whole head."""
     cos, sin = O.rope_tables(*w.grid, w.split, w.base)
     qn, kn, v = f64["Qn"][b, h], f64["Kn"][b, h], f64["V"][b, h]
     qr = O.round_to(O.rotate(qn, cos, sin), w.dtype)
@@ -55,19 +56,17 @@ def oracle_head(w: synth.Workload, f64: dict, b: int, h: int, q_blocks=None):
     nb = O.num_blocks(w.N, w.block)
     keep = O.keep_blocks(nb, w.sparsity)
     qbar, kbar = O.pool_blocks(qr, w.block), O.pool_blocks(kr, w.block)
-    qb = np.arange(nb) if q_blocks is None else np.asarray(sorted(set(q_blocks)))
-    scores = O.block_scores(qbar[qb], kbar)
-    idx_rows = O.select_blocks(scores, keep)
-    idx = np.zeros((nb, keep), dtype=np.int64)
-    idx[qb] = idx_rows
+    scores = O.block_scores(qbar, kbar)
+    idx = O.select_blocks(scores, keep)
+    qb = np.arange(nb) if q_blocks is None else np.asarray(sorted(set(int(i) for i in q_blocks)))
     rows = np.concatenate([np.arange(I * w.block, min(w.N, (I + 1) * w.block)) for I in qb])
     scale = 1.0 / math.sqrt(w.d_h)
-    o_s = O.sparse_attention_rows(qr, kr, v, idx, w.block, scale, rows)
+    o_s = O.sparse_attention_blocks(qr, kr, v, idx, w.block, scale, qb)
     C, z = O.lowrank_summary(kn, v, f64["Pk"][h], cos, sin)
     u = O.lowrank_features(qn[rows], f64["Pq"][h], cos[rows], sin[rows]) @ C
     o_lr = O.rms_normalize(u, 1e-6)
     out = O.combine(o_s, o_lr, f64["logits"][b, rows], 1e-6)
-    return dict(qb=qb, rows=rows, scores=scores, idx=idx_rows, keep=keep, o_s=o_s, C=C, z=z,
+    return dict(qb=qb, rows=rows, scores=scores, idx=idx, keep=keep, o_s=o_s, C=C, z=z,
                 o_lr=o_lr, out=out, qr=qr, kr=kr, cos=cos, sin=sin)
 
 

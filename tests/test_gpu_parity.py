@@ -30,13 +30,16 @@ def _report(name, **kv):
 
 
 def _compare_head(w, gpu, ora, b, h, dtype, check_fused=True, check_unfused=True):
+    """Selection on every query block (the acceptance rule, with the tie and swap counts), then
+    O^s, C, z, O^lr and the outputs on the oracle's rows."""
     rows = ora["rows"]
-    g_idx = gpu["idx"][b, h].cpu().numpy()[ora["qb"]]
+    g_idx = gpu["idx"][b, h].cpu().numpy()
     ties, differ = T.check_selection(ora["scores"], g_idx, ora["idx"], ora["keep"])
     # rows whose (valid) tie swap changed the block list are excluded from the O^s / O comparison
-    bad_blocks = set(int(ora["qb"][i]) for i in differ)
+    bad_blocks = set(int(i) for i in differ)
     keep_rows = np.array([r // w.block not in bad_blocks for r in rows])
-    res = {"tie_rows": ties, "swapped_rows": len(differ)}
+    res = {"rows_selected": len(g_idx), "tie_rows": ties, "tie_fraction": round(ties / len(g_idx), 4),
+           "swapped_rows": len(differ), "rows_compared": int(keep_rows.sum())}
     res["o_s"] = T.assert_close(T.to_np(gpu["o_s"][b, h])[rows][keep_rows], ora["o_s"][keep_rows],
                                 dtype, "O^s")
     res["C"] = T.assert_frob(T.to_np(gpu["C"][b, h]), ora["C"], dtype, "C")
@@ -45,7 +48,7 @@ def _compare_head(w, gpu, ora, b, h, dtype, check_fused=True, check_unfused=True
         res["o_lr"] = T.assert_close(T.to_np(gpu["o_lr"][b, h])[rows], ora["o_lr"], dtype, "O^lr")
         res["out"] = T.assert_close(T.to_np(gpu["out"][b, h])[rows][keep_rows], ora["out"][keep_rows],
                                     dtype, "O")
-    if check_fused:
+    if check_fused and "out_fused" in gpu:
         res["out_fused"] = T.assert_close(T.to_np(gpu["out_fused"][b, h])[rows][keep_rows],
                                           ora["out"][keep_rows], dtype, "O fused")
     if "out_epi" in gpu:
@@ -97,35 +100,78 @@ def test_bf16_small_every_element(name, grid, H, B, block, s, r):
             _report(f"{name} b{b} h{h}", **res)
 
 
-def _sampled(w, heads, q_blocks):
-    """Full-size layer on the GPU (the configuration the benchmark times); oracle on whole rows of
-    sampled query blocks of sampled heads, plus the whole-head summary C, z."""
+def _spread_blocks(nb, count, seed):
+    """`count` query blocks spread over the sequence (so over the frames), seeded: the first and
+    the last (possibly partial) block plus distinct random ones."""
+    rng = np.random.default_rng(seed)
+    rest = rng.choice(np.arange(1, nb - 1), size=count - 2, replace=False)
+    return sorted({0, nb - 1, *(int(i) for i in rest)})
+
+
+def _sampled(w, heads, count, unfused=False, ws_check=False):
+    """Full-size layer on the GPU (the configuration the benchmark times). Per sampled head the
+    oracle checks the selection of every query block (ties and swaps reported), O^s and O on the
+    whole rows of `count` query blocks spread over the frames (the ragged last one included), the
+    low-rank summary C, z over the whole head, and with `unfused` also the standalone readout O^lr
+    and the separate combine."""
     print(f"[parity] {w.name}: generating inputs on the GPU", flush=True)
     inp = synth.make_inputs(w, 0, device="cuda")
-    gpu = T.run_gpu(w, inp, fused_only=True)
+    gpu = T.run_gpu(w, inp, fused_only=not unfused)
     nb = O.num_blocks(w.N, w.block)
     keep = O.keep_blocks(nb, w.sparsity)
     idx = gpu["idx"]
     assert idx.shape == (w.B, w.H, nb, keep)
     assert bool((idx[..., 1:] > idx[..., :-1]).all())
     assert int(idx.min()) >= 0 and int(idx.max()) < nb
+    keys = ["idx", "o_s", "C", "z", "out_fused", "out_epi"] + (["o_lr", "out"] if unfused else [])
     for h in heads:
         head_in = {k: inp[k][:, h:h + 1] for k in ("Qn", "Kn", "V")}
         head_in.update(Pq=inp["Pq"][h:h + 1], Pk=inp["Pk"][h:h + 1], logits=inp["logits"])
-        ora = T.oracle_head(w, synth.to_f64(head_in), 0, 0, q_blocks=q_blocks)
-        sub = {k: gpu[k][:, h:h + 1] for k in ("idx", "o_s", "C", "z", "out_fused", "out_epi")}
-        res = _compare_head(w, sub, ora, 0, 0, "bf16", check_unfused=False)
-        _report(f"{w.name} h{h}", **res)
+        qb = _spread_blocks(nb, count, seed=1000 + h)
+        ora = T.oracle_head(w, synth.to_f64(head_in), 0, 0, q_blocks=qb)
+        sub = {k: gpu[k][:, h:h + 1] for k in keys}
+        res = _compare_head(w, sub, ora, 0, 0, "bf16", check_unfused=unfused)
+        _report(f"{w.name} h{h} blocks {len(qb)}", **res)
+    return inp, gpu
 
 
 def test_bf16_wan13b_480p_sampled():
-    w = synth.WAN_1_3B_480P
-    _sampled(w, heads=[0, 11], q_blocks=[0, 1, 255, 511])
+    _sampled(synth.WAN_1_3B_480P, heads=[0, 11], count=16)
 
 
 def test_bf16_wan14b_720p_sampled():
-    w = synth.WAN_14B_720P
-    _sampled(w, heads=[0, 13, 26, 39], q_blocks=[0, 590, 1181])
+    """The benchmarked layer: selection of all 1182 query blocks of four heads on the smooth-field
+    inputs (tie rows and swaps reported), 32 query blocks per head compared element by element,
+    the unfused readout and combine too."""
+    _sampled(synth.WAN_14B_720P, heads=[0, 13, 26, 39], count=32, unfused=True)
+
+
+def test_bf16_wan14b_720p_block128_sampled():
+    """The sparse sweep's 128-token blocks on the 14B grid (591 blocks, keep 59): sampled heads and
+    query blocks, the ragged last block (80 tokens) included."""
+    w = synth.WAN_14B_720P.replace(name="wan2.1-14b-720p block128", block=128)
+    _sampled(w, heads=[0, 39], count=24)
+
+
+def test_bf16_long_sequence_adjacent_pairs():
+    """4200 query blocks (a 21x80x160 grid, 268800 tokens): beyond the 4064 blocks that pairing by
+    overlap serves, so query blocks are paired with their neighbours. Sampled rows against the
+    oracle, and the whole output bitwise against one query block per workgroup walking each list in
+    the merged order."""
+    w = synth.WAN_14B_720P.replace(name="21x80x160 H2 (adjacent pairs)", grid=(21, 80, 160), H=2)
+    inp, gpu = _sampled(w, heads=[0, 1], count=8)
+    nb = O.num_blocks(w.N, 64)
+    keep = O.keep_blocks(nb, w.sparsity)
+    assert nb == 4200
+    g = w.grid
+    prob = R.problem(w.B, w.H, w.N, w.d_h, g, w.dtype)
+    ws = torch.empty(R.sparse_workspace_bytes(prob, 64, w.sparsity), dtype=torch.uint8,
+                     device="cuda")
+    shared = R.rola_sparse_attn(gpu["qr"], gpu["kr"], inp["V"], g, 64, w.sparsity, gpu["idx"], ws=ws)
+    single = R.rola_sparse_attn(gpu["qr"], gpu["kr"], inp["V"], g, 64, w.sparsity,
+                                T.walked_lists(ws, w.B, w.H, nb, keep, paired=False), share=False)
+    torch.cuda.synchronize()
+    assert torch.equal(shared, single)
 
 
 def test_bf16_long_merged_lists_sampled():
@@ -134,7 +180,7 @@ def test_bf16_long_merged_lists_sampled():
     heads, sampled query blocks against the oracle."""
     w = synth.WAN_14B_720P.replace(name="14B grid H2 s0.5 (lists past the LDS table)", H=2,
                                    sparsity=0.5)
-    _sampled(w, heads=[0, 1], q_blocks=[0, 591, 1181])
+    _sampled(w, heads=[0, 1], count=6)
 
 
 @pytest.mark.parametrize("dtype,grid,block", [("bf16", (3, 10, 13), 64), ("bf16", (3, 10, 13), 128),

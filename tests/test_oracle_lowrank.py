@@ -76,8 +76,8 @@ def test_whole_module_is_shift_invariant():
     cos0, sin0 = O.rope_tables(*grid, split)
     cos1, sin1 = O.rope_tables(*grid, split, offset=(3, -5, 7))
     def inside_u(cos, sin):
-        C = O.inside_features(Kn[0, 0], Pk[0], cos, sin).T @ V[0, 0]
-        return O.inside_features(Qn[0, 0], Pq[0], cos, sin) @ C
+        C = O.features(Kn[0, 0], Pk[0], cos, sin, "silu", "inside").T @ V[0, 0]
+        return O.features(Qn[0, 0], Pq[0], cos, sin, "silu", "inside") @ C
     assert np.abs(inside_u(cos0, sin0) - inside_u(cos1, sin1)).max() > 1e-3
 
 

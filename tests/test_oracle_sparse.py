@@ -3,12 +3,38 @@ block-sparse softmax (Algorithm steps 3-4; sparsity = fraction of query-key inte
 
 import itertools
 import math
+import os
 
 import numpy as np
 import pytest
 
 import oracle as O
 from tests import _pins as P
+
+
+def _golden_rows(name):
+    rows = {}
+    path = os.path.join(os.path.dirname(__file__), "golden", name)
+    with open(path) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                sec, row, *vals = line.split()
+                rows.setdefault(sec, {})[int(row)] = [float(v) for v in vals]
+    return {sec: np.array([r[i] for i in sorted(r)]) for sec, r in rows.items()}
+
+
+def test_block_scores_worked_example():
+    """Hand-computed selection of tests/golden/block_scores.txt (d_h = 4, block 2, a partial last
+    block): pooled means over valid tokens, scores with the 1/sqrt(d_h) factor, top-k with ties to
+    the lower block. A score without the factor (x2), with 1/d_h (x1/2) or transposed fails."""
+    g = _golden_rows("block_scores.txt")
+    qbar, kbar = O.pool_blocks(g["q"], 2), O.pool_blocks(g["k"], 2)
+    np.testing.assert_array_equal(qbar, g["qbar"])
+    np.testing.assert_array_equal(kbar, g["kbar"])
+    s = O.block_scores(qbar, kbar)
+    np.testing.assert_allclose(s, g["score"], rtol=0, atol=1e-15)
+    np.testing.assert_array_equal(O.select_blocks(s, 1), g["keep1"].astype(np.int64))
+    np.testing.assert_array_equal(O.select_blocks(s, 2), g["keep2"].astype(np.int64))
 
 
 def test_pool_uses_valid_tokens_only():
@@ -143,3 +169,18 @@ def test_block_sparse_equals_bruteforce_masked_softmax(grid, block, s):
     rows = np.array([0, N // 2, N - 1])
     np.testing.assert_allclose(O.sparse_attention_rows(qr, kr, v, idx, block, 1.0 / 8.0, rows),
                                want[rows], atol=1e-12)
+
+
+def test_sparse_attention_blocks_is_the_restriction():
+    """The block-wise form used for sampled parity rows equals the whole-head form on those blocks,
+    a partial last block included."""
+    rng = np.random.default_rng(9)
+    block, N, d = 8, 8 * 5 + 3, 6
+    qr, kr, v = (rng.standard_normal((N, d)) for _ in range(3))
+    nb = O.num_blocks(N, block)
+    idx = np.stack([np.sort(rng.choice(nb, 3, replace=False)) for _ in range(nb)])
+    full = O.sparse_attention(qr, kr, v, idx, block, 0.4)
+    blocks = [1, 3, 5]
+    rows = np.concatenate([np.arange(I * block, min(N, (I + 1) * block)) for I in blocks])
+    np.testing.assert_allclose(O.sparse_attention_blocks(qr, kr, v, idx, block, 0.4, blocks),
+                               full[rows], rtol=0, atol=1e-14)
