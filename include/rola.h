@@ -33,6 +33,11 @@
  *  - Every call validates all arguments first and launches nothing when one is invalid. It then
  *    enqueues its kernels on `stream` and returns without synchronising. A failed launch returns
  *    ROLA_ERR_HIP. rola_last_error() gives a per-thread message for the last non-OK status.
+ *  - Process-wide state: besides the per-thread error message, the library caches, per device and
+ *    per variant of the attention kernel, how many of its workgroups the device holds at once
+ *    (hipOccupancyMaxActiveBlocksPerMultiprocessor times the compute units, asked on first use of
+ *    the variant on that device). The cache is a set of atomics: calls from several threads are
+ *    safe, and the value never changes once set.
  *  - Supported: d_h in {64, 128} for fp32, d_h == 128 for bf16; block in {32, 64, 128} (fp32) or
  *    {64, 128} (bf16); r even with 2 <= r <= d_h (fp32) or r in {16, 32, 64, 128} (bf16).
  */
@@ -101,12 +106,25 @@ rola_status rola_rope_tables(const rola_problem* p, int32_t d_t, int32_t d_y, in
 rola_status rola_rope_apply(const rola_problem* p, const void* X, const float* cos_tab,
                             const float* sin_tab, int32_t rope_ld, void* Xr, hipStream_t stream);
 
+/* Backward of the main-path rotation, for fine-tuning (Algorithm step 3 transposed): dX += R(p)^T dY
+ * for every [d_h] row, i.e. the rotation by -angle, when rotate is nonzero (the gradient of
+ * Q^r = R(Q^n) reaching Q^n), else dX += dY (a plain accumulation, e.g. the two branches' shares
+ * of dV). dY and dX are fp32 [B, H, N, d_h] whatever p->dtype; dX is read and written, and must
+ * not overlap dY. Tables and rope_ld as in rola_rope_apply (read only when rotate is nonzero, but
+ * always checked). */
+rola_status rola_rope_backward_accumulate(const rola_problem* p, const float* dY,
+                                          const float* cos_tab, const float* sin_tab,
+                                          int32_t rope_ld, int32_t rotate, float* dX,
+                                          hipStream_t stream);
+
 /* ---- sparse branch (Algorithm step 4; Sec. 4 opening: standard block-sparse attention) -------- */
 
 /* Top-k key blocks for every query block. For each (b, h): q_bar_I, k_bar_J = means of Q^r, K^r over
- * the valid tokens of block I, J (fp32); score S_IJ = q_bar_I . k_bar_J / sqrt(d_h) (fp32); the
- * keep = rola_keep_blocks(n_blocks, sparsity) largest scores are kept, equal scores going to the
- * lower J, and written ascending to blk_idx [B, H, n_blocks, keep]. ws: >=
+ * the valid tokens of block I, J (fp32); the block score of the definition is
+ * q_bar_I . k_bar_J / sqrt(d_h); the kernels rank the fp32 dot products q_bar_I . k_bar_J themselves,
+ * since the positive factor 1/sqrt(d_h) cannot change which blocks are largest (and leaving it out
+ * adds no rounding). The keep = rola_keep_blocks(n_blocks, sparsity) largest scores are kept, equal
+ * scores going to the lower J, and written ascending to blk_idx [B, H, n_blocks, keep]. ws: >=
  * rola_select_workspace_bytes(p, block) bytes of device scratch. */
 rola_status rola_block_select(const rola_problem* p, const void* Qr, const void* Kr, int32_t block,
                               double sparsity, int32_t* blk_idx, void* ws, size_t ws_bytes,
@@ -137,7 +155,8 @@ rola_status rola_sparse_attn(const rola_problem* p, const void* Qr, const void* 
 /* The sparse branch, the low-rank readout and the gated combine in one call (Algorithm steps 4 and
  * 7-10): O = (O^s / r + g O^lr) r with O^s = rola_sparse_attn(...) and O^lr =
  * rola_lowrank_readout(...) of the summary C, without writing O^s or O^lr to memory. Arguments as in
- * those two calls and rola_combine; O: [B, H, N, d_h] in dtype (must not alias an input). ws:
+ * those two calls and rola_combine; O: [B, H, N, d_h] in dtype, must not overlap Q^r, K^r, V or
+ * Q^n (ROLA_ERR_INVALID_ARGUMENT: other workgroups still read them while O is written). ws:
  * rola_sparse_combine_workspace_bytes(p, block, sparsity, r) bytes, required (the pair lists of
  * rola_sparse_attn plus the C fragments of the epilogue). On the bf16 path with r in {16, 32, 64}
  * the readout and combine run in the attention kernel's epilogue; otherwise the attention and the

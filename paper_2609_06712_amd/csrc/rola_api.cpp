@@ -6,6 +6,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <initializer_list>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -43,18 +44,21 @@ rola_status check_problem(const rola_problem* p, const char* fn, rola::Shape* ou
   if (p->B < 1 || p->H < 1 || p->N < 1 || p->T < 1 || p->Hs < 1 || p->Ws < 1)
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: sizes must be positive (B=%d H=%d N=%d T=%d Hs=%d Ws=%d)",
                 fn, p->B, p->H, p->N, p->T, p->Hs, p->Ws);
-  if ((long long)p->T * p->Hs * p->Ws != (long long)p->N)
-    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: N=%d differs from T*Hs*Ws=%lld", fn, p->N,
-                (long long)p->T * p->Hs * p->Ws);
+  // products of positive int32 values in 128 bits: no overflow for any input
+  typedef unsigned __int128 u128;
+  const u128 grid = (u128)p->T * (u128)p->Hs * (u128)p->Ws;
+  if (grid != (u128)p->N)
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: N=%d differs from T*Hs*Ws (T=%d Hs=%d Ws=%d)", fn,
+                p->N, p->T, p->Hs, p->Ws);
   if (p->dtype != ROLA_DTYPE_F32 && p->dtype != ROLA_DTYPE_BF16)
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: unknown dtype %d", fn, p->dtype);
   if (p->d_h != 64 && p->d_h != 128)
     return fail(ROLA_ERR_UNSUPPORTED, "%s: d_h=%d (built: 64, 128)", fn, p->d_h);
   if (p->dtype == ROLA_DTYPE_BF16 && p->d_h != 128)
     return fail(ROLA_ERR_UNSUPPORTED, "%s: bf16 path is built for d_h=128 only (got %d)", fn, p->d_h);
-  if ((long long)p->B * p->H * p->N * p->d_h >= (1ll << 40))
+  if ((u128)p->B * (u128)p->H * (u128)p->N * (u128)p->d_h >= ((u128)1 << 40))
     return fail(ROLA_ERR_UNSUPPORTED, "%s: tensor too large", fn);
-  if ((long long)p->B * p->H * p->N > (1ll << 31) - 1)
+  if ((u128)p->B * (u128)p->H * (u128)p->N > (u128)((1ll << 31) - 1))
     return fail(ROLA_ERR_UNSUPPORTED, "%s: B*H*N must fit in int32", fn);
   *out = rola::Shape{p->B, p->H, p->N, p->d_h, p->T, p->Hs, p->Ws, p->dtype == ROLA_DTYPE_BF16};
   return ROLA_OK;
@@ -100,6 +104,34 @@ rola_status check_tables(const float* c, const float* s, int32_t ld, int32_t nee
 rola_status check_sparsity(double sparsity, const char* fn) {
   if (!(sparsity >= 0.0 && sparsity < 1.0))
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: sparsity %g outside [0, 1)", fn, sparsity);
+  return ROLA_OK;
+}
+
+// Whether the byte ranges [a, a + na) and [b, b + nb) overlap.
+bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return x < y + nb && y < x + na;
+}
+
+// Bytes of one [B, H, N, d] activation tensor.
+size_t act_bytes(const rola::Shape& s) {
+  return (size_t)s.B * s.H * s.N * s.d * (s.bf16 ? 2 : 4);
+}
+
+// An output activation must not overlap the input activations `ins` (other workgroups still read
+// them while it is written); `same` (nullable) is an input it may alias exactly (in-place forms).
+struct Named {
+  const void* p;
+  const char* name;
+};
+rola_status check_out(const rola::Shape& s, const void* out, std::initializer_list<Named> ins,
+                      const void* same, const char* fn) {
+  const size_t n = act_bytes(s);
+  for (const Named& in : ins) {
+    if (in.p == same && out == same) continue;
+    if (overlap(out, n, in.p, n))
+      return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: the output overlaps %s", fn, in.name);
+  }
   return ROLA_OK;
 }
 
@@ -174,8 +206,24 @@ rola_status rola_rope_apply(const rola_problem* p, const void* X, const float* c
   REQUIRE_PTR(X);
   REQUIRE_PTR(Xr);
   TRY(check_tables(cos_tab, sin_tab, rope_ld, s.d / 2, __func__));
-  if (X == Xr) return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: Xr must not alias X", __func__);
+  TRY(check_out(s, Xr, {{X, "X"}}, nullptr, __func__));
   return hip_status(rola::launch_rope_apply(s, X, cos_tab, sin_tab, rope_ld, Xr, stream), __func__);
+}
+
+rola_status rola_rope_backward_accumulate(const rola_problem* p, const float* dY,
+                                          const float* cos_tab, const float* sin_tab,
+                                          int32_t rope_ld, int32_t rotate, float* dX,
+                                          hipStream_t stream) {
+  rola::Shape s;
+  TRY(check_problem(p, __func__, &s));
+  REQUIRE_PTR(dY);
+  REQUIRE_PTR(dX);
+  TRY(check_tables(cos_tab, sin_tab, rope_ld, s.d / 2, __func__));
+  const size_t n = (size_t)s.B * s.H * s.N * s.d * sizeof(float);
+  if (overlap(dX, n, dY, n))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: dX overlaps dY", __func__);
+  return hip_status(rola::launch_rope_grad(s, dY, cos_tab, sin_tab, rope_ld, rotate != 0, dX, stream),
+                    __func__);
 }
 
 rola_status rola_block_select(const rola_problem* p, const void* Qr, const void* Kr, int32_t block,
@@ -218,6 +266,7 @@ rola_status rola_sparse_attn(const rola_problem* p, const void* Qr, const void* 
   REQUIRE_PTR(V);
   REQUIRE_PTR(blk_idx);
   REQUIRE_PTR(Os);
+  TRY(check_out(s, Os, {{Qr, "Qr"}, {Kr, "Kr"}, {V, "V"}}, nullptr, __func__));
   if (!(softmax_scale > 0.f) || !isfinite(softmax_scale))
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: softmax_scale must be finite and positive", __func__);
   const int keep = rola_keep_blocks(rola::num_blocks(s.N, block), sparsity);
@@ -241,6 +290,7 @@ rola_status rola_dense_attn(const rola_problem* p, const void* Qr, const void* K
   REQUIRE_PTR(Kr);
   REQUIRE_PTR(V);
   REQUIRE_PTR(O);
+  TRY(check_out(s, O, {{Qr, "Qr"}, {Kr, "Kr"}, {V, "V"}}, nullptr, __func__));
   if (!(softmax_scale > 0.f) || !isfinite(softmax_scale))
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: softmax_scale must be finite and positive", __func__);
   const int nb = rola::num_blocks(s.N, block);
@@ -263,6 +313,7 @@ rola_status rola_sparse_attn_lse(const rola_problem* p, const void* Qr, const vo
   REQUIRE_PTR(blk_idx);
   REQUIRE_PTR(Os);
   REQUIRE_PTR(lse);
+  TRY(check_out(s, Os, {{Qr, "Qr"}, {Kr, "Kr"}, {V, "V"}}, nullptr, __func__));
   if (!(softmax_scale > 0.f) || !isfinite(softmax_scale))
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: softmax_scale must be finite and positive", __func__);
   const int keep = rola_keep_blocks(rola::num_blocks(s.N, block), sparsity);
@@ -359,6 +410,7 @@ rola_status rola_sparse_attn_combine(const rola_problem* p, const void* Qr, cons
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: softmax_scale must be finite and positive", __func__);
   if (!(eps_lr >= 0.f) || !isfinite(eps_lr) || !(eps >= 0.f) || !isfinite(eps))
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: eps values must be finite and >= 0", __func__);
+  TRY(check_out(s, O, {{Qr, "Qr"}, {Kr, "Kr"}, {V, "V"}, {Qn, "Qn"}}, nullptr, __func__));
   const size_t need = rola_sparse_combine_workspace_bytes(p, block, sparsity, r);
   if (ws_bytes < need)
     return fail(ROLA_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", __func__, ws_bytes, need);
@@ -426,6 +478,7 @@ rola_status rola_lowrank_readout_ex(const rola_problem* p, const void* Qn, const
   REQUIRE_PTR(Pq);
   REQUIRE_PTR(C);
   REQUIRE_PTR(Olr);
+  TRY(check_out(s, Olr, {{Qn, "Qn"}}, nullptr, __func__));
   TRY(check_tables(cos_tab, sin_tab, rope_ld, r / 2, __func__));
   if (!(eps_lr >= 0.f) || !isfinite(eps_lr))
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: eps_lr must be finite and >= 0", __func__);
@@ -550,7 +603,7 @@ rola_status rola_combine(const rola_problem* p, const void* Os, const void* Olr,
   REQUIRE_PTR(Olr);
   REQUIRE_PTR(gate_logits);
   REQUIRE_PTR(O);
-  if (O == Olr) return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: O must not alias Olr", __func__);
+  TRY(check_out(s, O, {{Os, "Os"}, {Olr, "Olr"}}, Os, __func__));
   if (!(eps >= 0.f) || !isfinite(eps))
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: eps must be finite and >= 0", __func__);
   return hip_status(rola::launch_combine(s, Os, Olr, gate_logits, eps, O, stream), __func__);
@@ -573,6 +626,7 @@ rola_status rola_lowrank_readout_combine_ex(const rola_problem* p, const void* Q
   REQUIRE_PTR(Os);
   REQUIRE_PTR(gate_logits);
   REQUIRE_PTR(O);
+  TRY(check_out(s, O, {{Qn, "Qn"}, {Os, "Os"}}, Os, __func__));
   TRY(check_tables(cos_tab, sin_tab, rope_ld, r / 2, __func__));
   if (!(eps_lr >= 0.f) || !isfinite(eps_lr) || !(eps >= 0.f) || !isfinite(eps))
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: eps values must be finite and >= 0", __func__);

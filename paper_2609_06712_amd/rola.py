@@ -38,6 +38,7 @@ SIGNATURES = {
     "rola_last_error": (ctypes.c_char_p, []),
     "rola_rope_tables": (_i32, [_PP, _i32, _i32, _i32, _f64, _i32, _i32, _i32, _p, _p, _p]),
     "rola_rope_apply": (_i32, [_PP, _p, _p, _p, _i32, _p, _p]),
+    "rola_rope_backward_accumulate": (_i32, [_PP, _p, _p, _p, _i32, _i32, _p, _p]),
     "rola_block_select": (_i32, [_PP, _p, _p, _i32, _f64, _p, _p, _sz, _p]),
     "rola_sparse_workspace_bytes": (_sz, [_PP, _i32, _f64]),
     "rola_sparse_attn": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p, _sz, _p]),
@@ -125,9 +126,101 @@ def problem_of(x: torch.Tensor, grid) -> Problem:
     return problem(B, H, N, d, grid, x.dtype)
 
 
-def _act(x, name):
-    if not (x.is_cuda and x.is_contiguous() and x.dim() == 4):
-        raise ValueError(f"{name} must be a contiguous [B, H, N, d_h] device tensor")
+# ---- argument checks ------------------------------------------------------------------------------
+# Every tensor is checked before the ctypes call: first the element type and shape of every
+# argument, then the memory layout (contiguous, or a unit inner stride for the rotary tables) and
+# the device of every argument. A list or table of the wrong type or size would make the kernels
+# read past a buffer, so nothing reaches the library unchecked.
+
+_ACT_DTYPES = (torch.bfloat16, torch.float32)
+
+
+class _Args:
+    """Collects the tensors of one call: shapes and types are checked as they are added, the
+    layout and device of all of them by done()."""
+
+    def __init__(self):
+        self.placed = []
+
+    def tensor(self, x, name, shape, dtype, inner_only=False):
+        if not isinstance(x, torch.Tensor):
+            raise ValueError(f"{name} must be a tensor")
+        if x.dtype != dtype:
+            raise ValueError(f"{name} must be {dtype}, got {x.dtype}")
+        if tuple(x.shape) != tuple(shape):
+            raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(x.shape)}")
+        self.placed.append((x, name, inner_only))
+        return x
+
+    def act(self, x, name, like=None):
+        """A [B, H, N, d_h] activation (bf16 or fp32), of the same shape and type as `like`."""
+        if like is not None:
+            return self.tensor(x, name, like.shape, like.dtype)
+        if not isinstance(x, torch.Tensor):
+            raise ValueError(f"{name} must be a tensor")
+        if x.dtype not in _ACT_DTYPES:
+            raise ValueError(f"{name} must be bfloat16 or float32, got {x.dtype}")
+        if x.dim() != 4:
+            raise ValueError(f"{name} must be a [B, H, N, d_h] tensor, got shape {tuple(x.shape)}")
+        self.placed.append((x, name, False))
+        return x
+
+    def proj(self, P, name, like, r):
+        B, H, N, d = like.shape
+        return self.tensor(P, name, (H, r, d), like.dtype)
+
+    def tables(self, cos, sin, like, need):
+        """Rotary tables fp32 [N, ld] sharing one row stride ld (returned) with >= need columns."""
+        N = like.shape[2]
+        for t, name in ((cos, "cos"), (sin, "sin")):
+            if not isinstance(t, torch.Tensor) or t.dtype != torch.float32 or t.dim() != 2:
+                raise ValueError(f"{name} must be a float32 [N, ld] table")
+            if t.shape[0] != N or t.shape[1] < need:
+                raise ValueError(f"{name} must have {N} rows and >= {need} columns, got "
+                                 f"{tuple(t.shape)}")
+            self.placed.append((t, name, True))
+        if cos.stride(0) != sin.stride(0) or cos.stride(0) < need:
+            raise ValueError("cos and sin must share one row stride of at least the columns used")
+        return cos.stride(0)
+
+    def blk_idx(self, idx, like, block, sparsity):
+        B, H, N, _ = like.shape
+        nb = num_blocks(N, block)
+        keep = keep_blocks(nb, sparsity)
+        if nb < 1 or keep < 1:
+            raise ValueError(f"invalid block {block} or sparsity {sparsity}")
+        return self.tensor(idx, "blk_idx", (B, H, nb, keep), torch.int32)
+
+    def logits(self, lg, like):
+        B, H, N, _ = like.shape
+        return self.tensor(lg, "logits", (B, N), torch.float32)
+
+    def context(self, C, like, r):
+        B, H, N, d = like.shape
+        return self.tensor(C, "C", (B, H, r, d), torch.float32)
+
+    def workspace(self, ws):
+        if ws is None:
+            return None
+        if not isinstance(ws, torch.Tensor) or ws.dtype != torch.uint8 or ws.dim() != 1:
+            raise ValueError("ws must be a 1-D uint8 tensor")
+        self.placed.append((ws, "ws", False))
+        return ws
+
+    def done(self):
+        device = None
+        for x, name, inner_only in self.placed:
+            if inner_only:
+                if x.stride(-1) != 1:
+                    raise ValueError(f"{name} must have a unit inner stride")
+            elif not x.is_contiguous():
+                raise ValueError(f"{name} must be contiguous")
+            if not x.is_cuda:
+                raise ValueError(f"{name} must be a device tensor")
+            if device is None:
+                device = x.device
+            elif x.device != device:
+                raise ValueError(f"{name} is on {x.device}, the other arguments on {device}")
 
 
 # ---- host helpers ---------------------------------------------------------------------------------
@@ -165,25 +258,48 @@ def rola_rope_tables(prob: Problem, split, base=10000.0, offset=(0, 0, 0), strea
 
 
 def rola_rope_apply(X, cos, sin, grid, out=None, stream=None):
-    _act(X, "X")
-    out = torch.empty_like(X) if out is None else out
+    a = _Args()
+    a.act(X, "X")
+    ld = a.tables(cos, sin, X, X.shape[3] // 2)
+    out = torch.empty_like(X) if out is None else a.act(out, "out", X)
+    a.done()
     prob = problem_of(X, grid)
-    _check(LIB.rola_rope_apply(ctypes.byref(prob), _ptr(X), _ptr(cos), _ptr(sin), cos.stride(0),
-                               _ptr(out), _stream(stream)), "rola_rope_apply")
+    _check(LIB.rola_rope_apply(ctypes.byref(prob), _ptr(X), _ptr(cos), _ptr(sin), ld, _ptr(out),
+                               _stream(stream)), "rola_rope_apply")
     return out
 
 
+def rola_rope_backward_accumulate(dY, cos, sin, grid, dX, rotate=True, stream=None):
+    """dX += R(p)^T dY (rotate) or dX += dY, fp32 [B, H, N, d_h], in place; returns dX."""
+    a = _Args()
+    a.act(dY, "dY")
+    if dY.dtype != torch.float32:
+        raise ValueError("dY must be float32")
+    a.act(dX, "dX", dY)
+    ld = a.tables(cos, sin, dY, dY.shape[3] // 2)
+    a.done()
+    prob = problem_of(dY, grid)
+    _check(LIB.rola_rope_backward_accumulate(ctypes.byref(prob), _ptr(dY), _ptr(cos), _ptr(sin), ld,
+                                             1 if rotate else 0, _ptr(dX), _stream(stream)),
+           "rola_rope_backward_accumulate")
+    return dX
+
+
 def rola_block_select(Qr, Kr, grid, block, sparsity, out=None, ws=None, stream=None):
-    _act(Qr, "Qr")
-    _act(Kr, "Kr")
+    a = _Args()
+    a.act(Qr, "Qr")
+    a.act(Kr, "Kr", Qr)
     prob = problem_of(Qr, grid)
     nb = num_blocks(prob.N, block)
     keep = keep_blocks(nb, sparsity)
     if out is None:
         out = torch.empty((prob.B, prob.H, nb, keep), dtype=torch.int32, device=Qr.device)
+    a.blk_idx(out, Qr, block, sparsity)
     need = select_workspace_bytes(prob, block)
     if ws is None:
         ws = torch.empty(max(need, 16), dtype=torch.uint8, device=Qr.device)
+    a.workspace(ws)
+    a.done()
     _check(LIB.rola_block_select(ctypes.byref(prob), _ptr(Qr), _ptr(Kr), block, sparsity, _ptr(out),
                                  _ptr(ws), ws.numel(), _stream(stream)), "rola_block_select")
     return out
@@ -192,13 +308,19 @@ def rola_block_select(Qr, Kr, grid, block, sparsity, out=None, ws=None, stream=N
 def rola_sparse_attn(Qr, Kr, V, grid, block, sparsity, blk_idx, scale=None, out=None, ws=None,
                      stream=None, share=True):
     """share=False passes no workspace: each workgroup then serves one query block."""
-    _act(Qr, "Qr")
+    a = _Args()
+    a.act(Qr, "Qr")
+    a.act(Kr, "Kr", Qr)
+    a.act(V, "V", Qr)
+    a.blk_idx(blk_idx, Qr, block, sparsity)
     prob = problem_of(Qr, grid)
     scale = prob.d_h ** -0.5 if scale is None else scale
-    out = torch.empty_like(Qr) if out is None else out
+    out = torch.empty_like(Qr) if out is None else a.act(out, "out", Qr)
     if ws is None and share:
         need = sparse_workspace_bytes(prob, block, sparsity)
         ws = torch.empty(need, dtype=torch.uint8, device=Qr.device) if need else None
+    a.workspace(ws)
+    a.done()
     _check(LIB.rola_sparse_attn(ctypes.byref(prob), _ptr(Qr), _ptr(Kr), _ptr(V), block, sparsity,
                                 _ptr(blk_idx), scale, _ptr(out), _ptr(ws) if ws is not None else None,
                                 ws.numel() if ws is not None else 0, _stream(stream)),
@@ -207,46 +329,78 @@ def rola_sparse_attn(Qr, Kr, V, grid, block, sparsity, blk_idx, scale=None, out=
 
 
 def rola_dense_attn(Qr, Kr, V, grid, block=64, scale=None, out=None, stream=None):
-    _act(Qr, "Qr")
+    a = _Args()
+    a.act(Qr, "Qr")
+    a.act(Kr, "Kr", Qr)
+    a.act(V, "V", Qr)
     prob = problem_of(Qr, grid)
     scale = prob.d_h ** -0.5 if scale is None else scale
-    out = torch.empty_like(Qr) if out is None else out
+    out = torch.empty_like(Qr) if out is None else a.act(out, "out", Qr)
+    a.done()
     _check(LIB.rola_dense_attn(ctypes.byref(prob), _ptr(Qr), _ptr(Kr), _ptr(V), block, scale,
                                _ptr(out), _stream(stream)), "rola_dense_attn")
     return out
 
 
+def _summary_args(a, Kn, V, Pk, r, cos, sin, C, z, want_z):
+    a.act(Kn, "Kn")
+    a.act(V, "V", Kn)
+    a.proj(Pk, "Pk", Kn, r)
+    ld = a.tables(cos, sin, Kn, r // 2)
+    B, H, N, d = Kn.shape
+    if C is None:
+        C = torch.empty((B, H, r, d), dtype=torch.float32, device=Kn.device)
+    a.context(C, Kn, r)
+    if z is None and want_z:
+        z = torch.empty((B, H, r), dtype=torch.float32, device=Kn.device)
+    if z is not None:
+        a.tensor(z, "z", (B, H, r), torch.float32)
+    return ld, C, z
+
+
 def rola_lowrank_summary(Kn, V, Pk, r, cos, sin, grid, C=None, z=None, ws=None, stream=None,
                          want_z=True):
-    _act(Kn, "Kn")
+    a = _Args()
+    ld, C, z = _summary_args(a, Kn, V, Pk, r, cos, sin, C, z, want_z)
     prob = problem_of(Kn, grid)
-    if C is None:
-        C = torch.empty((prob.B, prob.H, r, prob.d_h), dtype=torch.float32, device=Kn.device)
-    if z is None and want_z:
-        z = torch.empty((prob.B, prob.H, r), dtype=torch.float32, device=Kn.device)
     need = summary_workspace_bytes(prob, r)
     if ws is None:
         ws = torch.empty(max(need, 16), dtype=torch.uint8, device=Kn.device)
+    a.workspace(ws)
+    a.done()
     _check(LIB.rola_lowrank_summary(ctypes.byref(prob), _ptr(Kn), _ptr(V), _ptr(Pk), r, _ptr(cos),
-                                    _ptr(sin), cos.stride(0), _ptr(C), _ptr(z), _ptr(ws), ws.numel(),
+                                    _ptr(sin), ld, _ptr(C), _ptr(z), _ptr(ws), ws.numel(),
                                     _stream(stream)), "rola_lowrank_summary")
     return C, z
 
 
+def _readout_args(a, Qn, Pq, r, cos, sin, C):
+    a.act(Qn, "Qn")
+    a.proj(Pq, "Pq", Qn, r)
+    a.context(C, Qn, r)
+    return a.tables(cos, sin, Qn, r // 2)
+
+
 def rola_lowrank_readout(Qn, Pq, r, cos, sin, C, grid, eps_lr=1e-6, out=None, stream=None):
-    _act(Qn, "Qn")
+    a = _Args()
+    ld = _readout_args(a, Qn, Pq, r, cos, sin, C)
+    out = torch.empty_like(Qn) if out is None else a.act(out, "out", Qn)
+    a.done()
     prob = problem_of(Qn, grid)
-    out = torch.empty_like(Qn) if out is None else out
     _check(LIB.rola_lowrank_readout(ctypes.byref(prob), _ptr(Qn), _ptr(Pq), r, _ptr(cos), _ptr(sin),
-                                    cos.stride(0), _ptr(C), eps_lr, _ptr(out), _stream(stream)),
+                                    ld, _ptr(C), eps_lr, _ptr(out), _stream(stream)),
            "rola_lowrank_readout")
     return out
 
 
 def rola_combine(Os, Olr, logits, grid, eps=1e-6, out=None, stream=None):
-    _act(Os, "Os")
+    a = _Args()
+    a.act(Os, "Os")
+    a.act(Olr, "Olr", Os)
+    a.logits(logits, Os)
+    out = torch.empty_like(Os) if out is None else a.act(out, "out", Os)
+    a.done()
     prob = problem_of(Os, grid)
-    out = torch.empty_like(Os) if out is None else out
     _check(LIB.rola_combine(ctypes.byref(prob), _ptr(Os), _ptr(Olr), _ptr(logits), eps, _ptr(out),
                             _stream(stream)), "rola_combine")
     return out
@@ -254,11 +408,15 @@ def rola_combine(Os, Olr, logits, grid, eps=1e-6, out=None, stream=None):
 
 def rola_lowrank_readout_combine(Qn, Pq, r, cos, sin, C, Os, logits, grid, eps_lr=1e-6, eps=1e-6,
                                  out=None, stream=None):
-    _act(Qn, "Qn")
+    a = _Args()
+    ld = _readout_args(a, Qn, Pq, r, cos, sin, C)
+    a.act(Os, "Os", Qn)
+    a.logits(logits, Qn)
+    out = torch.empty_like(Os) if out is None else a.act(out, "out", Qn)
+    a.done()
     prob = problem_of(Qn, grid)
-    out = torch.empty_like(Os) if out is None else out
     _check(LIB.rola_lowrank_readout_combine(ctypes.byref(prob), _ptr(Qn), _ptr(Pq), r, _ptr(cos),
-                                            _ptr(sin), cos.stride(0), _ptr(C), eps_lr, _ptr(Os),
+                                            _ptr(sin), ld, _ptr(C), eps_lr, _ptr(Os),
                                             _ptr(logits), eps, _ptr(out), _stream(stream)),
            "rola_lowrank_readout_combine")
     return out
@@ -266,17 +424,16 @@ def rola_lowrank_readout_combine(Qn, Pq, r, cos, sin, C, Os, logits, grid, eps_l
 
 def rola_lowrank_summary_ex(Kn, V, Pk, r, cos, sin, grid, phi="silu", rope_order="outside", C=None,
                             z=None, ws=None, stream=None, want_z=True):
-    _act(Kn, "Kn")
+    a = _Args()
+    ld, C, z = _summary_args(a, Kn, V, Pk, r, cos, sin, C, z, want_z)
     prob = problem_of(Kn, grid)
-    if C is None:
-        C = torch.empty((prob.B, prob.H, r, prob.d_h), dtype=torch.float32, device=Kn.device)
-    if z is None and want_z:
-        z = torch.empty((prob.B, prob.H, r), dtype=torch.float32, device=Kn.device)
     need = summary_workspace_bytes(prob, r)
     if ws is None:
         ws = torch.empty(max(need, 16), dtype=torch.uint8, device=Kn.device)
+    a.workspace(ws)
+    a.done()
     _check(LIB.rola_lowrank_summary_ex(ctypes.byref(prob), _ptr(Kn), _ptr(V), _ptr(Pk), r, _ptr(cos),
-                                       _ptr(sin), cos.stride(0), _code(PHI, phi),
+                                       _ptr(sin), ld, _code(PHI, phi),
                                        _code(ROPE_ORDER, rope_order), _ptr(C), _ptr(z), _ptr(ws),
                                        ws.numel(), _stream(stream)), "rola_lowrank_summary_ex")
     return C, z
@@ -284,11 +441,13 @@ def rola_lowrank_summary_ex(Kn, V, Pk, r, cos, sin, grid, phi="silu", rope_order
 
 def rola_lowrank_readout_ex(Qn, Pq, r, cos, sin, C, grid, phi="silu", rope_order="outside",
                             eps_lr=1e-6, out=None, stream=None):
-    _act(Qn, "Qn")
+    a = _Args()
+    ld = _readout_args(a, Qn, Pq, r, cos, sin, C)
+    out = torch.empty_like(Qn) if out is None else a.act(out, "out", Qn)
+    a.done()
     prob = problem_of(Qn, grid)
-    out = torch.empty_like(Qn) if out is None else out
     _check(LIB.rola_lowrank_readout_ex(ctypes.byref(prob), _ptr(Qn), _ptr(Pq), r, _ptr(cos),
-                                       _ptr(sin), cos.stride(0), _code(PHI, phi),
+                                       _ptr(sin), ld, _code(PHI, phi),
                                        _code(ROPE_ORDER, rope_order), _ptr(C), eps_lr, _ptr(out),
                                        _stream(stream)), "rola_lowrank_readout_ex")
     return out
@@ -297,11 +456,15 @@ def rola_lowrank_readout_ex(Qn, Pq, r, cos, sin, C, grid, phi="silu", rope_order
 def rola_lowrank_readout_combine_ex(Qn, Pq, r, cos, sin, C, Os, logits, grid, phi="silu",
                                     rope_order="outside", eps_lr=1e-6, eps=1e-6, out=None,
                                     stream=None):
-    _act(Qn, "Qn")
+    a = _Args()
+    ld = _readout_args(a, Qn, Pq, r, cos, sin, C)
+    a.act(Os, "Os", Qn)
+    a.logits(logits, Qn)
+    out = torch.empty_like(Os) if out is None else a.act(out, "out", Qn)
+    a.done()
     prob = problem_of(Qn, grid)
-    out = torch.empty_like(Os) if out is None else out
     _check(LIB.rola_lowrank_readout_combine_ex(ctypes.byref(prob), _ptr(Qn), _ptr(Pq), r, _ptr(cos),
-                                               _ptr(sin), cos.stride(0), _code(PHI, phi),
+                                               _ptr(sin), ld, _code(PHI, phi),
                                                _code(ROPE_ORDER, rope_order), _ptr(C), eps_lr,
                                                _ptr(Os), _ptr(logits), eps, _ptr(out),
                                                _stream(stream)), "rola_lowrank_readout_combine_ex")
@@ -311,24 +474,39 @@ def rola_lowrank_readout_combine_ex(Qn, Pq, r, cos, sin, C, Os, logits, grid, ph
 def rola_lowrank_features(X, P, r, cos, sin, grid, phi="silu", rope_order="outside", out=None,
                           stream=None):
     """q~ (X = Q^n, P = P_q) or k~ (X = K^n, P = P_k) of every token: fp32 [B, H, N, r]."""
-    _act(X, "X")
+    a = _Args()
+    a.act(X, "X")
+    a.proj(P, "P", X, r)
+    ld = a.tables(cos, sin, X, r // 2)
     prob = problem_of(X, grid)
+    shape = (prob.B, prob.H, prob.N, r)
     if out is None:
-        out = torch.empty((prob.B, prob.H, prob.N, r), dtype=torch.float32, device=X.device)
+        out = torch.empty(shape, dtype=torch.float32, device=X.device)
+    a.tensor(out, "out", shape, torch.float32)
+    a.done()
     _check(LIB.rola_lowrank_features(ctypes.byref(prob), _ptr(X), _ptr(P), r, _ptr(cos), _ptr(sin),
-                                     cos.stride(0), _code(PHI, phi), _code(ROPE_ORDER, rope_order),
+                                     ld, _code(PHI, phi), _code(ROPE_ORDER, rope_order),
                                      _ptr(out), _stream(stream)), "rola_lowrank_features")
     return out
 
 
+def _hidden(a, X, Wg):
+    if not isinstance(X, torch.Tensor) or X.dtype not in _ACT_DTYPES or X.dim() != 3:
+        raise ValueError("X must be a [B, N, d_model] bfloat16 or float32 tensor")
+    a.tensor(X, "X", X.shape, X.dtype)
+    a.tensor(Wg, "Wg", (X.shape[2],), X.dtype)
+    return X.shape
+
+
 def rola_gate_logits(X, Wg, bg, grid, H=1, d_h=128, out=None, stream=None):
     """Gate logits X W_g + b_g of every token: X [B, N, d_model], W_g [d_model] -> fp32 [B, N]."""
-    if not (X.is_cuda and X.dim() == 3 and X.is_contiguous()):
-        raise ValueError("X must be a contiguous [B, N, d_model] device tensor")
-    B, N, dm = X.shape
+    a = _Args()
+    B, N, dm = _hidden(a, X, Wg)
     prob = problem(B, H, N, d_h, grid, X.dtype)
     if out is None:
         out = torch.empty((B, N), dtype=torch.float32, device=X.device)
+    a.tensor(out, "out", (B, N), torch.float32)
+    a.done()
     _check(LIB.rola_gate_logits(ctypes.byref(prob), _ptr(X), dm, _ptr(Wg), bg, _ptr(out),
                                 _stream(stream)), "rola_gate_logits")
     return out
@@ -338,20 +516,33 @@ def sparse_combine_workspace_bytes(prob: Problem, block: int, sparsity: float, r
     return LIB.rola_sparse_combine_workspace_bytes(ctypes.byref(prob), block, sparsity, r)
 
 
+def _combine_args(a, Qr, Kr, V, block, sparsity, blk_idx, Qn, Pq, r, cos, sin, C, logits):
+    a.act(Qr, "Qr")
+    for t, name in ((Kr, "Kr"), (V, "V"), (Qn, "Qn")):
+        a.act(t, name, Qr)
+    a.blk_idx(blk_idx, Qr, block, sparsity)
+    ld = _readout_args(a, Qn, Pq, r, cos, sin, C)
+    a.logits(logits, Qr)
+    return ld
+
+
 def rola_sparse_attn_combine(Qr, Kr, V, grid, block, sparsity, blk_idx, Qn, Pq, r, cos, sin, C,
                              logits, scale=None, eps_lr=1e-6, eps=1e-6, out=None, ws=None,
                              stream=None):
     """O = combine(sparse attention, low-rank readout of C) in one call (fused epilogue)."""
-    _act(Qr, "Qr")
+    a = _Args()
+    ld = _combine_args(a, Qr, Kr, V, block, sparsity, blk_idx, Qn, Pq, r, cos, sin, C, logits)
     prob = problem_of(Qr, grid)
     scale = prob.d_h ** -0.5 if scale is None else scale
-    out = torch.empty_like(Qr) if out is None else out
+    out = torch.empty_like(Qr) if out is None else a.act(out, "out", Qr)
     if ws is None:
         need = sparse_combine_workspace_bytes(prob, block, sparsity, r)
         ws = torch.empty(need, dtype=torch.uint8, device=Qr.device)
+    a.workspace(ws)
+    a.done()
     _check(LIB.rola_sparse_attn_combine(ctypes.byref(prob), _ptr(Qr), _ptr(Kr), _ptr(V), block,
                                         sparsity, _ptr(blk_idx), scale, _ptr(Qn), _ptr(Pq), r,
-                                        _ptr(cos), _ptr(sin), cos.stride(0), _ptr(C), eps_lr,
+                                        _ptr(cos), _ptr(sin), ld, _ptr(C), eps_lr,
                                         _ptr(logits), eps, _ptr(out), _ptr(ws), ws.numel(),
                                         _stream(stream)), "rola_sparse_attn_combine")
     return out
@@ -361,15 +552,22 @@ def rola_sparse_attn_lse(Qr, Kr, V, grid, block, sparsity, blk_idx, scale=None, 
                          ws=None, stream=None, share=True):
     """Sparse attention that also returns the per-query log2-sum-exp2 (fp32 [B, H, N]); share=False
     passes no workspace (one query block per workgroup)."""
-    _act(Qr, "Qr")
+    a = _Args()
+    a.act(Qr, "Qr")
+    a.act(Kr, "Kr", Qr)
+    a.act(V, "V", Qr)
+    a.blk_idx(blk_idx, Qr, block, sparsity)
     prob = problem_of(Qr, grid)
     scale = prob.d_h ** -0.5 if scale is None else scale
-    out = torch.empty_like(Qr) if out is None else out
+    out = torch.empty_like(Qr) if out is None else a.act(out, "out", Qr)
     if lse is None:
         lse = torch.empty(Qr.shape[:3], dtype=torch.float32, device=Qr.device)
+    a.tensor(lse, "lse", Qr.shape[:3], torch.float32)
     if ws is None and share:
         need = sparse_workspace_bytes(prob, block, sparsity)
         ws = torch.empty(need, dtype=torch.uint8, device=Qr.device) if need else None
+    a.workspace(ws)
+    a.done()
     _check(LIB.rola_sparse_attn_lse(ctypes.byref(prob), _ptr(Qr), _ptr(Kr), _ptr(V), block, sparsity,
                                     _ptr(blk_idx), scale, _ptr(out), _ptr(lse),
                                     _ptr(ws) if ws is not None else None,
@@ -381,7 +579,12 @@ def rola_sparse_attn_lse(Qr, Kr, V, grid, block, sparsity, blk_idx, scale=None, 
 def rola_sparse_attn_backward(Qr, Kr, V, grid, block, sparsity, blk_idx, Os, lse, dOs, scale=None,
                               ws=None, stream=None):
     """Gradients (dQ^r, dK^r, dV), fp32, of <dOs, O^s> for fixed block lists."""
-    _act(Qr, "Qr")
+    a = _Args()
+    a.act(Qr, "Qr")
+    for t, name in ((Kr, "Kr"), (V, "V"), (Os, "Os"), (dOs, "dOs")):
+        a.act(t, name, Qr)
+    a.blk_idx(blk_idx, Qr, block, sparsity)
+    a.tensor(lse, "lse", Qr.shape[:3], torch.float32)
     prob = problem_of(Qr, grid)
     scale = prob.d_h ** -0.5 if scale is None else scale
     dQ = torch.empty(Qr.shape, dtype=torch.float32, device=Qr.device)
@@ -389,6 +592,8 @@ def rola_sparse_attn_backward(Qr, Kr, V, grid, block, sparsity, blk_idx, Os, lse
     if ws is None:
         need = LIB.rola_sparse_backward_workspace_bytes(ctypes.byref(prob), block, sparsity)
         ws = torch.empty(max(need, 16), dtype=torch.uint8, device=Qr.device)
+    a.workspace(ws)
+    a.done()
     _check(LIB.rola_sparse_attn_backward(ctypes.byref(prob), _ptr(Qr), _ptr(Kr), _ptr(V), block,
                                          sparsity, _ptr(blk_idx), scale, _ptr(Os), _ptr(lse),
                                          _ptr(dOs), _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(ws),
@@ -399,7 +604,12 @@ def rola_sparse_attn_backward(Qr, Kr, V, grid, block, sparsity, blk_idx, Os, lse
 def rola_lowrank_backward(Qn, Kn, V, Pq, Pk, r, cos, sin, C, Os, logits, dO, grid, eps_lr=1e-6,
                           eps=1e-6, ws=None, stream=None):
     """(dOs bf16, dQn, dKn, dV fp32 [B, H, N, d], dPq, dPk fp32 [H, r, d], dlogits fp32 [B, N])."""
-    _act(Qn, "Qn")
+    a = _Args()
+    ld = _readout_args(a, Qn, Pq, r, cos, sin, C)
+    for t, name in ((Kn, "Kn"), (V, "V"), (Os, "Os"), (dO, "dO")):
+        a.act(t, name, Qn)
+    a.proj(Pk, "Pk", Qn, r)
+    a.logits(logits, Qn)
     prob = problem_of(Qn, grid)
     dOs = torch.empty_like(Qn)
     f32 = dict(dtype=torch.float32, device=Qn.device)
@@ -409,8 +619,10 @@ def rola_lowrank_backward(Qn, Kn, V, Pq, Pk, r, cos, sin, C, Os, logits, dO, gri
     if ws is None:
         need = LIB.rola_lowrank_backward_workspace_bytes(ctypes.byref(prob), r)
         ws = torch.empty(max(need, 16), dtype=torch.uint8, device=Qn.device)
+    a.workspace(ws)
+    a.done()
     _check(LIB.rola_lowrank_backward(ctypes.byref(prob), _ptr(Qn), _ptr(Kn), _ptr(V), _ptr(Pq),
-                                     _ptr(Pk), r, _ptr(cos), _ptr(sin), cos.stride(0), _ptr(C),
+                                     _ptr(Pk), r, _ptr(cos), _ptr(sin), ld, _ptr(C),
                                      _ptr(Os), _ptr(logits), eps_lr, eps, _ptr(dO), _ptr(dOs),
                                      _ptr(dQn), _ptr(dKn), _ptr(dV), _ptr(dPq), _ptr(dPk),
                                      _ptr(dlog), _ptr(ws), ws.numel(), _stream(stream)),
@@ -421,7 +633,9 @@ def rola_lowrank_backward(Qn, Kn, V, Pq, Pk, r, cos, sin, C, Os, logits, dO, gri
 def rola_gate_logits_backward(X, Wg, dlogits, grid, H=1, d_h=128, want_dX=True, ws=None,
                               stream=None):
     """(dX fp32 [B, N, d_model] or None, dWg fp32 [d_model], dbg fp32 [1]) of X W_g + b_g."""
-    B, N, dm = X.shape
+    a = _Args()
+    B, N, dm = _hidden(a, X, Wg)
+    a.tensor(dlogits, "dlogits", (B, N), torch.float32)
     prob = problem(B, H, N, d_h, grid, X.dtype)
     f32 = dict(dtype=torch.float32, device=X.device)
     dX = torch.empty(X.shape, **f32) if want_dX else None
@@ -429,6 +643,8 @@ def rola_gate_logits_backward(X, Wg, dlogits, grid, H=1, d_h=128, want_dX=True, 
     if ws is None:
         need = LIB.rola_gate_backward_workspace_bytes(ctypes.byref(prob), dm)
         ws = torch.empty(max(need, 16), dtype=torch.uint8, device=X.device)
+    a.workspace(ws)
+    a.done()
     _check(LIB.rola_gate_logits_backward(ctypes.byref(prob), _ptr(X), dm, _ptr(Wg), _ptr(dlogits),
                                          _ptr(dX), _ptr(dWg), _ptr(dbg), _ptr(ws), ws.numel(),
                                          _stream(stream)), "rola_gate_logits_backward")

@@ -91,8 +91,22 @@ def test_status_strings():
 # Invalid-argument checks pass fake (aligned, never dereferenced) addresses. They are host logic and
 # run where no GPU is present, so a validation bug can never turn into a launch on a real device.
 no_gpu = pytest.mark.skipif(torch.cuda.device_count() > 0, reason="host-validation test: CPU only")
-FAKE = ctypes.c_void_p(1 << 20)
 MIS = ctypes.c_void_p((1 << 20) + 4)
+_fake_next = [1]
+
+
+class _Fake:
+    """Each use stands for a distinct aligned address (64 GiB apart), so that no two arguments of a
+    case overlap unless a case says so."""
+
+    @property
+    def _as_parameter_(self):
+        _fake_next[0] += 1
+        return ctypes.c_void_p(_fake_next[0] << 36)
+
+
+FAKE = _Fake()
+SAME = ctypes.c_void_p(1 << 44)   # one address passed for two arguments: an overlap
 
 
 def _call(name, *args):
@@ -130,10 +144,10 @@ def test_invalid_arguments_are_rejected_before_launch():
          64, FAKE, None, FAKE, 64, None),
         (R.ROLA_ERR_INVALID_ARGUMENT, "rola_lowrank_readout", P(ok), FAKE, FAKE, 32, FAKE, FAKE, 64,
          FAKE, -1.0, FAKE, None),
-        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_combine", P(ok), FAKE, FAKE, FAKE, 1e-6, FAKE, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_combine", P(ok), FAKE, FAKE, FAKE, -1.0, FAKE, None),
         (R.ROLA_ERR_INVALID_ARGUMENT, "rola_rope_tables", P(ok), 44, 42, 40, 10000.0, 0, 0, 0, FAKE,
          FAKE, None),
-        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_rope_apply", P(ok), FAKE, FAKE, FAKE, 64, FAKE, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_rope_apply", P(ok), FAKE, FAKE, FAKE, 60, FAKE, None),
         (R.ROLA_ERR_INVALID_ARGUMENT, "rola_lowrank_readout_combine", P(ok), FAKE, FAKE, 32, FAKE, FAKE,
          64, FAKE, 1e-6, None, FAKE, 1e-6, FAKE, None),
         # feature-map variants: unknown phi or rotation order
@@ -165,7 +179,74 @@ def test_invalid_arguments_are_rejected_before_launch():
         (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn_combine", P(ok), FAKE, FAKE, FAKE, 64, 0.9,
          FAKE, 0.1, FAKE, FAKE, 31, FAKE, FAKE, 64, FAKE, 1e-6, FAKE, 1e-6, FAKE, FAKE, 1 << 40, None),
     ]
+    # outputs that overlap an input
+    cases += [
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn", P(ok), FAKE, SAME, FAKE, 64, 0.9, FAKE, 0.1,
+         SAME, None, 0, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_dense_attn", P(ok), FAKE, FAKE, SAME, 64, 0.1, SAME, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn_combine", P(ok), FAKE, FAKE, FAKE, 64, 0.9,
+         FAKE, 0.1, SAME, FAKE, 32, FAKE, FAKE, 64, FAKE, 1e-6, FAKE, 1e-6, SAME, FAKE, 1 << 40, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_combine", P(ok), FAKE, SAME, FAKE, 1e-6, SAME, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_combine", P(ok), SAME, FAKE, FAKE, 1e-6,
+         ctypes.c_void_p((1 << 44) + 4096), None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_lowrank_readout", P(ok), SAME, FAKE, 32, FAKE, FAKE, 64,
+         FAKE, 1e-6, SAME, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_lowrank_readout_combine", P(ok), SAME, FAKE, 32, FAKE,
+         FAKE, 64, FAKE, 1e-6, FAKE, FAKE, 1e-6, SAME, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_rope_apply", P(ok), SAME, FAKE, FAKE, 64, SAME, None),
+        (R.ROLA_ERR_INVALID_ARGUMENT, "rola_rope_backward_accumulate",
+         P(R.problem(1, 2, 75600, 128, g, "f32")), SAME, FAKE, FAKE, 64, 1, SAME, None),
+    ]
     for want, name, *args in cases:
         got = _call(name, *args)
         assert got == want, (name, got, want, R.LIB.rola_last_error())
         assert R.LIB.rola_last_error()  # a message is always left behind
+
+
+def _cpu(shape, dtype=torch.bfloat16):
+    return torch.zeros(shape, dtype=dtype)
+
+
+def test_binding_rejects_bad_tensors():
+    """The binding checks type and shape of every tensor before anything reaches the library (and
+    layout and device after that), so wrong block lists, tables or outputs raise ValueError."""
+    g = (2, 4, 16)                                   # N = 128: 2 blocks of 64
+    q = _cpu((1, 2, 128, 128))
+    idx_ok = torch.zeros((1, 2, 2, 1), dtype=torch.int32)
+    cos = torch.zeros((128, 64))
+    bad = [
+        ("blk_idx int64", lambda: R.rola_sparse_attn(q, q, q, g, 64, 0.5, idx_ok.long())),
+        ("blk_idx keep", lambda: R.rola_sparse_attn(q, q, q, g, 64, 0.5,
+                                                    torch.zeros((1, 2, 2, 2), dtype=torch.int32))),
+        ("blk_idx other sparsity", lambda: R.rola_sparse_attn(q, q, q, g, 64, 0.0, idx_ok)),
+        ("blk_idx other block", lambda: R.rola_sparse_attn(q, q, q, g, 128, 0.5, idx_ok)),
+        ("V dtype", lambda: R.rola_sparse_attn(q, q, q.float(), g, 64, 0.5, idx_ok)),
+        ("Kr shape", lambda: R.rola_sparse_attn(q, q[:, :1], q, g, 64, 0.5, idx_ok)),
+        ("3-D activation", lambda: R.rola_dense_attn(q[0], q[0], q[0], g)),
+        ("int activation", lambda: R.rola_dense_attn(q.int(), q.int(), q.int(), g)),
+        ("table dtype", lambda: R.rola_rope_apply(q, cos.double(), cos.double(), g)),
+        ("table rows", lambda: R.rola_rope_apply(q, cos[:100], cos[:100], g)),
+        ("table columns", lambda: R.rola_rope_apply(q, cos[:, :32], cos[:, :32], g)),
+        ("table strides differ", lambda: R.rola_rope_apply(q, cos, torch.zeros((128, 72))[:, :64], g)),
+        ("Pk shape", lambda: R.rola_lowrank_summary(q, q, _cpu((2, 16, 128)), 32, cos, cos, g)),
+        ("C dtype", lambda: R.rola_lowrank_readout(q, _cpu((2, 32, 128)), 32, cos, cos,
+                                                   _cpu((1, 2, 32, 128)), g)),
+        ("logits shape", lambda: R.rola_combine(q, q, torch.zeros((1, 127)), g)),
+        ("logits dtype", lambda: R.rola_combine(q, q, torch.zeros((1, 128), dtype=torch.float64), g)),
+        ("out shape", lambda: R.rola_combine(q, q, torch.zeros((1, 128)), g, out=q[:, :1])),
+        ("ws dtype", lambda: R.rola_block_select(q, q, g, 64, 0.5, ws=torch.zeros(64))),
+        ("lse shape", lambda: R.rola_sparse_attn_lse(q, q, q, g, 64, 0.5, idx_ok,
+                                                     lse=torch.zeros((1, 2, 127)))),
+        ("Wg shape", lambda: R.rola_gate_logits(_cpu((1, 128, 64)), _cpu((65,)), 0.0, g)),
+        ("dY dtype", lambda: R.rola_rope_backward_accumulate(q, cos, cos, g, q.float())),
+        # right types and shapes: the layout and device checks come last
+        ("strided table", lambda: R.rola_rope_apply(q, torch.zeros((64, 128)).t(),
+                                                    torch.zeros((64, 128)).t(), g)),
+        ("non-contiguous", lambda: R.rola_dense_attn(q, q.transpose(2, 3).contiguous().transpose(2, 3),
+                                                     q, g)),
+        ("host tensors", lambda: R.rola_sparse_attn(q, q, q, g, 64, 0.5, idx_ok)),
+    ]
+    for what, fn in bad:
+        with pytest.raises(ValueError):
+            fn()
+            pytest.fail(what)
