@@ -21,6 +21,9 @@ hipError_t launch_rope_tables(const Shape& s, int dt, int dy, int dx, double bas
                               int ox, float* cos_tab, float* sin_tab, hipStream_t st);
 hipError_t launch_rope_apply(const Shape& s, const void* X, const float* cos_tab,
                              const float* sin_tab, int ld, void* Xr, hipStream_t st);
+// fp32 [B, H, N, d]: dX += R(p)^T dY (rotate) or dX += dY.
+hipError_t launch_rope_grad(const Shape& s, const float* dY, const float* cos_tab,
+                            const float* sin_tab, int ld, bool rotate, float* dX, hipStream_t st);
 
 // select.hip
 size_t select_workspace_bytes(const Shape& s, int block);

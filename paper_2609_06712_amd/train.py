@@ -5,8 +5,7 @@ forward() keeps what the backward needs: the rotated Q^r, K^r (Algorithm step 3)
 O^s with its per-query log-sum-exp, and the summary C. backward() runs the low-rank/fusion backward
 (which also yields dO^s and the gate-logit gradient), the block-sparse attention backward, and maps
 dQ^r, dK^r back through the backbone rotation (R(p)^T = R(-p)); the two branches' shares of dQ^n,
-dK^n and dV are added. Every step runs in the library's kernels; the additions and the sign flip of
-the sine table are tensor plumbing.
+dK^n and dV are added. Every step, the additions included, runs in the library's kernels.
 """
 
 from __future__ import annotations
@@ -40,8 +39,7 @@ def backward(Qn, Kn, V, Pq, Pk, logits, saved, dO):
     dQr, dKr, dVs = R.rola_sparse_attn_backward(saved["qr"], saved["kr"], V, g, saved["block"],
                                                 saved["sparsity"], saved["idx"], saved["os"],
                                                 saved["lse"], dOs)
-    neg = -sin  # R(p)^T = R(-p): the same tables with the sine negated
-    dQn += R.rola_rope_apply(dQr, cos, neg, g)
-    dKn += R.rola_rope_apply(dKr, cos, neg, g)
-    dV += dVs
+    R.rola_rope_backward_accumulate(dQr, cos, sin, g, dQn)           # dQ^n += R(p)^T dQ^r
+    R.rola_rope_backward_accumulate(dKr, cos, sin, g, dKn)           # dK^n += R(p)^T dK^r
+    R.rola_rope_backward_accumulate(dVs, cos, sin, g, dV, rotate=False)
     return dict(dQn=dQn, dKn=dKn, dV=dV, dPq=dPq, dPk=dPk, dlogits=dlog)

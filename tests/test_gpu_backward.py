@@ -219,3 +219,22 @@ def test_module_backward(grid, s):
         for n, e in errs.items():
             assert e <= 2e-2, (n, e)
     assert _rel(_f64(gr["dlogits"][0]), tot["dlogits"]) <= 2e-2
+
+
+def test_rope_backward_accumulate():
+    """dX += R(p)^T dY (the gradient through the main-path rotation) and dX += dY, against the
+    oracle's rotation by the negated angle (R(p)^T = R(-p)) in fp64, on a ragged 3x10x13 grid."""
+    w = synth.WAN_1_3B_480P.replace(grid=(3, 10, 13), H=2, B=2)
+    g = w.grid
+    gen = torch.Generator().manual_seed(11)
+    dY = torch.randn((w.B, w.H, w.N, 128), generator=gen)
+    dX0 = torch.randn((w.B, w.H, w.N, 128), generator=gen)
+    prob = R.problem(w.B, w.H, w.N, 128, g, "f32")
+    cos, sin = R.rola_rope_tables(prob, w.split)
+    rot = R.rola_rope_backward_accumulate(dY.cuda(), cos, sin, g, dX0.clone().cuda())
+    add = R.rola_rope_backward_accumulate(dY.cuda(), cos, sin, g, dX0.clone().cuda(), rotate=False)
+    torch.cuda.synchronize()
+    ocos, osin = O.rope_tables(*g, w.split)
+    want = dX0.double().numpy() + O.rotate(dY.double().numpy(), ocos, -osin)
+    np.testing.assert_allclose(_f64(rot), want, rtol=0, atol=2e-5)
+    np.testing.assert_allclose(_f64(add), (dX0.double() + dY.double()).numpy(), rtol=0, atol=1e-6)
