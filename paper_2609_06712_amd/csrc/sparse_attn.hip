@@ -28,26 +28,12 @@
 #include "common.h"
 #include "launch.h"
 
-#ifndef ROLA_B64_GROUP
-#define ROLA_B64_GROUP 2  // query blocks per workgroup of the 64-token-block kernel with a block list
-#endif
-#ifndef ROLA_B64_NBUF
-#define ROLA_B64_NBUF 3  // its LDS stages (16 KB each)
-#endif
-#ifndef ROLA_B64_PAIRING
-#define ROLA_B64_PAIRING 1  // pair query blocks by list overlap (1) or take adjacent pairs (0)
-#endif
-#ifndef ROLA_B64_WALK
-#define ROLA_B64_WALK 1  // merged lists in bit-reversed (1) or ascending (0) block order
-#endif
-#ifndef ROLA_B64_QUEUE
-#define ROLA_B64_QUEUE 1  // resident workgroups claim groups from per-XCD queues (1) or a static grid (0)
-#endif
-
 namespace rola {
 namespace {
 
 constexpr int kSub = 32;            // keys per sub-tile: one LDS stage holds its K and V (8 KB each)
+constexpr int kB64Group = 2;        // query blocks per workgroup of the 64-token path with a list
+constexpr int kB64Nbuf = 3;         // its LDS stages (16 KB each)
 constexpr float kRescaleTau = 8.f;  // log2 headroom before O is rescaled
 
 __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
@@ -187,10 +173,10 @@ __host__ __device__ inline int walk_bits(int nb) {
   return k;
 }
 __host__ __device__ inline int walk_words(int nb) {
-  return ROLA_B64_WALK ? ((1 << walk_bits(nb)) + 31) >> 5 : (nb + 31) >> 5;
+  return ((1 << walk_bits(nb)) + 31) >> 5;
 }
 __device__ __forceinline__ int walk_pos(int J, int kb) {
-  return ROLA_B64_WALK ? (int)(__brev((unsigned)J) >> (32 - kb)) : J;
+  return (int)(__brev((unsigned)J) >> (32 - kb));
 }
 
 // Start phase of a merged list (period > 0): the work queue hands group L out as entry i of its
@@ -1015,12 +1001,12 @@ hipError_t launch_simple(const Shape& s, const void* Qr, const void* Kr, const v
 }
 
 // Query blocks per workgroup when a workspace for the merged lists is given.
-int group_of(const Shape& s, int block) { return s.bf16 && block == 64 ? ROLA_B64_GROUP : 1; }
+int group_of(const Shape& s, int block) { return s.bf16 && block == 64 ? kB64Group : 1; }
 
 // Pairs are matched by overlap when G = 2 and one overlap workgroup's bitmaps fit in 64 KB of LDS
 // (up to 4064 query blocks); otherwise the pairs are adjacent blocks.
 bool pairing_on(int G, int nb) {
-  return ROLA_B64_PAIRING && G == 2 && kPairRows * pair_row_stride(nb) * 4 <= 65536 &&
+  return G == 2 && kPairRows * pair_row_stride(nb) * 4 <= 65536 &&
          (nb + 1) / 2 <= kMaxPairGroups;
 }
 
@@ -1050,7 +1036,7 @@ SparseWs sparse_ws_layout(const Shape& s, int block, int keep) {
 // for lists of stride - 1 entries and rank r; the dQ mode has no epilogue).
 template <int NBUF, bool DQ>
 int walk_period(int stride, int r) {
-  constexpr int G = ROLA_B64_GROUP;
+  constexpr int G = kB64Group;
   int n;
   if constexpr (DQ) {
     n = stride - 1 <= kTable ? queue_resident<64, G, NBUF, kTable, 0, true>()
@@ -1079,12 +1065,12 @@ struct Groups {
 template <bool DQ>
 hipError_t prepare_groups(const Shape& s, int keep, const int32_t* idx, void* ws, int r,
                           hipStream_t st, Groups& gr) {
-  constexpr int G = ROLA_B64_GROUP;
+  constexpr int G = kB64Group;
   const int nb = num_blocks(s.N, 64);
   const int ngroups = (nb + G - 1) / G, heads = s.B * s.H;
   const SparseWs lay = sparse_ws_layout(s, 64, keep);
   gr.stride = G * keep + 1;
-  gr.queue = ROLA_B64_QUEUE ? (int*)ws : nullptr;
+  gr.queue = (int*)ws;
   gr.pairs = lay.pair_bytes ? (int32_t*)((char*)ws + lay.queue_bytes) : nullptr;
   gr.lists = (int32_t*)((char*)ws + lay.queue_bytes + lay.pair_bytes);
   if (gr.pairs) {
@@ -1095,7 +1081,7 @@ hipError_t prepare_groups(const Shape& s, int keep, const int32_t* idx, void* ws
     hipLaunchKernelGGL(pair_greedy_kernel, dim3(heads), dim3(64), 0, st, nb, ngroups, nchunks,
                        (const uint8_t*)gr.lists, gr.pairs);
   }
-  const int period = gr.queue ? walk_period<DQ ? 3 : ROLA_B64_NBUF, DQ>(gr.stride, r) : 0;
+  const int period = gr.queue ? walk_period<DQ ? 3 : kB64Nbuf, DQ>(gr.stride, r) : 0;
   hipLaunchKernelGGL(group_union_kernel<G>, dim3(ngroups * heads), dim3(256),
                      (G * walk_words(nb) + 256) * sizeof(uint32_t), st, nb, keep, ngroups, gr.stride,
                      idx, (const int32_t*)gr.pairs, gr.lists, gr.queue, period);
@@ -1118,7 +1104,7 @@ size_t fuse_workspace_bytes(const Shape& s, int r) {
 bool fuse_supported(const Shape& s, int r) { return s.bf16 && s.d == 128 && r >= 16 && r <= 64; }
 
 bool dq_supported(const Shape& s, int block) {
-  return s.bf16 && s.d == 128 && block == 64 && ROLA_B64_GROUP == 2;
+  return s.bf16 && s.d == 128 && block == 64;
 }
 
 hipError_t launch_sparse_dq(const Shape& s, const void* Qr, const void* Kr, const void* V, int keep,
@@ -1156,13 +1142,13 @@ hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, co
   if (s.bf16) {
     const int nb = num_blocks(s.N, block);
     if (block == 64) {
-      constexpr int G = ROLA_B64_GROUP;
+      constexpr int G = kB64Group;
       if (!idx) return launch_bf16<64, 2, 3>(s, Qr, Kr, V, nullptr, nb, 0, scale, Os, st, nullptr, fp);
       if (ws && G > 1) {
         Groups gr;
         const hipError_t e = prepare_groups<false>(s, keep, idx, ws, lf ? lf->r : 0, st, gr);
         if (e != hipSuccess) return e;
-        return launch_bf16<64, G, ROLA_B64_NBUF>(s, Qr, Kr, V, gr.lists, 0, gr.stride, scale, Os, st,
+        return launch_bf16<64, G, kB64Nbuf>(s, Qr, Kr, V, gr.lists, 0, gr.stride, scale, Os, st,
                                                  gr.pairs, fp, gr.queue);
       }
       return launch_bf16<64, 1, 3>(s, Qr, Kr, V, idx, keep, keep, scale, Os, st, nullptr, fp);

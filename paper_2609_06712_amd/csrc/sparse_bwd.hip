@@ -239,14 +239,9 @@ __global__ __launch_bounds__(BLK * 2, 2) void sparse_dq_kernel(
 }
 
 // ---- dK, dV: one workgroup per (b, h, key block), BLK/32 waves of 32 keys --------------------------
-#ifndef ROLA_DKV_NBUF
-#define ROLA_DKV_NBUF 2  // LDS stages (34 KB each) of sparse_dkv_kernel
-#endif
-#ifndef ROLA_DKV_WAVES_PER_EU
-#define ROLA_DKV_WAVES_PER_EU 1  // waves per SIMD the register budget of sparse_dkv_kernel targets
-#endif
+constexpr int kDkvNbuf = 2;  // LDS stages (34 KB each) of sparse_dkv_kernel; one wave per SIMD
 template <int BLK, int NBUF>
-__global__ __launch_bounds__(BLK * 2) __attribute__((amdgpu_waves_per_eu(ROLA_DKV_WAVES_PER_EU)))
+__global__ __launch_bounds__(BLK * 2) __attribute__((amdgpu_waves_per_eu(1)))
 void sparse_dkv_kernel(
     int N, int nb, int total, const int32_t* __restrict__ rev, float scale_log2, float scale,
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
@@ -451,7 +446,7 @@ hipError_t launch_bwd(const Shape& s, const void* Qr, const void* Kr, const void
                        idx, keep, sl, scale, (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V,
                        (const bf16*)dOs, (const float2*)lseD, dQ);
   }
-  hipLaunchKernelGGL((sparse_dkv_kernel<BLK, ROLA_DKV_NBUF>), dim3(total), dim3(BLK * 2), 0, st, s.N, nb, total,
+  hipLaunchKernelGGL((sparse_dkv_kernel<BLK, kDkvNbuf>), dim3(total), dim3(BLK * 2), 0, st, s.N, nb, total,
                      (const int32_t*)rev, sl, scale, (const bf16*)Qr, (const bf16*)Kr,
                      (const bf16*)V, (const bf16*)dOs, (const float2*)lseD, dK, dV);
   return hipGetLastError();
