@@ -1,15 +1,19 @@
 """Benchmark of one RoLA attention layer (sparse + rotary low-rank branches) on one MI355X.
 
-One step = the whole hot path over one batch of synthetic input already resident in HBM:
-block selection -> block-sparse attention -> low-rank summary -> fused low-rank readout + gated combine,
-each a call of the C ABI on one HIP stream. Workload: the Wan2.1-14B-shaped 720p layer
+One step = the whole hot path over one batch of synthetic input already resident in HBM, as C-ABI
+calls on two HIP streams: on the main stream the block means of Q^r and K^r, the block scores and
+top-k, and the attention's pairing and list merge (rola_sparse_plan); on a second stream, once the
+pooling is done, the low-rank summary; after the two join, the block-sparse attention with the
+low-rank readout and the gated combine in its epilogue. Workload: the Wan2.1-14B-shaped 720p layer
 (B1 H40 d128, 21x45x80 grid = 75600 tokens, block 64, 90 % sparsity -> 118 of 1182 key blocks, r 32,
-bf16). The backbone's own steps (rotary tables, Q^r = R(Q^n), K^r = R(K^n)) run once, untimed.
+bf16). The backbone's own steps (rotary tables, Q^r = R(Q^n), K^r = R(K^n)) are the step's input;
+the same layer starting from Q^n, K^n (rotation fused into the pooling passes) is timed beside it.
 
 Prints one JSON line: effective TFLOP/s of the layer (sparse FLOPs actually performed + the paper's
-low-rank count 8 B H N d_h r, over the layer time), ms per layer, the roofline of the dominant kernel
-(block-sparse attention against the bf16 MFMA peak, timed with HIP events on its stream) and the CPU
-oracle timed on a bounded sample of the same layer.
+low-rank count 8 B H N d_h r, over the layer time), ms per layer (wall clock over the timed steps,
+and the median / p10 / p90 of the per-step spans), the roofline of the dominant kernel (block-sparse
+attention against the bf16 MFMA peak, timed with HIP events on its stream), the layer-level roofline
+fraction, and the CPU oracle timed on a bounded sample of the same layer.
 """
 
 from __future__ import annotations
@@ -75,44 +79,66 @@ def summary_bytes(w) -> float:
     return float(w.B * w.H * w.N * 2 * w.d_h * 2 + 2 * w.N * (w.r // 2) * 4)
 
 
-def cpu_baseline(w, inp_cpu_head0: dict, budget_s: float) -> dict:
-    """The fp64 oracle, as it stands, on head 0: the whole low-rank branch (summary over every token)
-    plus as many query blocks of selection + sparse attention + readout + combine as fit the budget."""
-    import math
-    import oracle as O
-    from threadpoolctl import threadpool_info
+CPU_HEADS = (0, 13, 26, 39)
 
-    f64 = synth.to_f64(inp_cpu_head0)
-    qn, kn, v = f64["Qn"][0, 0], f64["Kn"][0, 0], f64["V"][0, 0]
+
+def _oracle_head_worker(job):
+    """One (b, h) of the layer through the oracle (every step of forward_head), BLAS on one thread."""
+    import math
+    from threadpoolctl import threadpool_limits
+    import oracle as O
+    path, h, grid, split, base, block, sparsity, dtype = job
+    d = np.load(path)
+    with threadpool_limits(1):
+        t0 = time.perf_counter()
+        cos, sin = O.rope_tables(*grid, split, base)
+        r = O.forward_head(d["Qn"], d["Kn"], d["V"], d["Pq"], d["Pk"], d["logits"], cos, sin,
+                           block=block, sparsity=sparsity, dtype=dtype)
+        dt = time.perf_counter() - t0
+    N, dh = d["Qn"].shape
+    sizes = np.full(O.num_blocks(N, block), block, dtype=np.float64)
+    sizes[-1] = N - (len(sizes) - 1) * block
+    f_sparse = 4.0 * dh * float((sizes[r["idx"]].sum(axis=1) * sizes).sum())
+    f_lowrank = 8.0 * N * dh * d["Pq"].shape[0]
+    return h, dt, f_sparse + f_lowrank, math.isfinite(float(np.abs(r["out"]).max()))
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(w, heads: dict, tmpdir: str) -> dict:
+    """The fp64 oracle, as it stands, on the heads CPU_HEADS of the layer: one process per head
+    (spawned, BLAS on one thread each), every step of the module over the whole sequence. Reports the
+    oracle's throughput over the sample, the mean time per head and the layer time that implies
+    (per head x H, labelled extrapolated)."""
+    import multiprocessing as mp
+    jobs = []
+    for h, arrs in heads.items():
+        path = os.path.join(tmpdir, f"oracle_head{h}.npz")
+        np.savez(path, **arrs)
+        jobs.append((path, h, w.grid, w.split, w.base, w.block, w.sparsity, w.dtype))
     t0 = time.perf_counter()
-    cos, sin = O.rope_tables(*w.grid, w.split, w.base)
-    qr = O.round_to(O.rotate(qn, cos, sin), w.dtype)
-    kr = O.round_to(O.rotate(kn, cos, sin), w.dtype)
-    nb = O.num_blocks(w.N, w.block)
-    keep = O.keep_blocks(nb, w.sparsity)
-    qbar, kbar = O.pool_blocks(qr, w.block), O.pool_blocks(kr, w.block)
-    C, _ = O.lowrank_summary(kn, v, f64["Pk"][0], cos, sin)
-    flops = 4.0 * w.N * w.d_h * w.r                       # summary: projection + k~ v^T
-    scale = 1.0 / math.sqrt(w.d_h)
-    n_blocks = 0
-    for I in range(nb):
-        if time.perf_counter() - t0 > budget_s:
-            break
-        idx = np.zeros((nb, keep), dtype=np.int64)
-        idx[I] = O.select_blocks(O.block_scores(qbar[I:I + 1], kbar), keep)[0]
-        rows = np.arange(I * w.block, min(w.N, (I + 1) * w.block))
-        o_s = O.sparse_attention_rows(qr, kr, v, idx, w.block, scale, rows)
-        u = O.lowrank_features(qn[rows], f64["Pq"][0], cos[rows], sin[rows]) @ C
-        O.combine(o_s, O.rms_normalize(u, 1e-6), f64["logits"][0, rows], 1e-6)
-        nkeys = sum(min(w.N, (J + 1) * w.block) - J * w.block for J in idx[I])
-        flops += 4.0 * w.d_h * len(rows) * nkeys + 4.0 * len(rows) * w.d_h * w.r
-        n_blocks += 1
-    dt = time.perf_counter() - t0
-    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"head 0 of {w.H}: full low-rank summary over {w.N} tokens + selection, sparse "
-                      f"attention, readout and combine for query blocks 0..{n_blocks - 1} of {nb}; "
-                      f"{dt:.1f} s on {len(os.sched_getaffinity(0))} host cores"}
+    with mp.get_context("spawn").Pool(len(jobs)) as pool:
+        res = pool.map(_oracle_head_worker, jobs)
+    wall = time.perf_counter() - t0
+    assert all(ok for *_, ok in res)
+    flops = sum(f for _, _, f, _ in res)
+    per_head = float(np.mean([dt for _, dt, _, _ in res]))
+    return {"value": flops / wall / 1e12, "unit": "TFLOP/s", "cores": len(jobs), "kind": "oracle",
+            "sample": f"heads {list(heads)} of {w.H}, every step of the layer over all {w.N} tokens, "
+                      f"one spawned process per head with BLAS on one thread; {wall:.1f} s wall",
+            "cpu_model": cpu_model(), "host_cores_available": len(os.sched_getaffinity(0)),
+            "s_per_head": round(per_head, 2),
+            "layer_s_extrapolated": round(per_head * w.H * w.B, 1),
+            "layer_s_extrapolated_note": "mean time per (b, h) on one core x B*H: extrapolated"}
 
 
 def time_call(fn, reps: int, cold=None):
@@ -355,7 +381,6 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", action="store_true",
                     help="print the measurement sweeps (1.3B layer, low-rank N x r, sparse S x block) "
@@ -407,23 +432,53 @@ def main():
     out = torch.empty_like(inp["Qn"])
     C = torch.empty((w.B, w.H, w.r, w.d_h), dtype=torch.float32, device=dev)
     z = torch.empty((w.B, w.H, w.r), dtype=torch.float32, device=dev)
-    stream = torch.cuda.current_stream()
-    # the layer: selection, low-rank summary, then the sparse attention with the low-rank readout
-    # and the gated combine in its epilogue (O^s and O^lr never reach memory)
-    names = ["select", "summary", "sparse_readout_combine"]
+    main_st = torch.cuda.current_stream()
+    side_st = torch.cuda.Stream(device=dev)  # default priority
+    qbar = torch.empty((w.B, w.H, nb, w.d_h), dtype=torch.float32, device=dev)
+    kbar = torch.empty_like(qbar)
+    ws_pool = torch.empty(R.LIB.rola_select_pooled_workspace_bytes(ctypes.byref(prob), w.block),
+                          dtype=torch.uint8, device=dev)
+    # The layer (steps a1-a5 of the hot path; the backbone's rotation is the input) on two streams.
+    # Main stream: the block means of Q^r and K^r, the block scores and top-k, the attention's
+    # pairing and list merge; side stream, forked once the pooling (the HBM-bound part of the
+    # selection) is done: the low-rank summary, beside the compute-bound scores and top-k and the
+    # pairing (whose greedy pass keeps one wave per head busy). After both: the block-sparse
+    # attention with the low-rank readout and the gated combine in its epilogue (O^s and O^lr
+    # never reach memory). rotate=True starts from Q^n, K^n: the rotating pooling passes write Q^r
+    # and K^r (Algorithm step 3 fused with the pooling).
+    names = ["pool", "select", "plan", "attention_readout_combine"]
 
-    def step(ev=None):
+    def step(ev=None, sev=None, rotate=False):
         def mark(i):
             if ev is not None:
-                ev[i].record(stream)
+                ev[i].record(main_st)
+        fork, join = torch.cuda.Event(), torch.cuda.Event()
         mark(0)
-        R.rola_block_select(qr, kr, g, w.block, w.sparsity, out=idx, ws=ws_sel)
+        if rotate:
+            R.rola_rope_pool(inp["Qn"], cos, sin, g, w.block, xr=qr, xbar=qbar)
+            R.rola_rope_pool(inp["Kn"], cos, sin, g, w.block, xr=kr, xbar=kbar)
+        else:
+            R.rola_rope_pool(qr, None, None, g, w.block, xbar=qbar)
+            R.rola_rope_pool(kr, None, None, g, w.block, xbar=kbar)
         mark(1)
-        R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], w.r, cos, sin, g, C=C, z=z, ws=ws_sum)
+        fork.record(main_st)
+        side_st.wait_event(fork)
+        if sev is not None:
+            sev[0].record(side_st)
+        R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], w.r, cos, sin, g, C=C, z=z, ws=ws_sum,
+                               stream=side_st)
+        if sev is not None:
+            sev[1].record(side_st)
+        join.record(side_st)
+        R.rola_block_select_pooled(qbar, kbar, kr, g, w.block, w.sparsity, out=idx, ws=ws_pool)
         mark(2)
-        R.rola_sparse_attn_combine(qr, kr, inp["V"], g, w.block, w.sparsity, idx, inp["Qn"],
-                                   inp["Pq"], w.r, cos, sin, C, inp["logits"], out=out, ws=ws_sp)
+        R.rola_sparse_plan(idx, kr, g, w.block, w.sparsity, w.r, ws_sp)
+        main_st.wait_event(join)
         mark(3)
+        R.rola_sparse_attn_combine_planned(qr, kr, inp["V"], g, w.block, w.sparsity, idx, inp["Qn"],
+                                           inp["Pq"], w.r, cos, sin, C, inp["logits"], ws_sp,
+                                           out=out)
+        mark(4)
 
     if args.calibration_copy:  # a plain copy of known size, for scaling FETCH_SIZE / WRITE_SIZE
         scratch = torch.empty_like(inp["V"])
@@ -433,27 +488,58 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
-              for _ in range(args.steps)]
+    ev_t = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    events = [[ev_t() for _ in range(len(names) + 1)] for _ in range(args.steps)]
+    side_events = [[ev_t(), ev_t()] for _ in range(args.steps)]
     print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
-        step(events[k])
+        step(events[k], side_events[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     per_kernel = {n: [] for n in names}
+    spans = []
     for ev in events:
         for i, n in enumerate(names):
             per_kernel[n].append(ev[i].elapsed_time(ev[i + 1]))
+        spans.append(ev[0].elapsed_time(ev[-1]))
+    per_kernel["summary (side stream)"] = [a.elapsed_time(b) for a, b in side_events]
     kern_ms = {n: float(np.mean(v)) for n, v in per_kernel.items()}
     ms = wall * 1e3 / args.steps
+
+    # the summary alone on one stream (its bandwidth without the selection running beside it)
+    sum_ms = time_call(lambda: R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], w.r, cos, sin,
+                                                      g, C=C, z=z, ws=ws_sum), 20)[0]
+    # the layer as one stream of the three plain calls (selection, summary, attention with its
+    # epilogue), and the same preceded by the backbone's rotation of Q^n and K^n; the two-stream
+    # layer starting from Q^n, K^n (rotation fused with the pooling)
+    def one_stream():
+        R.rola_block_select(qr, kr, g, w.block, w.sparsity, out=idx, ws=ws_sel)
+        R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], w.r, cos, sin, g, C=C, z=z, ws=ws_sum)
+        R.rola_sparse_attn_combine(qr, kr, inp["V"], g, w.block, w.sparsity, idx, inp["Qn"],
+                                   inp["Pq"], w.r, cos, sin, C, inp["logits"], out=out, ws=ws_sp)
+
+    def one_stream_rotating():
+        R.rola_rope_apply(inp["Qn"], cos, sin, g, out=qr)
+        R.rola_rope_apply(inp["Kn"], cos, sin, g, out=kr)
+        one_stream()
+    one_ms = time_call(one_stream, 10)
+    one_rot_ms = time_call(one_stream_rotating, 10)
+    rot_ms = time_call(lambda: step(rotate=True), 10)
 
     f_sparse = sparse_flops_performed(idx, w.N, w.block, w.d_h)
     f_lowrank = 8.0 * w.B * w.H * w.N * w.d_h * w.r
     eff = (f_sparse + f_lowrank) / (ms * 1e-3) / 1e12
-    achieved = f_sparse / (kern_ms["sparse_readout_combine"] * 1e-3) / 1e12
-    sum_gbs = summary_bytes(w) / (kern_ms["summary"] * 1e-3) / 1e9
+    attn_ms = kern_ms["attention_readout_combine"]
+    achieved = f_sparse / (attn_ms * 1e-3) / 1e12
+    sum_gbs = summary_bytes(w) / (sum_ms * 1e-3) / 1e9
+    tensor = w.B * w.H * w.N * w.d_h * 2
+    # HBM bytes the streaming steps must move: the pooling reads Q^r and K^r; the summary reads K^n
+    # and V (+ its table columns); the epilogue reads Q^n and writes O
+    layer_bytes = 2 * tensor + summary_bytes(w) + 2 * tensor
+    layer_floor_ms = (f_sparse / (PEAK_BF16_TFLOPS * 1e12) + layer_bytes / (PEAK_HBM_GBS * 1e9)) * 1e3
+    med, p10, p90 = (float(np.percentile(spans, q)) for q in (50, 10, 90))
 
     res = {
         "metric": METRIC, "value": round(eff, 2), "unit": "TFLOP/s", "n_gpus": 1,
@@ -462,12 +548,30 @@ def main():
         "data": "synthetic (seeded smooth-field-plus-noise Q/K/V, random P_q/P_k, gate logits)",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "N": w.N, "grid": list(g), "d_h": w.d_h,
                    "block": w.block, "sparsity": w.sparsity, "keep": keep, "r": w.r,
-                   "parallelism": "single GPU"},
-        "roofline": {"bound": "mfma", "kernel": "rola_sparse_attn_combine (block-sparse attention "
-                     "with the low-rank readout and gated combine in its epilogue)",
+                   "parallelism": "single GPU", "streams": 2,
+                   "step": "block selection, sparse attention, low-rank summary and readout, gated "
+                           "combine from Q^r, K^r, Q^n, K^n, V (the backbone's rotation untimed)"},
+        "ms_per_step_spans": {"median": round(med, 4), "p10": round(p10, 4), "p90": round(p90, 4)},
+        "ms_per_step_one_stream": {
+            "median": round(one_ms[0], 4), "p10": round(one_ms[1], 4), "p90": round(one_ms[2], 4),
+            "note": "rola_block_select, rola_lowrank_summary, rola_sparse_attn_combine on one stream"},
+        "ms_per_step_from_qn_kn": {
+            "two_streams_rotating_pooling": round(rot_ms[0], 4),
+            "one_stream_rope_apply_then_layer": round(one_rot_ms[0], 4),
+            "note": "medians; the layer including the backbone's rotation R(Q^n), R(K^n) (Algorithm "
+                    "step 3): fused with the pooling passes, or as two rola_rope_apply calls"},
+        "roofline": {"bound": "mfma", "kernel": "sparse_attn_kernel via "
+                     "rola_sparse_attn_combine_planned (block-sparse attention with the low-rank "
+                     "readout and gated combine in its epilogue; the call also runs the 4 us "
+                     "C-fragment kernel)",
                      "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": measured_traffic()},
-        "summary_roofline": {"bound": "hbm", "kernels": "rola_lowrank_summary",
+        "layer_roofline": {"frac": round(layer_floor_ms / ms, 4),
+                           "floor_ms": round(layer_floor_ms, 4),
+                           "definition": "(F_sparse / 2.5 PFLOP/s + streamed bytes / 8 TB/s) / "
+                                         "ms_per_step",
+                           "streamed_bytes": layer_bytes},
+        "summary_roofline": {"bound": "hbm", "kernels": "rola_lowrank_summary (alone, one stream)",
                              "achieved": round(sum_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                              "frac": round(sum_gbs / PEAK_HBM_GBS, 4)},
         "kernels_ms": {k: round(v, 4) for k, v in kern_ms.items()},
@@ -475,10 +579,16 @@ def main():
                   "sparse_paper_formula": 4.0 * w.B * w.H * w.N ** 2 * (1 - w.sparsity) * w.d_h},
     }
     if not args.no_cpu_baseline:
-        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
-        head0 = {k: inp[k][:, :1].cpu() for k in ("Qn", "Kn", "V")}
-        head0.update(Pq=inp["Pq"][:1].cpu(), Pk=inp["Pk"][:1].cpu(), logits=inp["logits"].cpu())
-        res["cpu_baseline"] = cpu_baseline(w, head0, args.cpu_budget)
+        import tempfile
+        print("[bench] timing the CPU oracle on 4 heads", file=sys.stderr, flush=True)
+        heads = {}
+        for h in CPU_HEADS:
+            heads[h] = {k: inp[k][0, h].double().cpu().numpy() for k in ("Qn", "Kn", "V")}
+            heads[h].update(Pq=inp["Pq"][h].double().cpu().numpy(),
+                            Pk=inp["Pk"][h].double().cpu().numpy(),
+                            logits=inp["logits"][0].double().cpu().numpy())
+        with tempfile.TemporaryDirectory() as tmp:
+            res["cpu_baseline"] = cpu_baseline(w, heads, tmp)
     print(json.dumps(res), flush=True)
 
 

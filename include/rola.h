@@ -117,6 +117,19 @@ rola_status rola_rope_backward_accumulate(const rola_problem* p, const float* dY
                                           int32_t rope_ld, int32_t rotate, float* dX,
                                           hipStream_t stream);
 
+/* The backbone rotation and the block pooling of the selection in one pass (Algorithm steps 3-4):
+ * for every [d_h] row x_n of X (Q^n or K^n, [B, H, N, d_h]), R(p) x_n is rounded to dtype exactly
+ * as rola_rope_apply rounds it and written to Xr unless Xr is NULL, and Xbar[b, h, I, :] (fp32
+ * [B, H, n_blocks, d_h]) receives the mean of the rotated, rounded rows of block I over its valid
+ * tokens: bitwise the means rola_block_select computes from Xr. Xr and Xbar must not overlap X or
+ * each other. Tables as in rola_rope_apply (rope_ld >= d_h/2). Built for d_h = 128
+ * (ROLA_ERR_UNSUPPORTED otherwise). With both tables NULL, X is taken as already rotated (Q^r or
+ * K^r): only the means are computed (rope_ld is ignored, Xr must be NULL), on any supported d_h,
+ * bitwise those of rola_block_select. */
+rola_status rola_rope_pool(const rola_problem* p, const void* X, const float* cos_tab,
+                           const float* sin_tab, int32_t rope_ld, int32_t block, void* Xr,
+                           float* Xbar, hipStream_t stream);
+
 /* ---- sparse branch (Algorithm step 4; Sec. 4 opening: standard block-sparse attention) -------- */
 
 /* Top-k key blocks for every query block. For each (b, h): q_bar_I, k_bar_J = means of Q^r, K^r over
@@ -129,6 +142,13 @@ rola_status rola_rope_backward_accumulate(const rola_problem* p, const float* dY
 rola_status rola_block_select(const rola_problem* p, const void* Qr, const void* Kr, int32_t block,
                               double sparsity, int32_t* blk_idx, void* ws, size_t ws_bytes,
                               hipStream_t stream);
+
+/* rola_block_select from the block means (rola_rope_pool of Q^n and K^n): the same scores, top-k
+ * and lists, bitwise. ws: rola_select_pooled_workspace_bytes(p, block) bytes (the score matrix). */
+size_t rola_select_pooled_workspace_bytes(const rola_problem* p, int32_t block);
+rola_status rola_block_select_pooled(const rola_problem* p, const float* Qbar, const float* Kbar,
+                                     int32_t block, double sparsity, int32_t* blk_idx, void* ws,
+                                     size_t ws_bytes, hipStream_t stream);
 
 /* Block-sparse attention: for a query token p in block I, O^s_p = sum softmax(q^r_p . k^r_q * scale)
  * v_q over the valid key tokens q of the blocks blk_idx[b, h, I, :] (keep = rola_keep_blocks(
@@ -161,7 +181,12 @@ rola_status rola_sparse_attn(const rola_problem* p, const void* Qr, const void* 
  * rola_sparse_attn plus the C fragments of the epilogue). On the bf16 path with r in {16, 32, 64}
  * the readout and combine run in the attention kernel's epilogue; otherwise the attention and the
  * fused readout + combine run one after the other. Results agree with the separate calls to the
- * module's tolerance (the epilogue combines O^s before its bf16 rounding). */
+ * module's tolerance (the epilogue combines O^s before its bf16 rounding).
+ * Qr may be NULL on the fused path (bf16, r 16-64): the queries are then R(Q^n), rotated from Qn
+ * and the tables (rope_ld >= d_h/2 then) in the kernel's prologue and rounded exactly as
+ * rola_rope_apply rounds them, so Q^r need not exist in memory; the results are bitwise those with
+ * Qr = rola_rope_apply(Qn). Elsewhere Qr = NULL is ROLA_ERR_UNSUPPORTED. The same holds for the
+ * _planned form below. */
 size_t rola_sparse_combine_workspace_bytes(const rola_problem* p, int32_t block, double sparsity,
                                            int32_t r);
 rola_status rola_sparse_attn_combine(const rola_problem* p, const void* Qr, const void* Kr,
@@ -171,6 +196,24 @@ rola_status rola_sparse_attn_combine(const rola_problem* p, const void* Qr, cons
                                      const float* sin_tab, int32_t rope_ld, const float* C,
                                      float eps_lr, const float* gate_logits, float eps, void* O,
                                      void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* The same call in two parts, so that other work can run between them (e.g. the low-rank summary,
+ * which the epilogue needs, on a second stream while the pairs are planned). rola_sparse_plan
+ * pairs the query blocks and merges their lists into ws (the workspace of
+ * rola_sparse_attn_combine for the same p, block, sparsity and r, which it must also be given);
+ * rola_sparse_attn_combine_planned then runs the attention with its epilogue on that plan. The two
+ * must see the same blk_idx, and no other call may use ws in between. On paths without a plan
+ * (128-token blocks, fp32) rola_sparse_plan launches nothing. Results are bitwise those of
+ * rola_sparse_attn_combine. */
+rola_status rola_sparse_plan(const rola_problem* p, int32_t block, double sparsity,
+                             const int32_t* blk_idx, int32_t r, void* ws, size_t ws_bytes,
+                             hipStream_t stream);
+rola_status rola_sparse_attn_combine_planned(
+    const rola_problem* p, const void* Qr, const void* Kr, const void* V, int32_t block,
+    double sparsity, const int32_t* blk_idx, float softmax_scale, const void* Qn, const void* Pq,
+    int32_t r, const float* cos_tab, const float* sin_tab, int32_t rope_ld, const float* C,
+    float eps_lr, const float* gate_logits, float eps, void* O, void* ws, size_t ws_bytes,
+    hipStream_t stream);
 
 /* ---- backward of the sparse branch (fine-tuning, Sec. 4.5; Algorithm step 4) ------------------
  * rola_sparse_attn_lse is rola_sparse_attn (same workspace rule: ws NULL or ws_bytes >=

@@ -88,6 +88,14 @@ __device__ __forceinline__ float rows_sum(float x) {
   return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
+// Rotation of one interleaved pair (a, b) by the angle with cosine c and sine s (3D RoPE, turn by
+// +angle): x = a c - b s, y = a s + b c, with explicit fused multiply-adds so that every kernel that
+// rotates (the backbone rotation, the rotating pooling, the attention's query prologue) rounds alike.
+__device__ __forceinline__ void rope_pair(float a, float b, float c, float s, float& x, float& y) {
+  x = fmaf(a, c, -(b * s));
+  y = fmaf(a, s, b * c);
+}
+
 // SiLU and the logistic gate with a hardware reciprocal (1 ulp) instead of an IEEE divide.
 __device__ __forceinline__ float sigmoid(float x) { return __builtin_amdgcn_rcpf(1.0f + __expf(-x)); }
 __device__ __forceinline__ float silu(float x) { return x * sigmoid(x); }

@@ -29,6 +29,19 @@ hipError_t launch_rope_grad(const Shape& s, const float* dY, const float* cos_ta
 size_t select_workspace_bytes(const Shape& s, int block);
 hipError_t launch_block_select(const Shape& s, const void* Qr, const void* Kr, int block, int keep,
                                int32_t* idx, void* ws, hipStream_t st);
+// Means of the rotated rows per block from Q^n or K^n and the tables (fp32 [B, H, nb, d]); the
+// rotated rows also go to Xr unless it is null. Built for d = 128 (rope_pool_supported).
+bool rope_pool_supported(const Shape& s, int block);
+// Block means of an already rotated X (the pooling of launch_block_select alone).
+hipError_t launch_block_pool(const Shape& s, const void* X, int block, float* means,
+                             hipStream_t st);
+hipError_t launch_rope_pool(const Shape& s, const void* X, const float* cos_tab,
+                            const float* sin_tab, int ld, int block, void* Xr, float* means,
+                            hipStream_t st);
+// Scores and top-k from given means; ws: select_pooled_workspace_bytes(s, block).
+size_t select_pooled_workspace_bytes(const Shape& s, int block);
+hipError_t launch_select_pooled(const Shape& s, const float* qbar, const float* kbar, int block,
+                                int keep, int32_t* idx, void* ws, hipStream_t st);
 
 // sparse_attn.hip  (idx == nullptr: dense, every key block in order; keep must equal n_blocks)
 // ws: sparse_workspace_bytes(s, block, keep) bytes, or nullptr (then no K/V loads are shared
@@ -52,10 +65,18 @@ bool fuse_supported(const Shape& s, int r);
 size_t fuse_workspace_bytes(const Shape& s, int r);
 // lse (optional, bf16 path): [B, H, N] fp32, log2 of each query's softmax denominator of the
 // log2e-scaled scores, i.e. P = exp2(S * scale * log2e - lse).
+// planned: ws already holds the groups of these lists (launch_sparse_plan with the same r), so the
+// pairing and list merge are not launched again.
 hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, const void* V,
                               int block, int keep, const int32_t* idx, float scale, void* Os,
                               void* ws, hipStream_t st, const LowrankFuse* lf = nullptr,
-                              void* fuse_ws = nullptr, float* lse = nullptr);
+                              void* fuse_ws = nullptr, float* lse = nullptr, bool planned = false);
+// Whether the path of (s, block) uses a plan (pairs, merged lists, queue counters in ws).
+bool plan_used(const Shape& s, int block);
+// The pairing and list merge of the 64-token bf16 path into ws (sparse_workspace_bytes), for the
+// walk period of the kernel variant with fused rank r (0: plain attention). No-op elsewhere.
+hipError_t launch_sparse_plan(const Shape& s, int keep, const int32_t* idx, int r, void* ws,
+                              hipStream_t st);
 
 // lowrank_bwd.hip: gradients of the low-rank branch and the gated fusion (bf16, d 128, r <= 64, SiLU
 // with the rotation outside). dOs bf16; the other gradients fp32; dP_q, dP_k summed over the batch,

@@ -128,7 +128,7 @@ rola_status check_out(const rola::Shape& s, const void* out, std::initializer_li
                       const void* same, const char* fn) {
   const size_t n = act_bytes(s);
   for (const Named& in : ins) {
-    if (in.p == same && out == same) continue;
+    if (in.p == nullptr || (in.p == same && out == same)) continue;
     if (overlap(out, n, in.p, n))
       return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: the output overlaps %s", fn, in.name);
   }
@@ -140,6 +140,66 @@ rola_status check_out(const rola::Shape& s, const void* out, std::initializer_li
     rola_status _s = (expr);          \
     if (_s != ROLA_OK) return _s;     \
   } while (0)
+
+// Arguments of the attention + readout + combine calls, checked before anything is launched.
+// ws == nullptr: the call brings no workspace (the allocation-free form checks its static scratch).
+rola_status check_combine(const rola_problem* p, const void* Qr, const void* Kr, const void* V,
+                          int32_t block, double sparsity, const int32_t* blk_idx,
+                          float softmax_scale, const void* Qn, const void* Pq, int32_t r,
+                          const float* cos_tab, const float* sin_tab, int32_t rope_ld,
+                          const float* C, float eps_lr, const float* gate_logits, float eps,
+                          void* O, const char* fn, rola::Shape* s) {
+  TRY(check_problem(p, fn, s));
+  TRY(check_block(*s, block, fn));
+  TRY(check_sparsity(sparsity, fn));
+  TRY(check_rank(*s, r, fn));
+  const void* ptrs[] = {Kr, V, blk_idx, Qn, Pq, C, gate_logits, O};
+  const char* names[] = {"Kr", "V", "blk_idx", "Qn", "Pq", "C", "gate_logits", "O"};
+  for (int i = 0; i < 8; ++i)
+    if (!aligned(ptrs[i]))
+      return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: pointer '%s' is null or not 16-byte aligned", fn,
+                  names[i]);
+  if (Qr == nullptr) {  // queries rotated from Q^n in the kernel's prologue
+    if (!rola::fuse_supported(*s, r))
+      return fail(ROLA_ERR_UNSUPPORTED, "%s: Qr = NULL needs the fused bf16 path (r 16-64)", fn);
+    TRY(check_tables(cos_tab, sin_tab, rope_ld, s->d / 2, fn));
+  } else if (!aligned(Qr)) {
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: pointer 'Qr' is not 16-byte aligned", fn);
+  }
+  TRY(check_tables(cos_tab, sin_tab, rope_ld, r / 2, fn));
+  if (!(softmax_scale > 0.f) || !isfinite(softmax_scale))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: softmax_scale must be finite and positive", fn);
+  if (!(eps_lr >= 0.f) || !isfinite(eps_lr) || !(eps >= 0.f) || !isfinite(eps))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: eps values must be finite and >= 0", fn);
+  TRY(check_out(*s, O, {{Qr, "Qr"}, {Kr, "Kr"}, {V, "V"}, {Qn, "Qn"}}, nullptr, fn));
+  return ROLA_OK;
+}
+
+rola_status run_combine(const rola::Shape& s, const void* Qr, const void* Kr, const void* V,
+                        int32_t block, int keep, const int32_t* blk_idx, float softmax_scale,
+                        const void* Qn, const void* Pq, int32_t r, const float* cos_tab,
+                        const float* sin_tab, int32_t rope_ld, const float* C, float eps_lr,
+                        const float* gate_logits, float eps, void* O, void* ws, bool planned,
+                        hipStream_t stream, const char* fn) {
+  const size_t sp = rola::sparse_workspace_bytes(s, block, keep);
+  void* fuse_ws = static_cast<char*>(ws) + ((sp + 255) & ~(size_t)255);
+  if (rola::fuse_supported(s, r)) {
+    const rola::LowrankFuse lf{Qn, Pq, r, cos_tab, sin_tab, rope_ld, C, eps_lr, gate_logits, eps};
+    return hip_status(rola::launch_sparse_attn(s, Qr, Kr, V, block, keep, blk_idx, softmax_scale, O,
+                                               sp > 0 ? ws : nullptr, stream, &lf, fuse_ws, nullptr,
+                                               planned),
+                      fn);
+  }
+  // other shapes: the attention into O, then the readout and combine in place
+  hipError_t e = rola::launch_sparse_attn(s, Qr, Kr, V, block, keep, blk_idx, softmax_scale, O,
+                                          sp > 0 ? ws : nullptr, stream, nullptr, nullptr, nullptr,
+                                          planned);
+  if (e == hipSuccess)
+    e = rola::launch_lowrank_readout(s, Qn, Pq, r, cos_tab, sin_tab, rope_ld, 0, C, eps_lr, O,
+                                     gate_logits, eps, O, stream);
+  return hip_status(e, fn);
+}
+
 
 }  // namespace
 
@@ -223,6 +283,60 @@ rola_status rola_rope_backward_accumulate(const rola_problem* p, const float* dY
   if (overlap(dX, n, dY, n))
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: dX overlaps dY", __func__);
   return hip_status(rola::launch_rope_grad(s, dY, cos_tab, sin_tab, rope_ld, rotate != 0, dX, stream),
+                    __func__);
+}
+
+rola_status rola_rope_pool(const rola_problem* p, const void* X, const float* cos_tab,
+                           const float* sin_tab, int32_t rope_ld, int32_t block, void* Xr,
+                           float* Xbar, hipStream_t stream) {
+  rola::Shape s;
+  TRY(check_problem(p, __func__, &s));
+  TRY(check_block(s, block, __func__));
+  REQUIRE_PTR(X);
+  REQUIRE_PTR(Xbar);
+  if (Xr != nullptr && !aligned(Xr))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: Xr not 16-byte aligned", __func__);
+  const size_t nbar = (size_t)s.B * s.H * rola::num_blocks(s.N, block) * s.d * sizeof(float);
+  if (cos_tab == nullptr && sin_tab == nullptr) {  // X is already rotated: pooling only
+    if (Xr != nullptr)
+      return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: Xr must be NULL without tables", __func__);
+    if (overlap(Xbar, nbar, X, act_bytes(s)))
+      return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: Xbar overlaps X", __func__);
+    return hip_status(rola::launch_block_pool(s, X, block, Xbar, stream), __func__);
+  }
+  TRY(check_tables(cos_tab, sin_tab, rope_ld, s.d / 2, __func__));
+  if (!rola::rope_pool_supported(s, block))
+    return fail(ROLA_ERR_UNSUPPORTED, "%s: built for d_h = 128", __func__);
+  if (Xr) TRY(check_out(s, Xr, {{X, "X"}}, nullptr, __func__));
+  if (overlap(Xbar, nbar, X, act_bytes(s)) || (Xr && overlap(Xbar, nbar, Xr, act_bytes(s))))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: Xbar overlaps X or Xr", __func__);
+  return hip_status(rola::launch_rope_pool(s, X, cos_tab, sin_tab, rope_ld, block, Xr, Xbar, stream),
+                    __func__);
+}
+
+size_t rola_select_pooled_workspace_bytes(const rola_problem* p, int32_t block) {
+  rola::Shape s;
+  if (check_problem(p, __func__, &s) != ROLA_OK || check_block(s, block, __func__) != ROLA_OK) return 0;
+  return rola::select_pooled_workspace_bytes(s, block);
+}
+
+rola_status rola_block_select_pooled(const rola_problem* p, const float* Qbar, const float* Kbar,
+                                     int32_t block, double sparsity, int32_t* blk_idx, void* ws,
+                                     size_t ws_bytes, hipStream_t stream) {
+  rola::Shape s;
+  TRY(check_problem(p, __func__, &s));
+  TRY(check_block(s, block, __func__));
+  TRY(check_sparsity(sparsity, __func__));
+  REQUIRE_PTR(Qbar);
+  REQUIRE_PTR(Kbar);
+  REQUIRE_PTR(blk_idx);
+  REQUIRE_PTR(ws);
+  const size_t need = rola::select_pooled_workspace_bytes(s, block);
+  if (ws_bytes < need)
+    return fail(ROLA_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", __func__, ws_bytes, need);
+  const int nb = rola::num_blocks(s.N, block);
+  const int keep = rola_keep_blocks(nb, sparsity);
+  return hip_status(rola::launch_select_pooled(s, Qbar, Kbar, block, keep, blk_idx, ws, stream),
                     __func__);
 }
 
@@ -383,6 +497,7 @@ size_t rola_sparse_combine_workspace_bytes(const rola_problem* p, int32_t block,
   return sp + std::max<size_t>(rola::fuse_workspace_bytes(s, r), 16);
 }
 
+
 rola_status rola_sparse_attn_combine(const rola_problem* p, const void* Qr, const void* Kr,
                                      const void* V, int32_t block, double sparsity,
                                      const int32_t* blk_idx, float softmax_scale, const void* Qn,
@@ -391,45 +506,53 @@ rola_status rola_sparse_attn_combine(const rola_problem* p, const void* Qr, cons
                                      float eps_lr, const float* gate_logits, float eps, void* O,
                                      void* ws, size_t ws_bytes, hipStream_t stream) {
   rola::Shape s;
-  TRY(check_problem(p, __func__, &s));
-  TRY(check_block(s, block, __func__));
-  TRY(check_sparsity(sparsity, __func__));
-  TRY(check_rank(s, r, __func__));
-  REQUIRE_PTR(Qr);
-  REQUIRE_PTR(Kr);
-  REQUIRE_PTR(V);
-  REQUIRE_PTR(blk_idx);
-  REQUIRE_PTR(Qn);
-  REQUIRE_PTR(Pq);
-  REQUIRE_PTR(C);
-  REQUIRE_PTR(gate_logits);
-  REQUIRE_PTR(O);
+  TRY(check_combine(p, Qr, Kr, V, block, sparsity, blk_idx, softmax_scale, Qn, Pq, r, cos_tab,
+                    sin_tab, rope_ld, C, eps_lr, gate_logits, eps, O, __func__, &s));
   REQUIRE_PTR(ws);
-  TRY(check_tables(cos_tab, sin_tab, rope_ld, r / 2, __func__));
-  if (!(softmax_scale > 0.f) || !isfinite(softmax_scale))
-    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: softmax_scale must be finite and positive", __func__);
-  if (!(eps_lr >= 0.f) || !isfinite(eps_lr) || !(eps >= 0.f) || !isfinite(eps))
-    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: eps values must be finite and >= 0", __func__);
-  TRY(check_out(s, O, {{Qr, "Qr"}, {Kr, "Kr"}, {V, "V"}, {Qn, "Qn"}}, nullptr, __func__));
   const size_t need = rola_sparse_combine_workspace_bytes(p, block, sparsity, r);
   if (ws_bytes < need)
     return fail(ROLA_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", __func__, ws_bytes, need);
   const int keep = rola_keep_blocks(rola::num_blocks(s.N, block), sparsity);
-  const size_t sp = rola::sparse_workspace_bytes(s, block, keep);
-  void* fuse_ws = static_cast<char*>(ws) + ((sp + 255) & ~(size_t)255);
-  if (rola::fuse_supported(s, r)) {
-    const rola::LowrankFuse lf{Qn, Pq, r, cos_tab, sin_tab, rope_ld, C, eps_lr, gate_logits, eps};
-    return hip_status(rola::launch_sparse_attn(s, Qr, Kr, V, block, keep, blk_idx, softmax_scale, O,
-                                               sp > 0 ? ws : nullptr, stream, &lf, fuse_ws),
-                      __func__);
-  }
-  // other shapes: the attention into O, then the readout and combine in place
-  hipError_t e = rola::launch_sparse_attn(s, Qr, Kr, V, block, keep, blk_idx, softmax_scale, O,
-                                          sp > 0 ? ws : nullptr, stream);
-  if (e == hipSuccess)
-    e = rola::launch_lowrank_readout(s, Qn, Pq, r, cos_tab, sin_tab, rope_ld, 0, C, eps_lr, O,
-                                     gate_logits, eps, O, stream);
-  return hip_status(e, __func__);
+  return run_combine(s, Qr, Kr, V, block, keep, blk_idx, softmax_scale, Qn, Pq, r, cos_tab, sin_tab,
+                     rope_ld, C, eps_lr, gate_logits, eps, O, ws, false, stream, __func__);
+}
+
+rola_status rola_sparse_plan(const rola_problem* p, int32_t block, double sparsity,
+                             const int32_t* blk_idx, int32_t r, void* ws, size_t ws_bytes,
+                             hipStream_t stream) {
+  rola::Shape s;
+  TRY(check_problem(p, __func__, &s));
+  TRY(check_block(s, block, __func__));
+  TRY(check_sparsity(sparsity, __func__));
+  TRY(check_rank(s, r, __func__));
+  REQUIRE_PTR(blk_idx);
+  REQUIRE_PTR(ws);
+  const size_t need = rola_sparse_combine_workspace_bytes(p, block, sparsity, r);
+  if (ws_bytes < need)
+    return fail(ROLA_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", __func__, ws_bytes, need);
+  const int keep = rola_keep_blocks(rola::num_blocks(s.N, block), sparsity);
+  if (!rola::plan_used(s, block)) return ROLA_OK;
+  return hip_status(rola::launch_sparse_plan(s, keep, blk_idx, rola::fuse_supported(s, r) ? r : 0,
+                                             ws, stream),
+                    __func__);
+}
+
+rola_status rola_sparse_attn_combine_planned(
+    const rola_problem* p, const void* Qr, const void* Kr, const void* V, int32_t block,
+    double sparsity, const int32_t* blk_idx, float softmax_scale, const void* Qn, const void* Pq,
+    int32_t r, const float* cos_tab, const float* sin_tab, int32_t rope_ld, const float* C,
+    float eps_lr, const float* gate_logits, float eps, void* O, void* ws, size_t ws_bytes,
+    hipStream_t stream) {
+  rola::Shape s;
+  TRY(check_combine(p, Qr, Kr, V, block, sparsity, blk_idx, softmax_scale, Qn, Pq, r, cos_tab,
+                    sin_tab, rope_ld, C, eps_lr, gate_logits, eps, O, __func__, &s));
+  REQUIRE_PTR(ws);
+  const size_t need = rola_sparse_combine_workspace_bytes(p, block, sparsity, r);
+  if (ws_bytes < need)
+    return fail(ROLA_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", __func__, ws_bytes, need);
+  const int keep = rola_keep_blocks(rola::num_blocks(s.N, block), sparsity);
+  return run_combine(s, Qr, Kr, V, block, keep, blk_idx, softmax_scale, Qn, Pq, r, cos_tab, sin_tab,
+                     rope_ld, C, eps_lr, gate_logits, eps, O, ws, true, stream, __func__);
 }
 
 rola_status rola_lowrank_summary_ex(const rola_problem* p, const void* Kn, const void* V,

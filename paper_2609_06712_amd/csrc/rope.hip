@@ -44,10 +44,7 @@ __global__ void rope_apply_kernel(long rows, int N, int d, int ld, const T* __re
   const float4 s = *reinterpret_cast<const float4*>(sin_tab + (long)n * ld + g * 4);
   const float cc[4] = {c.x, c.y, c.z, c.w}, ss[4] = {s.x, s.y, s.z, s.w};
 #pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    o[2 * p] = v[2 * p] * cc[p] - v[2 * p + 1] * ss[p];
-    o[2 * p + 1] = v[2 * p] * ss[p] + v[2 * p + 1] * cc[p];
-  }
+  for (int p = 0; p < 4; ++p) rope_pair(v[2 * p], v[2 * p + 1], cc[p], ss[p], o[2 * p], o[2 * p + 1]);
   store8(Xr + row * d + g * 8, o);
 }
 

@@ -2,7 +2,9 @@
 // tokens, score every (query block, key block) pair with an fp32 dot product, keep the top-k key
 // blocks of every query block (ties to the lower index), written ascending.
 //
-//   pool_kernel   HBM-bound: reads Q^r and K^r once (coalesced 16-byte loads), writes means (fp32).
+//   pool_kernel   HBM-bound: reads Q^r and K^r once (coalesced 16-byte loads), writes means (fp32);
+//                 its rotating form reads Q^n or K^n instead, rotates each row (writing K^r) and
+//                 pools the rotated values: the backbone rotation and the pooling in one pass.
 //   score_kernel  per (b, h): S = q_bar k_bar^T, a small fp32 GEMM tiled 64 x 64 through LDS. The
 //                 positive factor 1/sqrt(d_h) is left out: it cannot change the ranking.
 //   topk_kernel   one wave per score row: 4-pass 8-bit radix select on order-preserving uint32 keys,
@@ -16,6 +18,8 @@ namespace {
 constexpr size_t kAlign = 256;
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
+// Block means of Q^r or K^r, one workgroup per (b, h, block), 16 threads of 8 channels per token
+// row. Summation order: per thread over its tokens in order, then over the 16 threads in order.
 template <typename T>
 __global__ __launch_bounds__(256) void pool_kernel(int N, int d, int block, const T* __restrict__ X,
                                                    float* __restrict__ out) {
@@ -41,6 +45,76 @@ __global__ __launch_bounds__(256) void pool_kernel(int N, int d, int block, cons
     float s = 0.f;
     for (int l = 0; l < L; ++l) s += red[(l * G + gc) * 8 + ic];
     out[(head * nb + I) * d + c] = s / (float)(n1 - n0);
+  }
+}
+
+// The rotating form (d_h = 128): X is Q^n or K^n. One workgroup per (block, group of HG heads): the
+// block's rotary-table entries are loaded into registers once and serve every head of the group
+// (the tables are twice the bytes of an activation row, so reading them per head would triple the
+// traffic). Each row is rotated (rope_pair, as rola_rope_apply), rounded to T, written to Xr unless
+// Xr is null, and pooled as rounded, in pool_kernel's thread layout and order: the means are
+// bitwise pool_kernel's over Xr. TPT = block / 16 tokens per thread.
+constexpr int kRopePoolHeads = 8;
+template <typename T, int TPT>
+__global__ __launch_bounds__(256) void rope_pool_kernel(int N, int block, int heads, int ld,
+                                                        const T* __restrict__ X,
+                                                        const float* __restrict__ cos_tab,
+                                                        const float* __restrict__ sin_tab,
+                                                        T* __restrict__ Xr, float* __restrict__ out) {
+  constexpr int D = 128, G = D / 8, L = 256 / G;
+  const int I = blockIdx.x, nb = gridDim.x;
+  const int h0 = blockIdx.y * kRopePoolHeads, h1 = min(heads, h0 + kRopePoolHeads);
+  const int g = threadIdx.x % G, lane = threadIdx.x / G;
+  const int n0 = I * block, n1 = min(N, n0 + block);
+  float cc[TPT][4], ss[TPT][4];
+#pragma unroll
+  for (int k = 0; k < TPT; ++k) {
+    const int n = min(n0 + lane + L * k, n1 - 1);  // rows past the block are not pooled
+    const float4 c = *reinterpret_cast<const float4*>(cos_tab + (long)n * ld + g * 4);
+    const float4 sn = *reinterpret_cast<const float4*>(sin_tab + (long)n * ld + g * 4);
+    cc[k][0] = c.x; cc[k][1] = c.y; cc[k][2] = c.z; cc[k][3] = c.w;
+    ss[k][0] = sn.x; ss[k][1] = sn.y; ss[k][2] = sn.z; ss[k][3] = sn.w;
+  }
+  __shared__ float red[256 * 8];
+  for (int head = h0; head < h1; ++head) {
+    const T* xh = X + (long)head * N * D;
+    float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    float v[TPT][8];
+#pragma unroll
+    for (int k = 0; k < TPT; ++k) {  // loads first: one memory latency per head
+      const int n = n0 + lane + L * k;
+      if (n < n1) load8(xh + (long)n * D + g * 8, v[k]);
+    }
+#pragma unroll
+    for (int k = 0; k < TPT; ++k) {
+      const int n = n0 + lane + L * k;
+      if (n < n1) {
+        T r[8];
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          float x, y;
+          rope_pair(v[k][2 * p], v[k][2 * p + 1], cc[k][p], ss[k][p], x, y);
+          r[2 * p] = from_f32<T>(x);
+          r[2 * p + 1] = from_f32<T>(y);
+        }
+        float o[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) o[i] = to_f32(r[i]);
+        if (Xr) store8(Xr + (long)head * N * D + (long)n * D + g * 8, o);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] += o[i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) red[threadIdx.x * 8 + i] = acc[i];
+    __syncthreads();
+    if (threadIdx.x < D) {
+      const int c = threadIdx.x, gc = c / 8, ic = c % 8;
+      float s = 0.f;
+      for (int l = 0; l < L; ++l) s += red[(l * G + gc) * 8 + ic];
+      out[((long)head * nb + I) * D + c] = s / (float)(n1 - n0);
+    }
+    __syncthreads();
   }
 }
 
@@ -208,7 +282,67 @@ __global__ __launch_bounds__(64) void topk_kernel(int nb, int keep, const float*
   }
 }
 
+hipError_t launch_pool(const Shape& s, const void* X, int block, float* means, hipStream_t st) {
+  const dim3 grid(num_blocks(s.N, block), s.H, s.B);
+  if (s.bf16)
+    hipLaunchKernelGGL(pool_kernel<bf16>, grid, dim3(256), 0, st, s.N, s.d, block, (const bf16*)X,
+                       means);
+  else
+    hipLaunchKernelGGL(pool_kernel<float>, grid, dim3(256), 0, st, s.N, s.d, block, (const float*)X,
+                       means);
+  return hipGetLastError();
+}
+
+template <typename T, int TPT>
+hipError_t launch_rope_pool_t(const Shape& s, const void* X, const float* cos_tab,
+                              const float* sin_tab, int ld, int block, void* Xr, float* means,
+                              hipStream_t st) {
+  const int heads = s.B * s.H;
+  const dim3 grid(num_blocks(s.N, block), (heads + kRopePoolHeads - 1) / kRopePoolHeads);
+  hipLaunchKernelGGL((rope_pool_kernel<T, TPT>), grid, dim3(256), 0, st, s.N, block, heads, ld,
+                     (const T*)X, cos_tab, sin_tab, (T*)Xr, means);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+size_t select_pooled_workspace_bytes(const Shape& s, int block) {
+  const size_t nb = (size_t)num_blocks(s.N, block);
+  return align_up((size_t)s.B * s.H * nb * nb * sizeof(float));
+}
+
+hipError_t launch_select_pooled(const Shape& s, const float* qbar, const float* kbar, int block,
+                                int keep, int32_t* idx, void* ws, hipStream_t st) {
+  const int nb = num_blocks(s.N, block);
+  const size_t heads = (size_t)s.B * s.H;
+  float* S = (float*)ws;
+  const int tiles = (nb + 63) / 64;
+  hipLaunchKernelGGL(score_kernel, dim3(tiles, tiles, (unsigned)heads), dim3(256), 0, st, nb, s.d,
+                     qbar, kbar, S);
+  hipLaunchKernelGGL(topk_kernel, dim3(nb, s.H, s.B), dim3(64), (size_t)nb * sizeof(uint32_t), st, nb,
+                     keep, S, idx);
+  return hipGetLastError();
+}
+
+hipError_t launch_block_pool(const Shape& s, const void* X, int block, float* means,
+                             hipStream_t st) {
+  return launch_pool(s, X, block, means, st);
+}
+
+bool rope_pool_supported(const Shape& s, int block) { return s.d == 128 && block >= 32; }
+
+hipError_t launch_rope_pool(const Shape& s, const void* X, const float* cos_tab,
+                            const float* sin_tab, int ld, int block, void* Xr, float* means,
+                            hipStream_t st) {
+  switch ((s.bf16 ? 1000 : 0) + block) {
+    case 1064: return launch_rope_pool_t<bf16, 4>(s, X, cos_tab, sin_tab, ld, block, Xr, means, st);
+    case 1128: return launch_rope_pool_t<bf16, 8>(s, X, cos_tab, sin_tab, ld, block, Xr, means, st);
+    case 32: return launch_rope_pool_t<float, 2>(s, X, cos_tab, sin_tab, ld, block, Xr, means, st);
+    case 64: return launch_rope_pool_t<float, 4>(s, X, cos_tab, sin_tab, ld, block, Xr, means, st);
+    case 128: return launch_rope_pool_t<float, 8>(s, X, cos_tab, sin_tab, ld, block, Xr, means, st);
+  }
+  return hipErrorInvalidValue;
+}
 
 size_t select_workspace_bytes(const Shape& s, int block) {
   const size_t nb = (size_t)num_blocks(s.N, block);
@@ -224,24 +358,10 @@ hipError_t launch_block_select(const Shape& s, const void* Qr, const void* Kr, i
   float* qbar = (float*)w;
   float* kbar = (float*)(w + align_up(heads * nb * s.d * sizeof(float)));
   float* S = (float*)(w + 2 * align_up(heads * nb * s.d * sizeof(float)));
-  const dim3 pgrid(nb, s.H, s.B);
-  if (s.bf16) {
-    hipLaunchKernelGGL(pool_kernel<bf16>, pgrid, dim3(256), 0, st, s.N, s.d, block, (const bf16*)Qr,
-                       qbar);
-    hipLaunchKernelGGL(pool_kernel<bf16>, pgrid, dim3(256), 0, st, s.N, s.d, block, (const bf16*)Kr,
-                       kbar);
-  } else {
-    hipLaunchKernelGGL(pool_kernel<float>, pgrid, dim3(256), 0, st, s.N, s.d, block,
-                       (const float*)Qr, qbar);
-    hipLaunchKernelGGL(pool_kernel<float>, pgrid, dim3(256), 0, st, s.N, s.d, block,
-                       (const float*)Kr, kbar);
-  }
-  const int tiles = (nb + 63) / 64;
-  hipLaunchKernelGGL(score_kernel, dim3(tiles, tiles, (unsigned)heads), dim3(256), 0, st, nb, s.d,
-                     qbar, kbar, S);
-  hipLaunchKernelGGL(topk_kernel, pgrid, dim3(64), (size_t)nb * sizeof(uint32_t), st, nb, keep, S,
-                     idx);
-  return hipGetLastError();
+  hipError_t e = launch_pool(s, Qr, block, qbar, st);
+  if (e == hipSuccess) e = launch_pool(s, Kr, block, kbar, st);
+  if (e == hipSuccess) e = launch_select_pooled(s, qbar, kbar, block, keep, idx, S, st);
+  return e;
 }
 
 }  // namespace rola

@@ -291,6 +291,7 @@ struct FuseArgs {
   int H, r, ld;
   float eps_lr, eps;
   float* lse_out;        // optional [B, H, N]: log2 of the softmax denominator of the scaled scores
+  int rot_q;             // the attention's Q is Q^n, rotated in the prologue with these tables
 };
 
 // C^T fragments: entry (head, w, t, s, lane) = {hi, lo} of the 8 values C[2J + s][32w + l%32],
@@ -456,6 +457,7 @@ struct AttnArgs {
   const float2* lseD;
   float* dQ;
   float scale;
+  int rot_q;  // Q holds Q^n: the prologue rotates it with fz's tables (rounded as rola_rope_apply)
 };
 
 // DQ: the backward's dQ^r = scale dS K^r over the same groups and lists (fine-tuning, Sec. 4.5):
@@ -589,6 +591,23 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void s
 #pragma unroll
     for (int s = 0; s < 8; ++s)
       qf[s] = qvalid ? *reinterpret_cast<const bf16x8*>(Qh + (long)q * D + 16 * s + 8 * hh) : bf16x8{};
+    if (ap->rot_q && qvalid) {  // Q^r = R(Q^n): pairs 8s + 4(l/32) .. +3 of this lane's query
+      const float* ct = fz.cos_tab + (long)q * fz.ld + 4 * hh;
+      const float* st = fz.sin_tab + (long)q * fz.ld + 4 * hh;
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        const float4 c = *reinterpret_cast<const float4*>(ct + 8 * s);
+        const float4 sn = *reinterpret_cast<const float4*>(st + 8 * s);
+        const float cc[4] = {c.x, c.y, c.z, c.w}, ss[4] = {sn.x, sn.y, sn.z, sn.w};
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          float x, y;
+          rope_pair((float)qf[s][2 * p], (float)qf[s][2 * p + 1], cc[p], ss[p], x, y);
+          qf[s][2 * p] = (bf16)x;
+          qf[s][2 * p + 1] = (bf16)y;
+        }
+      }
+    }
     bf16x8 df[DQ ? 8 : 1];  // dQ mode: dO^T fragments, same layout as qf
     float lse_q = 0.f, dsum_q = 0.f;
     if constexpr (DQ) {
@@ -639,14 +658,15 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void s
       for (int s = 0; s < 4; ++s)
         kf[s] = *reinterpret_cast<const bf16x8*>(lds + buf * STAGE + ko[s0 + s]);
     };
+    auto v_operand = [&](int buf, int u, int w) {  // V^T operand of channel tile w, key k-step u
+      const char* p = lds + buf * STAGE + vo[w] + 16 * u * 256;
+      const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p);
+      const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p + 8 * 256));
+      return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    };
     auto load_v = [&](int buf, int u, bf16x8 (&vf)[4]) {  // V^T operands of key k-step u
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const char* p = lds + buf * STAGE + vo[w] + 16 * u * 256;
-        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p);
-        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p + 8 * 256));
-        vf[w] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-      }
+      for (int w = 0; w < 4; ++w) vf[w] = v_operand(buf, u, w);
     };
     // Softmax pieces on S^T of one sub-tile (16 keys of this lane's query; the other 16 in lane l^32).
     auto row_max = [&](const f32x16& s) {
@@ -684,10 +704,6 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void s
 #pragma unroll
       for (int k = 0; k < 16; k += 2)
         l = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[k / 8][k % 8], pb[k / 8][k % 8 + 1]}, one2, l, false);
-    };
-    auto pv = [&](int u, const bf16x8 (&vf)[4], const bf16x8 (&pb)[2]) {
-#pragma unroll
-      for (int w = 0; w < 4; ++w) acc[w] = mfma32(vf[w], pb[u], acc[w]);
     };
     auto qk = [&](int s0, const bf16x8* kf, f32x16& sacc, int n) {  // k-steps s0 .. s0+n-1
 #pragma unroll
@@ -759,16 +775,38 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void s
           f32x16 sc = mfma32(kf[0], qf[0], f32x16{});
           qk(1, kf + 1, sc, 3);
           qk(4, kg, sc, 4);
+          // four K operand reads ahead of the chain of eight dependent products, then one read per
+          // product (the default schedule kept two in flight: 12.95 -> 12.82 ms for the fused call
+          // on the 14B layer, bitwise identical)
+          __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);  // DS reads
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          }
+          __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
           load_v(j, 0, vf);
           rescale(row_max(sc));
           probs(sc, cur.k0, pb);
           // the P V products at raised wave priority: a wave that has its probabilities issues its
           // MFMAs ahead of the other waves' score and softmax work (plain attention on the 14B
-          // layer: 12.80 -> 12.58 ms; the same priority around Q K^T costs a third more time)
+          // layer: 12.80 -> 12.58 ms; the same priority around Q K^T costs a third more time).
+          // The V^T operands of the second key step are read into each channel tile's registers
+          // right behind that tile's first product, so their LDS latency hides under the other
+          // three (fused call 12.90 -> 12.66 ms on one box, bitwise identical).
           __builtin_amdgcn_s_setprio(1);
-          pv(0, vf, pb);
-          load_v(j, 1, vf);
-          pv(1, vf, pb);
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            acc[w] = mfma32(vf[w], pb[0], acc[w]);
+            vf[w] = v_operand(j, 1, w);
+          }
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // its tile's two DS reads
+          }
+#pragma unroll
+          for (int w = 0; w < 4; ++w) acc[w] = mfma32(vf[w], pb[1], acc[w]);
           __builtin_amdgcn_s_setprio(0);
         }
         ++t;
@@ -947,7 +985,7 @@ hipError_t launch_bf16_tab(const Shape& s, const void* Qr, const void* Kr, const
   const int threads = G * BLK * 2;
   const AttnArgs a{s.N, nb, ngroups, total, lists, list_len, list_stride, pairs, sl,
                    (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V, (bf16*)Os, fz, queue,
-                   dq.dO, dq.lseD, dq.dQ, scale};
+                   dq.dO, dq.lseD, dq.dQ, scale, fz.rot_q};
   if (queue) {
     const int grid = std::min(total, queue_resident<BLK, G, NBUF, TAB, RJ, DQ>());
     hipLaunchKernelGGL((sparse_attn_kernel<BLK, G, NBUF, TAB, RJ, true, DQ>), dim3(grid),
@@ -1062,17 +1100,25 @@ struct Groups {
   int32_t* lists;
   int stride;
 };
+// Pointers of the groups inside the workspace (no device work).
+Groups groups_in(const Shape& s, int keep, void* ws) {
+  constexpr int G = kB64Group;
+  const SparseWs lay = sparse_ws_layout(s, 64, keep);
+  Groups gr;
+  gr.stride = G * keep + 1;
+  gr.queue = (int*)ws;
+  gr.pairs = lay.pair_bytes ? (int32_t*)((char*)ws + lay.queue_bytes) : nullptr;
+  gr.lists = (int32_t*)((char*)ws + lay.queue_bytes + lay.pair_bytes);
+  return gr;
+}
+
 template <bool DQ>
 hipError_t prepare_groups(const Shape& s, int keep, const int32_t* idx, void* ws, int r,
                           hipStream_t st, Groups& gr) {
   constexpr int G = kB64Group;
   const int nb = num_blocks(s.N, 64);
   const int ngroups = (nb + G - 1) / G, heads = s.B * s.H;
-  const SparseWs lay = sparse_ws_layout(s, 64, keep);
-  gr.stride = G * keep + 1;
-  gr.queue = (int*)ws;
-  gr.pairs = lay.pair_bytes ? (int32_t*)((char*)ws + lay.queue_bytes) : nullptr;
-  gr.lists = (int32_t*)((char*)ws + lay.queue_bytes + lay.pair_bytes);
+  gr = groups_in(s, keep, ws);
   if (gr.pairs) {
     const int nchunks = (nb + kPairWindow - 1) / kPairWindow;
     hipLaunchKernelGGL(pair_rank_kernel, dim3(nchunks * heads), dim3(256),
@@ -1081,7 +1127,7 @@ hipError_t prepare_groups(const Shape& s, int keep, const int32_t* idx, void* ws
     hipLaunchKernelGGL(pair_greedy_kernel, dim3(heads), dim3(64), 0, st, nb, ngroups, nchunks,
                        (const uint8_t*)gr.lists, gr.pairs);
   }
-  const int period = gr.queue ? walk_period<DQ ? 3 : kB64Nbuf, DQ>(gr.stride, r) : 0;
+  const int period = walk_period<DQ ? 3 : kB64Nbuf, DQ>(gr.stride, r);
   hipLaunchKernelGGL(group_union_kernel<G>, dim3(ngroups * heads), dim3(256),
                      (G * walk_words(nb) + 256) * sizeof(uint32_t), st, nb, keep, ngroups, gr.stride,
                      idx, (const int32_t*)gr.pairs, gr.lists, gr.queue, period);
@@ -1122,10 +1168,19 @@ hipError_t launch_sparse_dq(const Shape& s, const void* Qr, const void* Kr, cons
                                                nullptr, none, gr.queue, st, dq);
 }
 
+bool plan_used(const Shape& s, int block) { return s.bf16 && block == 64 && kB64Group > 1; }
+
+hipError_t launch_sparse_plan(const Shape& s, int keep, const int32_t* idx, int r, void* ws,
+                              hipStream_t st) {
+  if (!plan_used(s, 64)) return hipSuccess;
+  Groups gr;
+  return prepare_groups<false>(s, keep, idx, ws, r, st, gr);
+}
+
 hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, const void* V,
                               int block, int keep, const int32_t* idx, float scale, void* Os,
                               void* ws, hipStream_t st, const LowrankFuse* lf, void* fuse_ws,
-                              float* lse) {
+                              float* lse, bool planned) {
   FuseArgs fz{};
   fz.lse_out = lse;
   if (lf) {  // fused epilogue: C^T fragments first (fuse_ws: fuse_workspace_bytes)
@@ -1136,7 +1191,9 @@ hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, co
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     fz = FuseArgs{(const bf16*)lf->Qn, (const bf16*)lf->Pq, lf->cos_tab, lf->sin_tab,
-                  (const uint4*)fuse_ws, lf->logits, s.H, lf->r, lf->ld, lf->eps_lr, lf->eps, lse};
+                  (const uint4*)fuse_ws, lf->logits, s.H, lf->r, lf->ld, lf->eps_lr, lf->eps, lse,
+                  Qr == nullptr ? 1 : 0};
+    if (Qr == nullptr) Qr = lf->Qn;  // queries rotated from Q^n in the prologue
   }
   const FuseArgs* fp = (lf || lse) ? &fz : nullptr;
   if (s.bf16) {
@@ -1145,9 +1202,11 @@ hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, co
       constexpr int G = kB64Group;
       if (!idx) return launch_bf16<64, 2, 3>(s, Qr, Kr, V, nullptr, nb, 0, scale, Os, st, nullptr, fp);
       if (ws && G > 1) {
-        Groups gr;
-        const hipError_t e = prepare_groups<false>(s, keep, idx, ws, lf ? lf->r : 0, st, gr);
-        if (e != hipSuccess) return e;
+        Groups gr = groups_in(s, keep, ws);
+        if (!planned) {
+          const hipError_t e = prepare_groups<false>(s, keep, idx, ws, lf ? lf->r : 0, st, gr);
+          if (e != hipSuccess) return e;
+        }
         return launch_bf16<64, G, kB64Nbuf>(s, Qr, Kr, V, gr.lists, 0, gr.stride, scale, Os, st,
                                                  gr.pairs, fp, gr.queue);
       }

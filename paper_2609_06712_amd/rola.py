@@ -40,6 +40,9 @@ SIGNATURES = {
     "rola_rope_apply": (_i32, [_PP, _p, _p, _p, _i32, _p, _p]),
     "rola_rope_backward_accumulate": (_i32, [_PP, _p, _p, _p, _i32, _i32, _p, _p]),
     "rola_block_select": (_i32, [_PP, _p, _p, _i32, _f64, _p, _p, _sz, _p]),
+    "rola_rope_pool": (_i32, [_PP, _p, _p, _p, _i32, _i32, _p, _p, _p]),
+    "rola_select_pooled_workspace_bytes": (_sz, [_PP, _i32]),
+    "rola_block_select_pooled": (_i32, [_PP, _p, _p, _i32, _f64, _p, _p, _sz, _p]),
     "rola_sparse_workspace_bytes": (_sz, [_PP, _i32, _f64]),
     "rola_sparse_attn": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p, _sz, _p]),
     "rola_dense_attn": (_i32, [_PP, _p, _p, _p, _i32, _f32, _p, _p]),
@@ -68,6 +71,9 @@ SIGNATURES = {
                                          _p, _p, _sz, _p]),
     "rola_sparse_attn_combine": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p, _i32, _p, _p,
                                         _i32, _p, _f32, _p, _f32, _p, _p, _sz, _p]),
+    "rola_sparse_plan": (_i32, [_PP, _i32, _f64, _p, _i32, _p, _sz, _p]),
+    "rola_sparse_attn_combine_planned": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p, _i32,
+                                                _p, _p, _i32, _p, _f32, _p, _f32, _p, _p, _sz, _p]),
 }
 
 # Feature map and rotation order of the low-rank branch (rola_phi, rola_rope_order).
@@ -305,6 +311,58 @@ def rola_block_select(Qr, Kr, grid, block, sparsity, out=None, ws=None, stream=N
     return out
 
 
+def rola_rope_pool(X, cos, sin, grid, block, want_xr=True, xr=None, xbar=None, stream=None):
+    """(R(X) or None, block means of R(X) fp32 [B, H, n_blocks, d_h]) in one pass. With cos and sin
+    None, X is already rotated and only the means are computed."""
+    a = _Args()
+    a.act(X, "X")
+    if cos is None and sin is None:
+        ld, want_xr = 0, False
+        if xr is not None:
+            raise ValueError("xr needs the rotary tables")
+    else:
+        ld = a.tables(cos, sin, X, X.shape[3] // 2)
+    B, H, N, d = X.shape
+    if want_xr and xr is None:
+        xr = torch.empty_like(X)
+    if xr is not None:
+        a.act(xr, "xr", X)
+    shape = (B, H, num_blocks(N, block), d)
+    if xbar is None:
+        xbar = torch.empty(shape, dtype=torch.float32, device=X.device)
+    a.tensor(xbar, "xbar", shape, torch.float32)
+    a.done()
+    prob = problem_of(X, grid)
+    _check(LIB.rola_rope_pool(ctypes.byref(prob), _ptr(X), _ptr(cos), _ptr(sin), ld, block, _ptr(xr),
+                              _ptr(xbar), _stream(stream)), "rola_rope_pool")
+    return xr, xbar
+
+
+def rola_block_select_pooled(Qbar, Kbar, like, grid, block, sparsity, out=None, ws=None,
+                             stream=None):
+    """Block lists from the means of rola_rope_pool; `like`: an activation of the layer (shape)."""
+    a = _Args()
+    a.act(like, "like")
+    B, H, N, d = like.shape
+    shape = (B, H, num_blocks(N, block), d)
+    a.tensor(Qbar, "Qbar", shape, torch.float32)
+    a.tensor(Kbar, "Kbar", shape, torch.float32)
+    prob = problem_of(like, grid)
+    if out is None:
+        out = torch.empty((B, H, shape[2], keep_blocks(shape[2], sparsity)), dtype=torch.int32,
+                          device=like.device)
+    a.blk_idx(out, like, block, sparsity)
+    need = LIB.rola_select_pooled_workspace_bytes(ctypes.byref(prob), block)
+    if ws is None:
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=like.device)
+    a.workspace(ws)
+    a.done()
+    _check(LIB.rola_block_select_pooled(ctypes.byref(prob), _ptr(Qbar), _ptr(Kbar), block, sparsity,
+                                        _ptr(out), _ptr(ws), ws.numel(), _stream(stream)),
+           "rola_block_select_pooled")
+    return out
+
+
 def rola_sparse_attn(Qr, Kr, V, grid, block, sparsity, blk_idx, scale=None, out=None, ws=None,
                      stream=None, share=True):
     """share=False passes no workspace: each workgroup then serves one query block."""
@@ -517,12 +575,16 @@ def sparse_combine_workspace_bytes(prob: Problem, block: int, sparsity: float, r
 
 
 def _combine_args(a, Qr, Kr, V, block, sparsity, blk_idx, Qn, Pq, r, cos, sin, C, logits):
-    a.act(Qr, "Qr")
-    for t, name in ((Kr, "Kr"), (V, "V"), (Qn, "Qn")):
-        a.act(t, name, Qr)
-    a.blk_idx(blk_idx, Qr, block, sparsity)
+    """Qr may be None: the queries are then rotated from Qn in the attention's prologue."""
+    a.act(Qn, "Qn")
+    for t, name in ((Qr, "Qr"), (Kr, "Kr"), (V, "V")):
+        if t is not None or name != "Qr":
+            a.act(t, name, Qn)
+    a.blk_idx(blk_idx, Qn, block, sparsity)
     ld = _readout_args(a, Qn, Pq, r, cos, sin, C)
-    a.logits(logits, Qr)
+    a.logits(logits, Qn)
+    if Qr is None and cos.shape[1] < Qn.shape[3] // 2:
+        raise ValueError("Qr = None needs tables with d_h/2 columns")
     return ld
 
 
@@ -532,12 +594,12 @@ def rola_sparse_attn_combine(Qr, Kr, V, grid, block, sparsity, blk_idx, Qn, Pq, 
     """O = combine(sparse attention, low-rank readout of C) in one call (fused epilogue)."""
     a = _Args()
     ld = _combine_args(a, Qr, Kr, V, block, sparsity, blk_idx, Qn, Pq, r, cos, sin, C, logits)
-    prob = problem_of(Qr, grid)
+    prob = problem_of(Qn, grid)
     scale = prob.d_h ** -0.5 if scale is None else scale
-    out = torch.empty_like(Qr) if out is None else a.act(out, "out", Qr)
+    out = torch.empty_like(Qn) if out is None else a.act(out, "out", Qn)
     if ws is None:
         need = sparse_combine_workspace_bytes(prob, block, sparsity, r)
-        ws = torch.empty(need, dtype=torch.uint8, device=Qr.device)
+        ws = torch.empty(need, dtype=torch.uint8, device=Qn.device)
     a.workspace(ws)
     a.done()
     _check(LIB.rola_sparse_attn_combine(ctypes.byref(prob), _ptr(Qr), _ptr(Kr), _ptr(V), block,
@@ -545,6 +607,39 @@ def rola_sparse_attn_combine(Qr, Kr, V, grid, block, sparsity, blk_idx, Qn, Pq, 
                                         _ptr(cos), _ptr(sin), ld, _ptr(C), eps_lr,
                                         _ptr(logits), eps, _ptr(out), _ptr(ws), ws.numel(),
                                         _stream(stream)), "rola_sparse_attn_combine")
+    return out
+
+
+def rola_sparse_plan(blk_idx, like, grid, block, sparsity, r, ws, stream=None):
+    """Pairs and merged lists of rola_sparse_attn_combine_planned into ws (its workspace); `like` is
+    any of the call's activations (for the shape)."""
+    a = _Args()
+    a.act(like, "like")
+    a.blk_idx(blk_idx, like, block, sparsity)
+    a.workspace(ws)
+    a.done()
+    prob = problem_of(like, grid)
+    _check(LIB.rola_sparse_plan(ctypes.byref(prob), block, sparsity, _ptr(blk_idx), r, _ptr(ws),
+                                ws.numel(), _stream(stream)), "rola_sparse_plan")
+    return ws
+
+
+def rola_sparse_attn_combine_planned(Qr, Kr, V, grid, block, sparsity, blk_idx, Qn, Pq, r, cos, sin,
+                                     C, logits, ws, scale=None, eps_lr=1e-6, eps=1e-6, out=None,
+                                     stream=None):
+    """rola_sparse_attn_combine on the plan rola_sparse_plan left in ws."""
+    a = _Args()
+    ld = _combine_args(a, Qr, Kr, V, block, sparsity, blk_idx, Qn, Pq, r, cos, sin, C, logits)
+    prob = problem_of(Qn, grid)
+    scale = prob.d_h ** -0.5 if scale is None else scale
+    out = torch.empty_like(Qn) if out is None else a.act(out, "out", Qn)
+    a.workspace(ws)
+    a.done()
+    _check(LIB.rola_sparse_attn_combine_planned(ctypes.byref(prob), _ptr(Qr), _ptr(Kr), _ptr(V),
+                                                block, sparsity, _ptr(blk_idx), scale, _ptr(Qn),
+                                                _ptr(Pq), r, _ptr(cos), _ptr(sin), ld, _ptr(C), eps_lr,
+                                                _ptr(logits), eps, _ptr(out), _ptr(ws), ws.numel(),
+                                                _stream(stream)), "rola_sparse_attn_combine_planned")
     return out
 
 

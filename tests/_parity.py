@@ -16,6 +16,7 @@ from paper_2609_06712_amd import rola as R
 from paper_2609_06712_amd import synth
 
 TIE_GAP = 1e-4
+REPORTS = []  # one line per compared head, printed at the end of the run (tests/conftest.py)
 TOL = {"bf16": dict(max_abs=2e-2, mean_abs=5e-3, frob=1e-2),
        "f32": dict(max_abs=1e-5, mean_abs=1e-5, frob=1e-5)}
 

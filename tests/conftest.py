@@ -8,3 +8,14 @@ if ROOT not in sys.path:
 
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an AMD GPU (gfx950) and the built HIP library")
+
+
+def pytest_terminal_summary(terminalreporter):
+    """Prints the parity records the GPU tests collected (selection tie rows and swaps, error
+    statistics), so that they are part of the run's output even when every test passes."""
+    parity = sys.modules.get("tests._parity")
+    lines = getattr(parity, "REPORTS", None) if parity else None
+    if lines:
+        terminalreporter.section("parity records")
+        for line in lines:
+            terminalreporter.write_line(line)

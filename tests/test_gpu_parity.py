@@ -26,7 +26,9 @@ def _inputs(w, seed=0, device="cpu"):
 
 
 def _report(name, **kv):
-    print(f"[parity] {name}: " + ", ".join(f"{k}={v}" for k, v in kv.items()), flush=True)
+    line = f"[parity] {name}: " + ", ".join(f"{k}={v}" for k, v in kv.items())
+    T.REPORTS.append(line)
+    print(line, flush=True)
 
 
 def _compare_head(w, gpu, ora, b, h, dtype, check_fused=True, check_unfused=True):
@@ -400,3 +402,118 @@ def test_combine_in_place_matches_out_of_place():
     torch.cuda.synchronize()
     assert torch.equal(os_copy, res["out"])
     assert torch.equal(os_copy2, res["out_fused"])
+
+
+def test_plan_then_planned_attention_on_two_streams():
+    """rola_sparse_plan + rola_sparse_attn_combine_planned, with the low-rank summary on a second
+    stream between them (the benchmarked layer's schedule, on the 1.3B 480p layer), give bitwise the
+    output of the single call rola_sparse_attn_combine."""
+    w = synth.WAN_1_3B_480P
+    inp = synth.make_inputs(w, 0, device="cuda")
+    g = w.grid
+    prob = R.problem(w.B, w.H, w.N, w.d_h, g, w.dtype)
+    cos, sin = R.rola_rope_tables(prob, w.split)
+    qr = R.rola_rope_apply(inp["Qn"], cos, sin, g)
+    kr = R.rola_rope_apply(inp["Kn"], cos, sin, g)
+    idx = R.rola_block_select(qr, kr, g, w.block, w.sparsity)
+    C, _ = R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], w.r, cos, sin, g)
+    want = R.rola_sparse_attn_combine(qr, kr, inp["V"], g, w.block, w.sparsity, idx, inp["Qn"],
+                                      inp["Pq"], w.r, cos, sin, C, inp["logits"])
+    ws = torch.empty(R.sparse_combine_workspace_bytes(prob, w.block, w.sparsity, w.r),
+                     dtype=torch.uint8, device="cuda")
+    C2 = torch.zeros_like(C)
+    side = torch.cuda.Stream()
+    fork, join = torch.cuda.Event(), torch.cuda.Event()
+    torch.cuda.synchronize()
+    fork.record()
+    side.wait_event(fork)
+    R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], w.r, cos, sin, g, C=C2, stream=side)
+    join.record(side)
+    R.rola_sparse_plan(idx, qr, g, w.block, w.sparsity, w.r, ws)
+    torch.cuda.current_stream().wait_event(join)
+    got = R.rola_sparse_attn_combine_planned(qr, kr, inp["V"], g, w.block, w.sparsity, idx, inp["Qn"],
+                                             inp["Pq"], w.r, cos, sin, C2, inp["logits"], ws)
+    torch.cuda.synchronize()
+    assert torch.equal(C2, C)
+    assert torch.equal(got, want)
+    # block 128 has no plan: the planned call is the plain one
+    w2 = w.replace(grid=(3, 10, 13), H=2, block=128, sparsity=0.5)
+    inp2 = synth.make_inputs(w2, 1, device="cuda")
+    p2 = R.problem(w2.B, w2.H, w2.N, w2.d_h, w2.grid, w2.dtype)
+    c2, s2 = R.rola_rope_tables(p2, w2.split)
+    q2 = R.rola_rope_apply(inp2["Qn"], c2, s2, w2.grid)
+    k2 = R.rola_rope_apply(inp2["Kn"], c2, s2, w2.grid)
+    i2 = R.rola_block_select(q2, k2, w2.grid, 128, 0.5)
+    Cb, _ = R.rola_lowrank_summary(inp2["Kn"], inp2["V"], inp2["Pk"], w2.r, c2, s2, w2.grid)
+    ws2 = torch.empty(max(16, R.sparse_combine_workspace_bytes(p2, 128, 0.5, w2.r)), dtype=torch.uint8,
+                      device="cuda")
+    a2 = (q2, k2, inp2["V"], w2.grid, 128, 0.5, i2, inp2["Qn"], inp2["Pq"], w2.r, c2, s2, Cb,
+          inp2["logits"])
+    R.rola_sparse_plan(i2, q2, w2.grid, 128, 0.5, w2.r, ws2)
+    got2 = R.rola_sparse_attn_combine_planned(*a2, ws2)
+    want2 = R.rola_sparse_attn_combine(*a2)
+    torch.cuda.synchronize()
+    assert torch.equal(got2, want2)
+
+
+@pytest.mark.parametrize("grid,H,block", [((21, 30, 52), 12, 64), ((3, 10, 13), 2, 64),
+                                          ((3, 10, 13), 2, 128)],
+                         ids=["1.3B-480p", "ragged-b64", "ragged-b128"])
+def test_rope_pool_producer(grid, H, block):
+    """The rotating pooling pass (rola_rope_pool): its K^r is bitwise rola_rope_apply's, its block
+    means are the oracle's pool_blocks of the rounded rotation (fp32 sums of 64 or 128 rows), and the
+    selection from them (rola_block_select_pooled) is bitwise rola_block_select's lists."""
+    w = synth.WAN_1_3B_480P.replace(grid=grid, H=H, block=block)
+    inp, f64 = _inputs(w, seed=9)
+    g = w.grid
+    prob = R.problem(w.B, w.H, w.N, w.d_h, g, w.dtype)
+    cos, sin = R.rola_rope_tables(prob, w.split)
+    qr = R.rola_rope_apply(inp["Qn"], cos, sin, g)
+    kr = R.rola_rope_apply(inp["Kn"], cos, sin, g)
+    want_idx = R.rola_block_select(qr, kr, g, block, w.sparsity)
+    kr2, kbar = R.rola_rope_pool(inp["Kn"], cos, sin, g, block)
+    none, qbar = R.rola_rope_pool(inp["Qn"], cos, sin, g, block, want_xr=False)
+    idx = R.rola_block_select_pooled(qbar, kbar, qr, g, block, w.sparsity)
+    _, qbar_r = R.rola_rope_pool(qr, None, None, g, block)   # pooling of the rotated tensor
+    torch.cuda.synchronize()
+    assert none is None
+    assert torch.equal(kr2, kr)
+    assert torch.equal(idx, want_idx)
+    assert torch.equal(qbar_r, qbar)
+    ocos, osin = O.rope_tables(*g, w.split)
+    for h in range(w.H):
+        # the pooling arithmetic: the oracle's pool_blocks of the GPU's own rounded rotation
+        np.testing.assert_allclose(T.to_np(qbar[0, h]), O.pool_blocks(T.to_np(qr[0, h]), block),
+                                   rtol=0, atol=2e-6)
+        # against the oracle's fp64 rotation: the rounding of a few elements may differ by one bf16
+        # ulp (2^-8 relative), diluted over the block
+        q = O.round_to(O.rotate(f64["Qn"][0, h], ocos, osin), w.dtype)
+        np.testing.assert_allclose(T.to_np(qbar[0, h]), O.pool_blocks(q, block), rtol=0, atol=1e-3)
+    _report(f"rope_pool {grid} block {block}", heads=w.H, blocks=qbar.shape[2])
+
+
+@pytest.mark.parametrize("grid,H,r", [((21, 30, 52), 12, 32), ((3, 10, 13), 2, 16),
+                                      ((2, 9, 20), 3, 64)], ids=["1.3B-480p", "ragged-r16", "r64"])
+def test_attention_rotates_queries_in_prologue(grid, H, r):
+    """rola_sparse_attn_combine with Qr = None rotates Q^n in the attention's prologue: bitwise the
+    output with Qr = rola_rope_apply(Qn), and the planned form agrees."""
+    w = synth.WAN_1_3B_480P.replace(grid=grid, H=H, r=r)
+    inp = synth.make_inputs(w, 4, device="cuda")
+    g = w.grid
+    prob = R.problem(w.B, w.H, w.N, w.d_h, g, w.dtype)
+    cos, sin = R.rola_rope_tables(prob, w.split)
+    qr = R.rola_rope_apply(inp["Qn"], cos, sin, g)
+    kr = R.rola_rope_apply(inp["Kn"], cos, sin, g)
+    idx = R.rola_block_select(qr, kr, g, w.block, w.sparsity)
+    C, _ = R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], w.r, cos, sin, g)
+    rest = (kr, inp["V"], g, w.block, w.sparsity, idx, inp["Qn"], inp["Pq"], w.r, cos, sin, C,
+            inp["logits"])
+    want = R.rola_sparse_attn_combine(qr, *rest)
+    got = R.rola_sparse_attn_combine(None, *rest)
+    ws = torch.empty(R.sparse_combine_workspace_bytes(prob, w.block, w.sparsity, w.r),
+                     dtype=torch.uint8, device="cuda")
+    R.rola_sparse_plan(idx, inp["Qn"], g, w.block, w.sparsity, w.r, ws)
+    planned = R.rola_sparse_attn_combine_planned(None, *rest, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(got, want)
+    assert torch.equal(planned, want)
