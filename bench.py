@@ -382,6 +382,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--quick", action="store_true",
+                    help="only the timed steps (for profiler runs): no comparison timings")
     ap.add_argument("--sweep", action="store_true",
                     help="print the measurement sweeps (1.3B layer, low-rank N x r, sparse S x block) "
                          "as markdown instead of the JSON line")
@@ -510,7 +512,8 @@ def main():
 
     # the summary alone on one stream (its bandwidth without the selection running beside it)
     sum_ms = time_call(lambda: R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], w.r, cos, sin,
-                                                      g, C=C, z=z, ws=ws_sum), 20)[0]
+                                                      g, C=C, z=z, ws=ws_sum), 20)[0] if not args.quick \
+        else float("nan")
     # the layer as one stream of the three plain calls (selection, summary, attention with its
     # epilogue), and the same preceded by the backbone's rotation of Q^n and K^n; the two-stream
     # layer starting from Q^n, K^n (rotation fused with the pooling)
@@ -524,9 +527,10 @@ def main():
         R.rola_rope_apply(inp["Qn"], cos, sin, g, out=qr)
         R.rola_rope_apply(inp["Kn"], cos, sin, g, out=kr)
         one_stream()
-    one_ms = time_call(one_stream, 10)
-    one_rot_ms = time_call(one_stream_rotating, 10)
-    rot_ms = time_call(lambda: step(rotate=True), 10)
+    nan3 = (float("nan"),) * 3
+    one_ms = time_call(one_stream, 10) if not args.quick else nan3
+    one_rot_ms = time_call(one_stream_rotating, 10) if not args.quick else nan3
+    rot_ms = time_call(lambda: step(rotate=True), 10) if not args.quick else nan3
 
     f_sparse = sparse_flops_performed(idx, w.N, w.block, w.d_h)
     f_lowrank = 8.0 * w.B * w.H * w.N * w.d_h * w.r

@@ -39,7 +39,9 @@
  *    the variant on that device). The cache is a set of atomics: calls from several threads are
  *    safe, and the value never changes once set.
  *  - Supported: d_h in {64, 128} for fp32, d_h == 128 for bf16; block in {32, 64, 128} (fp32) or
- *    {64, 128} (bf16); r even with 2 <= r <= d_h (fp32) or r in {16, 32, 64, 128} (bf16).
+ *    {64, 128} (bf16); r even with 2 <= r <= d_h (fp32) or r in {16, 32, 64, 128} (bf16);
+ *    N d_h < 2^31 and B H N < 2^31 (ROLA_ERR_UNSUPPORTED beyond); rope_ld <= 65536 and, in the
+ *    attention calls with the epilogue, N rope_ld < 2^31 (per-query offsets are 32-bit).
  */
 #ifndef ROLA_H_
 #define ROLA_H_

@@ -58,6 +58,8 @@ rola_status check_problem(const rola_problem* p, const char* fn, rola::Shape* ou
     return fail(ROLA_ERR_UNSUPPORTED, "%s: bf16 path is built for d_h=128 only (got %d)", fn, p->d_h);
   if ((u128)p->B * (u128)p->H * (u128)p->N * (u128)p->d_h >= ((u128)1 << 40))
     return fail(ROLA_ERR_UNSUPPORTED, "%s: tensor too large", fn);
+  if ((u128)p->N * (u128)p->d_h > (u128)((1ll << 31) - 1))
+    return fail(ROLA_ERR_UNSUPPORTED, "%s: N*d_h must be below 2^31", fn);
   if ((u128)p->B * (u128)p->H * (u128)p->N > (u128)((1ll << 31) - 1))
     return fail(ROLA_ERR_UNSUPPORTED, "%s: B*H*N must fit in int32", fn);
   *out = rola::Shape{p->B, p->H, p->N, p->d_h, p->T, p->Hs, p->Ws, p->dtype == ROLA_DTYPE_BF16};
@@ -96,8 +98,9 @@ rola_status check_feature(int32_t phi, int32_t order, const char* fn, int* feat)
 rola_status check_tables(const float* c, const float* s, int32_t ld, int32_t need, const char* fn) {
   if (!aligned(c) || !aligned(s))
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: rotary tables null or not 16-byte aligned", fn);
-  if (ld < need || (ld % 4) != 0)
-    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: rope_ld=%d must be a multiple of 4 and >= %d", fn, ld, need);
+  if (ld < need || (ld % 4) != 0 || ld > (1 << 16))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: rope_ld=%d must be a multiple of 4, >= %d and <= 65536",
+                fn, ld, need);
   return ROLA_OK;
 }
 
@@ -141,8 +144,8 @@ rola_status check_out(const rola::Shape& s, const void* out, std::initializer_li
     if (_s != ROLA_OK) return _s;     \
   } while (0)
 
-// Arguments of the attention + readout + combine calls, checked before anything is launched.
-// ws == nullptr: the call brings no workspace (the allocation-free form checks its static scratch).
+// Arguments of the attention + readout + combine calls other than the workspace, checked before
+// anything is launched.
 rola_status check_combine(const rola_problem* p, const void* Qr, const void* Kr, const void* V,
                           int32_t block, double sparsity, const int32_t* blk_idx,
                           float softmax_scale, const void* Qn, const void* Pq, int32_t r,
@@ -167,6 +170,8 @@ rola_status check_combine(const rola_problem* p, const void* Qr, const void* Kr,
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: pointer 'Qr' is not 16-byte aligned", fn);
   }
   TRY(check_tables(cos_tab, sin_tab, rope_ld, r / 2, fn));
+  if ((unsigned __int128)s->N * (unsigned)rope_ld > (unsigned __int128)((1ll << 31) - 1))
+    return fail(ROLA_ERR_UNSUPPORTED, "%s: N*rope_ld must be below 2^31", fn);
   if (!(softmax_scale > 0.f) || !isfinite(softmax_scale))
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: softmax_scale must be finite and positive", fn);
   if (!(eps_lr >= 0.f) || !isfinite(eps_lr) || !(eps >= 0.f) || !isfinite(eps))

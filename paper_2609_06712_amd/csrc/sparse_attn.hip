@@ -324,6 +324,10 @@ __device__ __forceinline__ void fuse_epilogue(const FuseArgs& fz, f32x16 (&acc)[
                                               bool qvalid, long head, int N, int q, int lane,
                                               bf16* __restrict__ O) {
   constexpr int D = 128;
+  // the query index through an empty asm: the epilogue's address arithmetic is not hoisted in front
+  // of the main loop, where it held registers across it (and spilled); the per-query offsets are
+  // 32-bit (the ABI bounds N d_h and N rope_ld below 2^31)
+  asm volatile("" : "+v"(q));
   const int hh = lane / 32, half = fz.r / 2;
   const int h = (int)(head % fz.H);
   const long bidx = head / fz.H;
@@ -343,7 +347,7 @@ __device__ __forceinline__ void fuse_epilogue(const FuseArgs& fz, f32x16 (&acc)[
   }
   const float rs = sqrtf(ss * (1.0f / D) + fz.eps);
   // Q^n operand (query q, d = 16s + 8(l/32) .. +7) and the token's gate logit
-  const bf16* Qq = fz.Qn + head * (long)N * D + (long)q * D;
+  const bf16* Qq = fz.Qn + head * (long)N * D + (uint32_t)q * (uint32_t)D;
   bf16x8 qn[8];
 #pragma unroll
   for (int s = 0; s < 8; ++s)
@@ -370,8 +374,8 @@ __device__ __forceinline__ void fuse_epilogue(const FuseArgs& fz, f32x16 (&acc)[
       const int J0 = 16 * t + 8 * jp + 4 * hh;  // half is a multiple of 8: 4 pairs valid or none
       float4 c4 = {1.f, 1.f, 1.f, 1.f}, s4 = {0.f, 0.f, 0.f, 0.f};
       if (qvalid && J0 < half) {
-        c4 = *reinterpret_cast<const float4*>(fz.cos_tab + (long)q * fz.ld + J0);
-        s4 = *reinterpret_cast<const float4*>(fz.sin_tab + (long)q * fz.ld + J0);
+        c4 = *reinterpret_cast<const float4*>(fz.cos_tab + (uint32_t)q * (uint32_t)fz.ld + J0);
+        s4 = *reinterpret_cast<const float4*>(fz.sin_tab + (uint32_t)q * (uint32_t)fz.ld + J0);
       }
       const float cc[4] = {c4.x, c4.y, c4.z, c4.w}, sn[4] = {s4.x, s4.y, s4.z, s4.w};
 #pragma unroll
@@ -412,7 +416,7 @@ __device__ __forceinline__ void fuse_epilogue(const FuseArgs& fz, f32x16 (&acc)[
   // (O^s / r_s + g O^lr) r_s  ==  O^s + (g r_s / rms(u)) u
   const float coef = sigmoid(lg) * rs * inv_u;
   if (qvalid) {
-    bf16* Oq = O + head * (long)N * D + (long)q * D;
+    bf16* Oq = O + head * (long)N * D + (uint32_t)q * (uint32_t)D;
 #pragma unroll
     for (int w = 0; w < 4; ++w)
 #pragma unroll
@@ -590,10 +594,10 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void s
     bf16x8 qf[8];
 #pragma unroll
     for (int s = 0; s < 8; ++s)
-      qf[s] = qvalid ? *reinterpret_cast<const bf16x8*>(Qh + (long)q * D + 16 * s + 8 * hh) : bf16x8{};
+      qf[s] = qvalid ? *reinterpret_cast<const bf16x8*>(Qh + (uint32_t)q * (uint32_t)D + 16 * s + 8 * hh) : bf16x8{};
     if (ap->rot_q && qvalid) {  // Q^r = R(Q^n): pairs 8s + 4(l/32) .. +3 of this lane's query
-      const float* ct = fz.cos_tab + (long)q * fz.ld + 4 * hh;
-      const float* st = fz.sin_tab + (long)q * fz.ld + 4 * hh;
+      const float* ct = fz.cos_tab + (uint32_t)q * (uint32_t)fz.ld + 4 * hh;
+      const float* st = fz.sin_tab + (uint32_t)q * (uint32_t)fz.ld + 4 * hh;
 #pragma unroll
       for (int s = 0; s < 8; ++s) {
         const float4 c = *reinterpret_cast<const float4*>(ct + 8 * s);
@@ -611,7 +615,7 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void s
     bf16x8 df[DQ ? 8 : 1];  // dQ mode: dO^T fragments, same layout as qf
     float lse_q = 0.f, dsum_q = 0.f;
     if constexpr (DQ) {
-      const bf16* dOq = ap->dO + head * (long)N * D + (long)q * D;
+      const bf16* dOq = ap->dO + head * (long)N * D + (uint32_t)q * (uint32_t)D;
 #pragma unroll
       for (int s = 0; s < 8; ++s)
         df[s] = qvalid ? *reinterpret_cast<const bf16x8*>(dOq + 16 * s + 8 * hh) : bf16x8{};
@@ -815,7 +819,7 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void s
 
     if constexpr (DQ) {  // dQ^T: lane = query, rows = channels 32w + 8j + 4(l/32) + i
       if (qvalid) {
-        float* dq = ap->dQ + head * (long)N * D + (long)q * D;
+        float* dq = ap->dQ + head * (long)N * D + (uint32_t)q * (uint32_t)D;
         const float sc = ap->scale;
 #pragma unroll
         for (int w = 0; w < 4; ++w)
@@ -839,7 +843,7 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void s
     }
     if (qvalid) {
       const float inv = 1.0f / l;
-      bf16* Oq = O + head * (long)N * D + (long)q * D;
+      bf16* Oq = O + head * (long)N * D + (uint32_t)q * (uint32_t)D;
 #pragma unroll
       for (int w = 0; w < 4; ++w)
 #pragma unroll
