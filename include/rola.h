@@ -188,7 +188,7 @@ rola_status rola_sparse_attn(const rola_problem* p, const void* Qr, const void* 
  * and the tables (rope_ld >= d_h/2 then) in the kernel's prologue and rounded exactly as
  * rola_rope_apply rounds them, so Q^r need not exist in memory; the results are bitwise those with
  * Qr = rola_rope_apply(Qn). Elsewhere Qr = NULL is ROLA_ERR_UNSUPPORTED. The same holds for the
- * _planned form below. */
+ * _planned and _noalloc forms below. */
 size_t rola_sparse_combine_workspace_bytes(const rola_problem* p, int32_t block, double sparsity,
                                            int32_t r);
 rola_status rola_sparse_attn_combine(const rola_problem* p, const void* Qr, const void* Kr,
@@ -216,6 +216,25 @@ rola_status rola_sparse_attn_combine_planned(
     int32_t r, const float* cos_tab, const float* sin_tab, int32_t rope_ld, const float* C,
     float eps_lr, const float* gate_logits, float eps, void* O, void* ws, size_t ws_bytes,
     hipStream_t stream);
+
+/* ---- allocation-free form ---------------------------------------------------------------------
+ * For callers that cannot allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc. rola_sparse_attn_combine_noalloc is rola_sparse_attn_combine
+ * without a workspace argument: its scratch (the work-queue counters, pair table and merged lists,
+ * the C^T fragments of the epilogue) lives in a static device array of ROLA_NOALLOC_SCRATCH_BYTES
+ * bytes, which the library holds on every device it runs on until the process ends; the call
+ * itself allocates nothing. A problem whose scratch (rola_sparse_combine_workspace_bytes) is larger
+ * is ROLA_ERR_UNSUPPORTED (the Wan2.1-14B 720p layer needs about 23 MB). Every call on a device
+ * shares that device's array and leaves its contents behind; each call writes everything it reads
+ * (the queue counters are cleared by the call), but calls that overlap in time on one device, from
+ * other streams or threads, race on the array and must be ordered by the caller. Results are
+ * bitwise those of rola_sparse_attn_combine. */
+#define ROLA_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+rola_status rola_sparse_attn_combine_noalloc(
+    const rola_problem* p, const void* Qr, const void* Kr, const void* V, int32_t block,
+    double sparsity, const int32_t* blk_idx, float softmax_scale, const void* Qn, const void* Pq,
+    int32_t r, const float* cos_tab, const float* sin_tab, int32_t rope_ld, const float* C,
+    float eps_lr, const float* gate_logits, float eps, void* O, hipStream_t stream);
 
 /* ---- backward of the sparse branch (fine-tuning, Sec. 4.5; Algorithm step 4) ------------------
  * rola_sparse_attn_lse is rola_sparse_attn (same workspace rule: ws NULL or ws_bytes >=

@@ -77,6 +77,10 @@ bool plan_used(const Shape& s, int block);
 // walk period of the kernel variant with fused rank r (0: plain attention). No-op elsewhere.
 hipError_t launch_sparse_plan(const Shape& s, int keep, const int32_t* idx, int r, void* ws,
                               hipStream_t st);
+// The per-device static scratch of the allocation-free entry point: its size, and its address on
+// the current device (asked once per device, then cached).
+size_t static_scratch_bytes();
+hipError_t static_scratch(void** ptr);
 
 // lowrank_bwd.hip: gradients of the low-rank branch and the gated fusion (bf16, d 128, r <= 64, SiLU
 // with the rotation outside). dOs bf16; the other gradients fp32; dP_q, dP_k summed over the batch,

@@ -560,6 +560,28 @@ rola_status rola_sparse_attn_combine_planned(
                      rope_ld, C, eps_lr, gate_logits, eps, O, ws, true, stream, __func__);
 }
 
+rola_status rola_sparse_attn_combine_noalloc(
+    const rola_problem* p, const void* Qr, const void* Kr, const void* V, int32_t block,
+    double sparsity, const int32_t* blk_idx, float softmax_scale, const void* Qn, const void* Pq,
+    int32_t r, const float* cos_tab, const float* sin_tab, int32_t rope_ld, const float* C,
+    float eps_lr, const float* gate_logits, float eps, void* O, hipStream_t stream) {
+  rola::Shape s;
+  TRY(check_combine(p, Qr, Kr, V, block, sparsity, blk_idx, softmax_scale, Qn, Pq, r, cos_tab,
+                    sin_tab, rope_ld, C, eps_lr, gate_logits, eps, O, __func__, &s));
+  const size_t need = rola_sparse_combine_workspace_bytes(p, block, sparsity, r);
+  if (need > rola::static_scratch_bytes())
+    return fail(ROLA_ERR_UNSUPPORTED,
+                "%s: this problem needs %zu bytes of scratch; the static scratch holds %zu "
+                "(use rola_sparse_attn_combine with a workspace)",
+                __func__, need, rola::static_scratch_bytes());
+  void* ws = nullptr;
+  hipError_t e = rola::static_scratch(&ws);
+  if (e != hipSuccess) return hip_status(e, __func__);
+  const int keep = rola_keep_blocks(rola::num_blocks(s.N, block), sparsity);
+  return run_combine(s, Qr, Kr, V, block, keep, blk_idx, softmax_scale, Qn, Pq, r, cos_tab, sin_tab,
+                     rope_ld, C, eps_lr, gate_logits, eps, O, ws, false, stream, __func__);
+}
+
 rola_status rola_lowrank_summary_ex(const rola_problem* p, const void* Kn, const void* V,
                                     const void* Pk, int32_t r, const float* cos_tab,
                                     const float* sin_tab, int32_t rope_ld, int32_t phi,

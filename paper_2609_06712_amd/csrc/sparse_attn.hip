@@ -24,9 +24,11 @@
 #include <algorithm>
 #include <atomic>
 #include <climits>
+#include <mutex>
 
 #include "common.h"
 #include "launch.h"
+#include "rola.h"
 
 namespace rola {
 namespace {
@@ -1138,6 +1140,14 @@ hipError_t prepare_groups(const Shape& s, int keep, const int32_t* idx, void* ws
   return hipGetLastError();
 }
 
+// Device scratch of the allocation-free entry point: one copy per device, alive until the process
+// ends. Host code never names the array itself (its host-side name is no device address): the
+// address each device gives for it is asked once per device, with that device current, and kept.
+constexpr size_t kStaticScratchBytes = ROLA_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+std::mutex g_scratch_mutex;
+
 }  // namespace
 
 size_t sparse_workspace_bytes(const Shape& s, int block, int keep) {
@@ -1179,6 +1189,28 @@ hipError_t launch_sparse_plan(const Shape& s, int keep, const int32_t* idx, int 
   if (!plan_used(s, 64)) return hipSuccess;
   Groups gr;
   return prepare_groups<false>(s, keep, idx, ws, r, st, gr);
+}
+
+size_t static_scratch_bytes() { return kStaticScratchBytes; }
+
+hipError_t static_scratch(void** ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (e != hipSuccess) return e;
+      if (!p) return hipErrorInvalidSymbol;
+      g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *ptr = p;
+  return hipSuccess;
 }
 
 hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, const void* V,

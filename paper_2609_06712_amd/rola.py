@@ -72,6 +72,8 @@ SIGNATURES = {
     "rola_sparse_attn_combine": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p, _i32, _p, _p,
                                         _i32, _p, _f32, _p, _f32, _p, _p, _sz, _p]),
     "rola_sparse_plan": (_i32, [_PP, _i32, _f64, _p, _i32, _p, _sz, _p]),
+    "rola_sparse_attn_combine_noalloc": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p, _i32,
+                                                _p, _p, _i32, _p, _f32, _p, _f32, _p, _p]),
     "rola_sparse_attn_combine_planned": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p, _i32,
                                                 _p, _p, _i32, _p, _f32, _p, _f32, _p, _p, _sz, _p]),
 }
@@ -640,6 +642,25 @@ def rola_sparse_attn_combine_planned(Qr, Kr, V, grid, block, sparsity, blk_idx, 
                                                 _ptr(Pq), r, _ptr(cos), _ptr(sin), ld, _ptr(C), eps_lr,
                                                 _ptr(logits), eps, _ptr(out), _ptr(ws), ws.numel(),
                                                 _stream(stream)), "rola_sparse_attn_combine_planned")
+    return out
+
+
+def rola_sparse_attn_combine_noalloc(Qr, Kr, V, grid, block, sparsity, blk_idx, Qn, Pq, r, cos, sin,
+                                     C, logits, out, scale=None, eps_lr=1e-6, eps=1e-6,
+                                     stream=None):
+    """rola_sparse_attn_combine with the library's static device scratch instead of a workspace:
+    nothing is allocated (the output `out` is the caller's)."""
+    a = _Args()
+    ld = _combine_args(a, Qr, Kr, V, block, sparsity, blk_idx, Qn, Pq, r, cos, sin, C, logits)
+    a.act(out, "out", Qn)
+    a.done()
+    prob = problem_of(Qn, grid)
+    scale = prob.d_h ** -0.5 if scale is None else scale
+    _check(LIB.rola_sparse_attn_combine_noalloc(ctypes.byref(prob), _ptr(Qr), _ptr(Kr), _ptr(V),
+                                                block, sparsity, _ptr(blk_idx), scale, _ptr(Qn),
+                                                _ptr(Pq), r, _ptr(cos), _ptr(sin), ld, _ptr(C), eps_lr,
+                                                _ptr(logits), eps, _ptr(out), _stream(stream)),
+           "rola_sparse_attn_combine_noalloc")
     return out
 
 
