@@ -328,24 +328,43 @@ def train_bench(reps: int) -> None:
                         dtype=torch.uint8, device=dev)
     dOs = R.rola_lowrank_backward(inp["Qn"], inp["Kn"], inp["V"], inp["Pq"], inp["Pk"], w.r, cos, sin,
                                   C, os_, inp["logits"], dO, g, ws=ws_lr)[0]
+    # the paper's default rank: projections of rank 64 drawn like the workload's own
+    r64 = 64
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(64)
+    P64 = [(torch.randn((w.H, r64, w.d_h), generator=gen, device=dev) / w.d_h ** 0.5).to(torch.bfloat16)
+           for _ in range(2)]
+    C64, _ = R.rola_lowrank_summary(inp["Kn"], inp["V"], P64[1], r64, cos, sin, g)
+    ws_lr64 = torch.empty(R.LIB.rola_lowrank_backward_workspace_bytes(ctypes.byref(prob), r64),
+                          dtype=torch.uint8, device=dev)
+    # HBM bytes the low-rank backward must move: Q^n, K^n, V, O^s, dO read and dO^s written (bf16),
+    # dQ^n, dK^n, dV written (fp32)
+    act = w.B * w.H * w.N * w.d_h
+    lr_bytes = 6 * 2 * act + 3 * 4 * act
     rows = [
         ("sparse forward with lse", lambda: R.rola_sparse_attn_lse(qr, kr, inp["V"], g, w.block,
                                                                    w.sparsity, idx, out=os_, lse=lse),
-         f_fwd),
-        ("low-rank + fusion backward", lambda: R.rola_lowrank_backward(
+         f_fwd, None),
+        (f"low-rank + fusion backward, r {w.r}", lambda: R.rola_lowrank_backward(
             inp["Qn"], inp["Kn"], inp["V"], inp["Pq"], inp["Pk"], w.r, cos, sin, C, os_,
-            inp["logits"], dO, g, ws=ws_lr), None),
+            inp["logits"], dO, g, ws=ws_lr), None, lr_bytes),
+        (f"low-rank + fusion backward, r {r64}", lambda: R.rola_lowrank_backward(
+            inp["Qn"], inp["Kn"], inp["V"], P64[0], P64[1], r64, cos, sin, C64, os_,
+            inp["logits"], dO, g, ws=ws_lr64), None, lr_bytes),
         ("sparse attention backward", lambda: R.rola_sparse_attn_backward(
-            qr, kr, inp["V"], g, w.block, w.sparsity, idx, os_, lse, dOs, ws=ws_sp), 2.5 * f_fwd),
+            qr, kr, inp["V"], g, w.block, w.sparsity, idx, os_, lse, dOs, ws=ws_sp), 2.5 * f_fwd, None),
     ]
     print("## Fine-tuning pass of the module, " + w.name + "\n")
-    print("| step | ms (median) | TFLOP/s (algorithmic) | % of bf16 peak |")
-    print("|---|---|---|---|", flush=True)
-    for name, fn, flops in rows:
+    print("| step | ms (median) | TFLOP/s (algorithmic) | % of bf16 peak | TB/s (algorithmic bytes) | "
+          "% of HBM peak |")
+    print("|---|---|---|---|---|---|", flush=True)
+    for name, fn, flops, nbytes in rows:
         ms = time_call(fn, reps)[0]
         tf = f"{flops / ms / 1e9:.1f}" if flops else "-"
         pc = f"{100 * flops / ms / 1e9 / PEAK_BF16_TFLOPS:.1f}" if flops else "-"
-        print(f"| {name} | {ms:.3f} | {tf} | {pc} |", flush=True)
+        tb = f"{nbytes / ms / 1e9:.2f}" if nbytes else "-"
+        pb = f"{100 * nbytes / ms / 1e6 / PEAK_HBM_GBS:.1f}" if nbytes else "-"
+        print(f"| {name} | {ms:.3f} | {tf} | {pc} | {tb} | {pb} |", flush=True)
     print()
 
 

@@ -106,9 +106,12 @@ def test_sparse_backward_many_groups():
             assert e <= 1e-2, (n, e)
 
 
-@pytest.mark.parametrize("r,B", [(32, 1), (16, 2), (64, 1)])
-def test_lowrank_backward(r, B):
-    """The low-rank branch + fusion backward against the oracle, per head, from the GPU's own O^s."""
+@pytest.mark.parametrize("r,B,eps_lr", [(32, 1, 1e-6), (16, 2, 1e-6), (64, 1, 1e-6), (64, 2, 0.0),
+                                         (32, 1, 0.0)])
+def test_lowrank_backward(r, B, eps_lr):
+    """The low-rank branch + fusion backward against the oracle, per head, from the GPU's own O^s.
+    390 tokens: the last 64-token chunk holds 6, so padding tokens run through every step; with
+    eps_lr = 0 they must still contribute nothing (their RMSNorm denominator is 0)."""
     w = synth.WAN_1_3B_480P.replace(grid=(3, 10, 13), H=2, B=B, r=r)
     inp = synth.make_inputs(w, 8)
     d = {k: v.cuda() for k, v in inp.items()}
@@ -120,18 +123,21 @@ def test_lowrank_backward(r, B):
     os_ = torch.randn(d["Qn"].shape, generator=gen).to(torch.bfloat16).cuda()
     dO = torch.randn(d["Qn"].shape, generator=gen).to(torch.bfloat16).cuda()
     dOs, dQn, dKn, dV, dPq, dPk, dlog = R.rola_lowrank_backward(
-        d["Qn"], d["Kn"], d["V"], d["Pq"], d["Pk"], r, cos, sin, C, os_, d["logits"], dO, g)
+        d["Qn"], d["Kn"], d["V"], d["Pq"], d["Pk"], r, cos, sin, C, os_, d["logits"], dO, g,
+        eps_lr=eps_lr)
     torch.cuda.synchronize()
     ocos, osin = O.rope_tables(*g, w.split)
     f = synth.to_f64(inp)
     want = {(b, h): G.lowrank_combine_grads(f["Qn"][b, h], f["Kn"][b, h], f["V"][b, h], f["Pq"][h],
                                             f["Pk"][h], _f64(os_[b, h]), f["logits"][b], ocos, osin,
-                                            _f64(dO[b, h]))
+                                            _f64(dO[b, h]), eps_lr=eps_lr)
             for b in range(w.B) for h in range(w.H)}
+    for name, t in (("dPq", dPq), ("dPk", dPk), ("dlogits", dlog)):
+        assert torch.isfinite(t).all(), name
     for (b, h), wt in want.items():
         errs = {n: _rel(_f64(t[b, h]), wt[k]) for n, t, k in
                 (("dOs", dOs, "dos"), ("dQn", dQn, "dqn"), ("dKn", dKn, "dkn"), ("dV", dV, "dv"))}
-        print(f"[parity] lowrank backward r{r} b{b} h{h}: " +
+        print(f"[parity] lowrank backward r{r} eps_lr {eps_lr:g} b{b} h{h}: " +
               ", ".join(f"{n} rel {e:.2e}" for n, e in errs.items()), flush=True)
         for n, e in errs.items():
             assert e <= 1e-2, (n, e)
@@ -143,11 +149,12 @@ def test_lowrank_backward(r, B):
     assert _rel(_f64(dlog), ref) <= 1e-2
 
 
-def test_lowrank_backward_multistep():
+@pytest.mark.parametrize("r", [32, 64])
+def test_lowrank_backward_multistep(r):
     """40 heads of 7800 tokens: every chunk of the low-rank backward then spans two 64-token steps
     (the last one ragged), so the outer products accumulate across steps. Sampled heads against
     the oracle; dP summed over the batch (B = 1: the head's own)."""
-    w = synth.WAN_1_3B_480P.replace(grid=(5, 30, 52), H=40, B=1, r=32)
+    w = synth.WAN_1_3B_480P.replace(grid=(5, 30, 52), H=40, B=1, r=r)
     inp = synth.make_inputs(w, 11)
     d = {k: v.cuda() for k, v in inp.items()}
     g = w.grid
@@ -169,7 +176,7 @@ def test_lowrank_backward_multistep():
         errs = {n: _rel(_f64(t), wt[k]) for n, t, k in
                 (("dOs", dOs[0, h], "dos"), ("dQn", dQn[0, h], "dqn"), ("dKn", dKn[0, h], "dkn"),
                  ("dV", dV[0, h], "dv"), ("dPq", dPq[h], "dPq"), ("dPk", dPk[h], "dPk"))}
-        print(f"[parity] lowrank backward 40 heads x 7800 tokens h{h}: " +
+        print(f"[parity] lowrank backward r{r} 40 heads x 7800 tokens h{h}: " +
               ", ".join(f"{n} rel {e:.2e}" for n, e in errs.items()), flush=True)
         for n, e in errs.items():
             assert e <= 1e-2, (n, e)
