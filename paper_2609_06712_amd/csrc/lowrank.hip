@@ -91,9 +91,12 @@ int summary_chunk_len(const Shape& s) {
 // ------------------------------------------------------------------------------------------------
 // bf16 summary
 // ------------------------------------------------------------------------------------------------
+// split = 2: each (b, h, chunk) is served by two workgroups, one per half of the pair tiles (r = 128
+// as two r = 64 halves: one workgroup holding all four tiles spills). The two sit eight launch
+// slots apart, i.e. on the same XCD at about the same time, so the second reads K^n and V from L2.
 template <int JT, bool GENERIC>
 __global__ __launch_bounds__(256, JT == 1 ? 2 : 1) void summary_mfma_kernel(
-    int N, int H, int r, int chunk_len, int n_chunks, int total, int ld, int feat,
+    int N, int H, int r, int chunk_len, int n_chunks, int total, int split, int ld, int feat,
     const bf16* __restrict__ Kn, const bf16* __restrict__ V, const bf16* __restrict__ Pk,
     const float* __restrict__ cos_tab, const float* __restrict__ sin_tab,
     float* __restrict__ part) {
@@ -106,7 +109,12 @@ __global__ __launch_bounds__(256, JT == 1 ? 2 : 1) void summary_mfma_kernel(
   const int BH = total / n_chunks;
   // heads minor in launch order, dealt round-robin to the XCDs: 2.7 % faster at the 14B shape than
   // giving each XCD a contiguous token range of all heads (which shared the table rows in L2)
-  const int L = blockIdx.x;
+  int L = blockIdx.x, jt0 = 0;  // jt0: first pair tile of this workgroup
+  if (split == 2) {
+    L = (int)(blockIdx.x / 16) * 8 + blockIdx.x % 8;
+    jt0 = JT * ((blockIdx.x / 8) % 2);
+    if (L >= total) return;  // the grid is rounded up to whole groups of 16
+  }
   const int head = L % BH, chunk = L / BH;
   const int h = head % H;
   const int tid = threadIdx.x, lane = tid % 64, lr = lane % 16, g = lane / 16;
@@ -119,7 +127,7 @@ __global__ __launch_bounds__(256, JT == 1 ? 2 : 1) void summary_mfma_kernel(
   bf16x8 pe[JT][4], po[JT][4];
 #pragma unroll
   for (int jt = 0; jt < JT; ++jt) {
-    const int j = 16 * jt + lr;
+    const int j = 16 * (jt0 + jt) + lr;
 #pragma unroll
     for (int kc = 0; kc < 4; ++kc) {
       if (j < half) {
@@ -177,42 +185,49 @@ __global__ __launch_bounds__(256, JT == 1 ? 2 : 1) void summary_mfma_kernel(
   for (int w = 0; w < 8; ++w)
     vo[w] = vr * 256 + (((2 * w + (mp >> 1)) ^ ((vr & 7) << 1)) << 4) + ((mp & 1) << 3);
 
-  bf16x8 kf[2][4];  // K^n operand rows of the next step (prefetched one step ahead)
-  auto load_regs = [&](int base) {
+  // A step reads K^n operand rows from registers and V from the wave's own rows of an LDS stage.
+  // Each wave fills and reads only its own 32 rows of a stage, so the waves run their pipelines
+  // independently, with no workgroup barrier: the K^n and V loads of step t+1 are issued before the
+  // wave waits for those of step t, into registers and a stage that only this wave used at step
+  // t-1. The rotary-table entries (L2-resident rows shared by all heads) are loaded at the start of
+  // their own step: a second register set for them spills. At the 14B shape this loop is 1.5 %
+  // faster than a workgroup-synchronous one at r = 32 and 12 % at r = 64; double-buffered tables
+  // made it 19 % slower at r = 32.
+  struct StepRegs {
+    bf16x8 k[2][4];
+  };
+  float tcs[JT][2][4], tsn[JT][2][4];  // this step's table entries
+  auto issue_step = [&](int base, int buf, StepRegs& R) {
+    // the previous step's LDS reads of this stage are complete before the DMA may overwrite it
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+    issue_v(base, buf);
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt) {
       const int tok = base + wave * 32 + tt * 16 + lr;
 #pragma unroll
       for (int kc = 0; kc < 4; ++kc)
-        kf[tt][kc] = tok < t1 ? *reinterpret_cast<const bf16x8*>(Kh + (long)tok * D + 32 * kc + 8 * g)
-                              : bf16x8{};
+        R.k[tt][kc] = tok < t1 ? *reinterpret_cast<const bf16x8*>(Kh + (long)tok * D + 32 * kc + 8 * g)
+                               : bf16x8{};
     }
   };
-
-  auto step = [&](int base, int buf) {
-    bf16x8 kc_cur[2][4];
-#pragma unroll
-    for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-      for (int kc = 0; kc < 4; ++kc) kc_cur[tt][kc] = kf[tt][kc];
-    float tc[JT][2][4], ts[JT][2][4];  // rotary table entries of this step (L2-resident rows)
+  auto load_tables = [&](int base) {
 #pragma unroll
     for (int jt = 0; jt < JT; ++jt)
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const int tok = base + wave * 32 + tt * 16 + 4 * g + v, j = 16 * jt + lr;
+          const int tok = base + wave * 32 + tt * 16 + 4 * g + v, j = 16 * (jt0 + jt) + lr;
           const bool ok = tok < t1 && j < half;
-          tc[jt][tt][v] = ok ? cos_tab[(long)tok * ld + j] : 1.f;
-          ts[jt][tt][v] = ok ? sin_tab[(long)tok * ld + j] : 0.f;
+          tcs[jt][tt][v] = ok ? cos_tab[(long)tok * ld + j] : 1.f;
+          tsn[jt][tt][v] = ok ? sin_tab[(long)tok * ld + j] : 0.f;
         }
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's V tile loads (and register loads) of this step
-    __syncthreads();                // all waves' V loads landed; the other stage is free again
-    if (base + TOK < t1) {
-      issue_v(base + TOK, buf ^ 1);
-      load_regs(base + TOK);
-    }
+  };
+  // vector-memory instructions per wave of one issue_step
+  constexpr int kStepLoads = 8 + 8;
+  constexpr int kAhead = kStepLoads < 63 ? kStepLoads : 63;
+
+  auto compute = [&](const StepRegs& R, int buf) {
     const char* Vs = lds + buf * TILE;
     typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 #pragma unroll
@@ -223,14 +238,13 @@ __global__ __launch_bounds__(256, JT == 1 ? 2 : 1) void summary_mfma_kernel(
         f32x4 ye = {0.f, 0.f, 0.f, 0.f}, yo = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kc = 0; kc < 4; ++kc) {
-          ye = mfma16x16x32(kc_cur[tt][kc], pe[jt][kc], ye);
-          yo = mfma16x16x32(kc_cur[tt][kc], po[jt][kc], yo);
+          ye = mfma16x16x32(R.k[tt][kc], pe[jt][kc], ye);
+          yo = mfma16x16x32(R.k[tt][kc], po[jt][kc], yo);
         }
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const float c = tc[jt][tt][v], s = ts[jt][tt][v];
           float ke = ye[v], ko = yo[v];
-          feature_pair<GENERIC>(ke, ko, c, s, feat);
+          feature_pair<GENERIC>(ke, ko, tcs[jt][tt][v], tsn[jt][tt][v], feat);
           ze[jt] += ke;
           zo[jt] += ko;
           be[4 * tt + v] = (bf16)ke;
@@ -247,15 +261,27 @@ __global__ __launch_bounds__(256, JT == 1 ? 2 : 1) void summary_mfma_kernel(
       }
     }
   };
+  // One step: start the next step's loads, wait for this step's (the next step's stay in flight),
+  // compute.
+  auto step = [&](int base, int buf, const StepRegs& cur, StepRegs& nxt) {
+    load_tables(base);
+    if (base + TOK < t1) {
+      issue_step(base + TOK, buf ^ 1, nxt);
+      __builtin_amdgcn_s_waitcnt((kAhead & 15) | ((kAhead >> 4) << 14) | (7 << 4) | (15 << 8));
+    } else {
+      __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
+    }
+    compute(cur, buf);
+  };
 
-  issue_v(t0, 0);
-  load_regs(t0);
+  StepRegs ra, rb;
+  issue_step(t0, 0, ra);
   int base = t0;
   for (; base + TOK < t1; base += 2 * TOK) {
-    step(base, 0);
-    step(base + TOK, 1);
+    step(base, 0, ra, rb);
+    step(base + TOK, 1, rb, ra);
   }
-  if (base < t1) step(base, 0);
+  if (base < t1) step(base, 0, ra, rb);
 
   // z: the four lane groups hold different tokens of the same pair j
 #pragma unroll
@@ -299,7 +325,7 @@ __global__ __launch_bounds__(256, JT == 1 ? 2 : 1) void summary_mfma_kernel(
     float* P = part + ((long)head * n_chunks + chunk) * (long)(r * D + r);
 #pragma unroll
     for (int jt = 0; jt < JT; ++jt) {
-      const int j = 16 * jt + lr;
+      const int j = 16 * (jt0 + jt) + lr;
       if (j >= half) continue;
 #pragma unroll
       for (int w = 0; w < 8; ++w)
@@ -733,9 +759,11 @@ hipError_t summary_mfma(const Shape& s, const void* Kn, const void* V, const voi
                         const float* ct, const float* st_, int ld, int feat, float* part,
                         int chunk_len, int n_chunks, hipStream_t st) {
   const int total = s.B * s.H * n_chunks;
-  hipLaunchKernelGGL((summary_mfma_kernel<JT, GENERIC>), dim3(total), dim3(256), 0, st, s.N, s.H,
-                     r, chunk_len, n_chunks, total, ld, feat, (const bf16*)Kn, (const bf16*)V,
-                     (const bf16*)Pk, ct, st_, part);
+  const int split = r > 32 * JT ? 2 : 1;  // r = 128 on the two-tile kernel
+  const unsigned grid = split == 2 ? (unsigned)((total + 7) / 8 * 16) : (unsigned)total;
+  hipLaunchKernelGGL((summary_mfma_kernel<JT, GENERIC>), dim3(grid), dim3(256), 0, st, s.N, s.H,
+                     r, chunk_len, n_chunks, total, split, ld, feat, (const bf16*)Kn,
+                     (const bf16*)V, (const bf16*)Pk, ct, st_, part);
   return hipGetLastError();
 }
 
@@ -826,8 +854,8 @@ hipError_t launch_lowrank_summary(const Shape& s, const void* Kn, const void* V,
     else if (r <= 64)
       e = summary_mfma_feat<2>(s, Kn, V, Pk, r, cos_tab, sin_tab, ld, feat, part, chunk_len,
                                n_chunks, st);
-    else
-      e = summary_mfma_feat<4>(s, Kn, V, Pk, r, cos_tab, sin_tab, ld, feat, part, chunk_len,
+    else  // r = 128: two workgroups of two pair tiles each per chunk
+      e = summary_mfma_feat<2>(s, Kn, V, Pk, r, cos_tab, sin_tab, ld, feat, part, chunk_len,
                                n_chunks, st);
   } else {
     const dim3 grid(n_chunks, s.H, s.B);

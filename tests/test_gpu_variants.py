@@ -30,7 +30,7 @@ def _workload(dtype, r):
     return synth.WAN_1_3B_480P.replace(grid=(3, 10, 13), H=2, r=r)  # 390 tokens: ragged tiles
 
 
-@pytest.mark.parametrize("dtype,r", [("bf16", 32), ("bf16", 64), ("f32", 16)])
+@pytest.mark.parametrize("dtype,r", [("bf16", 32), ("bf16", 64), ("bf16", 128), ("f32", 16)])
 @pytest.mark.parametrize("phi,order", VARIANTS, ids=[f"{p}-{o}" for p, o in VARIANTS])
 def test_lowrank_variant_parity(dtype, r, phi, order):
     w = _workload(dtype, r)
@@ -70,6 +70,24 @@ def test_lowrank_variant_parity(dtype, r, phi, order):
             fw = O.features(qn, f64["Pq"][h], ocos, osin, phi, order)
             np.testing.assert_allclose(T.to_np(fq[b, h]), fw, rtol=1e-4, atol=1e-4,
                                        err_msg=f"features {phi}/{order}")
+
+
+def test_summary_r128_many_chunks():
+    """r = 128 runs the summary as two workgroups per chunk, one per half of the rotation pairs: a
+    1.3B-shaped grid (32760 tokens, 256 chunks per head), whole heads against the oracle."""
+    w = synth.WAN_1_3B_480P.replace(H=4, r=128)
+    inp = synth.make_inputs(w, 9, device="cuda")
+    g = w.grid
+    prob = R.problem(w.B, w.H, w.N, w.d_h, g, w.dtype)
+    cos, sin = R.rola_rope_tables(prob, w.split, w.base)
+    C, z = R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], w.r, cos, sin, g)
+    torch.cuda.synchronize()
+    ocos, osin = O.rope_tables(*g, w.split, w.base)
+    f64 = synth.to_f64({k: inp[k][0, [0, 3]] for k in ("Kn", "V")} | {"Pk": inp["Pk"][[0, 3]]})
+    for i, h in enumerate((0, 3)):
+        Cw, zw = O.lowrank_summary(f64["Kn"][i], f64["V"][i], f64["Pk"][i], ocos, osin)
+        T.assert_frob(T.to_np(C[0, h]), Cw, w.dtype, f"C r128 h{h}")
+        T.assert_frob(T.to_np(z[0, h]), zw, w.dtype, f"z r128 h{h}")
 
 
 @pytest.mark.parametrize("order", ["outside", "inside", "none"])
