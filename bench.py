@@ -461,12 +461,13 @@ def main():
                           dtype=torch.uint8, device=dev)
     # The layer (steps a1-a5 of the hot path; the backbone's rotation is the input) on two streams.
     # Main stream: the block means of Q^r and K^r, the block scores and top-k, the attention's
-    # pairing and list merge; side stream, forked once the pooling (the HBM-bound part of the
-    # selection) is done: the low-rank summary, beside the compute-bound scores and top-k and the
-    # pairing (whose greedy pass keeps one wave per head busy). After both: the block-sparse
-    # attention with the low-rank readout and the gated combine in its epilogue (O^s and O^lr
-    # never reach memory). rotate=True starts from Q^n, K^n: the rotating pooling passes write Q^r
-    # and K^r (Algorithm step 3 fused with the pooling).
+    # pairing and list merge; side stream, forked once the block lists exist: the low-rank summary,
+    # beside the pairing, whose passes are latency-bound (its greedy pass keeps one wave per head
+    # busy) and leave the chip's bandwidth to the summary. Forked after the pooling instead, the
+    # summary slows the score and top-k kernels beside it by more than it saves (0.1 ms per layer).
+    # After both: the block-sparse attention with the low-rank readout and the gated combine in its
+    # epilogue (O^s and O^lr never reach memory). rotate=True starts from Q^n, K^n: the rotating
+    # pooling passes write Q^r and K^r (Algorithm step 3 fused with the pooling).
     names = ["pool", "select", "plan", "attention_readout_combine"]
 
     def step(ev=None, sev=None, rotate=False):
@@ -482,6 +483,8 @@ def main():
             R.rola_rope_pool(qr, None, None, g, w.block, xbar=qbar)
             R.rola_rope_pool(kr, None, None, g, w.block, xbar=kbar)
         mark(1)
+        R.rola_block_select_pooled(qbar, kbar, kr, g, w.block, w.sparsity, out=idx, ws=ws_pool)
+        mark(2)
         fork.record(main_st)
         side_st.wait_event(fork)
         if sev is not None:
@@ -491,8 +494,6 @@ def main():
         if sev is not None:
             sev[1].record(side_st)
         join.record(side_st)
-        R.rola_block_select_pooled(qbar, kbar, kr, g, w.block, w.sparsity, out=idx, ws=ws_pool)
-        mark(2)
         R.rola_sparse_plan(idx, kr, g, w.block, w.sparsity, w.r, ws_sp)
         main_st.wait_event(join)
         mark(3)
