@@ -1,10 +1,12 @@
 """Benchmark of one RoLA attention layer (sparse + rotary low-rank branches) on one MI355X.
 
 One step = the whole hot path over one batch of synthetic input already resident in HBM, as C-ABI
-calls on two HIP streams: on the main stream the block means of Q^r and K^r, the block scores and
-top-k, and the attention's pairing and list merge (rola_sparse_plan); on a second stream, once the
-pooling is done, the low-rank summary; after the two join, the block-sparse attention with the
-low-rank readout and the gated combine in its epilogue. Workload: the Wan2.1-14B-shaped 720p layer
+calls on two HIP streams: on the main stream the block means of Q^r and K^r (with each key block's
+largest key norm), the block scores and top-k, and the attention's pairing and list merge
+(rola_sparse_plan); on a second stream, once the top-k is done, the low-rank summary; after the two
+join, the block-sparse attention with the low-rank readout and the gated combine in its epilogue,
+given the key norms so that it can take the score bound as its softmax reference. Workload: the
+Wan2.1-14B-shaped 720p layer
 (B1 H40 d128, 21x45x80 grid = 75600 tokens, block 64, 90 % sparsity -> 118 of 1182 key blocks, r 32,
 bf16). The backbone's own steps (rotary tables, Q^r = R(Q^n), K^r = R(K^n)) are the step's input;
 the same layer starting from Q^n, K^n (rotation fused into the pooling passes) is timed beside it.
@@ -457,6 +459,7 @@ def main():
     side_st = torch.cuda.Stream(device=dev)  # default priority
     qbar = torch.empty((w.B, w.H, nb, w.d_h), dtype=torch.float32, device=dev)
     kbar = torch.empty_like(qbar)
+    knorm = torch.empty((w.B, w.H, nb), dtype=torch.float32, device=dev)  # per key block max |k^r|
     ws_pool = torch.empty(R.LIB.rola_select_pooled_workspace_bytes(ctypes.byref(prob), w.block),
                           dtype=torch.uint8, device=dev)
     # The layer (steps a1-a5 of the hot path; the backbone's rotation is the input) on two streams.
@@ -478,10 +481,10 @@ def main():
         mark(0)
         if rotate:
             R.rola_rope_pool(inp["Qn"], cos, sin, g, w.block, xr=qr, xbar=qbar)
-            R.rola_rope_pool(inp["Kn"], cos, sin, g, w.block, xr=kr, xbar=kbar)
+            R.rola_rope_pool(inp["Kn"], cos, sin, g, w.block, xr=kr, xbar=kbar, xnorm=knorm)
         else:
             R.rola_rope_pool(qr, None, None, g, w.block, xbar=qbar)
-            R.rola_rope_pool(kr, None, None, g, w.block, xbar=kbar)
+            R.rola_rope_pool(kr, None, None, g, w.block, xbar=kbar, xnorm=knorm)
         mark(1)
         R.rola_block_select_pooled(qbar, kbar, kr, g, w.block, w.sparsity, out=idx, ws=ws_pool)
         mark(2)
@@ -499,7 +502,7 @@ def main():
         mark(3)
         R.rola_sparse_attn_combine_planned(qr, kr, inp["V"], g, w.block, w.sparsity, idx, inp["Qn"],
                                            inp["Pq"], w.r, cos, sin, C, inp["logits"], ws_sp,
-                                           out=out)
+                                           out=out, key_norm=knorm)
         mark(4)
 
     if args.calibration_copy:  # a plain copy of known size, for scaling FETCH_SIZE / WRITE_SIZE

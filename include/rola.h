@@ -127,10 +127,13 @@ rola_status rola_rope_backward_accumulate(const rola_problem* p, const float* dY
  * each other. Tables as in rola_rope_apply (rope_ld >= d_h/2). Built for d_h = 128
  * (ROLA_ERR_UNSUPPORTED otherwise). With both tables NULL, X is taken as already rotated (Q^r or
  * K^r): only the means are computed (rope_ld is ignored, Xr must be NULL), on any supported d_h,
- * bitwise those of rola_block_select. */
+ * bitwise those of rola_block_select. Xnorm (optional, 16-byte aligned, fp32 [B, H, n_blocks]):
+ * per block the largest norm |x| of its rows (rotated and rounded, fp32 sums of squares); for K
+ * this is the key_norm the fused attention calls take to bound their scores. It must not overlap
+ * the other buffers. */
 rola_status rola_rope_pool(const rola_problem* p, const void* X, const float* cos_tab,
                            const float* sin_tab, int32_t rope_ld, int32_t block, void* Xr,
-                           float* Xbar, hipStream_t stream);
+                           float* Xbar, float* Xnorm, hipStream_t stream);
 
 /* ---- sparse branch (Algorithm step 4; Sec. 4 opening: standard block-sparse attention) -------- */
 
@@ -187,8 +190,17 @@ rola_status rola_sparse_attn(const rola_problem* p, const void* Qr, const void* 
  * Qr may be NULL on the fused path (bf16, r 16-64): the queries are then R(Q^n), rotated from Qn
  * and the tables (rope_ld >= d_h/2 then) in the kernel's prologue and rounded exactly as
  * rola_rope_apply rounds them, so Q^r need not exist in memory; the results are bitwise those with
- * Qr = rola_rope_apply(Qn). Elsewhere Qr = NULL is ROLA_ERR_UNSUPPORTED. The same holds for the
- * _planned and _noalloc forms below. */
+ * Qr = rola_rope_apply(Qn). Elsewhere Qr = NULL is ROLA_ERR_UNSUPPORTED.
+ * key_norm (optional, 16-byte aligned, fp32 [B, H, n_blocks], must not overlap O): for every key
+ * block an upper bound on the norms |k^r| of its keys, e.g. the Xnorm of rola_rope_pool on K. On
+ * the fused bf16 path with 64-token blocks and a workspace, every pair of query blocks then takes
+ * b, the largest bound among the key blocks it walks: each scaled score of a query q lies within
+ * B = |q| b scale log2(e) of zero, and every wave of 32 queries whose B are all at most 40 uses B
+ * as the fixed reference of its online softmax (no running maximum, no rescaling), which keeps
+ * each probability in [2^-80, 1]; other waves track the running maximum as without key_norm. The
+ * two references give the same softmax up to rounding (the bf16 rounding of the probabilities and
+ * the order of the fp32 sums). With key_norm NULL, or on other paths, it is not read.
+ * The same holds for the _planned and _noalloc forms below. */
 size_t rola_sparse_combine_workspace_bytes(const rola_problem* p, int32_t block, double sparsity,
                                            int32_t r);
 rola_status rola_sparse_attn_combine(const rola_problem* p, const void* Qr, const void* Kr,
@@ -196,8 +208,9 @@ rola_status rola_sparse_attn_combine(const rola_problem* p, const void* Qr, cons
                                      const int32_t* blk_idx, float softmax_scale, const void* Qn,
                                      const void* Pq, int32_t r, const float* cos_tab,
                                      const float* sin_tab, int32_t rope_ld, const float* C,
-                                     float eps_lr, const float* gate_logits, float eps, void* O,
-                                     void* ws, size_t ws_bytes, hipStream_t stream);
+                                     float eps_lr, const float* gate_logits, float eps,
+                                     const float* key_norm, void* O, void* ws, size_t ws_bytes,
+                                     hipStream_t stream);
 
 /* The same call in two parts, so that other work can run between them (e.g. the low-rank summary,
  * which the epilogue needs, on a second stream while the pairs are planned). rola_sparse_plan
@@ -214,8 +227,8 @@ rola_status rola_sparse_attn_combine_planned(
     const rola_problem* p, const void* Qr, const void* Kr, const void* V, int32_t block,
     double sparsity, const int32_t* blk_idx, float softmax_scale, const void* Qn, const void* Pq,
     int32_t r, const float* cos_tab, const float* sin_tab, int32_t rope_ld, const float* C,
-    float eps_lr, const float* gate_logits, float eps, void* O, void* ws, size_t ws_bytes,
-    hipStream_t stream);
+    float eps_lr, const float* gate_logits, float eps, const float* key_norm, void* O, void* ws,
+    size_t ws_bytes, hipStream_t stream);
 
 /* ---- allocation-free form ---------------------------------------------------------------------
  * For callers that cannot allocate device memory: code under HIP graph capture, tight serving loops,
@@ -234,7 +247,8 @@ rola_status rola_sparse_attn_combine_noalloc(
     const rola_problem* p, const void* Qr, const void* Kr, const void* V, int32_t block,
     double sparsity, const int32_t* blk_idx, float softmax_scale, const void* Qn, const void* Pq,
     int32_t r, const float* cos_tab, const float* sin_tab, int32_t rope_ld, const float* C,
-    float eps_lr, const float* gate_logits, float eps, void* O, hipStream_t stream);
+    float eps_lr, const float* gate_logits, float eps, const float* key_norm, void* O,
+    hipStream_t stream);
 
 /* ---- backward of the sparse branch (fine-tuning, Sec. 4.5; Algorithm step 4) ------------------
  * rola_sparse_attn_lse is rola_sparse_attn (same workspace rule: ws NULL or ws_bytes >=

@@ -30,14 +30,15 @@ size_t select_workspace_bytes(const Shape& s, int block);
 hipError_t launch_block_select(const Shape& s, const void* Qr, const void* Kr, int block, int keep,
                                int32_t* idx, void* ws, hipStream_t st);
 // Means of the rotated rows per block from Q^n or K^n and the tables (fp32 [B, H, nb, d]); the
-// rotated rows also go to Xr unless it is null. Built for d = 128 (rope_pool_supported).
+// rotated rows also go to Xr unless it is null. Built for d = 128 (rope_pool_supported). nmax, if
+// not null: per block the largest fp32 norm of its (rotated, rounded) rows, [B, H, nb].
 bool rope_pool_supported(const Shape& s, int block);
 // Block means of an already rotated X (the pooling of launch_block_select alone).
-hipError_t launch_block_pool(const Shape& s, const void* X, int block, float* means,
+hipError_t launch_block_pool(const Shape& s, const void* X, int block, float* means, float* nmax,
                              hipStream_t st);
 hipError_t launch_rope_pool(const Shape& s, const void* X, const float* cos_tab,
                             const float* sin_tab, int ld, int block, void* Xr, float* means,
-                            hipStream_t st);
+                            float* nmax, hipStream_t st);
 // Scores and top-k from given means; ws: select_pooled_workspace_bytes(s, block).
 size_t select_pooled_workspace_bytes(const Shape& s, int block);
 hipError_t launch_select_pooled(const Shape& s, const float* qbar, const float* kbar, int block,
@@ -60,6 +61,7 @@ struct LowrankFuse {
   float eps_lr;
   const float* logits;
   float eps;
+  const float* knorm;  // optional: per key block the largest key norm, [B, H, nb] (score bound)
 };
 bool fuse_supported(const Shape& s, int r);
 size_t fuse_workspace_bytes(const Shape& s, int r);

@@ -151,7 +151,7 @@ rola_status check_combine(const rola_problem* p, const void* Qr, const void* Kr,
                           float softmax_scale, const void* Qn, const void* Pq, int32_t r,
                           const float* cos_tab, const float* sin_tab, int32_t rope_ld,
                           const float* C, float eps_lr, const float* gate_logits, float eps,
-                          void* O, const char* fn, rola::Shape* s) {
+                          const float* key_norm, void* O, const char* fn, rola::Shape* s) {
   TRY(check_problem(p, fn, s));
   TRY(check_block(*s, block, fn));
   TRY(check_sparsity(sparsity, fn));
@@ -177,6 +177,13 @@ rola_status check_combine(const rola_problem* p, const void* Qr, const void* Kr,
   if (!(eps_lr >= 0.f) || !isfinite(eps_lr) || !(eps >= 0.f) || !isfinite(eps))
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: eps values must be finite and >= 0", fn);
   TRY(check_out(*s, O, {{Qr, "Qr"}, {Kr, "Kr"}, {V, "V"}, {Qn, "Qn"}}, nullptr, fn));
+  if (key_norm != nullptr) {
+    if (!aligned(key_norm))
+      return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: key_norm not 16-byte aligned", fn);
+    const size_t nk = (size_t)s->B * s->H * rola::num_blocks(s->N, block) * sizeof(float);
+    if (overlap(key_norm, nk, O, act_bytes(*s)))
+      return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: key_norm overlaps O", fn);
+  }
   return ROLA_OK;
 }
 
@@ -184,12 +191,13 @@ rola_status run_combine(const rola::Shape& s, const void* Qr, const void* Kr, co
                         int32_t block, int keep, const int32_t* blk_idx, float softmax_scale,
                         const void* Qn, const void* Pq, int32_t r, const float* cos_tab,
                         const float* sin_tab, int32_t rope_ld, const float* C, float eps_lr,
-                        const float* gate_logits, float eps, void* O, void* ws, bool planned,
-                        hipStream_t stream, const char* fn) {
+                        const float* gate_logits, float eps, const float* key_norm, void* O,
+                        void* ws, bool planned, hipStream_t stream, const char* fn) {
   const size_t sp = rola::sparse_workspace_bytes(s, block, keep);
   void* fuse_ws = static_cast<char*>(ws) + ((sp + 255) & ~(size_t)255);
   if (rola::fuse_supported(s, r)) {
-    const rola::LowrankFuse lf{Qn, Pq, r, cos_tab, sin_tab, rope_ld, C, eps_lr, gate_logits, eps};
+    const rola::LowrankFuse lf{Qn, Pq, r, cos_tab, sin_tab, rope_ld, C, eps_lr, gate_logits, eps,
+                               key_norm};
     return hip_status(rola::launch_sparse_attn(s, Qr, Kr, V, block, keep, blk_idx, softmax_scale, O,
                                                sp > 0 ? ws : nullptr, stream, &lf, fuse_ws, nullptr,
                                                planned),
@@ -293,7 +301,7 @@ rola_status rola_rope_backward_accumulate(const rola_problem* p, const float* dY
 
 rola_status rola_rope_pool(const rola_problem* p, const void* X, const float* cos_tab,
                            const float* sin_tab, int32_t rope_ld, int32_t block, void* Xr,
-                           float* Xbar, hipStream_t stream) {
+                           float* Xbar, float* Xnorm, hipStream_t stream) {
   rola::Shape s;
   TRY(check_problem(p, __func__, &s));
   TRY(check_block(s, block, __func__));
@@ -301,13 +309,19 @@ rola_status rola_rope_pool(const rola_problem* p, const void* X, const float* co
   REQUIRE_PTR(Xbar);
   if (Xr != nullptr && !aligned(Xr))
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: Xr not 16-byte aligned", __func__);
-  const size_t nbar = (size_t)s.B * s.H * rola::num_blocks(s.N, block) * s.d * sizeof(float);
+  if (Xnorm != nullptr && !aligned(Xnorm))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: Xnorm not 16-byte aligned", __func__);
+  const size_t nblk = (size_t)s.B * s.H * rola::num_blocks(s.N, block);
+  const size_t nbar = nblk * s.d * sizeof(float), nnorm = Xnorm ? nblk * sizeof(float) : 0;
+  if (Xnorm && (overlap(Xnorm, nnorm, X, act_bytes(s)) || overlap(Xnorm, nnorm, Xbar, nbar) ||
+                (Xr && overlap(Xnorm, nnorm, Xr, act_bytes(s)))))
+    return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: Xnorm overlaps X, Xr or Xbar", __func__);
   if (cos_tab == nullptr && sin_tab == nullptr) {  // X is already rotated: pooling only
     if (Xr != nullptr)
       return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: Xr must be NULL without tables", __func__);
     if (overlap(Xbar, nbar, X, act_bytes(s)))
       return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: Xbar overlaps X", __func__);
-    return hip_status(rola::launch_block_pool(s, X, block, Xbar, stream), __func__);
+    return hip_status(rola::launch_block_pool(s, X, block, Xbar, Xnorm, stream), __func__);
   }
   TRY(check_tables(cos_tab, sin_tab, rope_ld, s.d / 2, __func__));
   if (!rola::rope_pool_supported(s, block))
@@ -315,7 +329,8 @@ rola_status rola_rope_pool(const rola_problem* p, const void* X, const float* co
   if (Xr) TRY(check_out(s, Xr, {{X, "X"}}, nullptr, __func__));
   if (overlap(Xbar, nbar, X, act_bytes(s)) || (Xr && overlap(Xbar, nbar, Xr, act_bytes(s))))
     return fail(ROLA_ERR_INVALID_ARGUMENT, "%s: Xbar overlaps X or Xr", __func__);
-  return hip_status(rola::launch_rope_pool(s, X, cos_tab, sin_tab, rope_ld, block, Xr, Xbar, stream),
+  return hip_status(rola::launch_rope_pool(s, X, cos_tab, sin_tab, rope_ld, block, Xr, Xbar, Xnorm,
+                                           stream),
                     __func__);
 }
 
@@ -508,18 +523,19 @@ rola_status rola_sparse_attn_combine(const rola_problem* p, const void* Qr, cons
                                      const int32_t* blk_idx, float softmax_scale, const void* Qn,
                                      const void* Pq, int32_t r, const float* cos_tab,
                                      const float* sin_tab, int32_t rope_ld, const float* C,
-                                     float eps_lr, const float* gate_logits, float eps, void* O,
-                                     void* ws, size_t ws_bytes, hipStream_t stream) {
+                                     float eps_lr, const float* gate_logits, float eps,
+                                     const float* key_norm, void* O, void* ws, size_t ws_bytes,
+                                     hipStream_t stream) {
   rola::Shape s;
   TRY(check_combine(p, Qr, Kr, V, block, sparsity, blk_idx, softmax_scale, Qn, Pq, r, cos_tab,
-                    sin_tab, rope_ld, C, eps_lr, gate_logits, eps, O, __func__, &s));
+                    sin_tab, rope_ld, C, eps_lr, gate_logits, eps, key_norm, O, __func__, &s));
   REQUIRE_PTR(ws);
   const size_t need = rola_sparse_combine_workspace_bytes(p, block, sparsity, r);
   if (ws_bytes < need)
     return fail(ROLA_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", __func__, ws_bytes, need);
   const int keep = rola_keep_blocks(rola::num_blocks(s.N, block), sparsity);
   return run_combine(s, Qr, Kr, V, block, keep, blk_idx, softmax_scale, Qn, Pq, r, cos_tab, sin_tab,
-                     rope_ld, C, eps_lr, gate_logits, eps, O, ws, false, stream, __func__);
+                     rope_ld, C, eps_lr, gate_logits, eps, key_norm, O, ws, false, stream, __func__);
 }
 
 rola_status rola_sparse_plan(const rola_problem* p, int32_t block, double sparsity,
@@ -546,28 +562,29 @@ rola_status rola_sparse_attn_combine_planned(
     const rola_problem* p, const void* Qr, const void* Kr, const void* V, int32_t block,
     double sparsity, const int32_t* blk_idx, float softmax_scale, const void* Qn, const void* Pq,
     int32_t r, const float* cos_tab, const float* sin_tab, int32_t rope_ld, const float* C,
-    float eps_lr, const float* gate_logits, float eps, void* O, void* ws, size_t ws_bytes,
-    hipStream_t stream) {
+    float eps_lr, const float* gate_logits, float eps, const float* key_norm, void* O, void* ws,
+    size_t ws_bytes, hipStream_t stream) {
   rola::Shape s;
   TRY(check_combine(p, Qr, Kr, V, block, sparsity, blk_idx, softmax_scale, Qn, Pq, r, cos_tab,
-                    sin_tab, rope_ld, C, eps_lr, gate_logits, eps, O, __func__, &s));
+                    sin_tab, rope_ld, C, eps_lr, gate_logits, eps, key_norm, O, __func__, &s));
   REQUIRE_PTR(ws);
   const size_t need = rola_sparse_combine_workspace_bytes(p, block, sparsity, r);
   if (ws_bytes < need)
     return fail(ROLA_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", __func__, ws_bytes, need);
   const int keep = rola_keep_blocks(rola::num_blocks(s.N, block), sparsity);
   return run_combine(s, Qr, Kr, V, block, keep, blk_idx, softmax_scale, Qn, Pq, r, cos_tab, sin_tab,
-                     rope_ld, C, eps_lr, gate_logits, eps, O, ws, true, stream, __func__);
+                     rope_ld, C, eps_lr, gate_logits, eps, key_norm, O, ws, true, stream, __func__);
 }
 
 rola_status rola_sparse_attn_combine_noalloc(
     const rola_problem* p, const void* Qr, const void* Kr, const void* V, int32_t block,
     double sparsity, const int32_t* blk_idx, float softmax_scale, const void* Qn, const void* Pq,
     int32_t r, const float* cos_tab, const float* sin_tab, int32_t rope_ld, const float* C,
-    float eps_lr, const float* gate_logits, float eps, void* O, hipStream_t stream) {
+    float eps_lr, const float* gate_logits, float eps, const float* key_norm, void* O,
+    hipStream_t stream) {
   rola::Shape s;
   TRY(check_combine(p, Qr, Kr, V, block, sparsity, blk_idx, softmax_scale, Qn, Pq, r, cos_tab,
-                    sin_tab, rope_ld, C, eps_lr, gate_logits, eps, O, __func__, &s));
+                    sin_tab, rope_ld, C, eps_lr, gate_logits, eps, key_norm, O, __func__, &s));
   const size_t need = rola_sparse_combine_workspace_bytes(p, block, sparsity, r);
   if (need > rola::static_scratch_bytes())
     return fail(ROLA_ERR_UNSUPPORTED,
@@ -579,7 +596,7 @@ rola_status rola_sparse_attn_combine_noalloc(
   if (e != hipSuccess) return hip_status(e, __func__);
   const int keep = rola_keep_blocks(rola::num_blocks(s.N, block), sparsity);
   return run_combine(s, Qr, Kr, V, block, keep, blk_idx, softmax_scale, Qn, Pq, r, cos_tab, sin_tab,
-                     rope_ld, C, eps_lr, gate_logits, eps, O, ws, false, stream, __func__);
+                     rope_ld, C, eps_lr, gate_logits, eps, key_norm, O, ws, false, stream, __func__);
 }
 
 rola_status rola_lowrank_summary_ex(const rola_problem* p, const void* Kn, const void* V,

@@ -20,9 +20,26 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 // Block means of Q^r or K^r, one workgroup per (b, h, block), 16 threads of 8 channels per token
 // row. Summation order: per thread over its tokens in order, then over the 16 threads in order.
+// Sum of x over the G consecutive lanes that share one row (G = 8 or 16, lanes aligned to G).
+__device__ __forceinline__ float row_group_sum(float x, int G) {
+  for (int off = G / 2; off >= 1; off >>= 1) x += __shfl_xor(x, off, G);
+  return x;
+}
+
+// *out = sqrt of the largest sq over the workgroup's 256 threads (every thread calls it).
+__device__ __forceinline__ void block_norm_max(float sq, float* out) {
+  __shared__ float wmax[4];
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) sq = fmaxf(sq, __shfl_xor(sq, off));
+  if (threadIdx.x % 64 == 0) wmax[threadIdx.x / 64] = sq;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    *out = sqrtf(fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3])));
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void pool_kernel(int N, int d, int block, const T* __restrict__ X,
-                                                   float* __restrict__ out) {
+                                                   float* __restrict__ out, float* __restrict__ nmax) {
   const int I = blockIdx.x, nb = gridDim.x;
   const long head = (long)blockIdx.z * gridDim.y + blockIdx.y;
   const T* xh = X + head * (long)N * d;
@@ -30,11 +47,17 @@ __global__ __launch_bounds__(256) void pool_kernel(int N, int d, int block, cons
   const int g = threadIdx.x % G, lane = threadIdx.x / G;
   const int n0 = I * block, n1 = min(N, n0 + block);
   float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  float sq = 0.f;  // largest squared row norm among this thread's rows (its G-lane share)
   for (int n = n0 + lane; n < n1; n += L) {
     float v[8];
     load8(xh + (long)n * d + g * 8, v);
+    float part = 0.f;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] += v[i];
+    for (int i = 0; i < 8; ++i) {
+      acc[i] += v[i];
+      part = fmaf(v[i], v[i], part);
+    }
+    if (nmax) sq = fmaxf(sq, row_group_sum(part, G));
   }
   __shared__ float red[256 * 8];
 #pragma unroll
@@ -46,6 +69,7 @@ __global__ __launch_bounds__(256) void pool_kernel(int N, int d, int block, cons
     for (int l = 0; l < L; ++l) s += red[(l * G + gc) * 8 + ic];
     out[(head * nb + I) * d + c] = s / (float)(n1 - n0);
   }
+  if (nmax) block_norm_max(sq, nmax + head * nb + I);
 }
 
 // The rotating form (d_h = 128): X is Q^n or K^n. One workgroup per (block, group of HG heads): the
@@ -60,7 +84,8 @@ __global__ __launch_bounds__(256) void rope_pool_kernel(int N, int block, int he
                                                         const T* __restrict__ X,
                                                         const float* __restrict__ cos_tab,
                                                         const float* __restrict__ sin_tab,
-                                                        T* __restrict__ Xr, float* __restrict__ out) {
+                                                        T* __restrict__ Xr, float* __restrict__ out,
+                                                        float* __restrict__ nmax) {
   constexpr int D = 128, G = D / 8, L = 256 / G;
   const int I = blockIdx.x, nb = gridDim.x;
   const int h0 = blockIdx.y * kRopePoolHeads, h1 = min(heads, h0 + kRopePoolHeads);
@@ -79,6 +104,7 @@ __global__ __launch_bounds__(256) void rope_pool_kernel(int N, int block, int he
   for (int head = h0; head < h1; ++head) {
     const T* xh = X + (long)head * N * D;
     float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    float sq = 0.f;  // largest squared norm of a rotated, rounded row (this thread's share of it)
     float v[TPT][8];
 #pragma unroll
     for (int k = 0; k < TPT; ++k) {  // loads first: one memory latency per head
@@ -101,8 +127,13 @@ __global__ __launch_bounds__(256) void rope_pool_kernel(int N, int block, int he
 #pragma unroll
         for (int i = 0; i < 8; ++i) o[i] = to_f32(r[i]);
         if (Xr) store8(Xr + (long)head * N * D + (long)n * D + g * 8, o);
+        float part = 0.f;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) acc[i] += o[i];
+        for (int i = 0; i < 8; ++i) {
+          acc[i] += o[i];
+          part = fmaf(o[i], o[i], part);
+        }
+        if (nmax) sq = fmaxf(sq, row_group_sum(part, G));
       }
     }
 #pragma unroll
@@ -114,6 +145,7 @@ __global__ __launch_bounds__(256) void rope_pool_kernel(int N, int block, int he
       for (int l = 0; l < L; ++l) s += red[(l * G + gc) * 8 + ic];
       out[((long)head * nb + I) * D + c] = s / (float)(n1 - n0);
     }
+    if (nmax) block_norm_max(sq, nmax + (long)head * nb + I);
     __syncthreads();
   }
 }
@@ -282,25 +314,26 @@ __global__ __launch_bounds__(64) void topk_kernel(int nb, int keep, const float*
   }
 }
 
-hipError_t launch_pool(const Shape& s, const void* X, int block, float* means, hipStream_t st) {
+hipError_t launch_pool(const Shape& s, const void* X, int block, float* means, hipStream_t st,
+                       float* nmax = nullptr) {
   const dim3 grid(num_blocks(s.N, block), s.H, s.B);
   if (s.bf16)
     hipLaunchKernelGGL(pool_kernel<bf16>, grid, dim3(256), 0, st, s.N, s.d, block, (const bf16*)X,
-                       means);
+                       means, nmax);
   else
     hipLaunchKernelGGL(pool_kernel<float>, grid, dim3(256), 0, st, s.N, s.d, block, (const float*)X,
-                       means);
+                       means, nmax);
   return hipGetLastError();
 }
 
 template <typename T, int TPT>
 hipError_t launch_rope_pool_t(const Shape& s, const void* X, const float* cos_tab,
                               const float* sin_tab, int ld, int block, void* Xr, float* means,
-                              hipStream_t st) {
+                              float* nmax, hipStream_t st) {
   const int heads = s.B * s.H;
   const dim3 grid(num_blocks(s.N, block), (heads + kRopePoolHeads - 1) / kRopePoolHeads);
   hipLaunchKernelGGL((rope_pool_kernel<T, TPT>), grid, dim3(256), 0, st, s.N, block, heads, ld,
-                     (const T*)X, cos_tab, sin_tab, (T*)Xr, means);
+                     (const T*)X, cos_tab, sin_tab, (T*)Xr, means, nmax);
   return hipGetLastError();
 }
 
@@ -324,22 +357,22 @@ hipError_t launch_select_pooled(const Shape& s, const float* qbar, const float* 
   return hipGetLastError();
 }
 
-hipError_t launch_block_pool(const Shape& s, const void* X, int block, float* means,
+hipError_t launch_block_pool(const Shape& s, const void* X, int block, float* means, float* nmax,
                              hipStream_t st) {
-  return launch_pool(s, X, block, means, st);
+  return launch_pool(s, X, block, means, st, nmax);
 }
 
 bool rope_pool_supported(const Shape& s, int block) { return s.d == 128 && block >= 32; }
 
 hipError_t launch_rope_pool(const Shape& s, const void* X, const float* cos_tab,
                             const float* sin_tab, int ld, int block, void* Xr, float* means,
-                            hipStream_t st) {
+                            float* nmax, hipStream_t st) {
   switch ((s.bf16 ? 1000 : 0) + block) {
-    case 1064: return launch_rope_pool_t<bf16, 4>(s, X, cos_tab, sin_tab, ld, block, Xr, means, st);
-    case 1128: return launch_rope_pool_t<bf16, 8>(s, X, cos_tab, sin_tab, ld, block, Xr, means, st);
-    case 32: return launch_rope_pool_t<float, 2>(s, X, cos_tab, sin_tab, ld, block, Xr, means, st);
-    case 64: return launch_rope_pool_t<float, 4>(s, X, cos_tab, sin_tab, ld, block, Xr, means, st);
-    case 128: return launch_rope_pool_t<float, 8>(s, X, cos_tab, sin_tab, ld, block, Xr, means, st);
+    case 1064: return launch_rope_pool_t<bf16, 4>(s, X, cos_tab, sin_tab, ld, block, Xr, means, nmax, st);
+    case 1128: return launch_rope_pool_t<bf16, 8>(s, X, cos_tab, sin_tab, ld, block, Xr, means, nmax, st);
+    case 32: return launch_rope_pool_t<float, 2>(s, X, cos_tab, sin_tab, ld, block, Xr, means, nmax, st);
+    case 64: return launch_rope_pool_t<float, 4>(s, X, cos_tab, sin_tab, ld, block, Xr, means, nmax, st);
+    case 128: return launch_rope_pool_t<float, 8>(s, X, cos_tab, sin_tab, ld, block, Xr, means, nmax, st);
   }
   return hipErrorInvalidValue;
 }

@@ -37,6 +37,9 @@ constexpr int kSub = 32;            // keys per sub-tile: one LDS stage holds it
 constexpr int kB64Group = 2;        // query blocks per workgroup of the 64-token path with a list
 constexpr int kB64Nbuf = 3;         // its LDS stages (16 KB each)
 constexpr float kRescaleTau = 8.f;  // log2 headroom before O is rescaled
+// Largest score bound (log2 units) that serves as the softmax reference of the BOUND variant:
+// probabilities then stay in [2^-80, 1], clear of fp32 and bf16 underflow for any V.
+constexpr float kBoundMax = 40.f;
 
 __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -464,6 +467,7 @@ struct AttnArgs {
   float* dQ;
   float scale;
   int rot_q;  // Q holds Q^n: the prologue rotates it with fz's tables (rounded as rola_rope_apply)
+  const float* knorm;  // BOUND: per key block the largest norm of its keys, [B, H, nb]
 };
 
 // DQ: the backward's dQ^r = scale dS K^r over the same groups and lists (fine-tuning, Sec. 4.5):
@@ -471,7 +475,9 @@ struct AttnArgs {
 // S^T), P = exp2(S^T scale log2e - lse) with the forward's log-sum-exp, dS^T = P (dP^T - D), and
 // dQ^T += K^T dS^T with K^T through transposing reads in the order the registers hold the keys. K
 // and V tiles use the swizzle that serves both row and transposing reads (bw_swizzle).
-template <int BLK, int G, int NBUF, int TAB, int RJ, bool QUEUE, bool DQ = false>
+// BOUND (merged lists, G > 1): the softmax reference of each wave is the bound on its scores that
+// the key-block norms give, where that bound is small enough (see the prologue).
+template <int BLK, int G, int NBUF, int TAB, int RJ, bool QUEUE, bool DQ = false, bool BOUND = false>
 __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void sparse_attn_kernel(
     const AttnArgs args) {
   static_assert(G == 1 || G == 2 || G == 4, "one, two or four query blocks per workgroup");
@@ -566,8 +572,18 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void s
     }
     const const_i32 slist = (const_i32)glist;
     const int T = E * SUBS;  // sub-tiles the workgroup walks
+    float kmax = 0.f;        // BOUND: the largest key-block norm among the group's entries
     if (TAB > 0 && glist) {
-      for (int i = tid; i < E; i += NW * 64) tab[i] = glist[i];
+      for (int i = tid; i < E; i += NW * 64) {
+        const int v = glist[i];
+        tab[i] = v;
+        if (BOUND && (v & 0xFFFF) < nb) kmax = fmaxf(kmax, ap->knorm[head * nb + (v & 0xFFFF)]);
+      }
+    } else if (BOUND && glist) {
+      for (int i = tid; i < E; i += NW * 64) {
+        const int v = glist[i];
+        if ((v & 0xFFFF) < nb) kmax = fmaxf(kmax, ap->knorm[head * nb + (v & 0xFFFF)]);
+      }
     }
     struct Step {
       int k0;    // first key, -1 if the block index is out of range
@@ -626,10 +642,40 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void s
       dsum_q = v.y;
     }
     __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
-    if (TAB > 0) __syncthreads();  // the list table is complete
+    __shared__ float kmax_w[BOUND ? NW : 1];
+    if constexpr (BOUND) {
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) kmax = fmaxf(kmax, __shfl_xor(kmax, off));
+      if (lane == 0) kmax_w[wave] = kmax;
+    }
+    if (TAB > 0 || BOUND) __syncthreads();  // the list table and the per-wave maxima are complete
 
     f32x16 acc[4];        // O^T channel tiles 32w .. 32w+31
-    float m = -INFINITY;  // running reference max (log2 units) of this lane's query
+    float m = -INFINITY;  // reference max (log2 units) of this lane's query
+    // BOUND: with b the largest norm of the keys the group selected, each scaled score of query q
+    // lies in [-B, B], B = scale_log2 |q| b, so m = B keeps every probability in [2^-2B, 1] and the
+    // walk needs no running max and no rescale. A wave where some B exceeds kBoundMax (or is not
+    // finite) tracks the running max instead. fixed_m is wave-uniform.
+    int fixed_m = 0;
+    if constexpr (BOUND) {
+      float b = kmax_w[0];
+#pragma unroll
+      for (int i = 1; i < NW; ++i) b = fmaxf(b, kmax_w[i]);
+      typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+      float q2 = 0.f;
+#pragma unroll
+      for (int s = 0; s < 8; ++s)
+#pragma unroll
+        for (int e = 0; e < 8; e += 2) {
+          const bf16x2_t v = {qf[s][e], qf[s][e + 1]};
+          q2 = __builtin_amdgcn_fdot2_f32_bf16(v, v, q2, false);
+        }
+      const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(q2), __float_as_uint(q2), false, false);
+      q2 = __uint_as_float(x[0]) + __uint_as_float(x[1]);
+      const float bound = scale_log2 * sqrtf(q2) * b;
+      fixed_m = __any(!(bound <= kBoundMax)) ? 0 : 1;
+      if (fixed_m) m = bound;
+    }
     float l = 0.f;        // running sum of this lane's 16 keys per sub-tile (the other 16: lane l^32)
 #pragma unroll
     for (int w = 0; w < 4; ++w) acc[w] = f32x16{};
@@ -792,7 +838,9 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void s
           }
           __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
           load_v(j, 0, vf);
-          rescale(row_max(sc));
+          // (BOUND re-reads the flag as uniform: taken as a per-lane value, the branch keeps the
+          // step's registers live on both sides and the kernel spills)
+          if (!BOUND || !wave_uniform(fixed_m)) rescale(row_max(sc));
           probs(sc, cur.k0, pb);
           // the P V products at raised wave priority: a wave that has its probabilities issues its
           // MFMAs ahead of the other waves' score and softmax work (plain attention on the 14B
@@ -972,18 +1020,20 @@ struct DqArgs {
 };
 
 // Resident workgroups of the work-queue variant of sparse_attn_kernel (a cache per variant).
-template <int BLK, int G, int NBUF, int TAB, int RJ, bool DQ>
+template <int BLK, int G, int NBUF, int TAB, int RJ, bool DQ, bool BOUND = false>
 int queue_resident() {
   static std::atomic<int> cache[kMaxDevices];
-  return resident_workgroups(sparse_attn_kernel<BLK, G, NBUF, TAB, RJ, true, DQ>, G * BLK * 2, cache);
+  return resident_workgroups(sparse_attn_kernel<BLK, G, NBUF, TAB, RJ, true, DQ, BOUND>, G * BLK * 2,
+                             cache);
 }
 
 // queue: kNumXcd zeroed counters, or nullptr for the static grid of one workgroup per group.
-template <int BLK, int G, int NBUF, int TAB, int RJ, bool DQ = false>
+template <int BLK, int G, int NBUF, int TAB, int RJ, bool DQ = false, bool BOUND = false>
 hipError_t launch_bf16_tab(const Shape& s, const void* Qr, const void* Kr, const void* V,
                            const int32_t* lists, int list_len, int list_stride,
                            const int32_t* pairs, float scale, void* Os, const FuseArgs& fz,
-                           int* queue, hipStream_t st, const DqArgs& dq = DqArgs{}) {
+                           int* queue, hipStream_t st, const DqArgs& dq = DqArgs{},
+                           const float* knorm = nullptr) {
   const int nb = num_blocks(s.N, BLK);
   const int ngroups = (nb + G - 1) / G;
   const int total = ngroups * s.H * s.B;
@@ -991,10 +1041,10 @@ hipError_t launch_bf16_tab(const Shape& s, const void* Qr, const void* Kr, const
   const int threads = G * BLK * 2;
   const AttnArgs a{s.N, nb, ngroups, total, lists, list_len, list_stride, pairs, sl,
                    (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V, (bf16*)Os, fz, queue,
-                   dq.dO, dq.lseD, dq.dQ, scale, fz.rot_q};
+                   dq.dO, dq.lseD, dq.dQ, scale, fz.rot_q, knorm};
   if (queue) {
-    const int grid = std::min(total, queue_resident<BLK, G, NBUF, TAB, RJ, DQ>());
-    hipLaunchKernelGGL((sparse_attn_kernel<BLK, G, NBUF, TAB, RJ, true, DQ>), dim3(grid),
+    const int grid = std::min(total, queue_resident<BLK, G, NBUF, TAB, RJ, DQ, BOUND>());
+    hipLaunchKernelGGL((sparse_attn_kernel<BLK, G, NBUF, TAB, RJ, true, DQ, BOUND>), dim3(grid),
                        dim3(threads), 0, st, a);
   } else {
     hipLaunchKernelGGL((sparse_attn_kernel<BLK, G, NBUF, TAB, RJ, false, DQ>), dim3(total),
@@ -1005,12 +1055,24 @@ hipError_t launch_bf16_tab(const Shape& s, const void* Qr, const void* Kr, const
 
 // Lists of up to kTable entries go through the LDS table; longer ones through scalar loads.
 constexpr int kTable = 1024;
+// knorm (merged lists with a work queue and a fused epilogue only): the BOUND variant.
 template <int BLK, int G, int NBUF, int RJ>
 hipError_t launch_bf16_rj(const Shape& s, const void* Qr, const void* Kr, const void* V,
                           const int32_t* lists, int list_len, int list_stride, float scale,
                           void* Os, const int32_t* pairs, const FuseArgs& fz, int* queue,
-                          hipStream_t st) {
+                          hipStream_t st, const float* knorm) {
   const int max_len = G > 1 ? list_stride - 1 : list_len;
+  if constexpr (G > 1 && RJ > 0) {
+    if (knorm && lists && queue) {
+      if (max_len <= kTable)
+        return launch_bf16_tab<BLK, G, NBUF, kTable, RJ, false, true>(
+            s, Qr, Kr, V, lists, list_len, list_stride, pairs, scale, Os, fz, queue, st, DqArgs{},
+            knorm);
+      return launch_bf16_tab<BLK, G, NBUF, 0, RJ, false, true>(
+          s, Qr, Kr, V, lists, list_len, list_stride, pairs, scale, Os, fz, queue, st, DqArgs{},
+          knorm);
+    }
+  }
   if (lists && max_len <= kTable)
     return launch_bf16_tab<BLK, G, NBUF, kTable, RJ>(s, Qr, Kr, V, lists, list_len, list_stride,
                                                      pairs, scale, Os, fz, queue, st);
@@ -1023,16 +1085,16 @@ template <int BLK, int G, int NBUF>
 hipError_t launch_bf16(const Shape& s, const void* Qr, const void* Kr, const void* V,
                        const int32_t* lists, int list_len, int list_stride, float scale, void* Os,
                        hipStream_t st, const int32_t* pairs = nullptr, const FuseArgs* fz = nullptr,
-                       int* queue = nullptr) {
+                       int* queue = nullptr, const float* knorm = nullptr) {
   static const FuseArgs none{};
   if (!fz || fz->r == 0)
     return launch_bf16_rj<BLK, G, NBUF, 0>(s, Qr, Kr, V, lists, list_len, list_stride, scale, Os,
-                                           pairs, fz ? *fz : none, queue, st);
+                                           pairs, fz ? *fz : none, queue, st, knorm);
   if (fz->r <= 32)
     return launch_bf16_rj<BLK, G, NBUF, 1>(s, Qr, Kr, V, lists, list_len, list_stride, scale, Os,
-                                           pairs, *fz, queue, st);
+                                           pairs, *fz, queue, st, knorm);
   return launch_bf16_rj<BLK, G, NBUF, 2>(s, Qr, Kr, V, lists, list_len, list_stride, scale, Os,
-                                         pairs, *fz, queue, st);
+                                         pairs, *fz, queue, st, knorm);
 }
 
 template <typename T, int D>
@@ -1244,7 +1306,7 @@ hipError_t launch_sparse_attn(const Shape& s, const void* Qr, const void* Kr, co
           if (e != hipSuccess) return e;
         }
         return launch_bf16<64, G, kB64Nbuf>(s, Qr, Kr, V, gr.lists, 0, gr.stride, scale, Os, st,
-                                                 gr.pairs, fp, gr.queue);
+                                                 gr.pairs, fp, gr.queue, lf ? lf->knorm : nullptr);
       }
       return launch_bf16<64, 1, 3>(s, Qr, Kr, V, idx, keep, keep, scale, Os, st, nullptr, fp);
     }

@@ -40,7 +40,7 @@ SIGNATURES = {
     "rola_rope_apply": (_i32, [_PP, _p, _p, _p, _i32, _p, _p]),
     "rola_rope_backward_accumulate": (_i32, [_PP, _p, _p, _p, _i32, _i32, _p, _p]),
     "rola_block_select": (_i32, [_PP, _p, _p, _i32, _f64, _p, _p, _sz, _p]),
-    "rola_rope_pool": (_i32, [_PP, _p, _p, _p, _i32, _i32, _p, _p, _p]),
+    "rola_rope_pool": (_i32, [_PP, _p, _p, _p, _i32, _i32, _p, _p, _p, _p]),
     "rola_select_pooled_workspace_bytes": (_sz, [_PP, _i32]),
     "rola_block_select_pooled": (_i32, [_PP, _p, _p, _i32, _f64, _p, _p, _sz, _p]),
     "rola_sparse_workspace_bytes": (_sz, [_PP, _i32, _f64]),
@@ -70,12 +70,12 @@ SIGNATURES = {
     "rola_sparse_attn_backward": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p, _p, _p, _p,
                                          _p, _p, _sz, _p]),
     "rola_sparse_attn_combine": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p, _i32, _p, _p,
-                                        _i32, _p, _f32, _p, _f32, _p, _p, _sz, _p]),
+                                        _i32, _p, _f32, _p, _f32, _p, _p, _p, _sz, _p]),
     "rola_sparse_plan": (_i32, [_PP, _i32, _f64, _p, _i32, _p, _sz, _p]),
     "rola_sparse_attn_combine_noalloc": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p, _i32,
-                                                _p, _p, _i32, _p, _f32, _p, _f32, _p, _p]),
+                                                _p, _p, _i32, _p, _f32, _p, _f32, _p, _p, _p]),
     "rola_sparse_attn_combine_planned": (_i32, [_PP, _p, _p, _p, _i32, _f64, _p, _f32, _p, _p, _i32,
-                                                _p, _p, _i32, _p, _f32, _p, _f32, _p, _p, _sz, _p]),
+                                                _p, _p, _i32, _p, _f32, _p, _f32, _p, _p, _p, _sz, _p]),
 }
 
 # Feature map and rotation order of the low-rank branch (rola_phi, rola_rope_order).
@@ -313,9 +313,11 @@ def rola_block_select(Qr, Kr, grid, block, sparsity, out=None, ws=None, stream=N
     return out
 
 
-def rola_rope_pool(X, cos, sin, grid, block, want_xr=True, xr=None, xbar=None, stream=None):
+def rola_rope_pool(X, cos, sin, grid, block, want_xr=True, xr=None, xbar=None, xnorm=None,
+                   stream=None):
     """(R(X) or None, block means of R(X) fp32 [B, H, n_blocks, d_h]) in one pass. With cos and sin
-    None, X is already rotated and only the means are computed."""
+    None, X is already rotated and only the means are computed. xnorm (optional, fp32
+    [B, H, n_blocks]) receives each block's largest row norm."""
     a = _Args()
     a.act(X, "X")
     if cos is None and sin is None:
@@ -333,10 +335,12 @@ def rola_rope_pool(X, cos, sin, grid, block, want_xr=True, xr=None, xbar=None, s
     if xbar is None:
         xbar = torch.empty(shape, dtype=torch.float32, device=X.device)
     a.tensor(xbar, "xbar", shape, torch.float32)
+    if xnorm is not None:
+        a.tensor(xnorm, "xnorm", shape[:3], torch.float32)
     a.done()
     prob = problem_of(X, grid)
     _check(LIB.rola_rope_pool(ctypes.byref(prob), _ptr(X), _ptr(cos), _ptr(sin), ld, block, _ptr(xr),
-                              _ptr(xbar), _stream(stream)), "rola_rope_pool")
+                              _ptr(xbar), _ptr(xnorm), _stream(stream)), "rola_rope_pool")
     return xr, xbar
 
 
@@ -576,9 +580,15 @@ def sparse_combine_workspace_bytes(prob: Problem, block: int, sparsity: float, r
     return LIB.rola_sparse_combine_workspace_bytes(ctypes.byref(prob), block, sparsity, r)
 
 
-def _combine_args(a, Qr, Kr, V, block, sparsity, blk_idx, Qn, Pq, r, cos, sin, C, logits):
-    """Qr may be None: the queries are then rotated from Qn in the attention's prologue."""
+def _combine_args(a, Qr, Kr, V, block, sparsity, blk_idx, Qn, Pq, r, cos, sin, C, logits,
+                  key_norm=None):
+    """Qr may be None: the queries are then rotated from Qn in the attention's prologue. key_norm
+    (optional): fp32 [B, H, n_blocks], per key block a bound on its keys' norms (rola_rope_pool's
+    xnorm of K), which lets the attention use a fixed softmax reference."""
     a.act(Qn, "Qn")
+    if key_norm is not None:
+        B, H, N, _ = Qn.shape
+        a.tensor(key_norm, "key_norm", (B, H, num_blocks(N, block)), torch.float32)
     for t, name in ((Qr, "Qr"), (Kr, "Kr"), (V, "V")):
         if t is not None or name != "Qr":
             a.act(t, name, Qn)
@@ -592,10 +602,11 @@ def _combine_args(a, Qr, Kr, V, block, sparsity, blk_idx, Qn, Pq, r, cos, sin, C
 
 def rola_sparse_attn_combine(Qr, Kr, V, grid, block, sparsity, blk_idx, Qn, Pq, r, cos, sin, C,
                              logits, scale=None, eps_lr=1e-6, eps=1e-6, out=None, ws=None,
-                             stream=None):
+                             stream=None, key_norm=None):
     """O = combine(sparse attention, low-rank readout of C) in one call (fused epilogue)."""
     a = _Args()
-    ld = _combine_args(a, Qr, Kr, V, block, sparsity, blk_idx, Qn, Pq, r, cos, sin, C, logits)
+    ld = _combine_args(a, Qr, Kr, V, block, sparsity, blk_idx, Qn, Pq, r, cos, sin, C, logits,
+                       key_norm)
     prob = problem_of(Qn, grid)
     scale = prob.d_h ** -0.5 if scale is None else scale
     out = torch.empty_like(Qn) if out is None else a.act(out, "out", Qn)
@@ -607,8 +618,8 @@ def rola_sparse_attn_combine(Qr, Kr, V, grid, block, sparsity, blk_idx, Qn, Pq, 
     _check(LIB.rola_sparse_attn_combine(ctypes.byref(prob), _ptr(Qr), _ptr(Kr), _ptr(V), block,
                                         sparsity, _ptr(blk_idx), scale, _ptr(Qn), _ptr(Pq), r,
                                         _ptr(cos), _ptr(sin), ld, _ptr(C), eps_lr,
-                                        _ptr(logits), eps, _ptr(out), _ptr(ws), ws.numel(),
-                                        _stream(stream)), "rola_sparse_attn_combine")
+                                        _ptr(logits), eps, _ptr(key_norm), _ptr(out), _ptr(ws),
+                                        ws.numel(), _stream(stream)), "rola_sparse_attn_combine")
     return out
 
 
@@ -628,10 +639,11 @@ def rola_sparse_plan(blk_idx, like, grid, block, sparsity, r, ws, stream=None):
 
 def rola_sparse_attn_combine_planned(Qr, Kr, V, grid, block, sparsity, blk_idx, Qn, Pq, r, cos, sin,
                                      C, logits, ws, scale=None, eps_lr=1e-6, eps=1e-6, out=None,
-                                     stream=None):
+                                     stream=None, key_norm=None):
     """rola_sparse_attn_combine on the plan rola_sparse_plan left in ws."""
     a = _Args()
-    ld = _combine_args(a, Qr, Kr, V, block, sparsity, blk_idx, Qn, Pq, r, cos, sin, C, logits)
+    ld = _combine_args(a, Qr, Kr, V, block, sparsity, blk_idx, Qn, Pq, r, cos, sin, C, logits,
+                       key_norm)
     prob = problem_of(Qn, grid)
     scale = prob.d_h ** -0.5 if scale is None else scale
     out = torch.empty_like(Qn) if out is None else a.act(out, "out", Qn)
@@ -640,18 +652,20 @@ def rola_sparse_attn_combine_planned(Qr, Kr, V, grid, block, sparsity, blk_idx, 
     _check(LIB.rola_sparse_attn_combine_planned(ctypes.byref(prob), _ptr(Qr), _ptr(Kr), _ptr(V),
                                                 block, sparsity, _ptr(blk_idx), scale, _ptr(Qn),
                                                 _ptr(Pq), r, _ptr(cos), _ptr(sin), ld, _ptr(C), eps_lr,
-                                                _ptr(logits), eps, _ptr(out), _ptr(ws), ws.numel(),
-                                                _stream(stream)), "rola_sparse_attn_combine_planned")
+                                                _ptr(logits), eps, _ptr(key_norm), _ptr(out), _ptr(ws),
+                                                ws.numel(), _stream(stream)),
+           "rola_sparse_attn_combine_planned")
     return out
 
 
 def rola_sparse_attn_combine_noalloc(Qr, Kr, V, grid, block, sparsity, blk_idx, Qn, Pq, r, cos, sin,
                                      C, logits, out, scale=None, eps_lr=1e-6, eps=1e-6,
-                                     stream=None):
+                                     stream=None, key_norm=None):
     """rola_sparse_attn_combine with the library's static device scratch instead of a workspace:
     nothing is allocated (the output `out` is the caller's)."""
     a = _Args()
-    ld = _combine_args(a, Qr, Kr, V, block, sparsity, blk_idx, Qn, Pq, r, cos, sin, C, logits)
+    ld = _combine_args(a, Qr, Kr, V, block, sparsity, blk_idx, Qn, Pq, r, cos, sin, C, logits,
+                       key_norm)
     a.act(out, "out", Qn)
     a.done()
     prob = problem_of(Qn, grid)
@@ -659,7 +673,8 @@ def rola_sparse_attn_combine_noalloc(Qr, Kr, V, grid, block, sparsity, blk_idx, 
     _check(LIB.rola_sparse_attn_combine_noalloc(ctypes.byref(prob), _ptr(Qr), _ptr(Kr), _ptr(V),
                                                 block, sparsity, _ptr(blk_idx), scale, _ptr(Qn),
                                                 _ptr(Pq), r, _ptr(cos), _ptr(sin), ld, _ptr(C), eps_lr,
-                                                _ptr(logits), eps, _ptr(out), _stream(stream)),
+                                                _ptr(logits), eps, _ptr(key_norm), _ptr(out),
+                                                _stream(stream)),
            "rola_sparse_attn_combine_noalloc")
     return out
 

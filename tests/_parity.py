@@ -36,8 +36,18 @@ def run_gpu(w: synth.Workload, inp: dict, fused_only=False):
     # the whole tail in one call: attention with the readout and combine in its epilogue
     out_epi = R.rola_sparse_attn_combine(qr, kr, inp["V"], g, w.block, w.sparsity, idx, inp["Qn"],
                                          inp["Pq"], w.r, cos, sin, C, inp["logits"])
+    # the benchmarked form: the planned call given each key block's largest norm (from the pooling
+    # pass), so that the attention may use the score bound as its softmax reference
+    knorm = torch.empty((w.B, w.H, R.num_blocks(w.N, w.block)), dtype=torch.float32, device=qr.device)
+    R.rola_rope_pool(kr, None, None, g, w.block, xnorm=knorm)
+    ws = torch.empty(max(16, R.sparse_combine_workspace_bytes(prob, w.block, w.sparsity, w.r)),
+                     dtype=torch.uint8, device=qr.device)
+    R.rola_sparse_plan(idx, qr, g, w.block, w.sparsity, w.r, ws)
+    out_bound = R.rola_sparse_attn_combine_planned(qr, kr, inp["V"], g, w.block, w.sparsity, idx,
+                                                   inp["Qn"], inp["Pq"], w.r, cos, sin, C,
+                                                   inp["logits"], ws, key_norm=knorm)
     res = dict(cos=cos, sin=sin, qr=qr, kr=kr, idx=idx, o_s=o_s, C=C, z=z, out_fused=out_fused,
-               out_epi=out_epi)
+               out_epi=out_epi, out_bound=out_bound, knorm=knorm)
     if not fused_only:
         o_lr = R.rola_lowrank_readout(inp["Qn"], inp["Pq"], w.r, cos, sin, C, g)
         res["o_lr"] = o_lr

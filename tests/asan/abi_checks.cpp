@@ -73,10 +73,10 @@ int main(void) {
   EXPECT(ROLA_ERR_WORKSPACE, rola_sparse_attn_backward(&ok, F(1), F(2), F(3), 64, 0.9, (int32_t*)F(4), 0.1f, F(5), (float*)F(6), F(7), (float*)F(8), (float*)F(9), (float*)F(10), F(11), 16, 0));
 
   // attention + readout + combine
-  EXPECT(ROLA_ERR_INVALID_ARGUMENT, rola_sparse_attn_combine(&ok, F(1), F(2), F(3), 64, 0.9, (int32_t*)F(4), 0.1f, F(5), F(6), 31, T, T, 64, (float*)F(7), 1e-6f, (float*)F(8), 1e-6f, F(9), F(10), BIG, 0));
-  EXPECT(ROLA_ERR_INVALID_ARGUMENT, rola_sparse_attn_combine(&ok, F(1), F(2), F(3), 64, 0.9, (int32_t*)F(4), 0.1f, F(5), F(6), 32, T, T, 64, (float*)F(7), 1e-6f, (float*)F(8), 1e-6f, F(5), F(10), BIG, 0));
-  EXPECT(ROLA_ERR_INVALID_ARGUMENT, rola_sparse_attn_combine(&ok, F(1), F(2), F(3), 64, 0.9, (int32_t*)F(4), 0.1f, F(5), F(6), 32, T, T, 64, (float*)F(7), -1.f, (float*)F(8), 1e-6f, F(9), F(10), BIG, 0));
-  EXPECT(ROLA_ERR_WORKSPACE, rola_sparse_attn_combine(&ok, F(1), F(2), F(3), 64, 0.9, (int32_t*)F(4), 0.1f, F(5), F(6), 32, T, T, 64, (float*)F(7), 1e-6f, (float*)F(8), 1e-6f, F(9), F(10), 64, 0));
+  EXPECT(ROLA_ERR_INVALID_ARGUMENT, rola_sparse_attn_combine(&ok, F(1), F(2), F(3), 64, 0.9, (int32_t*)F(4), 0.1f, F(5), F(6), 31, T, T, 64, (float*)F(7), 1e-6f, (float*)F(8), 1e-6f, NULL, F(9), F(10), BIG, 0));
+  EXPECT(ROLA_ERR_INVALID_ARGUMENT, rola_sparse_attn_combine(&ok, F(1), F(2), F(3), 64, 0.9, (int32_t*)F(4), 0.1f, F(5), F(6), 32, T, T, 64, (float*)F(7), 1e-6f, (float*)F(8), 1e-6f, NULL, F(5), F(10), BIG, 0));
+  EXPECT(ROLA_ERR_INVALID_ARGUMENT, rola_sparse_attn_combine(&ok, F(1), F(2), F(3), 64, 0.9, (int32_t*)F(4), 0.1f, F(5), F(6), 32, T, T, 64, (float*)F(7), -1.f, (float*)F(8), 1e-6f, NULL, F(9), F(10), BIG, 0));
+  EXPECT(ROLA_ERR_WORKSPACE, rola_sparse_attn_combine(&ok, F(1), F(2), F(3), 64, 0.9, (int32_t*)F(4), 0.1f, F(5), F(6), 32, T, T, 64, (float*)F(7), 1e-6f, (float*)F(8), 1e-6f, NULL, F(9), F(10), 64, 0));
 
   // low-rank branch and the combine
   EXPECT(ROLA_ERR_INVALID_ARGUMENT, rola_lowrank_summary(&ok, F(1), F(2), F(3), 31, T, T, 64, (float*)F(4), NULL, F(5), BIG, 0));

@@ -173,11 +173,12 @@ def test_invalid_arguments_are_rejected_before_launch():
         (R.ROLA_ERR_INVALID_ARGUMENT, "rola_gate_logits", P(ok), FAKE, 5120, FAKE, -1.9, None, None),
         # attention + readout + combine: no workspace, too small a workspace, odd rank
         (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn_combine", P(ok), FAKE, FAKE, FAKE, 64, 0.9,
-         FAKE, 0.1, FAKE, FAKE, 32, FAKE, FAKE, 64, FAKE, 1e-6, FAKE, 1e-6, FAKE, None, 0, None),
+         FAKE, 0.1, FAKE, FAKE, 32, FAKE, FAKE, 64, FAKE, 1e-6, FAKE, 1e-6, None, FAKE, None, 0, None),
         (R.ROLA_ERR_WORKSPACE, "rola_sparse_attn_combine", P(ok), FAKE, FAKE, FAKE, 64, 0.9, FAKE,
-         0.1, FAKE, FAKE, 32, FAKE, FAKE, 64, FAKE, 1e-6, FAKE, 1e-6, FAKE, FAKE, 64, None),
+         0.1, FAKE, FAKE, 32, FAKE, FAKE, 64, FAKE, 1e-6, FAKE, 1e-6, None, FAKE, FAKE, 64, None),
         (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn_combine", P(ok), FAKE, FAKE, FAKE, 64, 0.9,
-         FAKE, 0.1, FAKE, FAKE, 31, FAKE, FAKE, 64, FAKE, 1e-6, FAKE, 1e-6, FAKE, FAKE, 1 << 40, None),
+         FAKE, 0.1, FAKE, FAKE, 31, FAKE, FAKE, 64, FAKE, 1e-6, FAKE, 1e-6, None, FAKE, FAKE, 1 << 40,
+         None),
     ]
     # outputs that overlap an input
     cases += [
@@ -185,7 +186,8 @@ def test_invalid_arguments_are_rejected_before_launch():
          SAME, None, 0, None),
         (R.ROLA_ERR_INVALID_ARGUMENT, "rola_dense_attn", P(ok), FAKE, FAKE, SAME, 64, 0.1, SAME, None),
         (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn_combine", P(ok), FAKE, FAKE, FAKE, 64, 0.9,
-         FAKE, 0.1, SAME, FAKE, 32, FAKE, FAKE, 64, FAKE, 1e-6, FAKE, 1e-6, SAME, FAKE, 1 << 40, None),
+         FAKE, 0.1, SAME, FAKE, 32, FAKE, FAKE, 64, FAKE, 1e-6, FAKE, 1e-6, None, SAME, FAKE, 1 << 40,
+         None),
         (R.ROLA_ERR_INVALID_ARGUMENT, "rola_combine", P(ok), FAKE, SAME, FAKE, 1e-6, SAME, None),
         (R.ROLA_ERR_INVALID_ARGUMENT, "rola_combine", P(ok), SAME, FAKE, FAKE, 1e-6,
          ctypes.c_void_p((1 << 44) + 4096), None),

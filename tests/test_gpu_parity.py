@@ -56,6 +56,15 @@ def _compare_head(w, gpu, ora, b, h, dtype, check_fused=True, check_unfused=True
     if "out_epi" in gpu:
         res["out_epi"] = T.assert_close(T.to_np(gpu["out_epi"][b, h])[rows][keep_rows],
                                         ora["out"][keep_rows], dtype, "O attention epilogue")
+    if "out_bound" in gpu:
+        res["out_bound"] = T.assert_close(T.to_np(gpu["out_bound"][b, h])[rows][keep_rows],
+                                          ora["out"][keep_rows], dtype, "O with the score bound")
+    if "knorm" in gpu:  # each key block's largest row norm, from the GPU's own K^r
+        kr = T.to_np(gpu["kr"][b, h])
+        nb = gpu["knorm"].shape[2]
+        want = np.array([np.sqrt((kr[J * w.block:(J + 1) * w.block] ** 2).sum(1).max())
+                         for J in range(nb)])
+        np.testing.assert_allclose(T.to_np(gpu["knorm"][b, h]), want, rtol=1e-5, atol=0)
     return res
 
 
@@ -125,7 +134,8 @@ def _sampled(w, heads, count, unfused=False, ws_check=False):
     assert idx.shape == (w.B, w.H, nb, keep)
     assert bool((idx[..., 1:] > idx[..., :-1]).all())
     assert int(idx.min()) >= 0 and int(idx.max()) < nb
-    keys = ["idx", "o_s", "C", "z", "out_fused", "out_epi"] + (["o_lr", "out"] if unfused else [])
+    keys = ["idx", "o_s", "C", "z", "out_fused", "out_epi", "out_bound", "kr", "knorm"] + (
+        ["o_lr", "out"] if unfused else [])
     for h in heads:
         head_in = {k: inp[k][:, h:h + 1] for k in ("Qn", "Kn", "V")}
         head_in.update(Pq=inp["Pq"][h:h + 1], Pk=inp["Pk"][h:h + 1], logits=inp["logits"])
@@ -456,6 +466,38 @@ def test_plan_then_planned_attention_on_two_streams():
     assert torch.equal(got2, want2)
 
 
+def test_score_bound_reference():
+    """The planned call given each key block's largest norm takes B = |q| max|k| scale log2(e) as
+    its softmax reference for every wave whose B are all at most 40, and the running maximum for
+    the others. (a) On the 1.3B layer (B about 20 everywhere) it runs (not bitwise the call
+    without norms) and differs from it by the rounding of the probabilities only. (b) With every
+    query 8 times larger every wave falls back: bitwise the call without norms. (c) With the
+    queries of every other 32-token wave 8 times larger (waves of both kinds in one workgroup),
+    every element against the oracle."""
+    w = synth.WAN_1_3B_480P
+    inp = synth.make_inputs(w, 0, device="cuda")
+    gpu = T.run_gpu(w, inp, fused_only=True)
+    d = (gpu["out_bound"].float() - gpu["out_epi"].float()).abs()
+    _report("score bound, 1.3B layer", max_diff=float(d.max()), mean_diff=float(d.mean()))
+    assert not torch.equal(gpu["out_bound"], gpu["out_epi"])
+    assert float(d.max()) <= 0.04 and float(d.mean()) <= 1e-3
+    small = w.replace(name="score bound fallback", grid=(3, 10, 13), H=2)
+    inp, f64 = _inputs(small, seed=3)
+    big = dict(inp, Qn=inp["Qn"] * 8)  # exact in bf16, and the rotation commutes with it
+    gpu = T.run_gpu(small, big, fused_only=True)
+    assert torch.equal(gpu["out_bound"], gpu["out_epi"])
+    mixed = inp["Qn"].clone()
+    n = torch.arange(small.N, device="cuda")
+    mixed[:, :, (n // 32) % 2 == 0] *= 8
+    inp_m = dict(inp, Qn=mixed)
+    gpu = T.run_gpu(small, inp_m, fused_only=True)
+    f64_m = synth.to_f64({k: v.cpu() for k, v in inp_m.items()})
+    for h in range(small.H):
+        ora = T.oracle_head(small, f64_m, 0, h)
+        res = _compare_head(small, gpu, ora, 0, h, "bf16", check_unfused=False)
+        _report(f"score bound, mixed waves h{h}", **res)
+
+
 @pytest.mark.parametrize("grid,H,block", [((21, 30, 52), 12, 64), ((3, 10, 13), 2, 64),
                                           ((3, 10, 13), 2, 128)],
                          ids=["1.3B-480p", "ragged-b64", "ragged-b128"])
@@ -471,15 +513,27 @@ def test_rope_pool_producer(grid, H, block):
     qr = R.rola_rope_apply(inp["Qn"], cos, sin, g)
     kr = R.rola_rope_apply(inp["Kn"], cos, sin, g)
     want_idx = R.rola_block_select(qr, kr, g, block, w.sparsity)
-    kr2, kbar = R.rola_rope_pool(inp["Kn"], cos, sin, g, block)
+    nb = R.num_blocks(w.N, block)
+    knorm = torch.empty((w.B, w.H, nb), dtype=torch.float32, device="cuda")
+    knorm_r = torch.empty_like(knorm)
+    kr2, kbar = R.rola_rope_pool(inp["Kn"], cos, sin, g, block, xnorm=knorm)
     none, qbar = R.rola_rope_pool(inp["Qn"], cos, sin, g, block, want_xr=False)
     idx = R.rola_block_select_pooled(qbar, kbar, qr, g, block, w.sparsity)
     _, qbar_r = R.rola_rope_pool(qr, None, None, g, block)   # pooling of the rotated tensor
+    _, kbar_r = R.rola_rope_pool(kr, None, None, g, block, xnorm=knorm_r)
     torch.cuda.synchronize()
     assert none is None
     assert torch.equal(kr2, kr)
     assert torch.equal(idx, want_idx)
     assert torch.equal(qbar_r, qbar)
+    assert torch.equal(kbar_r, kbar)
+    # each block's largest row norm of the rounded rotation, both passes
+    k64 = kr.double()
+    rows = (k64 * k64).sum(-1).sqrt()
+    pad = nb * block - w.N
+    want = torch.nn.functional.pad(rows, (0, pad), value=0.0).view(w.B, w.H, nb, block).amax(-1)
+    torch.testing.assert_close(knorm.double(), want, rtol=1e-5, atol=0)
+    torch.testing.assert_close(knorm_r.double(), want, rtol=1e-5, atol=0)
     ocos, osin = O.rope_tables(*g, w.split)
     for h in range(w.H):
         # the pooling arithmetic: the oracle's pool_blocks of the GPU's own rounded rotation

@@ -40,9 +40,17 @@ def test_noalloc_matches_workspace_form():
         want = R.rola_sparse_attn_combine(*args)
         got = torch.full_like(want, float("nan"))
         R.rola_sparse_attn_combine_noalloc(*args, out=got)
+        # with the key-block norms (the score-bound softmax reference) as well
+        knorm = torch.empty((w.B, w.H, R.num_blocks(w.N, w.block)), dtype=torch.float32,
+                            device="cuda")
+        R.rola_rope_pool(args[1], None, None, w.grid, w.block, xnorm=knorm)
+        want_b = R.rola_sparse_attn_combine(*args, key_norm=knorm)
+        got_b = torch.full_like(want, float("nan"))
+        R.rola_sparse_attn_combine_noalloc(*args, out=got_b, key_norm=knorm)
         torch.cuda.synchronize()
         assert torch.equal(got, want), w.name
-        del args, want, got
+        assert torch.equal(got_b, want_b), w.name
+        del args, want, got, want_b, got_b
 
 
 def test_noalloc_rejects_a_problem_beyond_the_scratch():
