@@ -171,29 +171,16 @@ def sweep(reps: int) -> None:
     scratch = torch.empty(1 << 30, dtype=torch.uint8, device=dev)   # 1 GiB: evicts L2 and MALL
     evict = lambda: scratch.fill_(1)  # noqa: E731
 
-    # the 1.3B 480p layer (same step as the headline)
+    # the 1.3B 480p layer: the headline's two-stream step
     w = synth.WAN_1_3B_480P
-    g = w.grid
-    inp = synth.make_inputs(w, 0, device=dev)
-    prob = R.problem(w.B, w.H, w.N, w.d_h, g, w.dtype)
-    cos, sin = R.rola_rope_tables(prob, w.split, w.base)
-    qr = R.rola_rope_apply(inp["Qn"], cos, sin, g)
-    kr = R.rola_rope_apply(inp["Kn"], cos, sin, g)
-    ws_sp = torch.empty(R.sparse_combine_workspace_bytes(prob, w.block, w.sparsity, w.r),
-                        dtype=torch.uint8, device=dev)
-    idx = R.rola_block_select(qr, kr, g, w.block, w.sparsity)
-    o_s = torch.empty_like(qr)
-
-    def layer():
-        R.rola_block_select(qr, kr, g, w.block, w.sparsity, out=idx)
-        C, _ = R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], w.r, cos, sin, g)
-        R.rola_sparse_attn_combine(qr, kr, inp["V"], g, w.block, w.sparsity, idx, inp["Qn"], inp["Pq"],
-                                   w.r, cos, sin, C, inp["logits"], out=o_s, ws=ws_sp)
-    ms, lo, hi = time_call(layer, reps)
-    f = sparse_flops_performed(idx, w.N, w.block, w.d_h) + 8.0 * w.B * w.H * w.N * w.d_h * w.r
+    L = LayerStep(R, w, dev)
+    L.step()
+    torch.cuda.synchronize()
+    ms, lo, hi = time_call(L.step, reps)
+    f = sparse_flops_performed(L.idx, w.N, w.block, w.d_h) + 8.0 * w.B * w.H * w.N * w.d_h * w.r
     print(f"## Layer, {w.name}\n\n| ms (median) | p10 | p90 | eff. TFLOP/s |\n|---|---|---|---|")
     print(f"| {ms:.3f} | {lo:.3f} | {hi:.3f} | {f / ms / 1e9:.1f} |\n", flush=True)
-    del inp, qr, kr, idx, o_s
+    del L
 
     # low-rank branch: N x r, summary and readout separately (warm / cold cache)
     print("## Low-rank branch, H40 d128 bf16 (HBM roofline 8 TB/s)\n")
@@ -397,6 +384,87 @@ def dit_bench(reps: int) -> None:
     print()
 
 
+class LayerStep:
+    """The timed layer (steps a1-a5 of the hot path; the backbone's rotation is the input) on two
+    HIP streams, with its inputs and buffers for workload w. Main stream: the block means of Q^r and
+    K^r (with each key block's largest key norm), the block scores and top-k, the attention's
+    pairing and list merge; side stream, forked once the block lists exist: the low-rank summary,
+    beside the pairing, whose passes are latency-bound (its greedy pass keeps one wave per head
+    busy) and leave the chip's bandwidth to the summary. Forked after the pooling instead, the
+    summary slows the score and top-k kernels beside it by more than it saves (0.1 ms per layer).
+    After both: the block-sparse attention with the low-rank readout and the gated combine in its
+    epilogue (O^s and O^lr never reach memory), given the key norms so that it can take the score
+    bound as its softmax reference. step(rotate=True) starts from Q^n, K^n: the rotating pooling
+    passes write Q^r and K^r (Algorithm step 3 fused with the pooling)."""
+    NAMES = ["pool", "select", "plan", "attention_readout_combine"]
+
+    def __init__(self, R, w, dev):
+        self.R, self.w = R, w
+        g = w.grid
+        self.inp = inp = synth.make_inputs(w, 0, device=dev)
+        self.prob = prob = R.problem(w.B, w.H, w.N, w.d_h, g, w.dtype)
+        self.cos, self.sin = R.rola_rope_tables(prob, w.split, w.base)
+        self.qr = R.rola_rope_apply(inp["Qn"], self.cos, self.sin, g)
+        self.kr = R.rola_rope_apply(inp["Kn"], self.cos, self.sin, g)
+        nb = R.num_blocks(w.N, w.block)
+        self.keep = R.keep_blocks(nb, w.sparsity)
+        self.idx = torch.empty((w.B, w.H, nb, self.keep), dtype=torch.int32, device=dev)
+        u8 = dict(dtype=torch.uint8, device=dev)
+        self.ws_sel = torch.empty(R.select_workspace_bytes(prob, w.block), **u8)
+        self.ws_sum = torch.empty(R.summary_workspace_bytes(prob, w.r), **u8)
+        self.ws_sp = torch.empty(R.sparse_combine_workspace_bytes(prob, w.block, w.sparsity, w.r), **u8)
+        self.ws_pool = torch.empty(R.LIB.rola_select_pooled_workspace_bytes(ctypes.byref(prob),
+                                                                            w.block), **u8)
+        self.out = torch.empty_like(inp["Qn"])
+        self.C = torch.empty((w.B, w.H, w.r, w.d_h), dtype=torch.float32, device=dev)
+        self.z = torch.empty((w.B, w.H, w.r), dtype=torch.float32, device=dev)
+        self.qbar = torch.empty((w.B, w.H, nb, w.d_h), dtype=torch.float32, device=dev)
+        self.kbar = torch.empty_like(self.qbar)
+        self.knorm = torch.empty((w.B, w.H, nb), dtype=torch.float32, device=dev)
+        self.main_st = torch.cuda.current_stream()
+        self.side_st = torch.cuda.Stream(device=dev)  # default priority
+
+    def step(self, ev=None, sev=None, rotate=False):
+        """One layer; ev: 5 timing events on the main stream around the NAMES spans, sev: 2 around
+        the summary on the side stream."""
+        R, w, inp, g = self.R, self.w, self.inp, self.w.grid
+        main_st, side_st = self.main_st, self.side_st
+
+        def mark(i):
+            if ev is not None:
+                ev[i].record(main_st)
+        fork, join = torch.cuda.Event(), torch.cuda.Event()
+        mark(0)
+        if rotate:
+            R.rola_rope_pool(inp["Qn"], self.cos, self.sin, g, w.block, xr=self.qr, xbar=self.qbar)
+            R.rola_rope_pool(inp["Kn"], self.cos, self.sin, g, w.block, xr=self.kr, xbar=self.kbar,
+                             xnorm=self.knorm)
+        else:
+            R.rola_rope_pool(self.qr, None, None, g, w.block, xbar=self.qbar)
+            R.rola_rope_pool(self.kr, None, None, g, w.block, xbar=self.kbar, xnorm=self.knorm)
+        mark(1)
+        R.rola_block_select_pooled(self.qbar, self.kbar, self.kr, g, w.block, w.sparsity,
+                                   out=self.idx, ws=self.ws_pool)
+        mark(2)
+        fork.record(main_st)
+        side_st.wait_event(fork)
+        if sev is not None:
+            sev[0].record(side_st)
+        R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], w.r, self.cos, self.sin, g, C=self.C,
+                               z=self.z, ws=self.ws_sum, stream=side_st)
+        if sev is not None:
+            sev[1].record(side_st)
+        join.record(side_st)
+        R.rola_sparse_plan(self.idx, self.kr, g, w.block, w.sparsity, w.r, self.ws_sp)
+        main_st.wait_event(join)
+        mark(3)
+        R.rola_sparse_attn_combine_planned(self.qr, self.kr, inp["V"], g, w.block, w.sparsity,
+                                           self.idx, inp["Qn"], inp["Pq"], w.r, self.cos, self.sin,
+                                           self.C, inp["logits"], self.ws_sp, out=self.out,
+                                           key_norm=self.knorm)
+        mark(4)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -440,70 +508,10 @@ def main():
     g = w.grid
     dev = torch.device("cuda:0")
     print(f"[bench] generating {w.name} inputs", file=sys.stderr, flush=True)
-    inp = synth.make_inputs(w, 0, device=dev)
-    prob = R.problem(w.B, w.H, w.N, w.d_h, g, w.dtype)
-    cos, sin = R.rola_rope_tables(prob, w.split, w.base)
-    qr = R.rola_rope_apply(inp["Qn"], cos, sin, g)
-    kr = R.rola_rope_apply(inp["Kn"], cos, sin, g)
-    nb = R.num_blocks(w.N, w.block)
-    keep = R.keep_blocks(nb, w.sparsity)
-    idx = torch.empty((w.B, w.H, nb, keep), dtype=torch.int32, device=dev)
-    ws_sel = torch.empty(R.select_workspace_bytes(prob, w.block), dtype=torch.uint8, device=dev)
-    ws_sum = torch.empty(R.summary_workspace_bytes(prob, w.r), dtype=torch.uint8, device=dev)
-    ws_sp = torch.empty(R.sparse_combine_workspace_bytes(prob, w.block, w.sparsity, w.r),
-                        dtype=torch.uint8, device=dev)
-    out = torch.empty_like(inp["Qn"])
-    C = torch.empty((w.B, w.H, w.r, w.d_h), dtype=torch.float32, device=dev)
-    z = torch.empty((w.B, w.H, w.r), dtype=torch.float32, device=dev)
-    main_st = torch.cuda.current_stream()
-    side_st = torch.cuda.Stream(device=dev)  # default priority
-    qbar = torch.empty((w.B, w.H, nb, w.d_h), dtype=torch.float32, device=dev)
-    kbar = torch.empty_like(qbar)
-    knorm = torch.empty((w.B, w.H, nb), dtype=torch.float32, device=dev)  # per key block max |k^r|
-    ws_pool = torch.empty(R.LIB.rola_select_pooled_workspace_bytes(ctypes.byref(prob), w.block),
-                          dtype=torch.uint8, device=dev)
-    # The layer (steps a1-a5 of the hot path; the backbone's rotation is the input) on two streams.
-    # Main stream: the block means of Q^r and K^r, the block scores and top-k, the attention's
-    # pairing and list merge; side stream, forked once the block lists exist: the low-rank summary,
-    # beside the pairing, whose passes are latency-bound (its greedy pass keeps one wave per head
-    # busy) and leave the chip's bandwidth to the summary. Forked after the pooling instead, the
-    # summary slows the score and top-k kernels beside it by more than it saves (0.1 ms per layer).
-    # After both: the block-sparse attention with the low-rank readout and the gated combine in its
-    # epilogue (O^s and O^lr never reach memory). rotate=True starts from Q^n, K^n: the rotating
-    # pooling passes write Q^r and K^r (Algorithm step 3 fused with the pooling).
-    names = ["pool", "select", "plan", "attention_readout_combine"]
-
-    def step(ev=None, sev=None, rotate=False):
-        def mark(i):
-            if ev is not None:
-                ev[i].record(main_st)
-        fork, join = torch.cuda.Event(), torch.cuda.Event()
-        mark(0)
-        if rotate:
-            R.rola_rope_pool(inp["Qn"], cos, sin, g, w.block, xr=qr, xbar=qbar)
-            R.rola_rope_pool(inp["Kn"], cos, sin, g, w.block, xr=kr, xbar=kbar, xnorm=knorm)
-        else:
-            R.rola_rope_pool(qr, None, None, g, w.block, xbar=qbar)
-            R.rola_rope_pool(kr, None, None, g, w.block, xbar=kbar, xnorm=knorm)
-        mark(1)
-        R.rola_block_select_pooled(qbar, kbar, kr, g, w.block, w.sparsity, out=idx, ws=ws_pool)
-        mark(2)
-        fork.record(main_st)
-        side_st.wait_event(fork)
-        if sev is not None:
-            sev[0].record(side_st)
-        R.rola_lowrank_summary(inp["Kn"], inp["V"], inp["Pk"], w.r, cos, sin, g, C=C, z=z, ws=ws_sum,
-                               stream=side_st)
-        if sev is not None:
-            sev[1].record(side_st)
-        join.record(side_st)
-        R.rola_sparse_plan(idx, kr, g, w.block, w.sparsity, w.r, ws_sp)
-        main_st.wait_event(join)
-        mark(3)
-        R.rola_sparse_attn_combine_planned(qr, kr, inp["V"], g, w.block, w.sparsity, idx, inp["Qn"],
-                                           inp["Pq"], w.r, cos, sin, C, inp["logits"], ws_sp,
-                                           out=out, key_norm=knorm)
-        mark(4)
+    L = LayerStep(R, w, dev)
+    inp, cos, sin, qr, kr, idx, out, C, z = L.inp, L.cos, L.sin, L.qr, L.kr, L.idx, L.out, L.C, L.z
+    ws_sel, ws_sum, ws_sp, prob, keep = L.ws_sel, L.ws_sum, L.ws_sp, L.prob, L.keep
+    names, step = LayerStep.NAMES, L.step
 
     if args.calibration_copy:  # a plain copy of known size, for scaling FETCH_SIZE / WRITE_SIZE
         scratch = torch.empty_like(inp["V"])
