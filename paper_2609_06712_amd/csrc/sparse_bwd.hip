@@ -8,8 +8,10 @@
 //   sparse_dq_kernel   per query block, walking its own list (as the forward): Q and dO of the wave's
 //                      32 queries in registers, K and V sub-tiles through three LDS stages;
 //   sparse_dkv_kernel  per key block, walking the query blocks that selected it (lists transposed by
-//                      bwd_reverse_kernel): K and V of the wave's 32 keys in registers, Q and dO
-//                      sub-tiles (and the queries' lse and D) through three LDS stages.
+//                      bwd_reverse_kernel) in 32-query steps: one role of waves holds the keys' K
+//                      (S, P, dV), the other their V (dP, dS, dK) and takes P from the first one
+//                      step later; Q and dO rows (and the queries' lse and D) through four LDS
+//                      stages.
 // Products on v_mfma_f32_32x32x16_bf16. S and dP come out with one lane per key and the 32 queries
 // in its registers; the products that contract over keys (dQ) or queries (dK, dV) take their other
 // operand through the transposing LDS read ds_read_b64_tr_b16, in the order the registers hold the
@@ -25,6 +27,7 @@ namespace {
 constexpr int kBSub = 32;      // keys (dQ) or queries (dK, dV) per sub-tile
 constexpr int kLsePad = 128;  // zero entries after the packed lse/D array: a sub-tile of the last
                               // query block reads up to block - 1 entries past the last query
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
 __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -238,31 +241,41 @@ __global__ __launch_bounds__(BLK * 2, 2) void sparse_dq_kernel(
   }
 }
 
-// ---- dK, dV: one workgroup per (b, h, key block), BLK/32 waves of 32 keys --------------------------
-constexpr int kDkvNbuf = 2;  // LDS stages (34 KB each) of sparse_dkv_kernel; one wave per SIMD
+// ---- dK, dV: one workgroup per (b, h, key block) ------------------------------------------------
+// Two roles of BLK/32 waves each over the same 32-key column tiles. Role 0 holds the keys' K and
+// computes S, P = exp2(S scale log2e - lse) and dV += dO^T P; role 1 holds their V and computes
+// dP = dO V^T, dS = P (dP - D) and dK += Q^T dS, taking P from role 0 through LDS one step later
+// (double-buffered, so one barrier per step serves the tile stages and the hand-over). A wave then
+// needs one B operand set and one accumulator set (a wave doing both needs twice that, more than
+// half the register file, and the compiler then moves accumulators between the two register files
+// every step), so two waves run per SIMD. A step takes 32 queries. P goes over as fp16: it lies
+// in [0, 1], where fp16's relative error (2^-11; absolute 2^-25 below 2^-14) is an eighth of the
+// bf16 rounding dS takes next.
+constexpr int kDkvNbuf = 4;  // LDS stages of sparse_dkv_kernel: 32 Q rows, 32 dO rows, lse/D (17 KB)
 template <int BLK, int NBUF>
-__global__ __launch_bounds__(BLK * 2) __attribute__((amdgpu_waves_per_eu(1)))
+__global__ __launch_bounds__(BLK * 4) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void sparse_dkv_kernel(
     int N, int nb, int total, const int32_t* __restrict__ rev, float scale_log2, float scale,
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
     const bf16* __restrict__ dO, const float2* __restrict__ lseD, float* __restrict__ dK,
     float* __restrict__ dV) {
-  // A step takes 64 queries as two independent 32-query halves: one wave per SIMD (the dK, dV
-  // accumulators and the K, V operands hold most of the registers), so the second half's S and dP
-  // products are what overlaps the first half's softmax.
-  constexpr int D = 128, NW = BLK / 32, QS = 2 * kBSub;
-  constexpr int TILE = QS * D * 2;
-  constexpr int STAGE = 2 * TILE + NW * 1024;  // Q, dO, then each wave's copy of the rows' lse/D
-  constexpr int DMA_PER_WAVE = TILE / 1024 / NW, SUBS = BLK / QS;
-  static_assert(SUBS >= 1 && DMA_PER_WAVE >= 1, "64- or 128-query blocks");
-  __shared__ __attribute__((aligned(1024))) char lds[NBUF * STAGE];
+  constexpr int D = 128, NKW = BLK / 32, NW = 2 * NKW;
+  constexpr int TILE = kBSub * D * 2;          // 32 rows of 256 bytes
+  constexpr int STAGE = 2 * TILE + 1024;       // Q, dO, then lse/D of the 32 queries (256 B used)
+  constexpr int DPW = 2 * (TILE / 1024) / NW;  // 1 KB tile loads per wave and step
+  constexpr int SUBS = BLK / kBSub;            // steps per query block
+  constexpr int PBUF = NKW * 2048;             // P of a step, fp16: per key tile 16 values a lane
+  constexpr int AHEAD = NBUF - 2;              // stages loaded ahead (role 1 still reads one back)
+  static_assert(DPW >= 1 && 2 * (TILE / 1024) % NW == 0 && AHEAD >= 1, "64- or 128-key blocks");
+  __shared__ __attribute__((aligned(1024))) char lds[NBUF * STAGE + 2 * PBUF];
 
   const int L = xcd_remap(blockIdx.x, total);
   const int J = L % nb;
   const long head = L / nb;
   const int tid = threadIdx.x, lane = tid % 64, hh = lane / 32;
   const int wave = wave_uniform(tid / 64);
-  const int key = J * BLK + wave * 32 + lane % 32;  // B-operand column of this lane
+  const int role = wave / NKW, kw = wave % NKW;
+  const int key = J * BLK + kw * 32 + lane % 32;  // B-operand column of this lane
   const bool kvalid = key < N;
   const long hoff = head * (long)N * D;
   const char* Qh = reinterpret_cast<const char*>(Q + hoff);
@@ -272,134 +285,133 @@ void sparse_dkv_kernel(
   const int E = rl[0];
   const int T = E * SUBS;
 
-  bf16x8 kf[8], vf[8];
+  const bf16* bsrc = (role ? V : K) + hoff + (long)key * D + 8 * hh;
+  bf16x8 bf[8];
 #pragma unroll
-  for (int s = 0; s < 8; ++s) {
-    kf[s] = kvalid ? *reinterpret_cast<const bf16x8*>(K + hoff + (long)key * D + 16 * s + 8 * hh) : bf16x8{};
-    vf[s] = kvalid ? *reinterpret_cast<const bf16x8*>(V + hoff + (long)key * D + 16 * s + 8 * hh) : bf16x8{};
-  }
+  for (int s = 0; s < 8; ++s)
+    bf[s] = kvalid ? *reinterpret_cast<const bf16x8*>(bsrc + 16 * s) : bf16x8{};
   __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
 
-  f32x16 aK[4], aV[4];
+  f32x16 acc[4];
 #pragma unroll
-  for (int w = 0; w < 4; ++w) aK[w] = aV[w] = f32x16{};
+  for (int w = 0; w < 4; ++w) acc[w] = f32x16{};
 
-  uint32_t dsrc[DMA_PER_WAVE];
+  // Tile loads: load g = wave * DPW + i moves rows 4(g % 8) .. +3 of Q (g < 8) or dO (g >= 8).
+  uint32_t dsrc[DPW];
 #pragma unroll
-  for (int i = 0; i < DMA_PER_WAVE; ++i) {
-    const int row = 4 * (wave * DMA_PER_WAVE + i) + lane / 16, pos = lane % 16;
+  for (int i = 0; i < DPW; ++i) {
+    const int g = wave * DPW + i, row = 4 * (g % 8) + lane / 16, pos = lane % 16;
     dsrc[i] = row * D * 2 + ((pos ^ bw_swizzle(row)) << 4);
   }
   const uint32_t lds0 = lds_address(lds);
   const char* lsebase = reinterpret_cast<const char*>(lseD + head * (long)N);
-  auto query0 = [&](int t) { return rl[1 + t / SUBS] * BLK + (t % SUBS) * QS; };
-  auto issue = [&](int q0, int buf) {  // 2 * DMA_PER_WAVE + 1 loads per wave, always
+  auto query0 = [&](int t) { return rl[1 + t / SUBS] * BLK + (t % SUBS) * kBSub; };
+  auto issue = [&](int q0, int buf) {  // DPW loads per wave, and wave 0 one more (lse/D)
     const uint32_t dst = lds0 + buf * STAGE;
 #pragma unroll
-    for (int i = 0; i < DMA_PER_WAVE; ++i) {
-      const uint32_t slot = (wave * DMA_PER_WAVE + i) * 1024;
-      const int r = 4 * (wave * DMA_PER_WAVE + i) + lane / 16;
+    for (int i = 0; i < DPW; ++i) {
+      const int g = wave * DPW + i, r = 4 * (g % 8) + lane / 16;
       const uint32_t rowoff = (uint32_t)(min(q0 + r, N - 1) - r) * (D * 2);  // rows past N: N-1
-      dma16(Qh, rowoff + dsrc[i], dst + slot);
-      dma16(dOh, rowoff + dsrc[i], dst + TILE + slot);
+      dma16(g < 8 ? Qh : dOh, rowoff + dsrc[i], dst + (g / 8) * TILE + (g % 8) * 1024);
     }
-    // lse, D of the 64 queries (512 bytes, lanes 32-63 repeat lanes 0-31): the array is padded by
+    // lse, D of the 32 queries (256 bytes; lanes 16-63 repeat lanes 0-15): the array is padded by
     // kLsePad entries, and rows past N are masked below
-    dma16(lsebase, (uint32_t)(q0 * 8 + (lane % 32) * 16), dst + 2 * TILE + wave * 1024);
+    if (wave == 0) dma16(lsebase, (uint32_t)(q0 * 8 + (lane % 16) * 16), dst + 2 * TILE);
   };
 
-  constexpr int PER_STEP = 2 * DMA_PER_WAVE + 1;
   int issued = 0;
 #pragma unroll
-  for (int j = 0; j < NBUF - 1; ++j)
+  for (int j = 0; j < AHEAD; ++j)
     if (j < T) issue(query0(j), j), ++issued;
-  for (int t = 0; t < T;) {
+  char* pbase = lds + NBUF * STAGE + kw * 2048 + lane * 16;  // + buffer * PBUF + u * 1024
+  // Iteration t: role 0 takes step t (t < T), role 1 step t - 1 (t >= 1).
+  for (int t = 0; t <= T;) {
 #pragma unroll
     for (int b = 0; b < NBUF; ++b) {
-      if (t >= T) break;
-      if (issued == t + NBUF - 1) {
-        constexpr int allowed = PER_STEP * (NBUF - 2);
-        __builtin_amdgcn_s_waitcnt((allowed & 15) | ((allowed >> 4) << 14) | (7 << 4) | (15 << 8));
+      if (t > T) break;
+      if (t < T && issued == t + AHEAD) {
+        constexpr int a0 = (DPW + 1) * (AHEAD - 1), a1 = DPW * (AHEAD - 1);
+        if (wave == 0)
+          __builtin_amdgcn_s_waitcnt((a0 & 15) | ((a0 >> 4) << 14) | (7 << 4) | (15 << 8));
+        else
+          __builtin_amdgcn_s_waitcnt((a1 & 15) | ((a1 >> 4) << 14) | (7 << 4) | (15 << 8));
       } else {
         __builtin_amdgcn_s_waitcnt(0);
       }
       __syncthreads();
-      if (issued < T) issue(query0(issued), (b + NBUF - 1) % NBUF), ++issued;
-      const int q0 = query0(t);
-      const char* Qt = lds + b * STAGE;
-      const char* dOt = Qt + TILE;
-      const float2* lt = reinterpret_cast<const float2*>(Qt + 2 * TILE + wave * 1024);
-      // Phases, each kept apart by a scheduling barrier so that operand reads are not all hoisted
-      // to the top (which overflows the register file): S, dP of half 0; S, dP of half 1 beside
-      // the softmax of half 0; the dV, dK products of half 0 beside the softmax of half 1; the
-      // products of half 1.
-      auto scores = [&](int h, f32x16& S, f32x16& dP) {
-        S = f32x16{};
-        dP = f32x16{};
+      if (issued < T) issue(query0(issued), (b + AHEAD) % NBUF), ++issued;
+      if (role ? t >= 1 : t < T) {
+        const char* Qt = lds + (role ? (b + NBUF - 1) % NBUF : b) * STAGE;
+        const char* dOt = Qt + TILE;
+        const float2* lt = reinterpret_cast<const float2*>(Qt + 2 * TILE);
+        char* pb = pbase + ((b + role) % 2) * PBUF;  // role 0 writes step t's, role 1 reads t - 1's
+        // S (role 0) or dP (role 1): one lane per key; rows 8j + 4(l/32) + i are the step's queries
+        // All operand fragments of the step are read up front (the transposed ones do not wait
+        // for P), so that the products do not wait on LDS one fragment at a time.
+        const char* A1 = role ? dOt : Qt;
+        const char* A2 = role ? Qt : dOt;
+        bf16x8 fa[8], fb[8];
 #pragma unroll
-        for (int s = 0; s < 8; ++s) {
-          S = mfma32(row_frag(Qt, 32 * h + lane % 32, s, hh), kf[s], S);
-          dP = mfma32(row_frag(dOt, 32 * h + lane % 32, s, hh), vf[s], dP);
-        }
-      };
-      // one lane per key; rows 32h + 8j + 4(l/32) + i are the queries q0 + row
-      // The exponentials are computed unconditionally and rows past N zeroed in one uniform branch:
-      // a per-element condition around them splits the step into a basic block per element,
-      // across which no matrix instruction can be scheduled.
-      auto softmax = [&](int h, const f32x16& S, const f32x16& dP, bf16x8 (&pb)[2], bf16x8 (&sb)[2]) {
-        float p[16], dd[16];
-#pragma unroll
-        for (int k = 0; k < 16; ++k) {
-          const float2 ld = lt[32 * h + 8 * (k / 4) + 4 * hh + k % 4];
-          p[k] = __builtin_amdgcn_exp2f(fmaf(S[k], scale_log2, -ld.x));
-          dd[k] = dP[k] - ld.y;
-        }
-        if (q0 + QS > N) {  // ragged last query block (uniform)
-#pragma unroll
-          for (int k = 0; k < 16; ++k)
-            p[k] = q0 + 32 * h + 8 * (k / 4) + 4 * hh + k % 4 < N ? p[k] : 0.f;
-        }
-#pragma unroll
-        for (int k = 0; k < 16; ++k) {
-          pb[k / 8][k % 8] = (bf16)p[k];
-          sb[k / 8][k % 8] = (bf16)(p[k] * dd[k]);
-        }
-      };
-      auto grads = [&](int h, const bf16x8 (&pb)[2], const bf16x8 (&sb)[2]) {
+        for (int s = 0; s < 8; ++s) fa[s] = row_frag(A1, lane % 32, s, hh);
 #pragma unroll
         for (int w = 0; w < 4; ++w)
 #pragma unroll
-          for (int u = 0; u < 2; ++u) {
-            aV[w] = mfma32(tr_frag(dOt + h * (TILE / 2), w, u, lane), pb[u], aV[w]);
-            aK[w] = mfma32(tr_frag(Qt + h * (TILE / 2), w, u, lane), sb[u], aK[w]);
+          for (int u = 0; u < 2; ++u) fb[2 * w + u] = tr_frag(A2, w, u, lane);
+        __builtin_amdgcn_sched_barrier(0);
+        f32x16 X = f32x16{};
+#pragma unroll
+        for (int s = 0; s < 8; ++s) X = mfma32(fa[s], bf[s], X);
+        float p[16];
+        bf16x8 b2[2];
+        if (role == 0) {
+          const int q0 = query0(t);
+          // The exponentials are computed unconditionally and rows past N zeroed in one uniform
+          // branch: a per-element condition around them splits the step into a basic block per
+          // element, across which no matrix instruction can be scheduled.
+#pragma unroll
+          for (int k = 0; k < 16; ++k)
+            p[k] = __builtin_amdgcn_exp2f(fmaf(X[k], scale_log2, -lt[8 * (k / 4) + 4 * hh + k % 4].x));
+          if (q0 + kBSub > N) {  // ragged last query block (uniform)
+#pragma unroll
+            for (int k = 0; k < 16; ++k) p[k] = q0 + 8 * (k / 4) + 4 * hh + k % 4 < N ? p[k] : 0.f;
           }
-      };
-      f32x16 S0, dP0, S1, dP1;
-      bf16x8 pb0[2], sb0[2], pb1[2], sb1[2];
-      scores(0, S0, dP0);
-      __builtin_amdgcn_sched_barrier(0);
-      scores(1, S1, dP1);
-      softmax(0, S0, dP0, pb0, sb0);
-      __builtin_amdgcn_sched_barrier(0);
-      grads(0, pb0, sb0);
-      softmax(1, S1, dP1, pb1, sb1);
-      __builtin_amdgcn_sched_barrier(0);
-      grads(1, pb1, sb1);
+          f16x8 ph[2];
+#pragma unroll
+          for (int k = 0; k < 16; ++k) {
+            b2[k / 8][k % 8] = (bf16)p[k];
+            ph[k / 8][k % 8] = (_Float16)p[k];
+          }
+          *reinterpret_cast<f16x8*>(pb) = ph[0];
+          *reinterpret_cast<f16x8*>(pb + 1024) = ph[1];
+        } else {
+          const f16x8 ph0 = *reinterpret_cast<const f16x8*>(pb);
+          const f16x8 ph1 = *reinterpret_cast<const f16x8*>(pb + 1024);
+#pragma unroll
+          for (int k = 0; k < 16; ++k) {
+            const float pk = (float)(k < 8 ? ph0[k] : ph1[k - 8]);
+            b2[k / 8][k % 8] = (bf16)(pk * (X[k] - lt[8 * (k / 4) + 4 * hh + k % 4].y));
+          }
+        }
+        // dV^T += dO^T P (role 0) or dK^T += Q^T dS (role 1), the transposed operand in the order
+        // the registers hold the queries
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+#pragma unroll
+          for (int u = 0; u < 2; ++u) acc[w] = mfma32(fb[2 * w + u], b2[u], acc[w]);
+      }
       ++t;
     }
   }
-  if (kvalid) {  // dK^T, dV^T: lane = key, rows = channels 32w + 8j + 4(l/32) + i
-    float* dk = dK + hoff + (long)key * D;
-    float* dv = dV + hoff + (long)key * D;
+  if (kvalid) {  // dV^T (role 0), dK^T (role 1): lane = key, rows = channels 32w + 8j + 4(l/32) + i
+    float* out = (role ? dK : dV) + hoff + (long)key * D;
+    const float f = role ? scale : 1.f;
 #pragma unroll
     for (int w = 0; w < 4; ++w)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int c = 32 * w + 8 * j + 4 * hh;
-        *reinterpret_cast<float4*>(dk + c) = make_float4(aK[w][4 * j] * scale, aK[w][4 * j + 1] * scale,
-                                                         aK[w][4 * j + 2] * scale, aK[w][4 * j + 3] * scale);
-        *reinterpret_cast<float4*>(dv + c) = make_float4(aV[w][4 * j], aV[w][4 * j + 1],
-                                                         aV[w][4 * j + 2], aV[w][4 * j + 3]);
+        *reinterpret_cast<float4*>(out + c) = make_float4(acc[w][4 * j] * f, acc[w][4 * j + 1] * f,
+                                                          acc[w][4 * j + 2] * f, acc[w][4 * j + 3] * f);
       }
   }
 }
@@ -446,7 +458,7 @@ hipError_t launch_bwd(const Shape& s, const void* Qr, const void* Kr, const void
                        idx, keep, sl, scale, (const bf16*)Qr, (const bf16*)Kr, (const bf16*)V,
                        (const bf16*)dOs, (const float2*)lseD, dQ);
   }
-  hipLaunchKernelGGL((sparse_dkv_kernel<BLK, kDkvNbuf>), dim3(total), dim3(BLK * 2), 0, st, s.N, nb, total,
+  hipLaunchKernelGGL((sparse_dkv_kernel<BLK, kDkvNbuf>), dim3(total), dim3(BLK * 4), 0, st, s.N, nb, total,
                      (const int32_t*)rev, sl, scale, (const bf16*)Qr, (const bf16*)Kr,
                      (const bf16*)V, (const bf16*)dOs, (const float2*)lseD, dK, dV);
   return hipGetLastError();
