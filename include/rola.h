@@ -261,7 +261,8 @@ rola_status rola_sparse_attn_combine_noalloc(
  * is bf16 [B, H, N, d_h]. ws: rola_sparse_backward_workspace_bytes(p, block, sparsity) bytes (the
  * transposed block lists take 4 (n_b + 1) bytes per key block and head; with 64-token blocks the
  * dQ pass also keeps the pairs, merged lists and queue counters of rola_sparse_attn there). bf16
- * path only (ROLA_ERR_UNSUPPORTED otherwise), block 64 or 128. */
+ * path only, block 64 or 128, at most 16384 blocks per head (ROLA_ERR_UNSUPPORTED otherwise; the
+ * workspace size query returns 0 beyond that many blocks). */
 rola_status rola_sparse_attn_lse(const rola_problem* p, const void* Qr, const void* Kr,
                                  const void* V, int32_t block, double sparsity,
                                  const int32_t* blk_idx, float softmax_scale, void* Os, float* lse,

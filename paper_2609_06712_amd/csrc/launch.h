@@ -103,8 +103,10 @@ hipError_t launch_sparse_dq(const Shape& s, const void* Qr, const void* Kr, cons
                             const int32_t* idx, float scale, const void* dO, const void* lseD,
                             float* dQ, void* ws, hipStream_t st);
 
-// sparse_bwd.hip: gradients of the block-sparse attention (bf16, d 128, block 64 or 128); fp32
-// outputs; ws: sparse_backward_workspace_bytes(s, block, keep).
+// sparse_bwd.hip: gradients of the block-sparse attention (bf16, d 128, block 64 or 128, at most
+// kBwdMaxBlocks blocks per head: the transposed lists are built through one LDS word per block);
+// fp32 outputs; ws: sparse_backward_workspace_bytes(s, block, keep), 0 when unsupported.
+constexpr int kBwdMaxBlocks = 16384;
 size_t sparse_backward_workspace_bytes(const Shape& s, int block, int keep);
 hipError_t launch_sparse_backward(const Shape& s, const void* Qr, const void* Kr, const void* V,
                                   int block, int keep, const int32_t* idx, float scale,

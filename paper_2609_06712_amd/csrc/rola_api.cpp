@@ -482,6 +482,9 @@ rola_status rola_sparse_attn_backward(const rola_problem* p, const void* Qr, con
   TRY(check_block(s, block, __func__));
   TRY(check_sparsity(sparsity, __func__));
   if (!s.bf16) return fail(ROLA_ERR_UNSUPPORTED, "%s: built for the bf16 path", __func__);
+  if (rola::num_blocks(s.N, block) > rola::kBwdMaxBlocks)
+    return fail(ROLA_ERR_UNSUPPORTED, "%s: %d blocks per head, at most %d", __func__,
+                rola::num_blocks(s.N, block), rola::kBwdMaxBlocks);
   REQUIRE_PTR(Qr);
   REQUIRE_PTR(Kr);
   REQUIRE_PTR(V);

@@ -75,20 +75,55 @@ __global__ __launch_bounds__(64) void bwd_bits_kernel(int nb, int keep, int word
   for (int w = threadIdx.x; w < words; w += 64) bits[row * words + w] = row_bits[w];
 }
 
-// Transposed lists: rev[head][J] = count, then the query blocks I that selected J, ascending.
-__global__ __launch_bounds__(256) void bwd_reverse_kernel(int nb, int words, long heads,
-                                                          const uint32_t* __restrict__ bits,
-                                                          int32_t* __restrict__ rev) {
-  const long e = (long)blockIdx.x * 256 + threadIdx.x;
-  if (e >= heads * nb) return;
-  const long head = e / nb;
-  const int J = (int)(e % nb);
-  const uint32_t* b = bits + head * nb * (long)words + (J >> 5);
-  int32_t* out = rev + e * (long)(nb + 1);
+// Walk order of the transposed lists: query blocks by increasing bit-reversed index over the smallest
+// power of two >= nb, a low-discrepancy order in which every list's entries spread evenly. Key
+// blocks whose lists are about equally long then sit on about the same query blocks after the same
+// number of steps, and bwd_order_kernel has the dK/dV workgroups that run at once take key blocks
+// of about equal list length: concurrent workgroups share Q and dO rows in L2.
+__host__ __device__ inline int rev_walk_bits(int nb) {
+  int k = 1;
+  while ((1 << k) < nb) ++k;
+  return k;
+}
+
+// Transposed lists: rev[head][J] = count, then the query blocks I that selected J in walk order.
+// One wave per (head, 32 key blocks): the bitmap column of the 32 key blocks over every query block
+// goes to LDS (nb words), then lane j < 32 collects key block 32w + j's list.
+__global__ __launch_bounds__(64) void bwd_reverse_kernel(int nb, int words, int kb,
+                                                         const uint32_t* __restrict__ bits,
+                                                         int32_t* __restrict__ rev) {
+  extern __shared__ uint32_t col[];  // [nb]: bit j of col[I] = query block I selected J = 32w + j
+  const long head = blockIdx.x / words;
+  const int w = (int)(blockIdx.x % words), lane = threadIdx.x;
+  for (int I = lane; I < nb; I += 64) col[I] = bits[(head * nb + I) * words + w];
+  __syncthreads();
+  const int J = 32 * w + lane;
+  if (lane >= 32 || J >= nb) return;
+  int32_t* out = rev + (head * nb + J) * (long)(nb + 1);
   int cnt = 0;
-  for (int I = 0; I < nb; ++I)
-    if ((b[(long)I * words] >> (J & 31)) & 1u) out[1 + cnt++] = I;
+  for (int p = 0; p < (1 << kb); ++p) {
+    const int I = (int)(__brev((unsigned)p) >> (32 - kb));
+    if (I < nb && ((col[I] >> lane) & 1u)) out[1 + cnt++] = I;
+  }
   out[0] = cnt;
+}
+
+// Order of the key blocks for the dK/dV workgroups: longer lists first (equal lengths by ascending
+// J), order[head][rank] = J. One workgroup per (head, 256 key blocks): every list length of the
+// head goes to LDS, and each thread ranks one key block against all of them.
+__global__ __launch_bounds__(256) void bwd_order_kernel(int nb, int chunks,
+                                                        const int32_t* __restrict__ rev,
+                                                        int32_t* __restrict__ order) {
+  extern __shared__ int32_t len[];  // [nb]
+  const long head = blockIdx.x / chunks;
+  const int J = (int)(blockIdx.x % chunks) * 256 + threadIdx.x;
+  for (int K = threadIdx.x; K < nb; K += 256) len[K] = rev[(head * nb + K) * (long)(nb + 1)];
+  __syncthreads();
+  if (J >= nb) return;
+  const int e = len[J];
+  int rank = 0;
+  for (int K = 0; K < nb; ++K) rank += len[K] > e || (len[K] == e && K < J);
+  order[head * nb + rank] = J;
 }
 
 // ---- dQ: one workgroup per (b, h, query block), BLK/32 waves of 32 queries -------------------------
@@ -257,8 +292,8 @@ __global__ __launch_bounds__(BLK * 4) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void sparse_dkv_kernel(
     int N, int nb, int total, const int32_t* __restrict__ rev, float scale_log2, float scale,
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
-    const bf16* __restrict__ dO, const float2* __restrict__ lseD, float* __restrict__ dK,
-    float* __restrict__ dV) {
+    const bf16* __restrict__ dO, const float2* __restrict__ lseD, const int32_t* __restrict__ order,
+    float* __restrict__ dK, float* __restrict__ dV) {
   constexpr int D = 128, NKW = BLK / 32, NW = 2 * NKW;
   constexpr int TILE = kBSub * D * 2;          // 32 rows of 256 bytes
   constexpr int STAGE = 2 * TILE + 1024;       // Q, dO, then lse/D of the 32 queries (256 B used)
@@ -269,9 +304,10 @@ void sparse_dkv_kernel(
   static_assert(DPW >= 1 && 2 * (TILE / 1024) % NW == 0 && AHEAD >= 1, "64- or 128-key blocks");
   __shared__ __attribute__((aligned(1024))) char lds[NBUF * STAGE + 2 * PBUF];
 
+  typedef const __attribute__((address_space(4))) int32_t* const_i32;
   const int L = xcd_remap(blockIdx.x, total);
-  const int J = L % nb;
   const long head = L / nb;
+  const int J = ((const_i32)order)[L];  // key blocks of one head, longer lists first
   const int tid = threadIdx.x, lane = tid % 64, hh = lane / 32;
   const int wave = wave_uniform(tid / 64);
   const int role = wave / NKW, kw = wave % NKW;
@@ -280,7 +316,6 @@ void sparse_dkv_kernel(
   const long hoff = head * (long)N * D;
   const char* Qh = reinterpret_cast<const char*>(Q + hoff);
   const char* dOh = reinterpret_cast<const char*>(dO + hoff);
-  typedef const __attribute__((address_space(4))) int32_t* const_i32;
   const const_i32 rl = (const_i32)(rev + (head * nb + J) * (long)(nb + 1));
   const int E = rl[0];
   const int T = E * SUBS;
@@ -418,15 +453,15 @@ void sparse_dkv_kernel(
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Workspace: [lse, D per query][bitmaps][transposed lists][with dq_supported: the attention
-// workspace of the dQ pass (pairs, merged lists, queue counters)].
+// Workspace: [lse, D per query][bitmaps][transposed lists][key-block order][with dq_supported: the
+// attention workspace of the dQ pass (pairs, merged lists, queue counters)].
 struct BwdWs {
-  size_t lsed, bits, rev, dq;
+  size_t lsed, bits, rev, order, dq;
 };
 BwdWs bwd_layout(const Shape& s, int block, int keep) {
   const size_t heads = (size_t)s.B * s.H, nb = num_blocks(s.N, block), words = (nb + 31) / 32;
   return {align256((heads * s.N + kLsePad) * sizeof(float2)), align256(heads * nb * words * 4),
-          align256(heads * nb * (nb + 1) * 4),
+          align256(heads * nb * (nb + 1) * 4), align256(heads * nb * 4),
           dq_supported(s, block) ? align256(sparse_workspace_bytes(s, block, keep)) : 0};
 }
 
@@ -440,18 +475,23 @@ hipError_t launch_bwd(const Shape& s, const void* Qr, const void* Kr, const void
   float2* lseD = (float2*)ws;
   uint32_t* bits = (uint32_t*)((char*)ws + lay.lsed);
   int32_t* rev = (int32_t*)((char*)ws + lay.lsed + lay.bits);
+  int32_t* order = (int32_t*)((char*)ws + lay.lsed + lay.bits + lay.rev);
   const long rd_threads = (rows + kLsePad) * 16;
   hipLaunchKernelGGL(bwd_rowdot_kernel, dim3((unsigned)((rd_threads + 255) / 256)), dim3(256), 0,
                      st, rows, (const bf16*)Os, (const bf16*)dOs, lse, lseD);
   hipLaunchKernelGGL(bwd_bits_kernel, dim3((unsigned)(heads * nb)), dim3(64), words * sizeof(uint32_t),
                      st, nb, keep, words, idx, bits);
-  hipLaunchKernelGGL(bwd_reverse_kernel, dim3((unsigned)((heads * nb + 255) / 256)), dim3(256), 0,
-                     st, nb, words, heads, (const uint32_t*)bits, rev);
+  hipLaunchKernelGGL(bwd_reverse_kernel, dim3((unsigned)(heads * words)), dim3(64),
+                     nb * sizeof(uint32_t), st, nb, words, rev_walk_bits(nb), (const uint32_t*)bits,
+                     rev);
+  const int ochunks = (nb + 255) / 256;
+  hipLaunchKernelGGL(bwd_order_kernel, dim3((unsigned)(heads * ochunks)), dim3(256),
+                     nb * sizeof(int32_t), st, nb, ochunks, (const int32_t*)rev, order);
   const int total = (int)(heads * nb);
   const float sl = scale * 1.4426950408889634f;
   if (dq_supported(s, BLK)) {  // dQ on the paired, queued attention kernel
     const hipError_t e2 = launch_sparse_dq(s, Qr, Kr, V, keep, idx, scale, dOs, lseD, dQ,
-                                           (char*)ws + lay.lsed + lay.bits + lay.rev, st);
+                                           (char*)ws + lay.lsed + lay.bits + lay.rev + lay.order, st);
     if (e2 != hipSuccess) return e2;
   } else {
     hipLaunchKernelGGL((sparse_dq_kernel<BLK, 3>), dim3(total), dim3(BLK * 2), 0, st, s.N, nb, total,
@@ -460,16 +500,19 @@ hipError_t launch_bwd(const Shape& s, const void* Qr, const void* Kr, const void
   }
   hipLaunchKernelGGL((sparse_dkv_kernel<BLK, kDkvNbuf>), dim3(total), dim3(BLK * 4), 0, st, s.N, nb, total,
                      (const int32_t*)rev, sl, scale, (const bf16*)Qr, (const bf16*)Kr,
-                     (const bf16*)V, (const bf16*)dOs, (const float2*)lseD, dK, dV);
+                     (const bf16*)V, (const bf16*)dOs, (const float2*)lseD, (const int32_t*)order,
+                     dK, dV);
   return hipGetLastError();
 }
 
 }  // namespace
 
 size_t sparse_backward_workspace_bytes(const Shape& s, int block, int keep) {
-  if (!s.bf16 || s.d != 128 || (block != 64 && block != 128)) return 0;
+  if (!s.bf16 || s.d != 128 || (block != 64 && block != 128) ||
+      num_blocks(s.N, block) > kBwdMaxBlocks)
+    return 0;
   const BwdWs w = bwd_layout(s, block, keep);
-  return w.lsed + w.bits + w.rev + w.dq;
+  return w.lsed + w.bits + w.rev + w.order + w.dq;
 }
 
 hipError_t launch_sparse_backward(const Shape& s, const void* Qr, const void* Kr, const void* V,

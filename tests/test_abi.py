@@ -117,6 +117,7 @@ def _call(name, *args):
 def test_invalid_arguments_are_rejected_before_launch():
     g = (21, 45, 80)
     ok = R.problem(1, 2, 75600, 128, g, "bf16")
+    big = R.problem(1, 1, 16385 * 64, 128, (1, 1, 16385 * 64), "bf16")  # 16385 blocks of 64
     P = ctypes.byref
     cases = [
         (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn", P(ok), None, FAKE, FAKE, 64, 0.9, FAKE, 0.1, FAKE, None, 0, None),
@@ -179,7 +180,12 @@ def test_invalid_arguments_are_rejected_before_launch():
         (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn_combine", P(ok), FAKE, FAKE, FAKE, 64, 0.9,
          FAKE, 0.1, FAKE, FAKE, 31, FAKE, FAKE, 64, FAKE, 1e-6, FAKE, 1e-6, None, FAKE, FAKE, 1 << 40,
          None),
+        # sparse backward: more blocks per head than the transposed lists are built for
+        (R.ROLA_ERR_UNSUPPORTED, "rola_sparse_attn_backward", P(big), FAKE, FAKE, FAKE, 64, 0.9, FAKE,
+         0.1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 40, None),
     ]
+    assert R.LIB.rola_sparse_backward_workspace_bytes(P(big), 64, 0.9) == 0
+    assert R.LIB.rola_sparse_backward_workspace_bytes(P(R.problem(1, 1, 8192 * 64, 128, (1, 1, 8192 * 64), "bf16")), 64, 0.9) > 0
     # outputs that overlap an input
     cases += [
         (R.ROLA_ERR_INVALID_ARGUMENT, "rola_sparse_attn", P(ok), FAKE, SAME, FAKE, 64, 0.9, FAKE, 0.1,
