@@ -77,6 +77,46 @@ def test_sparse_backward(grid, block, s, B):
             assert colsum <= 1e-2 * np.abs(_f64(dk[b, h])).sum(0).max() + 1e-6
 
 
+@pytest.mark.parametrize("block", [64, 128])
+def test_sparse_backward_uneven_transposed_lists(block):
+    """4096 tokens at 90 % sparsity: the transposed lists (query blocks per key block) differ in
+    length, some key blocks are selected by no query block, and the dK/dV workgroups take the key
+    blocks longest list first while walking each list in its bit-reversed order. Every head
+    against the gradient oracle; unselected key blocks must get exactly zero gradients."""
+    w = synth.WAN_1_3B_480P.replace(grid=(8, 16, 32), H=2, B=1, block=block, sparsity=0.9)
+    inp = synth.make_inputs(w, 21)
+    d = {k: v.cuda() for k, v in inp.items()}
+    g = w.grid
+    prob = R.problem(w.B, w.H, w.N, w.d_h, g, w.dtype)
+    cos, sin = R.rola_rope_tables(prob, w.split)
+    qr = R.rola_rope_apply(d["Qn"], cos, sin, g)
+    kr = R.rola_rope_apply(d["Kn"], cos, sin, g)
+    idx = R.rola_block_select(qr, kr, g, block, w.sparsity)
+    os_, lse = R.rola_sparse_attn_lse(qr, kr, d["V"], g, block, w.sparsity, idx)
+    gen = torch.Generator().manual_seed(5)
+    dos = torch.randn(qr.shape, generator=gen).to(torch.bfloat16).cuda()
+    dq, dk, dv = R.rola_sparse_attn_backward(qr, kr, d["V"], g, block, w.sparsity, idx, os_, lse, dos)
+    torch.cuda.synchronize()
+    scale = 1.0 / math.sqrt(w.d_h)
+    nb = -(-w.N // block)
+    for h in range(w.H):
+        ix = idx[0, h].cpu().numpy()
+        counts = np.bincount(ix.ravel(), minlength=nb)
+        print(f"[parity] transposed list lengths block {block} h{h}: min {counts.min()} max "
+              f"{counts.max()} unselected {int((counts == 0).sum())} of {nb}", flush=True)
+        assert counts.max() > counts.min()  # uneven lists, as the case intends
+        want = G.sparse_attention_grads(_f64(qr[0, h]), _f64(kr[0, h]), _f64(d["V"][0, h]), ix, block,
+                                        scale, _f64(dos[0, h]))
+        errs = {n: _rel(_f64(t[0, h]), want[n]) for n, t in (("dqr", dq), ("dkr", dk), ("dv", dv))}
+        print(f"[parity] sparse backward uneven lists block {block} h{h}: " +
+              ", ".join(f"{n} rel {e:.2e}" for n, e in errs.items()), flush=True)
+        for n, e in errs.items():
+            assert e <= 1e-2, (n, e)
+        for J in np.flatnonzero(counts == 0):  # no query selected these keys
+            rows = slice(J * block, min(w.N, (J + 1) * block))
+            assert torch.count_nonzero(dk[0, h, rows]) == 0 and torch.count_nonzero(dv[0, h, rows]) == 0
+
+
 def test_sparse_backward_many_groups():
     """200 heads of 390 tokens: 800 (head, pair) groups, more than the chip holds at once, so the dQ
     pass's resident workgroups each take several groups from the work queues. Sampled heads against
