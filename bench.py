@@ -143,6 +143,24 @@ def cpu_baseline(w, heads: dict, tmpdir: str) -> dict:
             "layer_s_extrapolated_note": "mean time per (b, h) on one core x B*H: extrapolated"}
 
 
+def gemm_reference(dev, n: int = 16384, reps: int = 8) -> dict:
+    """The dense bf16 rate this machine sustains for the plainest contraction: torch.matmul (the
+    vendor GEMM library) on random n x n bf16 operands, HIP events like the layer. Context for the
+    attention kernel's fraction of the published peak, not a bound on it."""
+    g = torch.Generator(device=dev).manual_seed(0)
+    a = torch.randn(n, n, dtype=torch.bfloat16, device=dev, generator=g)
+    b = torch.randn(n, n, dtype=torch.bfloat16, device=dev, generator=g)
+    c = torch.empty(n, n, dtype=torch.bfloat16, device=dev)
+    for _ in range(2):
+        torch.matmul(a, b, out=c)
+    ms = time_call(lambda: torch.matmul(a, b, out=c), reps)[0]
+    del a, b, c
+    torch.cuda.empty_cache()
+    tf = 2.0 * n ** 3 / (ms * 1e-3) / 1e12
+    return {"what": f"torch.matmul, random bf16 {n}x{n} operands (vendor GEMM library), same box",
+            "achieved": round(tf, 1), "unit": "TFLOP/s", "frac_of_peak": round(tf / PEAK_BF16_TFLOPS, 4)}
+
+
 def time_call(fn, reps: int, cold=None):
     """Median, p10, p90 (ms) of fn() over reps runs, HIP events on the current stream; cold() runs
     between the timed intervals (e.g. a scratch write that evicts the caches)."""
@@ -613,6 +631,10 @@ def main():
         "flops": {"sparse_performed": f_sparse, "lowrank_paper": f_lowrank,
                   "sparse_paper_formula": 4.0 * w.B * w.H * w.N ** 2 * (1 - w.sparsity) * w.d_h},
     }
+    if not args.quick:
+        ref = gemm_reference(dev)
+        ref["attention_vs_gemm"] = round(achieved / ref["achieved"], 4)
+        res["gemm_reference"] = ref
     if not args.no_cpu_baseline:
         import tempfile
         print("[bench] timing the CPU oracle on 4 heads", file=sys.stderr, flush=True)
