@@ -285,7 +285,9 @@ __global__ __launch_bounds__(BLK * 2, 2) void sparse_dq_kernel(
 // half the register file, and the compiler then moves accumulators between the two register files
 // every step), so two waves run per SIMD. A step takes 32 queries. P goes over as fp16: it lies
 // in [0, 1], where fp16's relative error (2^-11; absolute 2^-25 below 2^-14) is an eighth of the
-// bf16 rounding dS takes next.
+// bf16 rounding dS takes next. Workgroups take a head's key blocks longest list first
+// (bwd_order_kernel) and walk each list in the bit-reversed order, so that workgroups running at
+// the same time sit on about the same query blocks and share their Q and dO rows in L2.
 constexpr int kDkvNbuf = 4;  // LDS stages of sparse_dkv_kernel: 32 Q rows, 32 dO rows, lse/D (17 KB)
 template <int BLK, int NBUF>
 __global__ __launch_bounds__(BLK * 4) __attribute__((amdgpu_waves_per_eu(2, 2)))
