@@ -48,16 +48,29 @@ __global__ __launch_bounds__(256) void pool_kernel(int N, int d, int block, cons
   const int n0 = I * block, n1 = min(N, n0 + block);
   float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
   float sq = 0.f;  // largest squared row norm among this thread's rows (its G-lane share)
-  for (int n = n0 + lane; n < n1; n += L) {
-    float v[8];
-    load8(xh + (long)n * d + g * 8, v);
-    float part = 0.f;
+  // Rows in batches of kPoolRows per thread, every load of a batch issued before the first is
+  // used (one row at a time, each load waited for before the next is issued, made every
+  // workgroup four serial memory round trips). Rows past n1 re-read row n1 - 1 and are left out
+  // by selects, so the batch has no branch between its loads and the sums are the row-by-row ones.
+  constexpr int kPoolRows = 4;
+  for (int nb0 = n0 + lane; nb0 < n1; nb0 += kPoolRows * L) {
+    float v[kPoolRows][8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      acc[i] += v[i];
-      part = fmaf(v[i], v[i], part);
+    for (int r = 0; r < kPoolRows; ++r) load8(xh + (long)min(nb0 + r * L, n1 - 1) * d + g * 8, v[r]);
+#pragma unroll
+    for (int r = 0; r < kPoolRows; ++r) {
+      const bool ok = nb0 + r * L < n1;  // the same for the G lanes of a row
+      float part = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        acc[i] = ok ? acc[i] + v[r][i] : acc[i];
+        part = fmaf(v[r][i], v[r][i], part);
+      }
+      if (nmax) {
+        const float rs = row_group_sum(part, G);
+        sq = ok ? fmaxf(sq, rs) : sq;
+      }
     }
-    if (nmax) sq = fmaxf(sq, row_group_sum(part, G));
   }
   __shared__ float red[256 * 8];
 #pragma unroll
@@ -107,10 +120,8 @@ __global__ __launch_bounds__(256) void rope_pool_kernel(int N, int block, int he
     float sq = 0.f;  // largest squared norm of a rotated, rounded row (this thread's share of it)
     float v[TPT][8];
 #pragma unroll
-    for (int k = 0; k < TPT; ++k) {  // loads first: one memory latency per head
-      const int n = n0 + lane + L * k;
-      if (n < n1) load8(xh + (long)n * D + g * 8, v[k]);
-    }
+    for (int k = 0; k < TPT; ++k)  // loads first, none under a branch: one memory latency per head
+      load8(xh + (long)min(n0 + lane + L * k, n1 - 1) * D + g * 8, v[k]);  // rows past n1 unused
 #pragma unroll
     for (int k = 0; k < TPT; ++k) {
       const int n = n0 + lane + L * k;
