@@ -424,8 +424,16 @@ __global__ __launch_bounds__(256) void summary_reduce_kernel(int rd, int r, int 
   const int per = rd + r;
   if (e >= per) return;
   const float* P = part + head * n_chunks * (long)per + e;
+  // chunk order kept; the loads of a batch are all issued before the first add
+  constexpr int kBatch = 8;
   float s = 0.f;
-  for (int c = 0; c < n_chunks; ++c) s += P[(long)c * per];
+  for (int c0 = 0; c0 < n_chunks; c0 += kBatch) {
+    float v[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) v[u] = P[(long)min(c0 + u, n_chunks - 1) * per];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) s = c0 + u < n_chunks ? s + v[u] : s;
+  }
   if (e < rd) C[head * rd + e] = s;
   else if (z) z[head * r + (e - rd)] = s;
 }
