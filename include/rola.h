@@ -139,9 +139,10 @@ rola_status rola_rope_pool(const rola_problem* p, const void* X, const float* co
 
 /* Top-k key blocks for every query block. For each (b, h): q_bar_I, k_bar_J = means of Q^r, K^r over
  * the valid tokens of block I, J (fp32); the block score of the definition is
- * q_bar_I . k_bar_J / sqrt(d_h); the kernels rank the fp32 dot products q_bar_I . k_bar_J themselves,
+ * q_bar_I . k_bar_J / sqrt(d_h); the kernels rank the dot products q_bar_I . k_bar_J themselves,
  * since the positive factor 1/sqrt(d_h) cannot change which blocks are largest (and leaving it out
- * adds no rounding). The keep = rola_keep_blocks(n_blocks, sparsity) largest scores are kept, equal
+ * adds no rounding). The dot products are fp32-accurate: each mean is split exactly into three
+ * bf16 terms and the six significant cross products are summed in fp32 on the matrix cores. The keep = rola_keep_blocks(n_blocks, sparsity) largest scores are kept, equal
  * scores going to the lower J, and written ascending to blk_idx [B, H, n_blocks, keep]. ws: >=
  * rola_select_workspace_bytes(p, block) bytes of device scratch. */
 rola_status rola_block_select(const rola_problem* p, const void* Qr, const void* Kr, int32_t block,

@@ -5,8 +5,9 @@
 //   pool_kernel   HBM-bound: reads Q^r and K^r once (coalesced 16-byte loads), writes means (fp32);
 //                 its rotating form reads Q^n or K^n instead, rotates each row (writing K^r) and
 //                 pools the rotated values: the backbone rotation and the pooling in one pass.
-//   score_kernel  per (b, h): S = q_bar k_bar^T, a small fp32 GEMM tiled 64 x 64 through LDS. The
-//                 positive factor 1/sqrt(d_h) is left out: it cannot change the ranking.
+//   score_kernel  per (b, h): S = q_bar k_bar^T, a small GEMM tiled 64 x 64 through LDS, fp32-accurate
+//                 from bf16 MFMA with each operand split into three bf16 terms. The positive
+//                 factor 1/sqrt(d_h) is left out: it cannot change the ranking.
 //   topk_kernel   one wave per score row: 4-pass 8-bit radix select on order-preserving uint32 keys,
 //                 then an ascending ballot/popcount compaction. Integer work, bit-reproducible.
 #include "common.h"
@@ -164,48 +165,87 @@ __global__ __launch_bounds__(256) void rope_pool_kernel(int N, int block, int he
 // S[I][J] = sum_c qbar[I][c] * kbar[J][c] for one (b, h) per blockIdx.z; 64 x 64 tile per workgroup
 // of 4 waves (32 x 32 each), on v_mfma_f32_16x16x4_f32: fp32 operands and fp32 accumulation, so the
 // scores keep fp32 accuracy (the 1e-4 tie gap of the selection rules out bf16 operands).
-__global__ __launch_bounds__(256) void score_kernel(int nb, int d, const float* __restrict__ qbar,
+// x = hi + mid + lo exactly: each term is the remainder of the ones before, rounded to bf16 (eight
+// significant bits each, and each remainder is exact in fp32). Dropping the three products of two
+// lower terms (mid lo, lo mid, lo lo: about 2^-24 of hi hi) leaves six bf16 MFMA products whose fp32
+// sum is as accurate as an fp32 dot product, at 16x the fp32 MFMA rate per product.
+__device__ __forceinline__ void split3(const float (&x)[8], bf16x8& hi, bf16x8& mid, bf16x8& lo) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    hi[i] = (bf16)x[i];
+    const float r1 = x[i] - (float)hi[i];
+    mid[i] = (bf16)r1;
+    lo[i] = (bf16)(r1 - (float)mid[i]);
+  }
+}
+
+// 64 x 64 tile of S per workgroup, four waves of 32 x 32; each chunk of 32 channels is split into
+// the three bf16 terms once, in LDS, and every 16 x 16 product takes the six significant products.
+// All global loads are issued up front (rows past nb re-read row nb-1; their scores are not stored).
+template <int D>
+__global__ __launch_bounds__(256) void score_kernel(int nb, const float* __restrict__ qbar,
                                                     const float* __restrict__ kbar,
                                                     float* __restrict__ S) {
-  constexpr int TS = 64, KC = 32, PAD = 4;
-  __shared__ float As[TS][KC + PAD];
-  __shared__ float Bs[TS][KC + PAD];
+  constexpr int TS = 64, KC = 32, NCH = D / KC;
+  constexpr int RS = KC + 8;  // row stride in bf16: 80 bytes, so 16 rows' 16-byte reads spread
+  __shared__ __attribute__((aligned(16))) bf16 As[3][TS][RS];
+  __shared__ __attribute__((aligned(16))) bf16 Bs[3][TS][RS];
   const long head = blockIdx.z;
-  const float* q = qbar + head * (long)nb * d;
-  const float* k = kbar + head * (long)nb * d;
+  const float* q = qbar + head * (long)nb * D;
+  const float* k = kbar + head * (long)nb * D;
   const int I0 = blockIdx.y * TS, J0 = blockIdx.x * TS;
   const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64, lr = lane % 16, g = lane / 16;
   const int wi = (wave >> 1) * 32, wj = (wave & 1) * 32;  // this wave's 32 x 32 sub-tile
   const int lrow = tid / 4, lcol = (tid % 4) * 8;
+  const float* qrow = q + (long)min(I0 + lrow, nb - 1) * D + lcol;
+  const float* krow = k + (long)min(J0 + lrow, nb - 1) * D + lcol;
+  float a[NCH][8], b[NCH][8];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    load8(qrow + c * KC, a[c]);
+    load8(krow + c * KC, b[c]);
+  }
   f32x4 acc[2][2];
 #pragma unroll
   for (int a2 = 0; a2 < 2; ++a2)
 #pragma unroll
     for (int b2 = 0; b2 < 2; ++b2) acc[a2][b2] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int c0 = 0; c0 < d; c0 += KC) {
-    float a[8], b[8];
-    if (I0 + lrow < nb) load8(q + (long)(I0 + lrow) * d + c0 + lcol, a);
-    else for (int i = 0; i < 8; ++i) a[i] = 0.f;
-    if (J0 + lrow < nb) load8(k + (long)(J0 + lrow) * d + c0 + lcol, b);
-    else for (int i = 0; i < 8; ++i) b[i] = 0.f;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    if (c) __syncthreads();  // the previous chunk's reads are done
+    {
+      bf16x8 h, m, l;
+      split3(a[c], h, m, l);
+      *reinterpret_cast<bf16x8*>(&As[0][lrow][lcol]) = h;
+      *reinterpret_cast<bf16x8*>(&As[1][lrow][lcol]) = m;
+      *reinterpret_cast<bf16x8*>(&As[2][lrow][lcol]) = l;
+      split3(b[c], h, m, l);
+      *reinterpret_cast<bf16x8*>(&Bs[0][lrow][lcol]) = h;
+      *reinterpret_cast<bf16x8*>(&Bs[1][lrow][lcol]) = m;
+      *reinterpret_cast<bf16x8*>(&Bs[2][lrow][lcol]) = l;
+    }
     __syncthreads();
+    // lane holds A[row lr][k 8g..8g+7] and B[k 8g..8g+7][col lr] of each 16 x 16 tile
+    bf16x8 av[2][3], bv[2][3];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) { As[lrow][lcol + i] = a[i]; Bs[lrow][lcol + i] = b[i]; }
-    __syncthreads();
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
-    for (int kk = 0; kk < KC; kk += 4) {
-      float av[2], bv[2];  // lane holds A[row lr][k g] and B[k g][col lr] of each 16 x 16 tile
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        av[t] = As[wi + 16 * t + lr][kk + g];
-        bv[t] = Bs[wj + 16 * t + lr][kk + g];
+      for (int p = 0; p < 3; ++p) {
+        av[t][p] = *reinterpret_cast<const bf16x8*>(&As[p][wi + 16 * t + lr][8 * g]);
+        bv[t][p] = *reinterpret_cast<const bf16x8*>(&Bs[p][wj + 16 * t + lr][8 * g]);
       }
 #pragma unroll
-      for (int a2 = 0; a2 < 2; ++a2)
+    for (int a2 = 0; a2 < 2; ++a2)
 #pragma unroll
-        for (int b2 = 0; b2 < 2; ++b2)
-          acc[a2][b2] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[a2], bv[b2], acc[a2][b2], 0, 0, 0);
-    }
+      for (int b2 = 0; b2 < 2; ++b2) {
+        f32x4 x = acc[a2][b2];  // smallest terms first
+        x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[a2][2], bv[b2][0], x, 0, 0, 0);
+        x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[a2][1], bv[b2][1], x, 0, 0, 0);
+        x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[a2][0], bv[b2][2], x, 0, 0, 0);
+        x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[a2][1], bv[b2][0], x, 0, 0, 0);
+        x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[a2][0], bv[b2][1], x, 0, 0, 0);
+        acc[a2][b2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[a2][0], bv[b2][0], x, 0, 0, 0);
+      }
   }
   float* Sh = S + head * (long)nb * nb;
 #pragma unroll
@@ -361,8 +401,12 @@ hipError_t launch_select_pooled(const Shape& s, const float* qbar, const float* 
   const size_t heads = (size_t)s.B * s.H;
   float* S = (float*)ws;
   const int tiles = (nb + 63) / 64;
-  hipLaunchKernelGGL(score_kernel, dim3(tiles, tiles, (unsigned)heads), dim3(256), 0, st, nb, s.d,
-                     qbar, kbar, S);
+  if (s.d == 128)
+    hipLaunchKernelGGL(score_kernel<128>, dim3(tiles, tiles, (unsigned)heads), dim3(256), 0, st, nb,
+                       qbar, kbar, S);
+  else
+    hipLaunchKernelGGL(score_kernel<64>, dim3(tiles, tiles, (unsigned)heads), dim3(256), 0, st, nb,
+                       qbar, kbar, S);
   hipLaunchKernelGGL(topk_kernel, dim3(nb, s.H, s.B), dim3(64), (size_t)nb * sizeof(uint32_t), st, nb,
                      keep, S, idx);
   return hipGetLastError();
