@@ -8,8 +8,11 @@
 //   score_kernel  per (b, h): S = q_bar k_bar^T, a small GEMM tiled 64 x 64 through LDS, fp32-accurate
 //                 from bf16 MFMA with each operand split into three bf16 terms. The positive
 //                 factor 1/sqrt(d_h) is left out: it cannot change the ranking.
-//   topk_kernel   one wave per score row: 4-pass 8-bit radix select on order-preserving uint32 keys,
+//   topk_reg_kernel  one wave per score row, the row's order-preserving uint32 keys in registers:
+//                 the k-th largest key found bit by bit from the top with ballot/popcount counts,
 //                 then an ascending ballot/popcount compaction. Integer work, bit-reproducible.
+//                 Rows of more than 2560 blocks take topk_kernel (4-pass 8-bit radix select with
+//                 the keys and histograms in LDS).
 #include "common.h"
 #include "launch.h"
 
@@ -264,9 +267,9 @@ __device__ __forceinline__ uint32_t order_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);  // larger float -> larger key
 }
 
-// One 64-lane workgroup per score row; dynamic LDS holds the row's nb keys. Every loop over the
-// row takes kBatch elements per lane at a time, loads first: one memory (or LDS) latency per batch
-// instead of one per element.
+// Rows too long for the register kernel: one 64-lane workgroup per score row; dynamic LDS holds the
+// row's nb keys. Every loop over the row takes kBatch elements per lane at a time, loads first: one
+// memory (or LDS) latency per batch instead of one per element.
 constexpr int kBatch = 8;
 __global__ __launch_bounds__(64) void topk_kernel(int nb, int keep, const float* __restrict__ S,
                                                   int32_t* __restrict__ idx) {
@@ -365,6 +368,144 @@ __global__ __launch_bounds__(64) void topk_kernel(int nb, int keep, const float*
   }
 }
 
+// Top-k of one score row per wave with the row in registers: lane l holds keys 64u + l, u < U
+// (padding key 0 lies below every finite score's key and is never counted). The k-th largest key T
+// is built from the top bit down: T | bit is kept when at least `keep` keys are >= it, a wave's
+// count being the popcounts of one ballot per slot. Once the upper 16 bits are fixed, only keys
+// whose upper half equals T's can decide the lower half; when at most 64 of them exist they are
+// gathered one per lane through LDS and the lower 16 bits are searched over that one slot (keys in
+// higher buckets are counted once). Otherwise (heavy exact ties) the search goes on over every slot.
+// Kept: every key > T, and of the keys == T the lowest indices (when exactly `keep` keys are >= T,
+// that is every key >= T), written ascending. Four rows per workgroup, no workgroup barrier.
+constexpr int kTopkMaxSlots = 40;
+template <int U>
+__global__ __launch_bounds__(256) void topk_reg_kernel(int nb, int keep, long rows,
+                                                       const float* __restrict__ S,
+                                                       int32_t* __restrict__ idx) {
+  __shared__ uint32_t cand[4][64];
+  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const long row = (long)blockIdx.x * 4 + wave;
+  if (row >= rows) return;
+  const float* s = S + row * nb;
+  int32_t* out = idx + row * keep;
+  uint32_t key[U];
+  {
+    float v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = s[min(64 * u + lane, nb - 1)];
+#pragma unroll
+    for (int u = 0; u < U; ++u) key[u] = 64 * u + lane < nb ? order_key(v[u]) : 0u;
+  }
+  const uint32_t ukeep = (uint32_t)keep;
+  uint32_t T = 0, nT = (uint32_t)nb;  // nT = number of (valid) keys >= T
+  for (int b = 31; b >= 16; --b) {
+    const uint32_t c = T | (1u << b);
+    uint32_t n = 0;
+#pragma unroll
+    for (int u = 0; u < U; ++u) n += (uint32_t)__popcll(__ballot(key[u] >= c));
+    if (n >= ukeep) { T = c; nT = n; }
+  }
+  const uint32_t hiT = T >> 16;
+  uint32_t above = 0, ncand = 0;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    above += (uint32_t)__popcll(__ballot((key[u] >> 16) > hiT));
+    ncand += (uint32_t)__popcll(__ballot((key[u] >> 16) == hiT));
+  }
+  if (ncand <= 64) {
+    uint32_t base = 0;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const bool c = (key[u] >> 16) == hiT;
+      const uint64_t m = __ballot(c);
+      const uint32_t below = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                       __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+      if (c) cand[wave][base + below] = key[u];
+      base += (uint32_t)__popcll(m);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const uint32_t ck = (uint32_t)lane < ncand ? cand[wave][lane] : 0u;
+    for (int b = 15; b >= 0; --b) {
+      const uint32_t c = T | (1u << b);
+      const uint32_t n = above + (uint32_t)__popcll(__ballot(ck >= c));
+      if (n >= ukeep) { T = c; nT = n; }
+    }
+  } else {
+    for (int b = 15; b >= 0; --b) {
+      const uint32_t c = T | (1u << b);
+      uint32_t n = 0;
+#pragma unroll
+      for (int u = 0; u < U; ++u) n += (uint32_t)__popcll(__ballot(key[u] >= c));
+      if (n >= ukeep) { T = c; nT = n; }
+    }
+  }
+  if (nT == ukeep && T != 0) {  // no surplus ties at the boundary: keep every key >= T
+    uint32_t written = 0;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const bool sel = key[u] >= T;
+      const uint64_t m = __ballot(sel);
+      const uint32_t pos = written + __builtin_amdgcn_mbcnt_hi(
+                                         (uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+      if (sel && pos < ukeep) out[pos] = 64 * u + lane;
+      written += (uint32_t)__popcll(m);
+    }
+    return;
+  }
+  uint32_t gt_total = 0;
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+    gt_total += (uint32_t)__popcll(__ballot(64 * u + lane < nb && key[u] > T));
+  const uint32_t remaining = ukeep - gt_total;
+  uint32_t written = 0, eq_seen = 0;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const bool valid = 64 * u + lane < nb;
+    const bool gt = valid && key[u] > T, eq = valid && key[u] == T;
+    const uint64_t eqm = __ballot(eq);
+    const uint32_t eq_rank = eq_seen + __builtin_amdgcn_mbcnt_hi(
+                                           (uint32_t)(eqm >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)eqm, 0u));
+    const bool sel = gt || (eq && eq_rank < remaining);
+    const uint64_t selm = __ballot(sel);
+    const uint32_t pos = written + __builtin_amdgcn_mbcnt_hi(
+                                       (uint32_t)(selm >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)selm, 0u));
+    if (sel && pos < ukeep) out[pos] = 64 * u + lane;
+    written += (uint32_t)__popcll(selm);
+    eq_seen += (uint32_t)__popcll(eqm);
+  }
+}
+
+template <int U>
+void launch_topk_reg(int nb, int keep, long rows, const float* S, int32_t* idx, hipStream_t st) {
+  hipLaunchKernelGGL(topk_reg_kernel<U>, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, st, nb,
+                     keep, rows, S, idx);
+}
+
+// Row top-k over the score matrix: the register kernel with the fewest slots that hold a row.
+void launch_topk(int nb, int keep, int B, int H, const float* S, int32_t* idx, hipStream_t st) {
+  const long rows = (long)B * H * nb;
+  const int need = (nb + 63) / 64;
+  if (keep >= nb || need > kTopkMaxSlots) {
+    hipLaunchKernelGGL(topk_kernel, dim3(nb, H, B), dim3(64), (size_t)nb * sizeof(uint32_t), st,
+                       nb, keep, S, idx);
+    return;
+  }
+  if (need <= 1) return launch_topk_reg<1>(nb, keep, rows, S, idx, st);
+  if (need <= 2) return launch_topk_reg<2>(nb, keep, rows, S, idx, st);
+  if (need <= 4) return launch_topk_reg<4>(nb, keep, rows, S, idx, st);
+  if (need <= 6) return launch_topk_reg<6>(nb, keep, rows, S, idx, st);
+  if (need <= 8) return launch_topk_reg<8>(nb, keep, rows, S, idx, st);
+  if (need <= 10) return launch_topk_reg<10>(nb, keep, rows, S, idx, st);
+  if (need <= 12) return launch_topk_reg<12>(nb, keep, rows, S, idx, st);
+  if (need <= 16) return launch_topk_reg<16>(nb, keep, rows, S, idx, st);
+  if (need <= 19) return launch_topk_reg<19>(nb, keep, rows, S, idx, st);
+  if (need <= 24) return launch_topk_reg<24>(nb, keep, rows, S, idx, st);
+  if (need <= 32) return launch_topk_reg<32>(nb, keep, rows, S, idx, st);
+  return launch_topk_reg<kTopkMaxSlots>(nb, keep, rows, S, idx, st);
+}
+
 hipError_t launch_pool(const Shape& s, const void* X, int block, float* means, hipStream_t st,
                        float* nmax = nullptr) {
   const dim3 grid(num_blocks(s.N, block), s.H, s.B);
@@ -407,8 +548,7 @@ hipError_t launch_select_pooled(const Shape& s, const float* qbar, const float* 
   else
     hipLaunchKernelGGL(score_kernel<64>, dim3(tiles, tiles, (unsigned)heads), dim3(256), 0, st, nb,
                        qbar, kbar, S);
-  hipLaunchKernelGGL(topk_kernel, dim3(nb, s.H, s.B), dim3(64), (size_t)nb * sizeof(uint32_t), st, nb,
-                     keep, S, idx);
+  launch_topk(nb, keep, s.B, s.H, S, idx, st);
   return hipGetLastError();
 }
 

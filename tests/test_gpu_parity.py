@@ -377,6 +377,45 @@ def test_block_select_rows(grid):
     _report("block select", n_b=nb, keep=keep, tie_rows=ties, differing=len(differ))
 
 
+@pytest.mark.parametrize("grid", [(21, 45, 80), (21, 45, 160), (21, 45, 180)],
+                         ids=["1182-blocks", "2363-blocks", "2658-blocks"])
+def test_topk_crafted_rows(grid):
+    """Top-k on score rows built to reach every branch of the selection: means that are one-hot
+    queries against key means holding a chosen value per block, so that row I's scores are exactly
+    the values of pattern I mod 5 (products with 1.0, exact in fp32 and fp64). Patterns: distinct
+    random values; values drawn from a few hundred levels (exact ties across the k-th score);
+    300 distinct values within one part in 2^20 of each other across the k-th (more than 64
+    candidates in the k-th key's upper-half bucket); 300 exactly equal values there; negative
+    values only. Rows of 1182 and 2363 blocks take the register kernel, 2658 the LDS kernel.
+    Every row against the oracle's top-k (ties to the lower block), bitwise."""
+    w = synth.WAN_1_3B_480P.replace(grid=grid, H=1, B=1, sparsity=0.9)
+    nb = O.num_blocks(w.N, 64)
+    keep = O.keep_blocks(nb, w.sparsity)
+    rng = np.random.default_rng(17)
+    pats = np.zeros((5, nb))
+    pats[0] = rng.standard_normal(nb)
+    pats[1] = rng.integers(0, 300, nb) / 7.0
+    mid = rng.permutation(nb)[:300]
+    pats[2] = rng.standard_normal(nb) - 10.0
+    pats[2][mid] = 1.0 + np.arange(300) * 2.0 ** -23
+    pats[3] = rng.standard_normal(nb) - 10.0
+    pats[3][mid] = 0.75
+    pats[4] = -np.abs(rng.standard_normal(nb)) - 1.0
+    pats = pats.astype(np.float32)
+    qbar = np.zeros((nb, 128), np.float32)
+    qbar[np.arange(nb), np.arange(nb) % 5] = 1.0
+    kbar = np.zeros((nb, 128), np.float32)
+    kbar[:, :5] = pats.T
+    like = torch.zeros((1, 1, w.N, 128), dtype=torch.bfloat16, device="cuda")
+    idx = R.rola_block_select_pooled(torch.from_numpy(qbar).view(1, 1, nb, 128).cuda(),
+                                     torch.from_numpy(kbar).view(1, 1, nb, 128).cuda(), like,
+                                     w.grid, 64, w.sparsity).cpu().numpy()[0, 0]
+    scores = qbar.astype(np.float64) @ kbar.astype(np.float64).T
+    want = O.select_blocks(scores, keep)
+    _report("crafted top-k", n_b=nb, keep=keep)
+    assert np.array_equal(idx, want)
+
+
 def test_exact_ties_go_to_lower_block():
     """Identical key blocks tie exactly: every row must keep the lowest block indices."""
     w = synth.WAN_1_3B_480P.replace(grid=(2, 8, 16), H=2)
