@@ -5,7 +5,7 @@
 //   pool_kernel   HBM-bound: reads Q^r and K^r once (coalesced 16-byte loads), writes means (fp32);
 //                 its rotating form reads Q^n or K^n instead, rotates each row (writing K^r) and
 //                 pools the rotated values: the backbone rotation and the pooling in one pass.
-//   score_kernel  per (b, h): S = q_bar k_bar^T, a small GEMM tiled 64 x 64 through LDS, fp32-accurate
+//   score_kernel  per (b, h): S = q_bar k_bar^T, a small GEMM tiled 128 x 128 through LDS, fp32-accurate
 //                 from bf16 MFMA with each operand split into three bf16 terms. The positive
 //                 factor 1/sqrt(d_h) is left out: it cannot change the ranking.
 //   topk_reg_kernel  one wave per score row, the row's order-preserving uint32 keys in registers:
@@ -165,9 +165,8 @@ __global__ __launch_bounds__(256) void rope_pool_kernel(int N, int block, int he
   }
 }
 
-// S[I][J] = sum_c qbar[I][c] * kbar[J][c] for one (b, h) per blockIdx.z; 64 x 64 tile per workgroup
-// of 4 waves (32 x 32 each), on v_mfma_f32_16x16x4_f32: fp32 operands and fp32 accumulation, so the
-// scores keep fp32 accuracy (the 1e-4 tie gap of the selection rules out bf16 operands).
+// S[I][J] = sum_c qbar[I][c] * kbar[J][c] for one (b, h) per blockIdx.z, with fp32 accuracy (the
+// 1e-4 tie gap of the selection rules out plain bf16 operands) from bf16 MFMA products:
 // x = hi + mid + lo exactly: each term is the remainder of the ones before, rounded to bf16 (eight
 // significant bits each, and each remainder is exact in fp32). Dropping the three products of two
 // lower terms (mid lo, lo mid, lo lo: about 2^-24 of hi hi) leaves six bf16 MFMA products whose fp32
@@ -182,14 +181,17 @@ __device__ __forceinline__ void split3(const float (&x)[8], bf16x8& hi, bf16x8& 
   }
 }
 
-// 64 x 64 tile of S per workgroup, four waves of 32 x 32; each chunk of 32 channels is split into
-// the three bf16 terms once, in LDS, and every 16 x 16 product takes the six significant products.
-// All global loads are issued up front (rows past nb re-read row nb-1; their scores are not stored).
+// 128 x 128 tile of S per workgroup, four waves of 64 x 64. Each chunk of 32 channels is split
+// into the three bf16 terms once, in LDS (the split costs a workgroup about half as much vector
+// work per product as a 64 x 64 tile would, and each mean crosses L2 half as often); the next
+// chunk's loads are in flight while this one is multiplied. Every 16 x 16 product takes the six
+// significant products, smallest terms first, chunks in order. Rows past nb re-read row nb-1;
+// their scores are not stored. Two workgroups per CU (60 KB of LDS each).
 template <int D>
-__global__ __launch_bounds__(256) void score_kernel(int nb, const float* __restrict__ qbar,
+__global__ __launch_bounds__(256, 2) void score_kernel(int nb, const float* __restrict__ qbar,
                                                     const float* __restrict__ kbar,
                                                     float* __restrict__ S) {
-  constexpr int TS = 64, KC = 32, NCH = D / KC;
+  constexpr int TS = 128, KC = 32, NCH = D / KC;
   constexpr int RS = KC + 8;  // row stride in bf16: 80 bytes, so 16 rows' 16-byte reads spread
   __shared__ __attribute__((aligned(16))) bf16 As[3][TS][RS];
   __shared__ __attribute__((aligned(16))) bf16 Bs[3][TS][RS];
@@ -198,68 +200,81 @@ __global__ __launch_bounds__(256) void score_kernel(int nb, const float* __restr
   const float* k = kbar + head * (long)nb * D;
   const int I0 = blockIdx.y * TS, J0 = blockIdx.x * TS;
   const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64, lr = lane % 16, g = lane / 16;
-  const int wi = (wave >> 1) * 32, wj = (wave & 1) * 32;  // this wave's 32 x 32 sub-tile
-  const int lrow = tid / 4, lcol = (tid % 4) * 8;
+  const int wi = (wave >> 1) * 64, wj = (wave & 1) * 64;  // this wave's 64 x 64 sub-tile
+  const int lrow = tid / 2, lcol = (tid % 2) * 16;         // 16 channels of one row per thread
   const float* qrow = q + (long)min(I0 + lrow, nb - 1) * D + lcol;
   const float* krow = k + (long)min(J0 + lrow, nb - 1) * D + lcol;
-  float a[NCH][8], b[NCH][8];
+  float a[16], b[16];  // this thread's 16 channels of the chunk being split
+  load8(qrow, a);
+  load8(qrow + 8, a + 8);
+  load8(krow, b);
+  load8(krow + 8, b + 8);
+  f32x4 acc[4][4];
 #pragma unroll
-  for (int c = 0; c < NCH; ++c) {
-    load8(qrow + c * KC, a[c]);
-    load8(krow + c * KC, b[c]);
-  }
-  f32x4 acc[2][2];
+  for (int a4 = 0; a4 < 4; ++a4)
 #pragma unroll
-  for (int a2 = 0; a2 < 2; ++a2)
-#pragma unroll
-    for (int b2 = 0; b2 < 2; ++b2) acc[a2][b2] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int b4 = 0; b4 < 4; ++b4) acc[a4][b4] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
     if (c) __syncthreads();  // the previous chunk's reads are done
-    {
+#pragma unroll
+    for (int h8 = 0; h8 < 2; ++h8) {
       bf16x8 h, m, l;
-      split3(a[c], h, m, l);
-      *reinterpret_cast<bf16x8*>(&As[0][lrow][lcol]) = h;
-      *reinterpret_cast<bf16x8*>(&As[1][lrow][lcol]) = m;
-      *reinterpret_cast<bf16x8*>(&As[2][lrow][lcol]) = l;
-      split3(b[c], h, m, l);
-      *reinterpret_cast<bf16x8*>(&Bs[0][lrow][lcol]) = h;
-      *reinterpret_cast<bf16x8*>(&Bs[1][lrow][lcol]) = m;
-      *reinterpret_cast<bf16x8*>(&Bs[2][lrow][lcol]) = l;
+      split3(*reinterpret_cast<const float(*)[8]>(a + 8 * h8), h, m, l);
+      *reinterpret_cast<bf16x8*>(&As[0][lrow][lcol + 8 * h8]) = h;
+      *reinterpret_cast<bf16x8*>(&As[1][lrow][lcol + 8 * h8]) = m;
+      *reinterpret_cast<bf16x8*>(&As[2][lrow][lcol + 8 * h8]) = l;
+      split3(*reinterpret_cast<const float(*)[8]>(b + 8 * h8), h, m, l);
+      *reinterpret_cast<bf16x8*>(&Bs[0][lrow][lcol + 8 * h8]) = h;
+      *reinterpret_cast<bf16x8*>(&Bs[1][lrow][lcol + 8 * h8]) = m;
+      *reinterpret_cast<bf16x8*>(&Bs[2][lrow][lcol + 8 * h8]) = l;
+    }
+    if (c + 1 < NCH) {  // the next chunk loads while this one is multiplied
+      load8(qrow + (c + 1) * KC, a);
+      load8(qrow + (c + 1) * KC + 8, a + 8);
+      load8(krow + (c + 1) * KC, b);
+      load8(krow + (c + 1) * KC + 8, b + 8);
     }
     __syncthreads();
     // lane holds A[row lr][k 8g..8g+7] and B[k 8g..8g+7][col lr] of each 16 x 16 tile
-    bf16x8 av[2][3], bv[2][3];
+    bf16x8 bv[4][3];
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int t = 0; t < 4; ++t)
 #pragma unroll
-      for (int p = 0; p < 3; ++p) {
-        av[t][p] = *reinterpret_cast<const bf16x8*>(&As[p][wi + 16 * t + lr][8 * g]);
+      for (int p = 0; p < 3; ++p)
         bv[t][p] = *reinterpret_cast<const bf16x8*>(&Bs[p][wj + 16 * t + lr][8 * g]);
-      }
 #pragma unroll
-    for (int a2 = 0; a2 < 2; ++a2)
+    for (int a4 = 0; a4 < 4; ++a4) {
+      bf16x8 av[3];
 #pragma unroll
-      for (int b2 = 0; b2 < 2; ++b2) {
-        f32x4 x = acc[a2][b2];  // smallest terms first
-        x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[a2][2], bv[b2][0], x, 0, 0, 0);
-        x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[a2][1], bv[b2][1], x, 0, 0, 0);
-        x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[a2][0], bv[b2][2], x, 0, 0, 0);
-        x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[a2][1], bv[b2][0], x, 0, 0, 0);
-        x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[a2][0], bv[b2][1], x, 0, 0, 0);
-        acc[a2][b2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[a2][0], bv[b2][0], x, 0, 0, 0);
+      for (int p = 0; p < 3; ++p)
+        av[p] = *reinterpret_cast<const bf16x8*>(&As[p][wi + 16 * a4 + lr][8 * g]);
+#pragma unroll
+      for (int b4 = 0; b4 < 4; ++b4) {
+        f32x4 x = acc[a4][b4];  // smallest terms first
+        x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[2], bv[b4][0], x, 0, 0, 0);
+        x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[1], bv[b4][1], x, 0, 0, 0);
+        x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[0], bv[b4][2], x, 0, 0, 0);
+        x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[1], bv[b4][0], x, 0, 0, 0);
+        x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[0], bv[b4][1], x, 0, 0, 0);
+        acc[a4][b4] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[0], bv[b4][0], x, 0, 0, 0);
       }
+    }
   }
   float* Sh = S + head * (long)nb * nb;
 #pragma unroll
-  for (int a2 = 0; a2 < 2; ++a2)
+  for (int a4 = 0; a4 < 4; ++a4)
 #pragma unroll
-    for (int b2 = 0; b2 < 2; ++b2)
+    for (int v = 0; v < 4; ++v) {
+      const int I = I0 + wi + 16 * a4 + 4 * g + v;
+      if (I < nb) {
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int I = I0 + wi + 16 * a2 + 4 * g + v, J = J0 + wj + 16 * b2 + lr;
-        if (I < nb && J < nb) Sh[(long)I * nb + J] = acc[a2][b2][v];
+        for (int b4 = 0; b4 < 4; ++b4) {
+          const int J = J0 + wj + 16 * b4 + lr;
+          if (J < nb) Sh[(long)I * nb + J] = acc[a4][b4][v];
+        }
       }
+    }
 }
 
 __device__ __forceinline__ uint32_t order_key(float f) {
@@ -541,7 +556,7 @@ hipError_t launch_select_pooled(const Shape& s, const float* qbar, const float* 
   const int nb = num_blocks(s.N, block);
   const size_t heads = (size_t)s.B * s.H;
   float* S = (float*)ws;
-  const int tiles = (nb + 63) / 64;
+  const int tiles = (nb + 127) / 128;
   if (s.d == 128)
     hipLaunchKernelGGL(score_kernel<128>, dim3(tiles, tiles, (unsigned)heads), dim3(256), 0, st, nb,
                        qbar, kbar, S);
