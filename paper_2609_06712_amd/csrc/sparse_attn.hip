@@ -602,7 +602,7 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void s
       v = TAB > 0 ? wave_uniform(v) : v;
       const int J = G > 1 ? (v & 0xFFFF) : v;
       const int mask = G > 1 ? (v >> 16) : 1;
-      return Step{(unsigned)J < (unsigned)nb ? J * BLK + (t % SUBS) * kSub : -1, mask};
+      return Step{(unsigned)J < (unsigned)nb ? J * BLK + (int)((unsigned)t % SUBS) * kSub : -1, mask};
     };
     auto active = [&](const Step& s) { return (s.mask & mybit) && s.k0 >= 0 && s.k0 < N; };
 
@@ -774,11 +774,21 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void s
         issue(step_of(raw(j / SUBS), j), j);
         ++issued;
       }
-    int pi = raw(issued / SUBS), pc = raw(0);  // entries the next step decodes
+    int pi = raw((unsigned)issued / SUBS), pc = raw(0);  // entries the next step decodes
     for (int t = 0; t < T;) {
 #pragma unroll
       for (int j = 0; j < NBUF; ++j) {
         if (t >= T) break;
+        // This step's entry and the one whose loads it issues are decoded before the wait and the
+        // barrier: only the loads themselves must follow the barrier, so the scalar decoding no
+        // longer sits between the barrier and the step's first LDS reads and products.
+        Step cur = step_of(pc, t), nxt = step_of(pi, issued);
+        int act = wave_uniform(active(cur) ? 1 : 0);
+        cur.k0 = wave_uniform(cur.k0);
+        nxt.k0 = wave_uniform(nxt.k0);
+        const bool more = issued < T;
+        // (pinned here: the compiler would otherwise sink the decoding to its uses)
+        asm volatile("" : "+s"(cur.k0), "+s"(nxt.k0), "+s"(act));
         if (issued == t + NBUF - 1) {  // loads of t+1 .. t+NBUF-2 may stay in flight
           constexpr int allowed = PER_STEP * (NBUF - 2);
           __builtin_amdgcn_s_waitcnt((allowed & 15) | ((allowed >> 4) << 14) | (7 << 4) | (15 << 8));
@@ -786,14 +796,13 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void s
           __builtin_amdgcn_s_waitcnt(0);
         }
         __syncthreads();  // sub-tile t landed for every wave; every wave is done with sub-tile t-1
-        if (issued < T) {
-          issue(step_of(pi, issued), (j + NBUF - 1) % NBUF);
+        if (more) {
+          issue(nxt, (j + NBUF - 1) % NBUF);
           ++issued;
         }
-        const Step cur = step_of(pc, t);
-        pi = raw(issued / SUBS);
-        pc = raw((t + 1) / SUBS);
-        if (DQ && active(cur)) {
+        pi = raw((unsigned)issued / SUBS);
+        pc = raw((unsigned)(t + 1) / SUBS);
+        if (DQ && act) {
           const char* Kt = lds + j * STAGE;
           const char* Vt = Kt + TILE;
           f32x16 sc = f32x16{}, dp = f32x16{};
@@ -820,7 +829,7 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void s
 #pragma unroll
             for (int u = 0; u < 2; ++u) acc[w] = mfma32(tr_frag(Kt, w, u, lane), ds[u], acc[w]);
           __builtin_amdgcn_s_setprio(0);
-        } else if (!DQ && active(cur)) {
+        } else if (!DQ && act) {
           bf16x8 kf[4], kg[4], vf[4], pb[2];
           load_k(j, 0, kf);
           load_k(j, 4, kg);
