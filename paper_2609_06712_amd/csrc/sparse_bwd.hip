@@ -342,7 +342,9 @@ void sparse_dkv_kernel(
   }
   const uint32_t lds0 = lds_address(lds);
   const char* lsebase = reinterpret_cast<const char*>(lseD + head * (long)N);
-  auto query0 = [&](int t) { return rl[1 + t / SUBS] * BLK + (t % SUBS) * kBSub; };
+  auto query0 = [&](int t) {  // t >= 0
+    return rl[1 + (unsigned)t / SUBS] * BLK + (int)((unsigned)t % SUBS) * kBSub;
+  };
   auto issue = [&](int q0, int buf) {  // DPW loads per wave, and wave 0 one more (lse/D)
     const uint32_t dst = lds0 + buf * STAGE;
 #pragma unroll
@@ -366,6 +368,11 @@ void sparse_dkv_kernel(
 #pragma unroll
     for (int b = 0; b < NBUF; ++b) {
       if (t > T) break;
+      // The first query of this step's tile and of the tile whose loads it issues, read from the
+      // list before the wait and the barrier (indices clamped into the list; pinned in SGPRs, or
+      // the compiler sinks the scalar loads behind the barrier).
+      int qcur = query0(max(0, min(t, T - 1))), qiss = query0(max(0, min(issued, T - 1)));
+      asm volatile("" : "+s"(qcur), "+s"(qiss));
       if (t < T && issued == t + AHEAD) {
         constexpr int a0 = (DPW + 1) * (AHEAD - 1), a1 = DPW * (AHEAD - 1);
         if (wave == 0)
@@ -376,7 +383,7 @@ void sparse_dkv_kernel(
         __builtin_amdgcn_s_waitcnt(0);
       }
       __syncthreads();
-      if (issued < T) issue(query0(issued), (b + AHEAD) % NBUF), ++issued;
+      if (issued < T) issue(qiss, (b + AHEAD) % NBUF), ++issued;
       if (role ? t >= 1 : t < T) {
         const char* Qt = lds + (role ? (b + NBUF - 1) % NBUF : b) * STAGE;
         const char* dOt = Qt + TILE;
@@ -401,7 +408,7 @@ void sparse_dkv_kernel(
         float p[16];
         bf16x8 b2[2];
         if (role == 0) {
-          const int q0 = query0(t);
+          const int q0 = qcur;
           // The exponentials are computed unconditionally and rows past N zeroed in one uniform
           // branch: a per-element condition around them splits the step into a basic block per
           // element, across which no matrix instruction can be scheduled.
