@@ -742,11 +742,11 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void s
     // max unchanged and only their probabilities are zeroed. The row sum adds exactly the bf16
     // probabilities that enter P V (v_dot2 against (1, 1), fp32 accumulation).
     typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-    auto probs = [&](const f32x16& s, int k0, bf16x8 (&pb)[2]) {
+    auto probs = [&](const f32x16& s, int k0, int tail, bf16x8 (&pb)[2]) {
 #pragma unroll
       for (int k = 0; k < 16; ++k)
         pb[k / 8][k % 8] = (bf16)__builtin_amdgcn_exp2f(fmaf(s[k], scale_log2, -m));
-      if (k0 + kSub > N) {  // value k holds key k0 + 8(k/4) + 4(l/32) + k%4
+      if (tail) {  // value k holds key k0 + 8(k/4) + 4(l/32) + k%4
         const int lim = N - k0 - 4 * hh;
 #pragma unroll
         for (int k = 0; k < 16; ++k)
@@ -783,12 +783,15 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void s
         // barrier: only the loads themselves must follow the barrier, so the scalar decoding no
         // longer sits between the barrier and the step's first LDS reads and products.
         Step cur = step_of(pc, t), nxt = step_of(pi, issued);
-        int act = wave_uniform(active(cur) ? 1 : 0);
         cur.k0 = wave_uniform(cur.k0);
         nxt.k0 = wave_uniform(nxt.k0);
+        const int cmask = wave_uniform(cur.mask);
+        // active(cur) in scalar arithmetic: k0 >= 0 && k0 < N as one unsigned compare
+        int act = wave_uniform(((cmask & mybit) != 0) & ((unsigned)cur.k0 < (unsigned)N));
+        int ctail = wave_uniform(cur.k0 + kSub > N);  // ragged last sub-tile
         const bool more = issued < T;
         // (pinned here: the compiler would otherwise sink the decoding to its uses)
-        asm volatile("" : "+s"(cur.k0), "+s"(nxt.k0), "+s"(act));
+        asm volatile("" : "+s"(cur.k0), "+s"(nxt.k0), "+s"(act), "+s"(ctail));
         if (issued == t + NBUF - 1) {  // loads of t+1 .. t+NBUF-2 may stay in flight
           constexpr int allowed = PER_STEP * (NBUF - 2);
           __builtin_amdgcn_s_waitcnt((allowed & 15) | ((allowed >> 4) << 14) | (7 << 4) | (15 << 8));
@@ -850,7 +853,7 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void s
           // (BOUND re-reads the flag as uniform: taken as a per-lane value, the branch keeps the
           // step's registers live on both sides and the kernel spills)
           if (!BOUND || !wave_uniform(fixed_m)) rescale(row_max(sc));
-          probs(sc, cur.k0, pb);
+          probs(sc, cur.k0, ctail, pb);
           // the P V products at raised wave priority: a wave that has its probabilities issues its
           // MFMAs ahead of the other waves' score and softmax work (plain attention on the 14B
           // layer: 12.80 -> 12.58 ms; the same priority around Q K^T costs a third more time).
