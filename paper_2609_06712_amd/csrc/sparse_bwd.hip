@@ -347,11 +347,20 @@ void sparse_dkv_kernel(
   };
   auto issue = [&](int q0, int buf) {  // DPW loads per wave, and wave 0 one more (lse/D)
     const uint32_t dst = lds0 + buf * STAGE;
+    if (q0 + kBSub <= N) {  // every row of the tile exists: one scalar base per tensor
+      const uint32_t base = (uint32_t)q0 * (D * 2);
 #pragma unroll
-    for (int i = 0; i < DPW; ++i) {
-      const int g = wave * DPW + i, r = 4 * (g % 8) + lane / 16;
-      const uint32_t rowoff = (uint32_t)(min(q0 + r, N - 1) - r) * (D * 2);  // rows past N: N-1
-      dma16(g < 8 ? Qh : dOh, rowoff + dsrc[i], dst + (g / 8) * TILE + (g % 8) * 1024);
+      for (int i = 0; i < DPW; ++i) {
+        const int g = wave * DPW + i;
+        dma16((g < 8 ? Qh : dOh) + base, dsrc[i], dst + (g / 8) * TILE + (g % 8) * 1024);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < DPW; ++i) {
+        const int g = wave * DPW + i, r = 4 * (g % 8) + lane / 16;
+        const uint32_t rowoff = (uint32_t)(min(q0 + r, N - 1) - r) * (D * 2);  // rows past N: N-1
+        dma16(g < 8 ? Qh : dOh, rowoff + dsrc[i], dst + (g / 8) * TILE + (g % 8) * 1024);
+      }
     }
     // lse, D of the 32 queries (256 bytes; lanes 16-63 repeat lanes 0-15): the array is padded by
     // kLsePad entries, and rows past N are masked below
