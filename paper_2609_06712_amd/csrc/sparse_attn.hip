@@ -604,7 +604,6 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void s
       const int mask = G > 1 ? (v >> 16) : 1;
       return Step{(unsigned)J < (unsigned)nb ? J * BLK + (int)((unsigned)t % SUBS) * kSub : -1, mask};
     };
-    auto active = [&](const Step& s) { return (s.mask & mybit) && s.k0 >= 0 && s.k0 < N; };
 
     // Q^T fragments of the 8 k-steps (d = 16s + 8(l/32) .. +7) stay in registers. They are complete
     // before the first K/V load is issued: a wait for them inside the loop would also drain the
@@ -786,7 +785,8 @@ __global__ __launch_bounds__(G * BLK * 2, QUEUE && RJ < 2 && !DQ ? 3 : 2) void s
         cur.k0 = wave_uniform(cur.k0);
         nxt.k0 = wave_uniform(nxt.k0);
         const int cmask = wave_uniform(cur.mask);
-        // active(cur) in scalar arithmetic: k0 >= 0 && k0 < N as one unsigned compare
+        // whether this wave computes the step, in scalar arithmetic: k0 >= 0 && k0 < N as one
+        // unsigned compare
         int act = wave_uniform(((cmask & mybit) != 0) & ((unsigned)cur.k0 < (unsigned)N));
         int ctail = wave_uniform(cur.k0 + kSub > N);  // ragged last sub-tile
         const bool more = issued < T;
