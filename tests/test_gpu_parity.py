@@ -416,6 +416,39 @@ def test_topk_crafted_rows(grid):
     assert np.array_equal(idx, want)
 
 
+def test_out_of_range_entries_skipped():
+    """Block lists a caller hands in may hold entries outside [0, n_b): here n_b + 3 as the last
+    entry of every other row and -1 as the first entry of every third. Every path skips them (the
+    pairing and the list merge drop them; the one-block walk decodes them as no keys), so O^s is
+    the oracle's attention over each row's valid entries, on the merged-list path and the
+    one-block path alike. Ragged grid: 390 tokens, 7 blocks of 64, the last of 6 tokens."""
+    w = synth.WAN_1_3B_480P.replace(grid=(3, 10, 13), H=2)
+    gen = torch.Generator().manual_seed(21)
+    qr = torch.randn((1, w.H, w.N, 128), generator=gen).to(torch.bfloat16)
+    kr = torch.randn((1, w.H, w.N, 128), generator=gen).to(torch.bfloat16)
+    v = torch.randn((1, w.H, w.N, 128), generator=gen).to(torch.bfloat16)
+    nb = O.num_blocks(w.N, 64)
+    idx = R.rola_block_select(qr.cuda(), kr.cuda(), w.grid, 64, 0.5)
+    bad = idx.clone()
+    bad[:, :, 0::2, -1] = nb + 3
+    bad[:, :, 0::3, 0] = -1
+    outs = {share: R.rola_sparse_attn(qr.cuda(), kr.cuda(), v.cuda(), w.grid, 64, 0.5, bad,
+                                      share=share).double().cpu().numpy()
+            for share in (True, False)}
+    lists = bad.cpu().numpy()
+    for h in range(w.H):
+        valid = np.empty(nb, dtype=object)
+        for I in range(nb):
+            valid[I] = np.array([J for J in lists[0, h, I] if 0 <= J < nb], dtype=np.int64)
+        want = O.sparse_attention(qr[0, h].double().numpy(), kr[0, h].double().numpy(),
+                                  v[0, h].double().numpy(), valid, 64, 128 ** -0.5)
+        for share, out in outs.items():
+            d = np.abs(out[0, h] - want)
+            _report("out-of-range entries", head=h, share=share, max_abs=float(d.max()),
+                    mean_abs=float(d.mean()))
+            assert d.max() <= T.TOL["bf16"]["max_abs"] and d.mean() <= T.TOL["bf16"]["mean_abs"]
+
+
 def test_exact_ties_go_to_lower_block():
     """Identical key blocks tie exactly: every row must keep the lowest block indices."""
     w = synth.WAN_1_3B_480P.replace(grid=(2, 8, 16), H=2)
